@@ -1,0 +1,439 @@
+/*
+ * bcjr_oracle.c -- plain fp64 CPU oracle.  TEST INFRASTRUCTURE ONLY: the
+ * product path never links or calls it (see bcjr_oracle.h).
+ *
+ * Everything is written from the definitions, state by state, with no
+ * grouping of states, no tiling and no reordering beyond what the equations
+ * state:
+ *   - the trellis (paper Sec. 3.1): next(s, b) = ((s << k) | b) & (S - 1);
+ *   - the local field h_t(s) = -(w_t - c(s))^2 / (2T) (Sec. 3.3, Eq. boltzmann);
+ *   - the forward / backward partition functions and their linear
+ *     recursions through the transfer matrix T_{s->s'} = 1[next(s, .) = s']
+ *     (Sec. 3.4, Eqs. alpha, beta and the two recursions that follow them),
+ *     carried in the log domain (Sec. 3.4, "Numerical stability");
+ *   - the marginal p_T(s_t = s) = alpha_t(s) beta_t(s) / Z_T and
+ *     Z_T = sum_s alpha_t(s) beta_t(s) (Eq. marginal);
+ *   - the soft codeword  sum_s c(s) p_T(s_t = s)  (Eqs. soft-codeword,
+ *     softcode-final);
+ *   - the VJP.  The paper gives no formula for its backward pass (Sec. 3.5
+ *     only names an implicit-differentiation shortcut), so it is derived
+ *     from Eq. boltzmann: with F = sum_t g_t c(s_t),  <g, w_soft> = E_p[F],
+ *     and since d(-E/T)/dw_tau = -(w_tau - c(s_tau))/T,
+ *        dW_tau = Cov_p(F, c(s_tau)) / T,
+ *        dc_sig = sum_t p_t(sig) [ g_t + (w_t - c_sig)(E[F | s_t = sig] - E[F]) / T ].
+ *     E[F | s_t = s] = A_t(s) + B_t(s) splits into the part of F up to t
+ *     (forward conditional expectation A) and after t (backward, B); both
+ *     follow recursions with the same weights as the alpha / beta sums;
+ *   - Viterbi (Sec. 3.2): min-sum dynamic programming with backtrack.
+ * The first state s_1 carries no prior weight: alpha_1(s) = exp(h_1(s)).
+ */
+#include "bcjr_oracle.h"
+
+#include <math.h>
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+static int bad_args(int64_t B, int64_t L, const void *w, const void *c, int n,
+                    int k, double T) {
+  if (B < 0 || L < 1 || !w || !c) return 1;
+  if (k < 1 || n < k || n > 16) return 1;
+  if (!(T > 0.0) || !isfinite(T)) return 1;
+  return 0;
+}
+
+/* log(exp(a) + exp(b)), exact in the limits a or b = -inf */
+static double log_add_exp(double a, double b) {
+  if (a == -INFINITY) return b;
+  if (b == -INFINITY) return a;
+  double m = a > b ? a : b;
+  return m + log1p(exp(-fabs(a - b)));
+}
+
+static double field(double w, double c, double T) {
+  double d = w - c;
+  return -(d * d) / (2.0 * T);
+}
+
+/* ------------------------------------------------------------------ */
+/* one block: forward-backward, optional VJP                            */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+  double *alpha; /* [L*S] */
+  double *A;     /* [L*S] or NULL */
+  double *acc;   /* [S] */
+  double *num;   /* [S] */
+  double *beta;  /* [S] current beta_t */
+  double *betap; /* [S] beta_{t-1} being built */
+  double *Bc;    /* [S] current B_t */
+  double *Bp;    /* [S] B_{t-1} */
+  double *p;     /* [S] */
+} work_t;
+
+static int work_alloc(work_t *wk, int64_t L, int64_t S, int want_vjp) {
+  memset(wk, 0, sizeof(*wk));
+  wk->alpha = (double *)malloc(sizeof(double) * (size_t)(L * S));
+  wk->A = want_vjp ? (double *)malloc(sizeof(double) * (size_t)(L * S)) : NULL;
+  wk->acc = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->num = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->beta = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->betap = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->Bc = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->Bp = (double *)malloc(sizeof(double) * (size_t)S);
+  wk->p = (double *)malloc(sizeof(double) * (size_t)S);
+  if (!wk->alpha || (want_vjp && !wk->A) || !wk->acc || !wk->num ||
+      !wk->beta || !wk->betap || !wk->Bc || !wk->Bp || !wk->p)
+    return -1;
+  return 0;
+}
+
+static void work_free(work_t *wk) {
+  free(wk->alpha);
+  free(wk->A);
+  free(wk->acc);
+  free(wk->num);
+  free(wk->beta);
+  free(wk->betap);
+  free(wk->Bc);
+  free(wk->Bp);
+  free(wk->p);
+}
+
+/* Forward sweep: log alpha_t(s) for all t (Eq. alpha and its recursion),
+ * and, when g != NULL, A_t(s) = E[sum_{tau<=t} g_tau c(s_tau) | s_t = s,
+ * w_1..w_t]: A_1(s) = g_1 c(s);
+ * A_t(s) = g_t c(s) + sum_{s'->s} alpha_{t-1}(s') A_{t-1}(s') / sum_{s'->s} alpha_{t-1}(s'). */
+static void forward_sweep(const double *w, int64_t L, const double *c, int n,
+                          int k, double T, const double *g, work_t *wk) {
+  const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
+  double *alpha = wk->alpha, *A = wk->A, *acc = wk->acc, *num = wk->num;
+  for (int64_t s = 0; s < S; ++s) {
+    alpha[s] = field(w[0], c[s], T);
+    if (g) A[s] = g[0] * c[s];
+  }
+  for (int64_t t = 1; t < L; ++t) {
+    const double *ap = alpha + (t - 1) * S;
+    double *at = alpha + t * S;
+    for (int64_t s = 0; s < S; ++s) acc[s] = -INFINITY;
+    /* sum over s' with T_{s' -> s} = 1, in the log domain */
+    for (int64_t sp = 0; sp < S; ++sp)
+      for (int64_t b = 0; b < K; ++b) {
+        int64_t d = ((sp << k) | b) & mask;
+        acc[d] = log_add_exp(acc[d], ap[sp]);
+      }
+    for (int64_t s = 0; s < S; ++s) at[s] = field(w[t], c[s], T) + acc[s];
+    if (g) {
+      const double *Ap = A + (t - 1) * S;
+      double *At = A + t * S;
+      for (int64_t s = 0; s < S; ++s) num[s] = 0.0;
+      for (int64_t sp = 0; sp < S; ++sp)
+        for (int64_t b = 0; b < K; ++b) {
+          int64_t d = ((sp << k) | b) & mask;
+          num[d] += exp(ap[sp] - acc[d]) * Ap[sp];
+        }
+      for (int64_t s = 0; s < S; ++s) At[s] = g[t] * c[s] + num[s];
+    }
+  }
+}
+
+static double lse_row(const double *x, int64_t S) {
+  double m = -INFINITY;
+  for (int64_t s = 0; s < S; ++s)
+    if (x[s] > m) m = x[s];
+  if (m == -INFINITY) return m;
+  double sum = 0.0;
+  for (int64_t s = 0; s < S; ++s) sum += exp(x[s] - m);
+  return m + log(sum);
+}
+
+/* Backward step: from log beta_t (beta, 0-based index t) build log beta_{t-1}:
+ * beta_{t-1}(s) = LSE_b [ h_t(next(s,b)) + beta_t(next(s,b)) ]  (recursion of
+ * Eq. beta), and, when g != NULL, the backward conditional expectation
+ * B_{t-1}(s) = E[sum_{tau>=t} g_tau c(s_tau) | s_{t-1} = s, w_t..w_L]. */
+static void backward_step(const double *w, int64_t t, const double *c, int n,
+                          int k, double T, const double *g, work_t *wk) {
+  const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
+  for (int64_t s = 0; s < S; ++s) {
+    double acc = -INFINITY;
+    for (int64_t b = 0; b < K; ++b) {
+      int64_t d = ((s << k) | b) & mask;
+      acc = log_add_exp(acc, field(w[t], c[d], T) + wk->beta[d]);
+    }
+    wk->betap[s] = acc;
+    if (g) {
+      double sum = 0.0;
+      for (int64_t b = 0; b < K; ++b) {
+        int64_t d = ((s << k) | b) & mask;
+        double r = exp(field(w[t], c[d], T) + wk->beta[d] - acc);
+        sum += r * (g[t] * c[d] + wk->Bc[d]);
+      }
+      wk->Bp[s] = sum;
+    }
+  }
+  double *tmp = wk->beta;
+  wk->beta = wk->betap;
+  wk->betap = tmp;
+  tmp = wk->Bc;
+  wk->Bc = wk->Bp;
+  wk->Bp = tmp;
+}
+
+static void block_run(const double *w, int64_t L, const double *c, int n,
+                      int k, double T, const double *g, double *w_soft,
+                      double *logZ_out, double *dW, double *dc, work_t *wk) {
+  const int64_t S = (int64_t)1 << n;
+  forward_sweep(w, L, c, n, k, T, g, wk);
+  const double *aL = wk->alpha + (L - 1) * S;
+  const double logZ = lse_row(aL, S); /* Z = sum_s alpha_L(s), beta_L = 1 */
+  if (logZ_out) *logZ_out = logZ;
+  double EF = 0.0; /* E[F] = sum_s p_L(s) A_L(s) */
+  if (g)
+    for (int64_t s = 0; s < S; ++s) EF += exp(aL[s] - logZ) * wk->A[(L - 1) * S + s];
+  for (int64_t s = 0; s < S; ++s) {
+    wk->beta[s] = 0.0; /* log beta_L = 0 */
+    wk->Bc[s] = 0.0;   /* B_L = 0 */
+  }
+  for (int64_t t = L - 1; t >= 0; --t) {
+    const double *at = wk->alpha + t * S;
+    double ws = 0.0;
+    for (int64_t s = 0; s < S; ++s) {
+      wk->p[s] = exp(at[s] + wk->beta[s] - logZ); /* Eq. marginal */
+      ws += c[s] * wk->p[s];                       /* Eq. soft-codeword */
+    }
+    if (w_soft) w_soft[t] = ws;
+    if (g) {
+      const double *At = wk->A + t * S;
+      double cov = 0.0;
+      for (int64_t s = 0; s < S; ++s) {
+        double X = At[s] + wk->Bc[s] - EF; /* E[F | s_t = s] - E[F] */
+        cov += wk->p[s] * (c[s] - ws) * X;
+        if (dc) dc[s] += wk->p[s] * (g[t] + (w[t] - c[s]) * X / T);
+      }
+      if (dW) dW[t] = cov / T;
+    }
+    if (t > 0) backward_step(w, t, c, n, k, T, g, wk);
+  }
+}
+
+/* ------------------------------------------------------------------ */
+/* threading over blocks                                                */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+  const double *w, *c, *g;
+  int64_t B, L;
+  int n, k;
+  double T;
+  double *w_soft, *logZ, *dW;
+  double *dc_part; /* [S] private to this thread, or NULL */
+  int tid, nthreads;
+  int status;
+} job_t;
+
+static void *job_main(void *arg) {
+  job_t *j = (job_t *)arg;
+  const int64_t S = (int64_t)1 << j->n;
+  work_t wk;
+  if (work_alloc(&wk, j->L, S, j->g != NULL) != 0) {
+    work_free(&wk);
+    j->status = -2;
+    return NULL;
+  }
+  for (int64_t b = j->tid; b < j->B; b += j->nthreads) {
+    block_run(j->w + b * j->L, j->L, j->c, j->n, j->k, j->T, j->g ? j->g + b * j->L : NULL,
+              j->w_soft ? j->w_soft + b * j->L : NULL, j->logZ ? j->logZ + b : NULL,
+              j->dW ? j->dW + b * j->L : NULL, j->dc_part, &wk);
+  }
+  work_free(&wk);
+  j->status = 0;
+  return NULL;
+}
+
+static int run_jobs(const double *w, int64_t B, int64_t L, const double *c,
+                    int n, int k, double T, const double *g, double *w_soft,
+                    double *logZ, double *dW, double *dc, int nthreads) {
+  const int64_t S = (int64_t)1 << n;
+  if (nthreads < 1) nthreads = 1;
+  if ((int64_t)nthreads > B && B > 0) nthreads = (int)B;
+  if (dc)
+    for (int64_t s = 0; s < S; ++s) dc[s] = 0.0;
+  if (B == 0) return 0;
+  job_t *jobs = (job_t *)calloc((size_t)nthreads, sizeof(job_t));
+  pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+  double *parts = dc ? (double *)calloc((size_t)(nthreads * S), sizeof(double)) : NULL;
+  if (!jobs || !th || (dc && !parts)) {
+    free(jobs);
+    free(th);
+    free(parts);
+    return -2;
+  }
+  for (int i = 0; i < nthreads; ++i) {
+    job_t *j = &jobs[i];
+    j->w = w; j->c = c; j->g = g; j->B = B; j->L = L; j->n = n; j->k = k;
+    j->T = T; j->w_soft = w_soft; j->logZ = logZ; j->dW = dW;
+    j->dc_part = dc ? parts + (int64_t)i * S : NULL;
+    j->tid = i; j->nthreads = nthreads; j->status = -3;
+  }
+  for (int i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, job_main, &jobs[i]);
+  job_main(&jobs[0]);
+  for (int i = 1; i < nthreads; ++i) pthread_join(th[i], NULL);
+  int status = 0;
+  for (int i = 0; i < nthreads; ++i)
+    if (jobs[i].status != 0) status = jobs[i].status;
+  if (dc)
+    for (int i = 0; i < nthreads; ++i)
+      for (int64_t s = 0; s < S; ++s) dc[s] += parts[(int64_t)i * S + s];
+  free(jobs);
+  free(th);
+  free(parts);
+  return status;
+}
+
+int oracle_soft_codeword(const double *w, int64_t B, int64_t L, const double *c,
+                         int n, int k, double T, double *w_soft, double *logZ,
+                         int nthreads) {
+  if (bad_args(B, L, w, c, n, k, T)) return -1;
+  return run_jobs(w, B, L, c, n, k, T, NULL, w_soft, logZ, NULL, NULL, nthreads);
+}
+
+int oracle_soft_codeword_vjp(const double *w, int64_t B, int64_t L,
+                             const double *c, int n, int k, double T,
+                             const double *g, double *w_soft, double *logZ,
+                             double *dW, double *dc, int nthreads) {
+  if (bad_args(B, L, w, c, n, k, T) || !g) return -1;
+  return run_jobs(w, B, L, c, n, k, T, g, w_soft, logZ, dW, dc, nthreads);
+}
+
+int oracle_block_tables(const double *w, int64_t L, const double *c, int n,
+                        int k, double T, const double *g, double *alpha,
+                        double *beta, double *A, double *Bt) {
+  if (bad_args(1, L, w, c, n, k, T) || !alpha || !beta) return -1;
+  if (g && (!A || !Bt)) return -1;
+  const int64_t S = (int64_t)1 << n;
+  work_t wk;
+  if (work_alloc(&wk, L, S, g != NULL) != 0) {
+    work_free(&wk);
+    return -2;
+  }
+  forward_sweep(w, L, c, n, k, T, g, &wk);
+  memcpy(alpha, wk.alpha, sizeof(double) * (size_t)(L * S));
+  if (g) memcpy(A, wk.A, sizeof(double) * (size_t)(L * S));
+  for (int64_t s = 0; s < S; ++s) {
+    wk.beta[s] = 0.0;
+    wk.Bc[s] = 0.0;
+  }
+  for (int64_t t = L - 1; t >= 0; --t) {
+    memcpy(beta + t * S, wk.beta, sizeof(double) * (size_t)S);
+    if (g) memcpy(Bt + t * S, wk.Bc, sizeof(double) * (size_t)S);
+    if (t > 0) backward_step(w, t, c, n, k, T, g, &wk);
+  }
+  work_free(&wk);
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Viterbi                                                              */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+  const double *w, *c;
+  int64_t B, L;
+  int n, k;
+  int32_t *states;
+  double *cost;
+  int tid, nthreads, status;
+} vjob_t;
+
+/* squared distortion, multiply and add rounded separately (no fused ops;
+ * the file is compiled with -ffp-contract=off) */
+static double sqdist(double w, double c) {
+  double d = w - c;
+  return d * d;
+}
+
+static void viterbi_block(const double *w, int64_t L, const double *c, int n,
+                          int k, int32_t *states, double *cost, double *m,
+                          double *mn, double *best, int32_t *from) {
+  const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
+  for (int64_t s = 0; s < S; ++s) m[s] = sqdist(w[0], c[s]);
+  for (int64_t t = 1; t < L; ++t) {
+    int32_t *ft = from + t * S;
+    for (int64_t s = 0; s < S; ++s) {
+      best[s] = INFINITY;
+      ft[s] = -1;
+    }
+    /* predecessors visited in increasing state order; strict '<' keeps the
+     * smallest predecessor among equal minima */
+    for (int64_t sp = 0; sp < S; ++sp)
+      for (int64_t b = 0; b < K; ++b) {
+        int64_t d = ((sp << k) | b) & mask;
+        if (ft[d] < 0 || m[sp] < best[d]) {
+          best[d] = m[sp];
+          ft[d] = (int32_t)sp;
+        }
+      }
+    for (int64_t s = 0; s < S; ++s) mn[s] = sqdist(w[t], c[s]) + best[s];
+    double *tmp = m;
+    m = mn;
+    mn = tmp;
+  }
+  int64_t sb = 0;
+  for (int64_t s = 1; s < S; ++s)
+    if (m[s] < m[sb]) sb = s;
+  if (cost) *cost = m[sb];
+  states[L - 1] = (int32_t)sb;
+  for (int64_t t = L - 1; t >= 1; --t) states[t - 1] = from[t * S + states[t]];
+}
+
+static void *vjob_main(void *arg) {
+  vjob_t *j = (vjob_t *)arg;
+  const int64_t S = (int64_t)1 << j->n;
+  double *m = (double *)malloc(sizeof(double) * (size_t)S);
+  double *mn = (double *)malloc(sizeof(double) * (size_t)S);
+  double *best = (double *)malloc(sizeof(double) * (size_t)S);
+  int32_t *from = (int32_t *)malloc(sizeof(int32_t) * (size_t)(j->L * S));
+  if (!m || !mn || !best || !from) {
+    j->status = -2;
+  } else {
+    for (int64_t b = j->tid; b < j->B; b += j->nthreads)
+      viterbi_block(j->w + b * j->L, j->L, j->c, j->n, j->k, j->states + b * j->L,
+                    j->cost ? j->cost + b : NULL, m, mn, best, from);
+    j->status = 0;
+  }
+  free(m);
+  free(mn);
+  free(best);
+  free(from);
+  return NULL;
+}
+
+int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
+                   int n, int k, int32_t *states, double *cost, int nthreads) {
+  if (bad_args(B, L, w, c, n, k, 1.0) || !states) return -1;
+  if (B == 0) return 0;
+  if (nthreads < 1) nthreads = 1;
+  if ((int64_t)nthreads > B) nthreads = (int)B;
+  vjob_t *jobs = (vjob_t *)calloc((size_t)nthreads, sizeof(vjob_t));
+  pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+  if (!jobs || !th) {
+    free(jobs);
+    free(th);
+    return -2;
+  }
+  for (int i = 0; i < nthreads; ++i) {
+    vjob_t *j = &jobs[i];
+    j->w = w; j->c = c; j->B = B; j->L = L; j->n = n; j->k = k;
+    j->states = states; j->cost = cost; j->tid = i; j->nthreads = nthreads;
+    j->status = -3;
+  }
+  for (int i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, vjob_main, &jobs[i]);
+  vjob_main(&jobs[0]);
+  for (int i = 1; i < nthreads; ++i) pthread_join(th[i], NULL);
+  int status = 0;
+  for (int i = 0; i < nthreads; ++i)
+    if (jobs[i].status != 0) status = jobs[i].status;
+  free(jobs);
+  free(th);
+  return status;
+}

@@ -1,0 +1,66 @@
+/*
+ * bcjr_oracle.h -- plain fp64 CPU oracle for the temperature-T BCJR soft
+ * codeword over a bitshift trellis, its vector-Jacobian product, and the
+ * Viterbi (T -> 0) decode.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or
+ * calls this library: only the tests, the package smoke check and the CPU
+ * baseline leg of the benchmark do.  It shares no code, header, table or
+ * helper with the HIP implementation.
+ *
+ * Model (paper, Sec. 3.1 "Trellis setup", Eq. boltzmann):
+ *   states s in {0..S-1}, S = 2^n, K = 2^k inputs per step,
+ *   transition  next(s, b) = ((s << k) | b) & (S - 1),
+ *   a block is w[0..L-1]; a path is s_1..s_L (every state may start),
+ *   energy E(path) = sum_t (w_t - c(s_t))^2 / 2,
+ *   p_T(path) = exp(-E/T) / Z_T.
+ * Indices here are 0-based: w[t], t = 0..L-1, corresponds to w_{t+1}.
+ *
+ * All inputs are double.  Callers holding fp32 data convert it exactly, so
+ * the oracle and the GPU see the same numbers.  T > 0.
+ * Every function returns 0 on success and a negative value on bad arguments.
+ */
+#ifndef BCJR_ORACLE_H
+#define BCJR_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Soft codeword (Eq. soft-codeword via Eqs. alpha, beta, marginal,
+ * softcode-final) and log Z_T (natural log) for B independent blocks.
+ * w[B*L], c[S]; outputs w_soft[B*L], logZ[B].  nthreads <= 0 means one. */
+int oracle_soft_codeword(const double *w, int64_t B, int64_t L,
+                         const double *c, int n, int k, double T,
+                         double *w_soft, double *logZ, int nthreads);
+
+/* Forward outputs plus the VJP of  <g, w_soft>  with respect to w and c.
+ * g[B*L] is the upstream gradient.  dW[B*L] (may be NULL); dc[S] (may be
+ * NULL) is summed over the B blocks.  w_soft/logZ may be NULL. */
+int oracle_soft_codeword_vjp(const double *w, int64_t B, int64_t L,
+                             const double *c, int n, int k, double T,
+                             const double *g, double *w_soft, double *logZ,
+                             double *dW, double *dc, int nthreads);
+
+/* Minimum-distortion path (paper Sec. 3.2): argmin over legal paths of
+ * sum_t (w_t - c(s_t))^2.  Ties: the predecessor with the smallest state
+ * index, then the smallest final state.  states[B*L] (s_1..s_L per block),
+ * cost[B] (may be NULL). */
+int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
+                   int n, int k, int32_t *states, double *cost, int nthreads);
+
+/* Full log-domain tables of ONE block for invariant checks:
+ * alpha[L*S] = log alpha_t(s), beta[L*S] = log beta_t(s) (Eqs. alpha, beta);
+ * optional A[L*S], Bt[L*S] = forward / backward conditional expectations of
+ * the partial sums of g_t c(s_t) (used by the VJP), only if g != NULL. */
+int oracle_block_tables(const double *w, int64_t L, const double *c, int n,
+                        int k, double T, const double *g, double *alpha,
+                        double *beta, double *A, double *Bt);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

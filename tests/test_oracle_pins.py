@@ -1,0 +1,312 @@
+"""Pins for the fp64 CPU oracle (runs without a GPU).
+
+Each test ties the oracle to something other than itself: explicit path
+enumeration, identities of the paper's equations, closed-form limits,
+finite differences, or exact-arithmetic tie cases.
+"""
+import numpy as np
+import pytest
+
+import bruteforce as bf
+from oracle import oracle as O
+
+RNG = np.random.default_rng(20260510)
+
+# (n, k, L): S = 2^n states, K = 2^k inputs per step, L steps.  Covers n >= 2k,
+# n < 2k, n == k (fully connected) and k = 1, 3.
+TINY = [(4, 2, 1), (4, 2, 2), (4, 2, 5), (4, 2, 6), (2, 1, 9), (3, 1, 10),
+        (2, 2, 6), (3, 2, 6), (5, 2, 4), (4, 1, 8), (6, 3, 3), (3, 3, 4)]
+
+
+def _case(n, k, L, seed):
+    r = np.random.default_rng(seed)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    g = r.standard_normal(L)
+    return w, c, g
+
+
+@pytest.mark.parametrize("n,k,L", TINY)
+@pytest.mark.parametrize("T", [1.0, 0.25])
+def test_forward_matches_enumeration(n, k, L, T):
+    """Eq. soft-codeword and Z_T of Eq. boltzmann against all S*K^(L-1) paths."""
+    w, c, _ = _case(n, k, L, 17 * n + 3 * k + L)
+    ref = bf.expectations(w, c, n, k, T)
+    ws, lz = O.soft_codeword(w[None], c, n, k, T)
+    np.testing.assert_allclose(ws[0], ref["w_soft"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lz[0], ref["logZ"], rtol=1e-13, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,k,L", TINY)
+def test_marginals_match_enumeration(n, k, L):
+    """Eq. marginal: alpha_t(s) beta_t(s) / Z is the path marginal."""
+    T = 0.6
+    w, c, _ = _case(n, k, L, 5 * n + k + 11 * L)
+    ref = bf.expectations(w, c, n, k, T)
+    al, be, _, _ = O.block_tables(w, c, n, k, T)
+    lz = O.soft_codeword(w[None], c, n, k, T)[1][0]
+    p = np.exp(al + be - lz)
+    np.testing.assert_allclose(p, ref["marg"], rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,k,L", TINY)
+@pytest.mark.parametrize("T", [1.0, 0.3])
+def test_vjp_matches_enumerated_covariances(n, k, L, T):
+    """dW and dc against path-level covariances (derivative of Eq. boltzmann)."""
+    w, c, g = _case(n, k, L, 101 * n + 7 * k + L)
+    ref = bf.expectations(w, c, n, k, T, g)
+    ws, lz, dW, dc = O.soft_codeword_vjp(w[None], c, n, k, T, g[None])
+    scale = max(1.0, np.abs(ref["dW"]).max())
+    np.testing.assert_allclose(dW[0], ref["dW"], rtol=0, atol=1e-11 * scale)
+    scale = max(1.0, np.abs(ref["dc"]).max())
+    np.testing.assert_allclose(dc, ref["dc"], rtol=0, atol=1e-11 * scale)
+    np.testing.assert_allclose(ws[0], ref["w_soft"], atol=1e-12)
+
+
+def test_partition_function_same_at_every_step():
+    """Eq. marginal: Z = sum_s alpha_t(s) beta_t(s) for any t; marginals sum to 1."""
+    n, k, L, T = 8, 2, 40, 0.2
+    w, c, _ = _case(n, k, L, 3)
+    al, be, _, _ = O.block_tables(w, c, n, k, T)
+    lz = O.soft_codeword(w[None], c, n, k, T)[1][0]
+    x = al + be
+    m = x.max(1, keepdims=True)
+    per_t = (m[:, 0] + np.log(np.exp(x - m).sum(1)))
+    np.testing.assert_allclose(per_t, lz, rtol=1e-13)
+    np.testing.assert_allclose(np.exp(x - lz).sum(1), 1.0, rtol=1e-12)
+
+
+def _fd_logZ(w, c, n, k, T, h):
+    L = w.shape[0]
+    W = np.repeat(w[None], 2 * L, 0)
+    for t in range(L):
+        W[2 * t, t] += h
+        W[2 * t + 1, t] -= h
+    lz = O.soft_codeword(W, c, n, k, T)[1]
+    return (lz[0::2] - lz[1::2]) / (2 * h)
+
+
+@pytest.mark.parametrize("n,k", [(6, 2), (8, 2), (5, 1)])
+def test_soft_codeword_is_gradient_of_logZ(n, k):
+    """w_soft = w + T d logZ / dw  (Eq. boltzmann), by central differences of
+    the forward-only log Z: pins w_soft independently of the beta sweep."""
+    L, T = 12, 0.4
+    w, c, _ = _case(n, k, L, 9 + n)
+    ws = O.soft_codeword(w[None], c, n, k, T)[0][0]
+    grad = _fd_logZ(w, c, n, k, T, 1e-5)
+    np.testing.assert_allclose(ws, w + T * grad, rtol=0, atol=1e-8)
+
+
+def _gdot(w, c, n, k, T, g):
+    return (O.soft_codeword(w, c, n, k, T)[0] * g).sum()
+
+
+@pytest.mark.parametrize("n,k,T", [(6, 2, 0.5), (8, 2, 0.2), (4, 1, 1.0)])
+def test_vjp_matches_finite_differences(n, k, T):
+    """dW and dc against central differences of <g, w_soft>."""
+    B, L, h = 2, 10, 1e-5
+    r = np.random.default_rng(n * 1000 + k)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal((B, L))
+    g = r.standard_normal((B, L))
+    _, _, dW, dc = O.soft_codeword_vjp(w, c, n, k, T, g)
+    fd = np.zeros((B, L))
+    for b in range(B):
+        for t in range(L):
+            wp = w.copy(); wp[b, t] += h
+            wm = w.copy(); wm[b, t] -= h
+            fd[b, t] = (_gdot(wp, c, n, k, T, g) - _gdot(wm, c, n, k, T, g)) / (2 * h)
+    np.testing.assert_allclose(dW, fd, rtol=0, atol=2e-7 * max(1, np.abs(fd).max()))
+    idx = r.choice(1 << n, size=12, replace=False)
+    for s in idx:
+        cp = c.copy(); cp[s] += h
+        cm = c.copy(); cm[s] -= h
+        f = (_gdot(w, cp, n, k, T, g) - _gdot(w, cm, n, k, T, g)) / (2 * h)
+        assert abs(dc[s] - f) <= 2e-7 * max(1, abs(f)), (s, dc[s], f)
+
+
+def test_jacobian_symmetric_and_psd():
+    """J_{t,tau} = Cov(c(s_t), c(s_tau)) / T is symmetric positive semi-definite:
+    g2 . VJP(g1) = g1 . VJP(g2) and g . VJP(g) >= 0."""
+    n, k, L, T = 8, 2, 16, 0.15
+    r = np.random.default_rng(4)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal((3, L))
+    for _ in range(3):
+        g1 = r.standard_normal((3, L))
+        g2 = r.standard_normal((3, L))
+        d1 = O.soft_codeword_vjp(w, c, n, k, T, g1, want_dc=False)[2]
+        d2 = O.soft_codeword_vjp(w, c, n, k, T, g2, want_dc=False)[2]
+        a, b = (g2 * d1).sum(), (g1 * d2).sum()
+        assert abs(a - b) <= 1e-10 * max(1, abs(a))
+        assert (g1 * d1).sum() >= -1e-12
+    # full Jacobian of one block: symmetric, eigenvalues >= 0
+    J = np.stack([O.soft_codeword_vjp(w[:1], c, n, k, T, np.eye(L)[i][None], want_dc=False)[2][0]
+                  for i in range(L)])
+    np.testing.assert_allclose(J, J.T, atol=1e-10 * np.abs(J).max())
+    assert np.linalg.eigvalsh(0.5 * (J + J.T)).min() >= -1e-10 * np.abs(J).max()
+
+
+def test_translation_invariance():
+    """Shifting w and c together by a shifts w_soft by a, so
+    sum(dW) + sum(dc) = sum(g) over the blocks of a call."""
+    n, k, L, T = 8, 2, 20, 0.1
+    r = np.random.default_rng(5)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal((4, L))
+    g = r.standard_normal((4, L))
+    _, _, dW, dc = O.soft_codeword_vjp(w, c, n, k, T, g)
+    assert abs(dW.sum() + dc.sum() - g.sum()) <= 1e-9 * (np.abs(dW).sum() + np.abs(dc).sum())
+    ws0 = O.soft_codeword(w, c, n, k, T)[0]
+    ws1 = O.soft_codeword(w + 0.75, c + 0.75, n, k, T)[0]
+    np.testing.assert_allclose(ws1, ws0 + 0.75, atol=1e-12)
+
+
+def test_scaling():
+    """(lam w, lam c, lam^2 T) gives lam * w_soft and the same log Z."""
+    n, k, L, T, lam = 6, 2, 15, 0.3, 2.5
+    r = np.random.default_rng(6)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal((3, L))
+    ws0, lz0 = O.soft_codeword(w, c, n, k, T)
+    ws1, lz1 = O.soft_codeword(lam * w, lam * c, n, k, lam * lam * T)
+    np.testing.assert_allclose(ws1, lam * ws0, atol=1e-12)
+    np.testing.assert_allclose(lz1, lz0, rtol=1e-12)
+
+
+def test_high_temperature_limit():
+    """T -> inf: every legal path equally likely; w_soft -> mean(c) and
+    log Z + E_avg/T -> log(#paths) = log S + (L-1) k log 2."""
+    n, k, L, T = 8, 2, 10, 1e9
+    r = np.random.default_rng(7)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    ws, lz = O.soft_codeword(w[None], c, n, k, T)
+    np.testing.assert_allclose(ws[0], c.mean(), atol=1e-8)
+    Eavg = 0.5 * ((w[:, None] - c[None, :]) ** 2).mean(1).sum()
+    np.testing.assert_allclose(lz[0] + Eavg / T, n * np.log(2) + (L - 1) * k * np.log(2), atol=1e-8)
+
+
+@pytest.mark.parametrize("n", [2, 3])
+def test_fully_connected_trellis_is_independent_soft_quantizer(n):
+    """n == k: every state reaches every state, so positions decouple:
+    w_soft_t = sum_s c_s softmax_s(-(w_t - c_s)^2 / 2T) and the Jacobian is
+    diagonal with J_tt = Var_t(c) / T."""
+    k, L, T = n, 7, 0.4
+    r = np.random.default_rng(8 + n)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    g = r.standard_normal(L)
+    ws, lz, dW, _ = O.soft_codeword_vjp(w[None], c, n, k, T, g[None])
+    a = -(w[:, None] - c[None, :]) ** 2 / (2 * T)
+    p = np.exp(a - a.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    mean = (p * c).sum(1)
+    var = (p * c * c).sum(1) - mean ** 2
+    np.testing.assert_allclose(ws[0], mean, atol=1e-13)
+    np.testing.assert_allclose(dW[0], g * var / T, atol=1e-12)
+    lz_ref = sum(np.log(np.exp(a[t] - a[t].max()).sum()) + a[t].max() for t in range(L))
+    np.testing.assert_allclose(lz[0], lz_ref, rtol=1e-13)
+
+
+def test_single_step_block():
+    """L = 1: the marginal is a softmax over all S states."""
+    n, k, T = 8, 2, 0.05
+    r = np.random.default_rng(9)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal((5, 1))
+    ws, lz = O.soft_codeword(w, c, n, k, T)
+    a = -(w - c[None, :]) ** 2 / (2 * T)
+    m = a.max(1, keepdims=True)
+    p = np.exp(a - m)
+    np.testing.assert_allclose(ws[:, 0], (p * c).sum(1) / p.sum(1), atol=1e-13)
+    np.testing.assert_allclose(lz, m[:, 0] + np.log(p.sum(1)), rtol=1e-13)
+
+
+@pytest.mark.parametrize("n,k,L", [(8, 2, 30), (6, 1, 25), (10, 2, 12)])
+def test_low_temperature_marginals_concentrate_on_viterbi(n, k, L):
+    """Sec. 3.3 identity 1: as T -> 0+ the Boltzmann distribution concentrates
+    on the minimum-distortion path, so argmax_s p_t(s) is the Viterbi path."""
+    T = 1e-9
+    r = np.random.default_rng(n + 31 * L)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    al, be, _, _ = O.block_tables(w, c, n, k, T)
+    st, _ = O.viterbi(w[None], c, n, k)
+    np.testing.assert_array_equal(np.argmax(al + be, 1), st[0])
+    # at T = 1e-9 the log-domain values are ~1e9, so fp64 rounding alone
+    # leaves ~1e-7 of normalisation error; check the value at T = 1e-6
+    ws = O.soft_codeword(w[None], c, n, k, 1e-6)[0][0]
+    np.testing.assert_allclose(ws, c[st[0]], atol=1e-8)
+
+
+@pytest.mark.parametrize("n,k,L", [(4, 2, 6), (3, 1, 10), (5, 2, 5), (2, 2, 7), (6, 3, 3)])
+def test_viterbi_matches_enumeration(n, k, L):
+    r = np.random.default_rng(n * 7 + L)
+    for _ in range(4):
+        c = r.standard_normal(1 << n)
+        w = r.standard_normal(L)
+        st, cost = O.viterbi(w[None], c, n, k)
+        p, best = bf.viterbi(w, c, n, k)
+        np.testing.assert_array_equal(st[0], p)
+        assert cost[0] == best
+
+
+@pytest.mark.parametrize("n,k,L", [(4, 2, 6), (3, 1, 9), (4, 1, 8)])
+def test_viterbi_tie_break_rule(n, k, L):
+    """Exact ties (dyadic values; every sum is exact): the decode keeps the
+    smallest final state, then the smallest predecessor at each step, i.e.
+    the reverse-lexicographically smallest optimal path."""
+    r = np.random.default_rng(n + k + L)
+    for _ in range(6):
+        c = r.integers(-3, 4, 1 << n) / 4.0      # many equal codewords
+        w = r.integers(-6, 7, L) / 8.0
+        st, cost = O.viterbi(w[None], c, n, k)
+        p, best = bf.viterbi(w, c, n, k)
+        np.testing.assert_array_equal(st[0], p)
+        assert cost[0] == best
+
+
+def test_monotone_in_own_weight():
+    """d w_soft_t / d w_t = Var_p(c(s_t)) / T >= 0 (diagonal of the VJP)."""
+    n, k, L, T = 8, 2, 12, 0.1
+    r = np.random.default_rng(10)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    al, be, _, _ = O.block_tables(w, c, n, k, T)
+    lz = O.soft_codeword(w[None], c, n, k, T)[1][0]
+    p = np.exp(al + be - lz)
+    var = (p * c * c).sum(1) - ((p * c).sum(1)) ** 2
+    for t in range(L):
+        d = O.soft_codeword_vjp(w[None], c, n, k, T, np.eye(L)[t][None], want_dc=False)[2][0, t]
+        assert d >= 0
+        np.testing.assert_allclose(d, var[t] / T, rtol=1e-9, atol=1e-12)
+
+
+def test_tangent_tables_are_conditional_expectations():
+    """A_t(s) + B_t(s) = E[F | s_t = s] with F = sum_t g_t c(s_t), checked
+    against the enumerated conditional expectation."""
+    n, k, L, T = 4, 2, 5, 0.5
+    w, c, g = _case(n, k, L, 12)
+    _, _, A, Bt = O.block_tables(w, c, n, k, T, g)
+    P = bf.paths(n, k, L)
+    cP = c[P]
+    a = -0.5 * ((w[None] - cP) ** 2).sum(1) / T
+    p = np.exp(a - a.max()); p /= p.sum()
+    F = (g[None] * cP).sum(1)
+    for t in range(L):
+        for s in range(1 << n):
+            sel = P[:, t] == s
+            ref = (p[sel] * F[sel]).sum() / p[sel].sum()
+            assert abs(A[t, s] + Bt[t, s] - ref) <= 1e-11 * max(1, abs(ref))
+
+
+def test_oracle_rejects_bad_arguments():
+    c = np.zeros(16)
+    w = np.zeros((1, 4))
+    with pytest.raises(RuntimeError):
+        O.soft_codeword(w, c, 4, 5, 1.0)     # k > n
+    with pytest.raises(RuntimeError):
+        O.soft_codeword(w, c, 4, 2, 0.0)     # T <= 0
+    with pytest.raises(RuntimeError):
+        O.soft_codeword(w, c, 4, 2, float("nan"))
