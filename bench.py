@@ -1,0 +1,162 @@
+#!/usr/bin/env python3
+"""Benchmark: trellis edge-updates/s of the fused BCJR soft codeword + VJP.
+
+Workload: S = 65536 states (16 state bits), k = 2, L = 256, a 2048 x 2048
+unit-variance Gaussian weight matrix (the q/o-projection shape of a
+Llama-3.2-1B layer) = 16384 blocks, random N(0,1) codebook, T = 0.05, one
+call computing w_soft, logZ and dW (bcjr_soft_codeword_fwd_vjp).  Inputs are
+seeded synthetic data resident in HBM before timing starts.
+
+A step is one such call over the whole matrix.  Edges per step are
+B * L * S * 2^k.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# Roofline of the fused kernel ("Roofline").
+CUS, CLOCK_HZ = 256, 2.4e9
+VALU_LANES_PER_CLK = 64          # per CU: 4 SIMDs x 16 fp32 lanes (packed fp32 math disabled)
+TRANS_LANES_PER_CLK = 32         # per CU: v_exp/v_log/v_rcp at half rate (measured)
+# algorithmic work per K x K group-step, K = 4, fwd + w_soft + logZ + dW
+ALG_VALU_PER_GROUP = 97.0
+ALG_TRANS_PER_GROUP = 11.0
+EDGES_PER_GROUP = 16.0           # K^2
+
+
+def roofline_edges_per_s() -> float:
+    t_group = (ALG_VALU_PER_GROUP / VALU_LANES_PER_CLK + ALG_TRANS_PER_GROUP / TRANS_LANES_PER_CLK)
+    return EDGES_PER_GROUP * CUS * CLOCK_HZ / t_group
+
+
+def cpu_baseline(target_s: float = 15.0):
+    """The fp64 oracle on a bounded sample of the same workload (host cores)."""
+    import numpy as np
+    from oracle import oracle as O
+    from paper_2605_10655_amd import workloads as WL
+    wl = WL.workload(4)
+    cores = O.default_threads()
+    c = WL.codebook(4)
+    w = WL.weights(4, rows=8)                       # 64 blocks available
+    g = WL.upstream(4, B=w.shape[0])
+    T = float(np.float32(wl.temps[0]))
+    # calibrate with one block per core, then scale to ~target_s
+    nb = min(cores, w.shape[0])
+    t0 = time.time()
+    O.soft_codeword_vjp(w[:nb], c, wl.state_bits, wl.k, T, g[:nb], want_dc=False, nthreads=cores)
+    t1 = time.time() - t0
+    rounds = max(1, min(int(target_s / max(t1, 1e-3)), w.shape[0] // nb))
+    if rounds > 1:
+        nb2 = nb * rounds
+        t0 = time.time()
+        O.soft_codeword_vjp(w[:nb2], c, wl.state_bits, wl.k, T, g[:nb2], want_dc=False,
+                            nthreads=cores)
+        nb, t1 = nb2, time.time() - t0
+    edges = nb * wl.L * wl.S * (1 << wl.k)
+    return {"value": edges / t1, "unit": "edge-updates/s", "cores": cores, "kind": "oracle",
+            "sample": f"{nb} blocks of the same matrix (first rows), fwd+logZ+dW, fp64, {t1:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(blocks are independent: N GPUs would each run B/N blocks, see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2605_10655_amd as P
+    from paper_2605_10655_amd import workloads as WL
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    P.load_library()
+    wl = WL.workload(4)
+    n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0]
+    dev = torch.device("cuda:0")
+    w = torch.from_numpy(WL.weights(4)).to(dev)
+    c = torch.from_numpy(WL.codebook(4)).to(dev)
+    g = torch.from_numpy(WL.upstream(4)).to(dev)
+    B = w.shape[0]
+    w_soft = torch.empty_like(w)
+    logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    dW = torch.empty_like(w)
+    ws = torch.empty(P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
+                                     want_dCodebook=False, workspace=ws, stream=stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+
+    # events recorded on the stream the kernels are launched on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = wall * 1e3 / args.steps
+    edges = wl.edges
+    value = edges / (ms_per_step / 1e3)
+    kern_avg_s = float(np.mean(kernel_ms)) / 1e3
+    achieved = edges / kern_avg_s
+    peak = roofline_edges_per_s()
+    print(f"timed {args.steps} steps: {ms_per_step:.1f} ms/step (events avg {kern_avg_s * 1e3:.1f} ms)",
+          file=sys.stderr, flush=True)
+
+    rec = {
+        "metric": "trellis edge-updates/s fwd+VJP at S=65536,k=2,L=256; % VALU roofline",
+        "value": value,
+        "unit": "edge-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "2048x2048 N(0,1) weights as 16384 blocks of L=256; S=65536, k=2, "
+                               "T=0.05; fused w_soft+logZ+dW",
+                   "B": B, "L": L, "S": wl.S, "k": k, "T": T},
+        "blocks_per_s": B / (ms_per_step / 1e3),
+        "roofline": {"bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
+                     "unit": "Gedge/s", "frac": achieved / peak, "traffic": None,
+                     "kernel_ms": kern_avg_s * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        print("timing the oracle on the host cores ...", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,114 @@
+/*
+ * bcjr.h -- C ABI of the MI355X (gfx950) BCJR soft-codeword library.
+ *
+ * What is computed (paper Sec. 3, "Method"):
+ *   A weight block w[0..L-1] is encoded by a path s_1..s_L through a bitshift
+ *   trellis with S = 2^state_bits states and K = 2^k branches per step:
+ *       next(s, b) = ((s << k) | b) & (S - 1)            (Sec. 3.1)
+ *   Every state may start a path (no prior weight on s_1).  At temperature T
+ *   the paths follow the Boltzmann distribution
+ *       p_T(path) ~ exp(-(1/T) sum_t (w_t - c(s_t))^2 / 2)   (Eq. boltzmann)
+ *   and the soft codeword is the per-step expectation of the emitted codeword
+ *       w_soft_t = sum_s c(s) p_T(s_t = s | w)              (Eq. soft-codeword)
+ *   computed by the log-domain forward-backward recursions (Sec. 3.4,
+ *   Eqs. alpha, beta, marginal, softcode-final).  logZ is the natural log of
+ *   the partition function Z_T of Eq. boltzmann.
+ *   The VJP (Sec. 3.5) of  <g, w_soft>  is returned for an upstream gradient
+ *   g: dW = d<g, w_soft>/dw per block and dCodebook = d<g, w_soft>/dc summed
+ *   over the call's blocks.  T is a constant of the call (no dT).
+ *   viterbi_decode returns the minimum-distortion path (Sec. 3.2), the
+ *   T -> 0 limit of the soft codeword (Sec. 3.3).
+ *
+ * Conventions for every entry point:
+ *   - w, grad_w_soft, w_soft, dW, w_hard are row-major [B, L] float32; block
+ *     b occupies elements [b*L, (b+1)*L).  codebook and dCodebook are [S].
+ *     logZ is [B].  states is [B, L] int32 holding s_1..s_L of each block.
+ *   - All array pointers are DEVICE pointers owned by the caller, 4-byte
+ *     aligned (16-byte for codebook), contiguous.  Inputs are never written;
+ *     requested outputs are fully overwritten.  Optional outputs may be NULL.
+ *   - workspace is caller-owned device memory.  bcjr_workspace_bytes() gives
+ *     the size for full-speed operation; any smaller size that holds at least
+ *     one block slot is accepted and runs with fewer blocks in flight.  The
+ *     library allocates nothing.  A workspace must not be shared by calls
+ *     that may run concurrently.
+ *   - Calls are asynchronous on `stream`; the returned status covers argument
+ *     validation and launch errors only.  No exception crosses the ABI.
+ *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12)
+ *     (k = 1: 2..14, k = 2: 4..16, k = 3: 6..16).  Other valid (state_bits, k)
+ *     return BCJR_ERR_UNSUPPORTED.
+ *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
+ *   - Non-finite w or codebook values give non-finite outputs; they are not
+ *     checked.
+ */
+#ifndef BCJR_H
+#define BCJR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BCJR_OK = 0,
+  BCJR_ERR_INVALID_ARG = -1,  /* bad size, k, state_bits, T, or NULL pointer */
+  BCJR_ERR_UNSUPPORTED = -2,  /* valid arguments outside the supported shapes */
+  BCJR_ERR_WORKSPACE = -3,    /* workspace NULL or smaller than one block slot */
+  BCJR_ERR_HIP = -4           /* a HIP call or kernel launch failed */
+} bcjr_status;
+
+enum {
+  BCJR_OP_FWD = 0,      /* bcjr_soft_codeword */
+  BCJR_OP_VJP = 1,      /* bcjr_soft_codeword_vjp */
+  BCJR_OP_FWD_VJP = 2,  /* bcjr_soft_codeword_fwd_vjp */
+  BCJR_OP_VITERBI = 3   /* viterbi_decode */
+};
+
+/* Workspace bytes for full-speed operation of `op` on B blocks of length L.
+ * Pure host arithmetic.  Returns 0 for invalid or unsupported arguments. */
+size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op);
+
+/* Soft codeword (Eq. soft-codeword) and natural-log partition function.
+ * Inputs: w[B*L], codebook[S], temperature T > 0 (finite).
+ * Outputs: w_soft[B*L] (required), logZ[B] (may be NULL). */
+int bcjr_soft_codeword(const float *w, int64_t B, int64_t L, const float *codebook,
+                       int state_bits, int k, float T, float *w_soft, float *logZ,
+                       void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* VJP of <grad_w_soft, w_soft> with respect to w and the codebook
+ * (Sec. 3.5; the covariance form d w_soft_t / d w_tau = Cov(c(s_t), c(s_tau)) / T
+ * follows from Eq. boltzmann).  dW[B*L] and dCodebook[S] may each be NULL;
+ * dCodebook is the sum over the B blocks of this call. */
+int bcjr_soft_codeword_vjp(const float *w, int64_t B, int64_t L, const float *codebook,
+                           int state_bits, int k, float T, const float *grad_w_soft,
+                           float *dW, float *dCodebook, void *workspace, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* Forward outputs and the VJP in one pass over the data (the upstream
+ * gradient is known up front).  Any of w_soft, logZ, dW, dCodebook may be
+ * NULL. */
+int bcjr_soft_codeword_fwd_vjp(const float *w, int64_t B, int64_t L, const float *codebook,
+                               int state_bits, int k, float T, const float *grad_w_soft,
+                               float *w_soft, float *logZ, float *dW, float *dCodebook,
+                               void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Minimum-distortion path, sum_t (w_t - c(s_t))^2 evaluated in fp64 with the
+ * product and the sum rounded separately (Sec. 3.2).  Ties go to the
+ * predecessor with the smallest state index, then to the smallest final
+ * state.  states[B*L] (required) holds s_1..s_L; w_hard[B*L] = codebook[states]
+ * (may be NULL). */
+int viterbi_decode(const float *w, int64_t B, int64_t L, const float *codebook,
+                   int state_bits, int k, int32_t *states, float *w_hard, void *workspace,
+                   size_t ws_bytes, hipStream_t stream);
+
+/* Static description of a status code; never NULL. */
+const char *bcjr_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BCJR_H */

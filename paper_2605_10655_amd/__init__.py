@@ -1,0 +1,213 @@
+"""MI355X (gfx950) BCJR soft-codeword library: Python binding.
+
+Thin ctypes marshalling over the C ABI declared in ``include/bcjr.h``
+(``libbcjr.so``, built in-tree by ``build.py``).  Every step of the
+computation runs in the library's HIP kernels; this module only checks
+tensor shapes, allocates outputs and the workspace through PyTorch, and
+passes raw device pointers and the current HIP stream.
+
+Functions keep the C names:
+    bcjr_soft_codeword(w, codebook, state_bits, k, T)            -> (w_soft, logZ)
+    bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, g)     -> (dW, dCodebook)
+    bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, g) -> (w_soft, logZ, dW, dCodebook)
+    viterbi_decode(w, codebook, state_bits, k)                   -> (states, w_hard)
+    bcjr_workspace_bytes(B, L, state_bits, k, op)                -> int
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "BcjrError", "OP_FWD", "OP_VJP", "OP_FWD_VJP", "OP_VITERBI", "library_path", "load_library",
+    "bcjr_workspace_bytes", "bcjr_status_string", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
+    "bcjr_soft_codeword_fwd_vjp", "viterbi_decode",
+]
+
+OP_FWD, OP_VJP, OP_FWD_VJP, OP_VITERBI = 0, 1, 2, 3
+STATUS = {0: "BCJR_OK", -1: "BCJR_ERR_INVALID_ARG", -2: "BCJR_ERR_UNSUPPORTED",
+          -3: "BCJR_ERR_WORKSPACE", -4: "BCJR_ERR_HIP"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_lib = None
+
+
+class BcjrError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} returned {STATUS.get(status, status)}: {bcjr_status_string(status)}")
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libbcjr.so")
+
+
+def load_library():
+    """Load libbcjr.so.  Raises ImportError if it was not built: there is no
+    fallback implementation."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2605_10655_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i64, ci, cf, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    L.bcjr_workspace_bytes.argtypes = [i64, i64, ci, ci, ci]
+    L.bcjr_workspace_bytes.restype = sz
+    L.bcjr_status_string.argtypes = [ci]
+    L.bcjr_status_string.restype = ctypes.c_char_p
+    L.bcjr_soft_codeword.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, sz, vp]
+    L.bcjr_soft_codeword_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, sz, vp]
+    L.bcjr_soft_codeword_fwd_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, vp,
+                                             sz, vp]
+    L.viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, vp, vp, vp, sz, vp]
+    for f in (L.bcjr_soft_codeword, L.bcjr_soft_codeword_vjp, L.bcjr_soft_codeword_fwd_vjp,
+              L.viterbi_decode):
+        f.restype = ci
+    _lib = L
+    return L
+
+
+def bcjr_workspace_bytes(B: int, L: int, state_bits: int, k: int, op: int) -> int:
+    return int(load_library().bcjr_workspace_bytes(B, L, state_bits, k, op))
+
+
+def bcjr_status_string(status: int) -> str:
+    return load_library().bcjr_status_string(status).decode()
+
+
+# ---------------------------------------------------------------- helpers
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check_in(name, t, shape=None, dtype=None):
+    torch = _torch()
+    dtype = dtype or torch.float32
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _workspace(workspace, B, L, state_bits, k, op, device):
+    torch = _torch()
+    if workspace is not None:
+        return workspace
+    nbytes = bcjr_workspace_bytes(B, L, state_bits, k, op)
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _shape(w):
+    if w.dim() != 2:
+        raise ValueError("w must be [B, L]")
+    return int(w.shape[0]), int(w.shape[1])
+
+
+def _raise(fn, rc):
+    if rc != 0:
+        raise BcjrError(fn, rc)
+
+
+# ---------------------------------------------------------------- API
+def bcjr_soft_codeword(w, codebook, state_bits, k, T, *, w_soft=None, logZ=None, want_logZ=True,
+                       workspace=None, stream=None):
+    """Soft codeword w_soft[B, L] and natural-log partition function logZ[B]."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _check_in("codebook", codebook, (1 << state_bits,))
+    if w_soft is None:
+        w_soft = torch.empty_like(w)
+    if logZ is None and want_logZ:
+        logZ = torch.empty(B, dtype=torch.float32, device=w.device)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_FWD, w.device)
+    rc = lib.bcjr_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
+                                _ptr(w_soft), _ptr(logZ), _ptr(ws), ws.numel(), _stream(stream))
+    _raise("bcjr_soft_codeword", rc)
+    return w_soft, logZ
+
+
+def bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, want_dW=True,
+                           want_dCodebook=True, dW=None, dCodebook=None, workspace=None,
+                           stream=None):
+    """VJP of <grad_w_soft, w_soft>: (dW[B, L] or None, dCodebook[S] or None)."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _check_in("codebook", codebook, (1 << state_bits,))
+    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    if dW is None and want_dW:
+        dW = torch.empty_like(w)
+    if dCodebook is None and want_dCodebook:
+        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=w.device)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, w.device)
+    rc = lib.bcjr_soft_codeword_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
+                                    _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws),
+                                    ws.numel(), _stream(stream))
+    _raise("bcjr_soft_codeword_vjp", rc)
+    return dW, dCodebook
+
+
+def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, want_w_soft=True,
+                               want_logZ=True, want_dW=True, want_dCodebook=True, w_soft=None,
+                               logZ=None, dW=None, dCodebook=None, workspace=None, stream=None):
+    """Forward outputs and the VJP in one call: (w_soft, logZ, dW, dCodebook)."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _check_in("codebook", codebook, (1 << state_bits,))
+    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    dev = w.device
+    if w_soft is None and want_w_soft:
+        w_soft = torch.empty_like(w)
+    if logZ is None and want_logZ:
+        logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    if dW is None and want_dW:
+        dW = torch.empty_like(w)
+    if dCodebook is None and want_dCodebook:
+        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=dev)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_FWD_VJP, dev)
+    rc = lib.bcjr_soft_codeword_fwd_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
+                                        _ptr(grad_w_soft), _ptr(w_soft), _ptr(logZ), _ptr(dW),
+                                        _ptr(dCodebook), _ptr(ws), ws.numel(), _stream(stream))
+    _raise("bcjr_soft_codeword_fwd_vjp", rc)
+    return w_soft, logZ, dW, dCodebook
+
+
+def viterbi_decode(w, codebook, state_bits, k, *, want_w_hard=True, states=None, w_hard=None,
+                   workspace=None, stream=None):
+    """Minimum-distortion path: (states[B, L] int32, w_hard[B, L] or None)."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _check_in("codebook", codebook, (1 << state_bits,))
+    if states is None:
+        states = torch.empty((B, L), dtype=torch.int32, device=w.device)
+    if w_hard is None and want_w_hard:
+        w_hard = torch.empty_like(w)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VITERBI, w.device)
+    rc = lib.viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, _ptr(states),
+                            _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
+    _raise("viterbi_decode", rc)
+    return states, w_hard

@@ -1,0 +1,336 @@
+// bcjr_capi.hip -- C ABI entry points (declared in include/bcjr.h): argument
+// validation, kernel-family choice, workspace carving and launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstddef>
+#include <cstdint>
+
+#include "bcjr.h"
+#include "bcjr_internal.h"
+#include "bcjr_kernels.h"
+
+namespace bcjr {
+namespace {
+
+constexpr int kDeviceCUs = 256;     // MI355X; used only to size the workspace query
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Kernel family for a given (n, k): threads per workgroup, the super-group
+// slots per thread compiled in, the runtime super-groups per thread.
+struct Family {
+  int nt = 0;       // threads per workgroup
+  int sgmax = 0;    // compiled super-groups per thread
+  int sgt = 0;      // super-groups per thread at run time
+  int bpw = 0;      // blocks per workgroup
+  int occ_est = 0;  // workgroups per CU assumed by the workspace query
+};
+
+bool supported(int n, int k) {
+  if (k < 1 || k > 3 || n < 2 * k || n > 16) return false;
+  const int nsg_bits = n - 2 * k;
+  if (nsg_bits > 12) return false;           // at most 4096 super-groups
+  if (k == 3 && nsg_bits > 8) return false;  // 64-state super-groups: one per thread
+  return true;
+}
+
+Family family(int n, int k, bool dc) {
+  Family f;
+  const int nsg = 1 << (n - 2 * k);
+  if (nsg <= 256) {
+    f.nt = 256; f.sgmax = 1; f.sgt = 1; f.occ_est = 8;
+  } else if (nsg <= 2048) {
+    f.nt = 256; f.sgt = nsg / 256; f.sgmax = f.sgt; f.occ_est = 4;
+  } else if (!dc) {
+    f.nt = 1024; f.sgt = nsg / 1024; f.sgmax = f.sgt; f.occ_est = 1;
+  } else {
+    // 4 KB super-groups with per-state dCodebook accumulators: 512 threads
+    // (two waves per SIMD) leave room for 8 x K^2 accumulators per thread
+    f.nt = 512; f.sgt = nsg / 512; f.sgmax = f.sgt; f.occ_est = 1;
+  }
+  const int tpb = nsg / f.sgt;
+  f.bpw = f.nt / tpb;
+  return f;
+}
+
+struct FbLayout {
+  size_t histH, histGA, small, dc, slot;
+};
+
+FbLayout fb_layout(int64_t L, int n, int k, bool vjp) {
+  const size_t gs = (size_t)1 << (n - k);
+  FbLayout l;
+  l.histH = align_up((size_t)L * gs * sizeof(float));
+  l.histGA = vjp ? align_up((size_t)L * 2 * gs * sizeof(float)) : 0;
+  l.small = align_up((size_t)4 * L * sizeof(float));
+  l.dc = vjp ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
+  l.slot = l.histH + l.histGA + l.small + l.dc;
+  return l;
+}
+
+size_t vit_slot_bytes(int64_t L, int n, int k) {
+  return align_up((size_t)L * ((size_t)1 << (n - k)));
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+size_t fb_lds_bytes(const Family& f, int n, int k) {
+  const size_t gs = (size_t)1 << (n - k);
+  return (size_t)f.bpw * 2 * gs * sizeof(float) + (size_t)(f.nt / 64) * 4 * sizeof(float);
+}
+
+size_t vit_lds_bytes(const Family& f, int n, int k) {
+  const size_t gs = (size_t)1 << (n - k);
+  return (size_t)f.bpw * gs * sizeof(double) + (size_t)(f.nt / 64) * (sizeof(double) + sizeof(int));
+}
+
+// ----------------------------------------------------------------- dispatch
+using FbFn = void (*)(FbArgs);
+using VitFn = void (*)(VitArgs);
+
+// Families with one super-group per thread take the state bits at run time;
+// the others are compiled per state-bit count so that every LDS and codebook
+// offset folds into an immediate.
+template <int KB, int NB, int SGM, int NT>
+FbFn fb_variant(bool vjp, bool dc) {
+  if (!vjp) return fb_kernel<KB, NB, SGM, NT, false, false>;
+  if (!dc) return fb_kernel<KB, NB, SGM, NT, true, false>;
+  return fb_kernel<KB, NB, SGM, NT, true, true>;
+}
+
+template <int KB>
+FbFn fb_pick_kb(int n, const Family& f, bool vjp, bool dc) {
+  if (f.sgmax == 1) return fb_variant<KB, 0, 1, 256>(vjp, dc);
+  if constexpr (KB < 3) {
+    // nsg = 2^(n - 2KB): 512, 1024, 2048 -> 256 threads; 4096 -> 1024, or
+    // 512 with dCodebook
+    constexpr int n512 = 2 * KB + 9;
+    if (f.nt == 256) {
+      if (n == n512) return fb_variant<KB, n512, 2, 256>(vjp, dc);
+      if (n == n512 + 1) return fb_variant<KB, n512 + 1, 4, 256>(vjp, dc);
+      if (n == n512 + 2) return fb_variant<KB, n512 + 2, 8, 256>(vjp, dc);
+    }
+    if (n == n512 + 3) {
+      if (f.nt == 1024) return fb_variant<KB, n512 + 3, 4, 1024>(vjp, dc);
+      if (f.nt == 512 && dc) return fb_kernel<KB, n512 + 3, 8, 512, true, true>;
+    }
+  }
+  return nullptr;
+}
+
+FbFn fb_pick(int n, int k, const Family& f, bool vjp, bool dc) {
+  switch (k) {
+    case 1: return fb_pick_kb<1>(n, f, vjp, dc);
+    case 2: return fb_pick_kb<2>(n, f, vjp, dc);
+    case 3: return fb_pick_kb<3>(n, f, vjp, dc);
+    default: return nullptr;
+  }
+}
+
+template <int KB>
+VitFn vit_pick_kb(int n, const Family& f) {
+  if (f.sgmax == 1) return viterbi_kernel<KB, 0, 1, 256>;
+  if constexpr (KB < 3) {
+    constexpr int n512 = 2 * KB + 9;
+    if (n == n512) return viterbi_kernel<KB, n512, 2, 256>;
+    if (n == n512 + 1) return viterbi_kernel<KB, n512 + 1, 4, 256>;
+    if (n == n512 + 2) return viterbi_kernel<KB, n512 + 2, 8, 256>;
+    if (n == n512 + 3) return viterbi_kernel<KB, n512 + 3, 4, 1024>;
+  }
+  return nullptr;
+}
+
+VitFn vit_pick(int n, int k, const Family& f) {
+  switch (k) {
+    case 1: return vit_pick_kb<1>(n, f);
+    case 2: return vit_pick_kb<2>(n, f);
+    case 3: return vit_pick_kb<3>(n, f);
+    default: return nullptr;
+  }
+}
+
+int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k) {
+  if (B < 0 || L < 1 || k < 1 || n < k || n > 16) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && (!w || !codebook)) return BCJR_ERR_INVALID_ARG;
+  if (codebook && ((uintptr_t)codebook & 15u)) return BCJR_ERR_INVALID_ARG;
+  if (w && ((uintptr_t)w & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (!supported(n, k)) return BCJR_ERR_UNSUPPORTED;
+  return BCJR_OK;
+}
+
+bool temperature_ok(float T) { return std::isfinite(T) && T > 0.f; }
+
+// Number of workgroups to launch.  0 means the workspace holds less than one
+// workgroup's slots.
+int64_t grid_size(const void* kernel, const Family& f, size_t lds, int64_t B, size_t ws_bytes,
+                  size_t slot_bytes, int* hip_err) {
+  *hip_err = 0;
+  int dev = 0, cus = kDeviceCUs, occ = 1;
+  if (hipGetDevice(&dev) != hipSuccess) { *hip_err = 1; return 0; }
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    *hip_err = 1;
+    return 0;
+  }
+  if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+      hipSuccess) {
+    *hip_err = 1;
+    return 0;
+  }
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, f.nt, lds) != hipSuccess ||
+      occ < 1)
+    occ = 1;
+  const int64_t want = ceil_div(B, f.bpw);
+  const int64_t fit = (int64_t)(ws_bytes / slot_bytes) / f.bpw;
+  int64_t grid = want < (int64_t)cus * occ ? want : (int64_t)cus * occ;
+  if (grid > fit) grid = fit;
+  return grid;
+}
+
+int fill_zero(float* p, int64_t count, hipStream_t stream) {
+  if (!p || count <= 0) return BCJR_OK;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, stream, p,
+                     count, 0.f);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
+           const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
+           void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
+  const bool dc = vjp && dCodebook != nullptr;
+  const Family f = family(n, k, dc);
+  const FbLayout lay = fb_layout(L, n, k, vjp);
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  FbFn fn = fb_pick(n, k, f, vjp, dc);
+  if (!fn) return BCJR_ERR_UNSUPPORTED;
+  const size_t lds = fb_lds_bytes(f, n, k);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, lay.slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const int64_t slots = grid * f.bpw;
+  char* base = static_cast<char*>(workspace);
+  FbArgs a;
+  a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
+  const double Td = (double)T;
+  a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
+  a.invT = (float)(1.0 / Td);
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  a.histH = reinterpret_cast<float*>(base);
+  a.histGA = vjp ? reinterpret_cast<float*>(base + slots * lay.histH) : nullptr;
+  a.small = reinterpret_cast<float*>(base + slots * (lay.histH + lay.histGA));
+  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.histH + lay.histGA + lay.small))
+                 : nullptr;
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dc) {
+    const int64_t S = (int64_t)1 << n;
+    const int64_t used = slots < B ? slots : B;
+    hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
+                       a.dc_part, used, S, dCodebook);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
+}  // namespace
+}  // namespace bcjr
+
+using namespace bcjr;
+
+extern "C" {
+
+size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op) {
+  if (B < 0 || L < 1 || k < 1 || state_bits < k || state_bits > 16) return 0;
+  if (!supported(state_bits, k)) return 0;
+  if (B == 0) return 0;
+  if (op == BCJR_OP_VITERBI) {
+    const Family f = family(state_bits, k, false);
+    const int64_t grid = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
+    return (size_t)(grid * f.bpw) * vit_slot_bytes(L, state_bits, k);
+  }
+  if (op != BCJR_OP_FWD && op != BCJR_OP_VJP && op != BCJR_OP_FWD_VJP) return 0;
+  const bool vjp = op != BCJR_OP_FWD;
+  // a VJP workspace is sized for the dCodebook family (never smaller)
+  const Family f = family(state_bits, k, vjp);
+  const Family f2 = family(state_bits, k, false);
+  const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
+  const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
+  const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
+  return (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
+}
+
+int bcjr_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,
+                       int k, float T, float* w_soft, float* logZ, void* workspace,
+                       size_t ws_bytes, hipStream_t stream) {
+  int st = common_checks(w, B, L, codebook, state_bits, k);
+  if (st != BCJR_OK) return st;
+  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && !w_soft) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return BCJR_OK;
+  return run_fb(w, B, L, codebook, state_bits, k, T, nullptr, w_soft, logZ, nullptr, nullptr,
+                workspace, ws_bytes, stream, false);
+}
+
+int bcjr_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
+                               int state_bits, int k, float T, const float* grad_w_soft,
+                               float* w_soft, float* logZ, float* dW, float* dCodebook,
+                               void* workspace, size_t ws_bytes, hipStream_t stream) {
+  int st = common_checks(w, B, L, codebook, state_bits, k);
+  if (st != BCJR_OK) return st;
+  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
+  if (grad_w_soft && ((uintptr_t)grad_w_soft & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return fill_zero(dCodebook, (int64_t)1 << state_bits, stream);
+  if (!w_soft && !logZ && !dW && !dCodebook) return BCJR_OK;
+  return run_fb(w, B, L, codebook, state_bits, k, T, grad_w_soft, w_soft, logZ, dW, dCodebook,
+                workspace, ws_bytes, stream, true);
+}
+
+int bcjr_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
+                           int state_bits, int k, float T, const float* grad_w_soft, float* dW,
+                           float* dCodebook, void* workspace, size_t ws_bytes,
+                           hipStream_t stream) {
+  return bcjr_soft_codeword_fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, nullptr,
+                                    nullptr, dW, dCodebook, workspace, ws_bytes, stream);
+}
+
+int viterbi_decode(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,
+                   int k, int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
+                   hipStream_t stream) {
+  int st = common_checks(w, B, L, codebook, state_bits, k);
+  if (st != BCJR_OK) return st;
+  if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return BCJR_OK;
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  const Family f = family(state_bits, k, false);
+  VitFn fn = vit_pick(state_bits, k, f);
+  if (!fn) return BCJR_ERR_UNSUPPORTED;
+  const size_t lds = vit_lds_bytes(f, state_bits, k);
+  const size_t slot = vit_slot_bytes(L, state_bits, k);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  VitArgs a;
+  a.w = w; a.c = codebook; a.B = B; a.L = L; a.n = state_bits; a.sgt = f.sgt;
+  a.states = states; a.w_hard = w_hard;
+  a.bp = static_cast<uint8_t*>(workspace);
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+const char* bcjr_status_string(int status) {
+  switch (status) {
+    case BCJR_OK: return "ok";
+    case BCJR_ERR_INVALID_ARG: return "invalid argument";
+    case BCJR_ERR_UNSUPPORTED: return "unsupported (state_bits, k)";
+    case BCJR_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case BCJR_ERR_HIP: return "HIP runtime or launch error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

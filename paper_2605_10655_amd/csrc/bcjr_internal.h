@@ -1,0 +1,37 @@
+// bcjr_internal.h -- kernel argument blocks shared by the host dispatcher and
+// the kernels.  Not part of the public ABI.
+#pragma once
+#include <stdint.h>
+
+namespace bcjr {
+
+struct FbArgs {
+  const float* w;      // [B, L]
+  const float* g;      // [B, L] upstream gradient (VJP only)
+  const float* c;      // [S] codebook
+  int64_t B, L;
+  int n;               // state bits
+  int sgt;             // super-groups per thread
+  float k2;            // log2(e) / (2T): h_t(s) in log2 units = -(w_t - c(s))^2 * k2
+  float invT;          // 1 / T
+  float* w_soft;       // [B, L] or null
+  float* logZ;         // [B] or null
+  float* dW;           // [B, L] or null
+  double* dc_part;     // [slots][S] fp64 partial sums of dCodebook, or null
+  float* histH;        // [slots][L][S/K]   H_t as read by each super-group
+  float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group
+  float* small;        // [slots][4][L]     shifts of H, lambda_t, w_soft_t
+};
+
+struct VitArgs {
+  const float* w;
+  const float* c;
+  int64_t B, L;
+  int n;
+  int sgt;
+  int32_t* states;     // [B, L]
+  float* w_hard;       // [B, L] or null
+  uint8_t* bp;         // [slots][L][S/K] winning predecessor digit
+};
+
+}  // namespace bcjr

@@ -1,0 +1,692 @@
+// bcjr_kernels.h -- gfx950 kernels for the temperature-T BCJR soft codeword
+// over a bitshift trellis, its VJP, and the min-sum (Viterbi) decode.
+//
+// Index algebra (paper Sec. 3.1, next(s, b) = ((s << k) | b) & (S - 1)):
+//   n = state bits, K = 2^k, S = 2^n.  Write a state as three digit fields
+//       s = (j, sg, u)   j: top k bits, sg: middle n - 2k bits, u: low k bits.
+//   The predecessors of s are (i, j, sg_hi...) -- all states whose low n - k
+//   bits equal s >> k -- and the successors of s are (s & (S/K - 1)) * K + b.
+//   Hence the log forward variable factors as
+//       log alpha_t(s) = h_t(s) + G_t(s >> k)            (Eq. alpha, its recursion)
+//       G_{t+1}(v)     = LSE_{j<K} log alpha_t(j * S/K + v),   v < S/K
+//   and the log backward variable depends only on the low n - k bits:
+//       log beta_t(s)  = H_t(s & (S/K - 1))              (Eq. beta, its recursion)
+//       H_{t-1}(v)     = LSE_{b<K} [h_t(v*K + b) + H_t((v*K + b) & (S/K - 1))].
+//   h_t(s) = -(w_t - c(s))^2 / (2T) is the local field of Eq. boltzmann.
+//   The K^2 states (j, sg, u) for a fixed sg form one "super-group": they
+//   read G_t(j, sg) (j < K) and produce G_{t+1}(sg, u) (u < K), and read
+//   H_t(sg, u) and produce H_{t-1}(j, sg).  One thread owns a fixed set of
+//   super-groups for the whole call, so every per-state quantity it
+//   accumulates stays in its registers.
+//
+// All logs here are base 2 (v_exp_f32 / v_log_f32); natural-log results
+// are converted at the end.  After every step the new G or H vector is
+// shifted by floor(max) so that its largest entry is in [0, 1); the shifts
+// are integers, so their sums are exact.
+//
+// Marginals (Eq. marginal) are formed inside the sweeps:
+//   p_t(s) = 2^(log2 alpha + log2 beta - lambda_t),  lambda_t = log2 of the
+//   normaliser in the shifted frame, carried from step to step and re-anchored
+//   with the exact sum of the step.
+//
+// VJP (the paper's Sec. 3.5 gives no formula; it follows from Eq. boltzmann).
+//   With F = sum_t g_t c(s_t):  dW_tau = Cov(F, c(s_tau)) / T and
+//   dc_sig = sum_t p_t(sig)[g_t + (w_t - c_sig)(E[F|s_t=sig] - E[F]) / T].
+//   E[F | s_t = s] = A_t(s) + B_t(s) with forward / backward tangent
+//   recursions that reuse the alpha / beta softmax weights.  Both tangents are
+//   centred on the soft codeword: they accumulate g_t (c(s_t) - w_soft_t), so
+//   E_p[A_t + B_t] = 0 and the tangents stay small exactly where p is large
+//   (fp32 keeps relative precision at low T).  That needs w_soft before the
+//   forward tangent runs, so the VJP is three sweeps per block:
+//     S0 backward: H only (stored per step);
+//     S1 forward:  G, marginals -> w_soft_t, lambda_t; A centred at write time;
+//     S2 backward: H read back from S0, B tangent, combine -> dW_t, dc.
+//   The soft codeword alone is S0 + S1.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bcjr_internal.h"
+
+namespace bcjr {
+
+namespace {
+
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Materialises a value in a register at this point.  Results that are held
+// across a barrier are pinned so the compiler cannot sink the arithmetic that
+// produces them below the barrier (which would keep its inputs live instead).
+__device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
+
+// Keeps the scheduler from hoisting the next super-group's loads above the
+// current one: that hoisting multiplies the live registers by SGMAX.
+__device__ __forceinline__ void sg_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int N>
+__device__ __forceinline__ void ld_vec(const float* p, float (&v)[N]) {
+  static_assert(N == 1 || N == 2 || N % 4 == 0, "vector width");
+  if constexpr (N == 1) {
+    v[0] = p[0];
+  } else if constexpr (N == 2) {
+    const float2 t = *reinterpret_cast<const float2*>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+#pragma unroll
+    for (int q = 0; q < N / 4; ++q) {
+      const float4 t = reinterpret_cast<const float4*>(p)[q];
+      v[4 * q + 0] = t.x; v[4 * q + 1] = t.y; v[4 * q + 2] = t.z; v[4 * q + 3] = t.w;
+    }
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void st_vec(float* p, const float (&v)[N]) {
+  if constexpr (N == 1) {
+    p[0] = v[0];
+  } else if constexpr (N == 2) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < N / 4; ++q)
+      reinterpret_cast<float4*>(p)[q] =
+          make_float4(v[4 * q + 0], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Reductions over the TPB threads that own one block.  TPB is a power of two.
+// Below 64 the threads are an aligned lane segment of one wave; above, whole
+// waves, combined through a small LDS area after the caller's barrier.
+// xor butterflies give every lane bitwise-identical results.
+// ---------------------------------------------------------------------------
+struct RedCtx {
+  int width;     // lanes combined inside a wave: min(TPB, 64)
+  int rw;        // waves per block (1 when TPB <= 64)
+  int lane, wave;
+  float* red;    // [waves][4] floats
+};
+
+template <int NQ, unsigned MAXMASK>
+__device__ __forceinline__ void red_pre(float (&v)[NQ], const RedCtx& r) {
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+    for (int off = 1; off < r.width; off <<= 1) {
+      const float o = __shfl_xor(v[q], off);
+      v[q] = ((MAXMASK >> q) & 1u) ? fmaxf(v[q], o) : v[q] + o;
+    }
+  if (r.rw > 1 && r.lane == 0) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) r.red[r.wave * 4 + q] = v[q];
+  }
+}
+
+// call after a barrier that follows red_pre
+template <int NQ, unsigned MAXMASK>
+__device__ __forceinline__ void red_post(float (&v)[NQ], const RedCtx& r) {
+  if (r.rw > 1) {
+    const int first = (r.wave / r.rw) * r.rw;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      float acc = r.red[first * 4 + q];
+      for (int i = 1; i < r.rw; ++i) {
+        const float o = r.red[(first + i) * 4 + q];
+        acc = ((MAXMASK >> q) & 1u) ? fmaxf(acc, o) : acc + o;
+      }
+      v[q] = acc;
+    }
+  }
+}
+
+// (max, scaled sum) pairs: combine((m1,s1),(m2,s2)) = (M, s1 2^(m1-M) + s2 2^(m2-M))
+__device__ __forceinline__ void lse_pair(float& m, float& s, float mo, float so) {
+  const float M = fmaxf(m, mo);
+  s = s * ex2(m - M) + so * ex2(mo - M);
+  m = M;
+}
+
+__device__ __forceinline__ void lse_pre(float& m, float& s, const RedCtx& r) {
+  for (int off = 1; off < r.width; off <<= 1) {
+    const float mo = __shfl_xor(m, off);
+    const float so = __shfl_xor(s, off);
+    lse_pair(m, s, mo, so);
+  }
+  if (r.rw > 1 && r.lane == 0) {
+    r.red[r.wave * 4 + 0] = m;
+    r.red[r.wave * 4 + 1] = s;
+  }
+}
+
+__device__ __forceinline__ void lse_post(float& m, float& s, const RedCtx& r) {
+  if (r.rw > 1) {
+    const int first = (r.wave / r.rw) * r.rw;
+    m = r.red[first * 4 + 0];
+    s = r.red[first * 4 + 1];
+    for (int i = 1; i < r.rw; ++i) lse_pair(m, s, r.red[(first + i) * 4 + 0], r.red[(first + i) * 4 + 1]);
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Forward-backward kernel.  One workgroup runs BPW blocks side by side (BPW =
+// NT / TPB), each block's group vectors living in LDS (two vectors of S/K
+// floats).  The grid is persistent: workgroup x handles blocks
+// x*BPW + bw, x*BPW + bw + grid*BPW, ...  Per-step histories go to the
+// workgroup's workspace slot.
+// ---------------------------------------------------------------------------
+// NB > 0 fixes the state bits at compile time (then SGT = SGMAX); NB == 0
+// reads them from the arguments.
+template <int KB, int NB, int SGMAX, int NT, bool VJP, bool DC>
+__global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
+  constexpr int K = 1 << KB;
+  extern __shared__ float lds[];
+  const int n = NB ? NB : a.n;
+  const int GS = 1 << (n - KB);          // size of a group vector (S / K)
+  const int NSG = 1 << (n - 2 * KB);     // super-groups per block
+  const int SGT = NB ? SGMAX : a.sgt;    // super-groups per thread (<= SGMAX)
+  const int TPB = NSG / SGT;             // threads per block
+  const int BPW = NT / TPB;              // blocks per workgroup
+  const int tid = threadIdx.x;
+  const int bw = tid / TPB;
+  const int tb = tid - bw * TPB;
+  const int64_t L = a.L;
+  const float k2 = a.k2;
+  // Addresses are written as (block-uniform base) + (32-bit thread offset) so
+  // that the loads use a scalar base and a single offset register.
+  const uint32_t toK = (uint32_t)tb << KB;  // thread's first super-group * K
+
+  RedCtx rc;
+  rc.width = TPB < 64 ? TPB : 64;
+  rc.rw = TPB > 64 ? TPB / 64 : 1;
+  rc.lane = tid & 63;
+  rc.wave = tid >> 6;
+  rc.red = lds + (size_t)BPW * 2 * GS;
+
+  float* v0 = lds + (size_t)bw * 2 * GS;  // G (forward) or H (backward)
+  float* v1 = v0 + GS;                    // A or B tangent
+
+  float dcacc[DC ? SGMAX * K * K : 1];
+
+  for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    const int64_t blk = base + bw;
+    const bool valid = blk < a.B;
+    const int64_t bb = valid ? blk : a.B - 1;
+    const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const float* wb = a.w + bb * L;
+    const float* gb = VJP ? a.g + bb * L : nullptr;
+    float* hH = a.histH + slot * L * GS;
+    float* hGA = VJP ? a.histGA + slot * L * 2 * GS : nullptr;
+    float* sm_mB = a.small + slot * 4 * L;  // shift applied to H_t
+    float* sm_lam = sm_mB + L;              // lambda_t
+    float* sm_ws = sm_lam + L;              // w_soft_t
+
+    // ------------------------------------------------------------------ S0
+    // Backward sweep for H alone.  v0 / v1 alternate as the H_t being read and
+    // the H_{t-1} being written, so one barrier per step suffices; the shift
+    // of H_{t-1} (floor of its max, known after the barrier) is subtracted
+    // when it is read back.
+    for (int i = tb; i < GS; i += TPB) v0[i] = 0.f;
+    __syncthreads();
+    double shiftB = 0.0;  // sum of the integer shifts of H (exact)
+    float lam0 = 0.f;
+    float offc = 0.f;     // shift of the H vector being read
+    for (int64_t t = L - 1;; --t) {
+      const float wt = wb[t];
+      float* cur = ((L - 1 - t) & 1) ? v1 : v0;
+      float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
+      if (t == 0) {
+        // lambda_0 = LSE_s [h_0(s) + H_0(s & (S/K-1))]  (log2 alpha_0 = h_0)
+        float lm = -INFINITY, ls = 0.f;
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+            float Hin[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) Hin[b] = cur[sg * K + b] - offc;
+            st_vec<K>(hH + ((i * TPB) << KB) + toK, Hin);
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              float cc[K];
+              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+              float x[K];
+              float m = -INFINITY;
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                const float d = wt - cc[b];
+                x[b] = Hin[b] - d * d * k2;
+                m = fmaxf(m, x[b]);
+              }
+              float s = 0.f;
+#pragma unroll
+              for (int b = 0; b < K; ++b) s += ex2(x[b] - m);
+              lse_pair(lm, ls, m, s);
+            }
+            sg_fence();
+          }
+        }
+        lse_pre(lm, ls, rc);
+        if (tb == 0) sm_mB[L - 1] = 0.f;
+        __syncthreads();
+        lse_post(lm, ls, rc);
+        lam0 = lm + lg2(ls);
+        if (tb == 0 && valid && a.logZ)
+          a.logZ[bb] = (float)((shiftB + (double)lam0) * 0.69314718055994530942);
+        __syncthreads();
+        break;
+      }
+      float vmax[1] = {-INFINITY};
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          float Hin[K];
+#pragma unroll
+          for (int b = 0; b < K; ++b) Hin[b] = cur[sg * K + b] - offc;
+          st_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            float cc[K];
+            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+            float x[K];
+            float m = -INFINITY;
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const float d = wt - cc[b];
+              x[b] = Hin[b] - d * d * k2;
+              m = fmaxf(m, x[b]);
+            }
+            float s = 0.f;
+#pragma unroll
+            for (int b = 0; b < K; ++b) s += ex2(x[b] - m);
+            const float h = m + lg2(s);
+            nxt[j * NSG + sg] = h;
+            vmax[0] = fmaxf(vmax[0], h);
+          }
+          sg_fence();
+        }
+      }
+      red_pre<1, 1u>(vmax, rc);
+      __syncthreads();
+      red_post<1, 1u>(vmax, rc);
+      offc = floorf(vmax[0]);
+      shiftB += (double)offc;
+      if (tb == 0) sm_mB[t - 1] = offc;
+    }
+
+    // ------------------------------------------------------------------ S1
+    for (int i = tb; i < GS; i += TPB) {
+      v0[i] = 0.f;
+      if (VJP) v1[i] = 0.f;
+    }
+    __syncthreads();
+    float lam_est = lam0;
+    for (int64_t t = 0; t < L; ++t) {
+      const float wt = wb[t];
+      const float gt = VJP ? gb[t] : 0.f;
+      const float mBt = sm_mB[t];
+      float Gout[SGMAX][K];
+      float Aout[VJP ? SGMAX : 1][K];
+      float rv[3] = {-INFINITY, 0.f, 0.f};  // max G_{t+1}, sum p, sum p*c
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          float Gin[K], Ain[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            Gin[j] = v0[j * NSG + sg];
+            Ain[j] = VJP ? v1[j * NSG + sg] : 0.f;
+          }
+          if (VJP) {
+            st_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Gin);
+            st_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Ain);
+          }
+          float Hc[K];
+          ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
+          float cc[K][K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            float al[K];
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              const float d = wt - cc[j][u];
+              al[j] = Gin[j] - d * d * k2;
+              m = fmaxf(m, al[j]);
+            }
+            float E[K];
+            float s = 0.f, sc = 0.f;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              E[j] = ex2(al[j] - m);
+              s += E[j];
+              sc += E[j] * cc[j][u];
+            }
+            Gout[i][u] = m + lg2(s);
+            pin(Gout[i][u]);
+            rv[0] = fmaxf(rv[0], Gout[i][u]);
+            const float fac = ex2(m + Hc[u] - lam_est);
+            rv[1] += fac * s;
+            rv[2] += fac * sc;
+            if constexpr (VJP) {
+              float num = 0.f;
+#pragma unroll
+              for (int j = 0; j < K; ++j) num += E[j] * (gt * cc[j][u] + Ain[j]);
+              Aout[i][u] = num * rcp(s);
+              pin(Aout[i][u]);
+            }
+          }
+          sg_fence();
+        }
+      }
+      red_pre<3, 1u>(rv, rc);
+      __syncthreads();
+      red_post<3, 1u>(rv, rc);
+      const float off = floorf(rv[0]);
+      const float wst = rv[2] / rv[1];
+      const float lamt = lam_est + lg2(rv[1]);
+      if (t < L - 1) {
+        const float gws = gt * wst;
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+            float go[K];
+#pragma unroll
+            for (int u = 0; u < K; ++u) go[u] = Gout[i][u] - off;
+            st_vec<K>(v0 + sg * K, go);
+            if constexpr (VJP) {
+              float ao[K];
+#pragma unroll
+              for (int u = 0; u < K; ++u) ao[u] = Aout[i][u] - gws;
+              st_vec<K>(v1 + sg * K, ao);
+            }
+          }
+        }
+      }
+      if (tb == 0) {
+        sm_lam[t] = lamt;
+        sm_ws[t] = wst;
+        if (valid && a.w_soft) a.w_soft[bb * L + t] = wst;
+      }
+      lam_est = lamt - off + mBt;
+      __syncthreads();
+    }
+
+    // ------------------------------------------------------------------ S2
+    // Backward sweep for the B tangent and the combine.  H_t is read back from
+    // S0's history (the exact values S1 used), so only B lives in LDS, again
+    // alternating between v0 and v1 with one barrier per step.
+    if constexpr (VJP) {
+      if constexpr (DC) {
+#pragma unroll
+        for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
+      }
+      for (int i = tb; i < GS; i += TPB) v0[i] = 0.f;
+      __syncthreads();
+      const float invT = a.invT;
+      float xbar = 0.f;  // E_p[X] of the previous step (lagged mean removal)
+      for (int64_t t = L - 1; t >= 0; --t) {
+        const float wt = wb[t];
+        const float gt = gb[t];
+        const float wst = sm_ws[t];
+        const float lamt = sm_lam[t];
+        const float gws = gt * wst;
+        float* cur = ((L - 1 - t) & 1) ? v1 : v0;
+        float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
+        float rv[3] = {0.f, 0.f, 0.f};  // sum p (c - ws) X, sum p X, sum p
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+            float Hin[K], Bin[K], Gt[K], At[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) Bin[b] = cur[sg * K + b];
+            ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+            ld_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Gt);
+            ld_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, At);
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              float cc[K];
+              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+              float x[K], y[K];
+              float m = -INFINITY;
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                const float d = wt - cc[b];
+                x[b] = Hin[b] - d * d * k2;
+                y[b] = gt * cc[b] - gws + Bin[b];
+                m = fmaxf(m, x[b]);
+              }
+              float E[K];
+              float s = 0.f, sy = 0.f;
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                E[b] = ex2(x[b] - m);
+                s += E[b];
+                sy += E[b] * y[b];
+              }
+              nxt[j * NSG + sg] = sy * rcp(s);  // B_{t-1}; unused after t = 0
+              const float fac = ex2(Gt[j] + m - lamt);
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                const float p = E[b] * fac;
+                const float X = y[b] + At[j];
+                const float pX = p * X;
+                rv[0] += pX * (cc[b] - wst);
+                rv[1] += pX;
+                rv[2] += p;
+                if constexpr (DC)
+                  dcacc[(i * K + j) * K + b] += p * (gt + (wt - cc[b]) * (X - xbar) * invT);
+              }
+            }
+            sg_fence();
+          }
+        }
+        red_pre<3, 0u>(rv, rc);
+        __syncthreads();
+        red_post<3, 0u>(rv, rc);
+        const float rinv = 1.f / rv[2];
+        xbar = rv[1] * rinv;
+        if (tb == 0 && valid && a.dW) a.dW[bb * L + t] = rv[0] * rinv * invT;
+      }
+      if constexpr (DC) {
+        if (valid) {
+          const bool first = base == (int64_t)blockIdx.x * BPW;
+          double* part = a.dc_part + slot * ((int64_t)1 << n);
+#pragma unroll
+          for (int i = 0; i < SGMAX; ++i) {
+            if (i < SGT) {
+              const int sg = tb + i * TPB;
+#pragma unroll
+              for (int j = 0; j < K; ++j) {
+                double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
+                if (first) {
+#pragma unroll
+                  for (int b = 0; b < K; ++b) pj[b] = (double)dcacc[(i * K + j) * K + b];
+                } else {
+#pragma unroll
+                  for (int b = 0; b < K; ++b) pj[b] += (double)dcacc[(i * K + j) * K + b];
+                }
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// dCodebook[s] = sum over used slots of the fp64 partials, in slot order.
+__global__ void dc_reduce_kernel(const double* part, int64_t nslots, int64_t S, float* out) {
+  const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  double acc = 0.0;
+  for (int64_t q = 0; q < nslots; ++q) acc += part[q * S + s];
+  out[s] = (float)acc;
+}
+
+__global__ void fill_kernel(float* out, int64_t count, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) out[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Min-sum decode (paper Sec. 3.2), fp64 path metrics.  Same super-group
+// layout as the forward sweep: Mn_{t+1}(v) = min_j [d_t(j*S/K + v) + Mn_t(j, v >> k)]
+// with d_t(s) = (w_t - c(s))^2; the winning j is kept per (t, v).
+// ---------------------------------------------------------------------------
+template <int KB, int NB, int SGMAX, int NT>
+__global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
+  constexpr int K = 1 << KB;
+  extern __shared__ double ldsd[];
+  const int n = NB ? NB : a.n;
+  const int GS = 1 << (n - KB);
+  const int NSG = 1 << (n - 2 * KB);
+  const int SGT = NB ? SGMAX : a.sgt;
+  const int TPB = NSG / SGT;
+  const int BPW = NT / TPB;
+  const int tid = threadIdx.x;
+  const int bw = tid / TPB;
+  const int tb = tid - bw * TPB;
+  const uint32_t toK = (uint32_t)tb << KB;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int width = TPB < 64 ? TPB : 64;
+  const int rw = TPB > 64 ? TPB / 64 : 1;
+  const int64_t L = a.L;
+  double* mv = ldsd + (size_t)bw * GS;
+  double* redv = ldsd + (size_t)BPW * GS;            // [waves]
+  int* redi = reinterpret_cast<int*>(redv + NT / 64); // [waves]
+
+  for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    const int64_t blk = base + bw;
+    const bool valid = blk < a.B;
+    const int64_t bb = valid ? blk : a.B - 1;
+    const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const float* wb = a.w + bb * L;
+    uint8_t* bp = a.bp + slot * L * GS;
+
+    for (int i = tb; i < GS; i += TPB) mv[i] = 0.0;
+    __syncthreads();
+    double bestv = INFINITY;
+    int besti = 0x7fffffff;
+    for (int64_t t = 0; t < L; ++t) {
+      const double wt = (double)wb[t];
+      double Mout[SGMAX][K];
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          double Min[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) Min[j] = mv[j * NSG + sg];
+          float cc[K][K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
+          if (t < L - 1) {
+            uint8_t arg[K];
+#pragma unroll
+            for (int u = 0; u < K; ++u) {
+              double best = 0.0;
+              int bj = 0;
+#pragma unroll
+              for (int j = 0; j < K; ++j) {
+                const double d = wt - (double)cc[j][u];
+                const double v = __dadd_rn(__dmul_rn(d, d), Min[j]);
+                if (j == 0 || v < best) {
+                  best = v;
+                  bj = j;
+                }
+              }
+              Mout[i][u] = best;
+              arg[u] = (uint8_t)bj;
+            }
+            // bp[t+1][sg*K + u] = winning j of G-entry (sg, u)
+#pragma unroll
+            for (int u = 0; u < K; ++u) bp[(t + 1) * GS + sg * K + u] = arg[u];
+          } else {
+#pragma unroll
+            for (int j = 0; j < K; ++j)
+#pragma unroll
+              for (int u = 0; u < K; ++u) {
+                const double d = wt - (double)cc[j][u];
+                const double v = __dadd_rn(__dmul_rn(d, d), Min[j]);
+                const int s = (j << (n - KB)) | (sg << KB) | u;
+                if (v < bestv || (v == bestv && s < besti)) {
+                  bestv = v;
+                  besti = s;
+                }
+              }
+          }
+          sg_fence();
+        }
+      }
+      if (t < L - 1) {
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+#pragma unroll
+            for (int u = 0; u < K; ++u) mv[sg * K + u] = Mout[i][u];
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // block argmin (value, then state index)
+    for (int off = 1; off < width; off <<= 1) {
+      const double ov = __shfl_xor(bestv, off);
+      const int oi = __shfl_xor(besti, off);
+      if (ov < bestv || (ov == bestv && oi < besti)) {
+        bestv = ov;
+        besti = oi;
+      }
+    }
+    if (rw > 1 && lane == 0) {
+      redv[wave] = bestv;
+      redi[wave] = besti;
+    }
+    __syncthreads();  // also publishes every thread's bp stores to the block
+    if (rw > 1) {
+      const int first = (wave / rw) * rw;
+      bestv = redv[first];
+      besti = redi[first];
+      for (int q = 1; q < rw; ++q) {
+        const double ov = redv[first + q];
+        const int oi = redi[first + q];
+        if (ov < bestv || (ov == bestv && oi < besti)) {
+          bestv = ov;
+          besti = oi;
+        }
+      }
+    }
+    if (tb == 0 && valid) {
+      int32_t* st = a.states + bb * L;
+      float* wh = a.w_hard ? a.w_hard + bb * L : nullptr;
+      int s = besti;
+      st[L - 1] = s;
+      if (wh) wh[L - 1] = a.c[s];
+      for (int64_t t = L - 1; t >= 1; --t) {
+        const int v = s >> KB;
+        const int j = bp[t * GS + v];
+        s = (j << (n - KB)) | v;
+        st[t - 1] = s;
+        if (wh) wh[t - 1] = a.c[s];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace bcjr

@@ -1,0 +1,123 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every function declared in include/bcjr.h,
+size workspaces by pure host arithmetic, and reject bad arguments before
+touching the device.  No call here reaches a kernel launch.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2605_10655_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bcjr.h")
+
+FAKE = 1 << 20          # 16-byte aligned non-null address, never dereferenced
+MISALIGNED = FAKE + 4
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"if", "sizeof"})
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(P.library_path()):
+        pytest.skip("libbcjr.so not built")
+    return P.load_library()
+
+
+def test_library_exports_every_declared_function(lib):
+    names = header_functions()
+    assert set(names) >= {"bcjr_workspace_bytes", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
+                          "bcjr_soft_codeword_fwd_vjp", "viterbi_decode", "bcjr_status_string"}
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4):
+        assert P.bcjr_status_string(code)
+    assert P.bcjr_status_string(12345) == "unknown status"
+
+
+def test_workspace_bytes_host_arithmetic(lib):
+    ws = P.bcjr_workspace_bytes
+    # invalid / unsupported / empty
+    assert ws(10, 0, 4, 2, P.OP_FWD) == 0
+    assert ws(10, 16, 4, 5, P.OP_FWD) == 0
+    assert ws(10, 16, 17, 2, P.OP_FWD) == 0
+    assert ws(10, 16, 3, 2, P.OP_FWD) == 0          # n < 2k: unsupported
+    assert ws(0, 16, 4, 2, P.OP_FWD) == 0
+    assert ws(10, 16, 4, 2, 9) == 0
+    # supported shapes give positive sizes that grow with L and with the VJP
+    for n, k in [(4, 2), (8, 2), (12, 2), (16, 2), (2, 1), (14, 1), (6, 3), (14, 3)]:
+        f = ws(100, 32, n, k, P.OP_FWD)
+        v = ws(100, 32, n, k, P.OP_FWD_VJP)
+        assert 0 < f < v
+        assert ws(100, 64, n, k, P.OP_FWD) > f
+        assert ws(100, 32, n, k, P.OP_VITERBI) > 0
+    assert ws(100, 32, 15, 3, P.OP_FWD) == 0           # k = 3 stops at 14 state bits
+    # the S = 65536 histories: per block L * S/K * (4 + 8) bytes plus small arrays
+    B, L = 16384, 256
+    per_slot = L * (1 << 14) * 12
+    assert ws(B, L, 16, 2, P.OP_FWD_VJP) >= 256 * per_slot
+
+
+def _soft(lib, w=FAKE, B=4, L=8, c=FAKE, n=4, k=2, T=1.0, out=FAKE, lz=None, ws=None, wsb=0):
+    return lib.bcjr_soft_codeword(w, B, L, c, n, k, T, out, lz, ws, wsb, None)
+
+
+def test_soft_codeword_argument_validation(lib):
+    E = -1
+    assert _soft(lib, B=-1) == E
+    assert _soft(lib, L=0) == E
+    assert _soft(lib, k=0) == E
+    assert _soft(lib, n=1, k=2) == E
+    assert _soft(lib, n=17) == E
+    assert _soft(lib, T=0.0) == E
+    assert _soft(lib, T=-1.0) == E
+    assert _soft(lib, T=float("nan")) == E
+    assert _soft(lib, T=float("inf")) == E
+    assert _soft(lib, w=None) == E
+    assert _soft(lib, c=None) == E
+    assert _soft(lib, out=None) == E
+    assert _soft(lib, c=MISALIGNED) == E
+    assert _soft(lib, w=FAKE + 2) == E
+    assert _soft(lib, n=3, k=2) == -2                 # valid but unsupported
+    assert _soft(lib, n=16, k=1) == -2
+    assert _soft(lib, n=16, k=4) == -2
+    assert _soft(lib, ws=None) == -3                  # no workspace
+    assert _soft(lib, ws=FAKE + 8, wsb=1 << 20) == -3  # misaligned workspace
+    assert _soft(lib, B=0) == 0                       # empty batch is a no-op
+
+
+def test_vjp_and_viterbi_argument_validation(lib):
+    f = lib.bcjr_soft_codeword_fwd_vjp
+    assert f(FAKE, 4, 8, FAKE, 4, 2, 1.0, None, FAKE, None, None, None, None, 0, None) == -1
+    assert f(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE + 1, FAKE, None, None, None, None, 0, None) == -1
+    assert f(FAKE, 4, 8, FAKE, 4, 2, 0.0, FAKE, FAKE, None, None, None, None, 0, None) == -1
+    assert f(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, FAKE, None, FAKE, None, None, 0, None) == -3
+    assert f(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, None, None, None, None, None, 0, None) == 0
+    assert f(FAKE, 0, 8, FAKE, 4, 2, 1.0, FAKE, None, None, None, None, None, 0, None) == 0
+    v = lib.bcjr_soft_codeword_vjp
+    assert v(FAKE, 4, 8, FAKE, 4, 2, 1.0, None, FAKE, None, None, 0, None) == -1
+    assert v(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, None, None, None, 0, None) == 0
+    vd = lib.viterbi_decode
+    assert vd(FAKE, 4, 8, FAKE, 4, 2, None, None, FAKE, 1 << 20, None) == -1
+    assert vd(FAKE, 4, 8, FAKE, 4, 2, FAKE, None, None, 0, None) == -3
+    assert vd(FAKE, 4, 8, FAKE, 3, 2, FAKE, None, FAKE, 1 << 20, None) == -2
+    assert vd(FAKE, 0, 8, FAKE, 4, 2, FAKE, None, None, 0, None) == 0
+
+
+def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    """No silent fallback: a missing library is an ImportError."""
+    monkeypatch.setattr(P, "_lib", None)
+    monkeypatch.setattr(P, "library_path", lambda: str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        P.load_library()
