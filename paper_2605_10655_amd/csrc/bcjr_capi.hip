@@ -56,9 +56,53 @@ Family family(int n, int k, bool dc) {
   return f;
 }
 
+// The VJP switches to fp64 log vectors when the field scale log2(e)/(2T)
+// exceeds this value (T < 0.024 for unit-variance data): below it the states
+// that carry the posterior sit hundreds of log2 units from the per-step
+// maximum and fp32 storage no longer keeps the VJP within 1e-4.
+constexpr double kHighPrecisionK2 = 30.0;
+
+bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
+
+Family family_hp(int n, int k) {
+  Family f;
+  const int nsg = 1 << (n - 2 * k);
+  if (nsg <= 256) {
+    f.nt = 256; f.sgmax = 1; f.sgt = 1; f.occ_est = 8;
+  } else if (nsg <= 2048) {
+    f.nt = 256; f.sgt = nsg / 256; f.sgmax = f.sgt; f.occ_est = 4;
+  } else {
+    f.nt = 512; f.sgt = nsg / 512; f.sgmax = f.sgt; f.occ_est = 1;
+  }
+  f.bpw = f.nt / (nsg / f.sgt);
+  return f;
+}
+
 struct FbLayout {
   size_t histH, histGA, small, dc, slot;
 };
+
+struct HpLayout {
+  size_t histH, histG, histA, xA, small, dc, slot;
+};
+
+HpLayout hp_layout(int64_t L, int n, int k) {
+  const size_t gs = (size_t)1 << (n - k);
+  HpLayout l;
+  l.histH = align_up((size_t)L * gs * sizeof(double));
+  l.histG = align_up((size_t)L * gs * sizeof(double));
+  l.histA = align_up((size_t)L * gs * sizeof(float));
+  l.xA = align_up(2 * gs * sizeof(float));
+  l.small = align_up((size_t)3 * L * sizeof(double));
+  l.dc = align_up(((size_t)1 << n) * sizeof(double));
+  l.slot = l.histH + l.histG + l.histA + l.xA + l.small + l.dc;
+  return l;
+}
+
+size_t hp_lds_bytes(const Family& f, int n, int k) {
+  const size_t gs = (size_t)1 << (n - k);
+  return (size_t)f.bpw * gs * sizeof(double) + (size_t)(f.nt / 64) * 4 * (sizeof(double) + sizeof(float));
+}
 
 FbLayout fb_layout(int64_t L, int n, int k, bool vjp) {
   const size_t gs = (size_t)1 << (n - k);
@@ -119,6 +163,31 @@ FbFn fb_pick_kb(int n, const Family& f, bool vjp, bool dc) {
     }
   }
   return nullptr;
+}
+
+template <int KB>
+FbFn hp_pick_kb(int n, const Family& f, bool dc) {
+  if (f.sgmax == 1) return dc ? fb_kernel_hp<KB, 0, 1, 256, true> : fb_kernel_hp<KB, 0, 1, 256, false>;
+  if constexpr (KB < 3) {
+    constexpr int n512 = 2 * KB + 9;
+    if (n == n512) return dc ? fb_kernel_hp<KB, n512, 2, 256, true> : fb_kernel_hp<KB, n512, 2, 256, false>;
+    if (n == n512 + 1)
+      return dc ? fb_kernel_hp<KB, n512 + 1, 4, 256, true> : fb_kernel_hp<KB, n512 + 1, 4, 256, false>;
+    if (n == n512 + 2)
+      return dc ? fb_kernel_hp<KB, n512 + 2, 8, 256, true> : fb_kernel_hp<KB, n512 + 2, 8, 256, false>;
+    if (n == n512 + 3)
+      return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 8, 512, false>;
+  }
+  return nullptr;
+}
+
+FbFn hp_pick(int n, int k, const Family& f, bool dc) {
+  switch (k) {
+    case 1: return hp_pick_kb<1>(n, f, dc);
+    case 2: return hp_pick_kb<2>(n, f, dc);
+    case 3: return hp_pick_kb<3>(n, f, dc);
+    default: return nullptr;
+  }
 }
 
 FbFn fb_pick(int n, int k, const Family& f, bool vjp, bool dc) {
@@ -196,13 +265,56 @@ int fill_zero(float* p, int64_t count, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
+              const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
+              void* workspace, size_t ws_bytes, hipStream_t stream) {
+  const bool dc = dCodebook != nullptr;
+  const Family f = family_hp(n, k);
+  const HpLayout lay = hp_layout(L, n, k);
+  FbFn fn = hp_pick(n, k, f, dc);
+  if (!fn) return BCJR_ERR_UNSUPPORTED;
+  const size_t lds = hp_lds_bytes(f, n, k);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, lay.slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const int64_t slots = grid * f.bpw;
+  char* p = static_cast<char*>(workspace);
+  FbArgs a = {};
+  a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
+  const double Td = (double)T;
+  a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
+  a.k2d = 1.4426950408889634074 / (2.0 * Td);
+  a.invT = (float)(1.0 / Td);
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  a.histHd = reinterpret_cast<double*>(p);            p += slots * lay.histH;
+  a.histGd = reinterpret_cast<double*>(p);            p += slots * lay.histG;
+  a.histA = reinterpret_cast<float*>(p);              p += slots * lay.histA;
+  a.xA = reinterpret_cast<float*>(p);                 p += slots * lay.xA;
+  a.smalld = reinterpret_cast<double*>(p);            p += slots * lay.small;
+  a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dc) {
+    const int64_t S = (int64_t)1 << n;
+    const int64_t used = slots < B ? slots : B;
+    hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
+                       a.dc_part, used, S, dCodebook);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
 int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
            const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
            void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  if (vjp && use_high_precision(T))
+    return run_fb_hp(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace,
+                     ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
   const Family f = family(n, k, dc);
   const FbLayout lay = fb_layout(L, n, k, vjp);
-  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
   const size_t lds = fb_lds_bytes(f, n, k);
@@ -212,7 +324,7 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (grid < 1) return BCJR_ERR_WORKSPACE;
   const int64_t slots = grid * f.bpw;
   char* base = static_cast<char*>(workspace);
-  FbArgs a;
+  FbArgs a = {};
   a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   const double Td = (double)T;
   a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
@@ -259,7 +371,13 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
   const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
-  return (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
+  size_t bytes = (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
+  if (vjp) {  // the temperature decides the variant at call time: cover both
+    const Family fh = family_hp(state_bits, k);
+    const int64_t gh = std::min<int64_t>(ceil_div(B, fh.bpw), (int64_t)kDeviceCUs * fh.occ_est);
+    bytes = std::max(bytes, (size_t)(gh * fh.bpw) * hp_layout(L, state_bits, k).slot);
+  }
+  return bytes;
 }
 
 int bcjr_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,

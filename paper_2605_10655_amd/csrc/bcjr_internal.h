@@ -21,6 +21,13 @@ struct FbArgs {
   float* histH;        // [slots][L][S/K]   H_t as read by each super-group
   float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group
   float* small;        // [slots][4][L]     shifts of H, lambda_t, w_soft_t
+  // high-precision variant (fp64 log vectors)
+  double k2d;          // log2(e) / (2T) in fp64
+  double* histHd;      // [slots][L][S/K] fp64
+  double* histGd;      // [slots][L][S/K] fp64
+  float* histA;        // [slots][L][S/K]
+  float* xA;           // [slots][2][S/K] exchange buffer of the A tangent
+  double* smalld;      // [slots][3][L]   shifts of H, lambda_t (fp64), w_soft_t (fp32)
 };
 
 struct VitArgs {

@@ -61,6 +61,34 @@ __device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x);
 // produces them below the barrier (which would keep its inputs live instead).
 __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
+template <int K, class T>
+__device__ __forceinline__ T max_of(const T (&x)[K]) {
+  T m = x[0];
+#pragma unroll
+  for (int b = 1; b < K; ++b) m = fmax(m, x[b]);
+  return m;
+}
+
+// s = sum E, sy = sum E y, scw = sum E cw, scwy = sum E cw y
+template <int K>
+__device__ __forceinline__ void group_sums(const float (&E)[K], const float (&y)[K],
+                                           const float (&cw)[K], float& s, float& sy, float& scw,
+                                           float& scwy) {
+  s = E[0];
+  sy = E[0] * y[0];
+  float e = E[0] * cw[0];
+  scw = e;
+  scwy = e * y[0];
+#pragma unroll
+  for (int b = 1; b < K; ++b) {
+    s += E[b];
+    sy = fmaf(E[b], y[b], sy);
+    e = E[b] * cw[b];
+    scw += e;
+    scwy = fmaf(e, y[b], scwy);
+  }
+}
+
 // Keeps the scheduler from hoisting the next super-group's loads above the
 // current one: that hoisting multiplies the live registers by SGMAX.
 __device__ __forceinline__ void sg_fence() {
@@ -193,8 +221,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const int TPB = NSG / SGT;             // threads per block
   const int BPW = NT / TPB;              // blocks per workgroup
   const int tid = threadIdx.x;
-  const int bw = tid / TPB;
-  const int tb = tid - bw * TPB;
+  const int bw = BPW == 1 ? 0 : tid / TPB;
+  const int tb = BPW == 1 ? tid : tid - bw * TPB;
   const int64_t L = a.L;
   const float k2 = a.k2;
   // Addresses are written as (block-uniform base) + (32-bit thread offset) so
@@ -256,16 +284,15 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               float cc[K];
               ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
               float x[K];
-              float m = -INFINITY;
 #pragma unroll
               for (int b = 0; b < K; ++b) {
                 const float d = wt - cc[b];
                 x[b] = Hin[b] - d * d * k2;
-                m = fmaxf(m, x[b]);
               }
-              float s = 0.f;
+              const float m = max_of<K>(x);
+              float s = ex2(x[0] - m);
 #pragma unroll
-              for (int b = 0; b < K; ++b) s += ex2(x[b] - m);
+              for (int b = 1; b < K; ++b) s += ex2(x[b] - m);
               lse_pair(lm, ls, m, s);
             }
             sg_fence();
@@ -295,16 +322,15 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             float cc[K];
             ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
             float x[K];
-            float m = -INFINITY;
 #pragma unroll
             for (int b = 0; b < K; ++b) {
               const float d = wt - cc[b];
               x[b] = Hin[b] - d * d * k2;
-              m = fmaxf(m, x[b]);
             }
-            float s = 0.f;
+            const float m = max_of<K>(x);
+            float s = ex2(x[0] - m);
 #pragma unroll
-            for (int b = 0; b < K; ++b) s += ex2(x[b] - m);
+            for (int b = 1; b < K; ++b) s += ex2(x[b] - m);
             const float h = m + lg2(s);
             nxt[j * NSG + sg] = h;
             vmax[0] = fmaxf(vmax[0], h);
@@ -356,20 +382,20 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             float al[K];
-            float m = -INFINITY;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               const float d = wt - cc[j][u];
               al[j] = Gin[j] - d * d * k2;
-              m = fmaxf(m, al[j]);
             }
+            const float m = max_of<K>(al);
             float E[K];
-            float s = 0.f, sc = 0.f;
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-              E[j] = ex2(al[j] - m);
+            for (int j = 0; j < K; ++j) E[j] = ex2(al[j] - m);
+            float s = E[0], sc = E[0] * cc[0][u];
+#pragma unroll
+            for (int j = 1; j < K; ++j) {
               s += E[j];
-              sc += E[j] * cc[j][u];
+              sc = fmaf(E[j], cc[j][u], sc);
             }
             Gout[i][u] = m + lg2(s);
             pin(Gout[i][u]);
@@ -378,10 +404,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             rv[1] += fac * s;
             rv[2] += fac * sc;
             if constexpr (VJP) {
-              float num = 0.f;
+              // E-weighted mean of g_t c + A_t over the K predecessors
+              float num = E[0] * Ain[0];
 #pragma unroll
-              for (int j = 0; j < K; ++j) num += E[j] * (gt * cc[j][u] + Ain[j]);
-              Aout[i][u] = num * rcp(s);
+              for (int j = 1; j < K; ++j) num = fmaf(E[j], Ain[j], num);
+              Aout[i][u] = fmaf(gt, sc, num) * rcp(s);
               pin(Aout[i][u]);
             }
           }
@@ -440,7 +467,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         const float gt = gb[t];
         const float wst = sm_ws[t];
         const float lamt = sm_lam[t];
-        const float gws = gt * wst;
         float* cur = ((L - 1 - t) & 1) ? v1 : v0;
         float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
         float rv[3] = {0.f, 0.f, 0.f};  // sum p (c - ws) X, sum p X, sum p
@@ -458,35 +484,37 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             for (int j = 0; j < K; ++j) {
               float cc[K];
               ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-              float x[K], y[K];
-              float m = -INFINITY;
+              // per state: x = h + log beta (beta-side LSE term), cw = c - w_soft,
+              // y = g (c - w_soft) + B_t (the B-tangent summand); X = y + A_t.
+              float x[K], y[K], cw[K];
 #pragma unroll
               for (int b = 0; b < K; ++b) {
                 const float d = wt - cc[b];
                 x[b] = Hin[b] - d * d * k2;
-                y[b] = gt * cc[b] - gws + Bin[b];
-                m = fmaxf(m, x[b]);
+                cw[b] = cc[b] - wst;
+                y[b] = fmaf(gt, cw[b], Bin[b]);
               }
+              const float m = max_of<K>(x);
+              // marginals of the K states: p_b = E_b * fac; group sums give
+              //   sum p = fac s, sum p X = fac (sy + A s),
+              //   sum p (c - w_soft) X = fac (scwy + A scw)
               float E[K];
-              float s = 0.f, sy = 0.f;
 #pragma unroll
-              for (int b = 0; b < K; ++b) {
-                E[b] = ex2(x[b] - m);
-                s += E[b];
-                sy += E[b] * y[b];
-              }
+              for (int b = 0; b < K; ++b) E[b] = ex2(x[b] - m);
+              float s, sy, scw, scwy;
+              group_sums<K>(E, y, cw, s, sy, scw, scwy);
               nxt[j * NSG + sg] = sy * rcp(s);  // B_{t-1}; unused after t = 0
               const float fac = ex2(Gt[j] + m - lamt);
+              rv[0] = fmaf(fac, fmaf(At[j], scw, scwy), rv[0]);
+              rv[1] = fmaf(fac, fmaf(At[j], s, sy), rv[1]);
+              rv[2] = fmaf(fac, s, rv[2]);
+              if constexpr (DC) {
 #pragma unroll
-              for (int b = 0; b < K; ++b) {
-                const float p = E[b] * fac;
-                const float X = y[b] + At[j];
-                const float pX = p * X;
-                rv[0] += pX * (cc[b] - wst);
-                rv[1] += pX;
-                rv[2] += p;
-                if constexpr (DC)
-                  dcacc[(i * K + j) * K + b] += p * (gt + (wt - cc[b]) * (X - xbar) * invT);
+                for (int b = 0; b < K; ++b) {
+                  const float p = E[b] * fac;
+                  const float X = y[b] + At[j];
+                  dcacc[(i * K + j) * K + b] += p * fmaf((wt - cc[b]) * (X - xbar), invT, gt);
+                }
               }
             }
             sg_fence();
@@ -524,6 +552,429 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       }
       __syncthreads();
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// High-precision VJP kernel for low temperatures.  At small T the log-domain
+// values of the states that carry the posterior lie hundreds of log2 units
+// from the per-step maximum (|h_t| ~ (w - c)^2 / 2T), so fp32 storage of G
+// and H rounds them at ~1e-5 and the VJP loses its 1e-4 relative accuracy.
+// Here the field, the K-way maxima, the LSE results and their storage (LDS
+// and histories) are fp64; only the normalised exponentials, their sums and
+// the tangents stay fp32 (they are well conditioned).  Structure:
+//   S0: H (fp64) in LDS, in place (reads, barrier, writes, barrier);
+//   S1: G (fp64) in LDS in place; the A tangent travels through a per-slot
+//       global double buffer (L2 resident), written uncentred and centred on
+//       the soft codeword when read back;
+//   S2: as in fb_kernel (B in LDS, ping-pong), with H, G read in fp64.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void lse_pair_d(double& m, float& s, double mo, float so) {
+  const double M = fmax(m, mo);
+  s = s * ex2((float)(m - M)) + so * ex2((float)(mo - M));
+  m = M;
+}
+
+template <int NQ, unsigned MAXMASK>
+__device__ __forceinline__ void red_pre_d(double (&v)[NQ], const RedCtx& r, double* redd) {
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+    for (int off = 1; off < r.width; off <<= 1) {
+      const double o = __shfl_xor(v[q], off);
+      v[q] = ((MAXMASK >> q) & 1u) ? fmax(v[q], o) : v[q] + o;
+    }
+  if (r.rw > 1 && r.lane == 0) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) redd[r.wave * 4 + q] = v[q];
+  }
+}
+
+template <int NQ, unsigned MAXMASK>
+__device__ __forceinline__ void red_post_d(double (&v)[NQ], const RedCtx& r, const double* redd) {
+  if (r.rw > 1) {
+    const int first = (r.wave / r.rw) * r.rw;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      double acc = redd[first * 4 + q];
+      for (int i = 1; i < r.rw; ++i) {
+        const double o = redd[(first + i) * 4 + q];
+        acc = ((MAXMASK >> q) & 1u) ? fmax(acc, o) : acc + o;
+      }
+      v[q] = acc;
+    }
+  }
+}
+
+template <int K>
+__device__ __forceinline__ void ld_vec_d(const double* p, double (&v)[K]) {
+  if constexpr (K == 1) {
+    v[0] = p[0];
+  } else {
+#pragma unroll
+    for (int q = 0; q < K / 2; ++q) {
+      const double2 t = reinterpret_cast<const double2*>(p)[q];
+      v[2 * q] = t.x;
+      v[2 * q + 1] = t.y;
+    }
+  }
+}
+
+template <int K>
+__device__ __forceinline__ void st_vec_d(double* p, const double (&v)[K]) {
+  if constexpr (K == 1) {
+    p[0] = v[0];
+  } else {
+#pragma unroll
+    for (int q = 0; q < K / 2; ++q)
+      reinterpret_cast<double2*>(p)[q] = make_double2(v[2 * q], v[2 * q + 1]);
+  }
+}
+
+template <int KB, int NB, int SGMAX, int NT, bool DC>
+__global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
+  constexpr int K = 1 << KB;
+  extern __shared__ double ldsh[];
+  const int n = NB ? NB : a.n;
+  const int GS = 1 << (n - KB);
+  const int NSG = 1 << (n - 2 * KB);
+  const int SGT = NB ? SGMAX : a.sgt;
+  const int TPB = NSG / SGT;
+  const int BPW = NT / TPB;
+  const int tid = threadIdx.x;
+  const int bw = BPW == 1 ? 0 : tid / TPB;
+  const int tb = BPW == 1 ? tid : tid - bw * TPB;
+  const uint32_t toK = (uint32_t)tb << KB;
+  const int64_t L = a.L;
+  const double k2 = (double)a.k2d;
+
+  RedCtx rc;
+  rc.width = TPB < 64 ? TPB : 64;
+  rc.rw = TPB > 64 ? TPB / 64 : 1;
+  rc.lane = tid & 63;
+  rc.wave = tid >> 6;
+  double* vd = ldsh + (size_t)bw * GS;                              // G or H (fp64)
+  double* redd = ldsh + (size_t)BPW * GS;                           // [waves][4] fp64
+  rc.red = reinterpret_cast<float*>(redd + (NT / 64) * 4);          // [waves][4] fp32
+  float* vf0 = reinterpret_cast<float*>(vd);                        // S2: B ping-pong
+  float* vf1 = vf0 + GS;
+
+  float dcacc[DC ? SGMAX * K * K : 1];
+
+  for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    const int64_t blk = base + bw;
+    const bool valid = blk < a.B;
+    const int64_t bb = valid ? blk : a.B - 1;
+    const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const float* wb = a.w + bb * L;
+    const float* gb = a.g + bb * L;
+    double* hH = a.histHd + slot * L * GS;
+    double* hG = a.histGd + slot * L * GS;
+    float* hA = a.histA + slot * L * GS;
+    float* gA = a.xA + slot * 2 * GS;
+    double* sm_mB = a.smalld + slot * 3 * L;
+    double* sm_lam = sm_mB + L;
+    float* sm_ws = reinterpret_cast<float*>(sm_lam + L);
+
+    // ------------------------------------------------------------------ S0
+    for (int i = tb; i < GS; i += TPB) vd[i] = 0.0;
+    __syncthreads();
+    double shiftB = 0.0;
+    double lam0 = 0.0;
+    for (int64_t t = L - 1;; --t) {
+      const double wt = (double)wb[t];
+      double Hin[SGMAX][K];
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+#pragma unroll
+          for (int b = 0; b < K; ++b) Hin[i][b] = vd[sg * K + b];
+          st_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin[i]);
+        }
+      }
+      if (t == 0) {
+        double lm = -INFINITY;
+        float ls = 0.f;
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              float cc[K];
+              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+              double x[K];
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                const double d = wt - (double)cc[b];
+                x[b] = Hin[i][b] - d * d * k2;
+              }
+              const double m = max_of<K>(x);
+              float s = ex2((float)(x[0] - m));
+#pragma unroll
+              for (int b = 1; b < K; ++b) s += ex2((float)(x[b] - m));
+              lse_pair_d(lm, ls, m, s);
+            }
+            sg_fence();
+          }
+        }
+        for (int off = 1; off < rc.width; off <<= 1) {
+          const double mo = __shfl_xor(lm, off);
+          const float so = __shfl_xor(ls, off);
+          lse_pair_d(lm, ls, mo, so);
+        }
+        if (rc.rw > 1 && rc.lane == 0) {
+          redd[rc.wave * 4 + 0] = lm;
+          rc.red[rc.wave * 4 + 0] = ls;
+        }
+        if (tb == 0) sm_mB[L - 1] = 0.0;
+        __syncthreads();
+        if (rc.rw > 1) {
+          const int first = (rc.wave / rc.rw) * rc.rw;
+          lm = redd[first * 4];
+          ls = rc.red[first * 4];
+          for (int q = 1; q < rc.rw; ++q) lse_pair_d(lm, ls, redd[(first + q) * 4], rc.red[(first + q) * 4]);
+        }
+        lam0 = lm + (double)lg2(ls);
+        if (tb == 0 && valid && a.logZ)
+          a.logZ[bb] = (float)((shiftB + lam0) * 0.69314718055994530942);
+        __syncthreads();
+        break;
+      }
+      double Hout[SGMAX][K];
+      double vmax[1] = {-INFINITY};
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            float cc[K];
+            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+            double x[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const double d = wt - (double)cc[b];
+              x[b] = Hin[i][b] - d * d * k2;
+            }
+            const double m = max_of<K>(x);
+            float s = ex2((float)(x[0] - m));
+#pragma unroll
+            for (int b = 1; b < K; ++b) s += ex2((float)(x[b] - m));
+            Hout[i][j] = m + (double)lg2(s);
+            vmax[0] = fmax(vmax[0], Hout[i][j]);
+          }
+          sg_fence();
+        }
+      }
+      red_pre_d<1, 1u>(vmax, rc, redd);
+      __syncthreads();
+      red_post_d<1, 1u>(vmax, rc, redd);
+      const double off = floor(vmax[0]);
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+#pragma unroll
+          for (int j = 0; j < K; ++j) vd[j * NSG + sg] = Hout[i][j] - off;
+        }
+      }
+      shiftB += off;
+      if (tb == 0) sm_mB[t - 1] = off;
+      __syncthreads();
+    }
+
+    // ------------------------------------------------------------------ S1
+    for (int i = tb; i < GS; i += TPB) {
+      vd[i] = 0.0;
+      gA[i] = 0.f;
+    }
+    __syncthreads();
+    double lam_est = lam0;
+    float gws_prev = 0.f;  // centring of the A values read this step
+    for (int64_t t = 0; t < L; ++t) {
+      const double wt = (double)wb[t];
+      const float wtf = wb[t];
+      const float gt = gb[t];
+      const double mBt = sm_mB[t];
+      const float* Acur = gA + (t & 1) * GS;
+      float* Anext = gA + ((t + 1) & 1) * GS;
+      double Gout[SGMAX][K];
+      double vmax[1] = {-INFINITY};
+      float rv[2] = {0.f, 0.f};  // sum p, sum p c
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          double Gin[K];
+          float Ain[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            Gin[j] = vd[j * NSG + sg];
+            Ain[j] = Acur[j * NSG + sg] - gws_prev;
+          }
+          st_vec_d<K>(hG + t * GS + ((i * TPB) << KB) + toK, Gin);
+          st_vec<K>(hA + t * GS + ((i * TPB) << KB) + toK, Ain);
+          double Hc[K];
+          ld_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
+          float cc[K][K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
+          float ao[K];
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            double al[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              const double d = wt - (double)cc[j][u];
+              al[j] = Gin[j] - d * d * k2;
+            }
+            const double m = max_of<K>(al);
+            float E[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
+            float s = E[0], sc = E[0] * cc[0][u], num = E[0] * Ain[0];
+#pragma unroll
+            for (int j = 1; j < K; ++j) {
+              s += E[j];
+              sc = fmaf(E[j], cc[j][u], sc);
+              num = fmaf(E[j], Ain[j], num);
+            }
+            Gout[i][u] = m + (double)lg2(s);
+            vmax[0] = fmax(vmax[0], Gout[i][u]);
+            const float fac = ex2((float)(m + Hc[u] - lam_est));
+            rv[0] = fmaf(fac, s, rv[0]);
+            rv[1] = fmaf(fac, sc, rv[1]);
+            ao[u] = fmaf(gt, sc, num) * rcp(s);  // uncentred A_{t+1}
+          }
+          st_vec<K>(Anext + ((i * TPB) << KB) + toK, ao);
+          (void)wtf;
+          sg_fence();
+        }
+      }
+      red_pre_d<1, 1u>(vmax, rc, redd);
+      red_pre<2, 0u>(rv, rc);
+      __syncthreads();
+      red_post_d<1, 1u>(vmax, rc, redd);
+      red_post<2, 0u>(rv, rc);
+      const double off = floor(vmax[0]);
+      const float wst = rv[1] / rv[0];
+      const double lamt = lam_est + (double)lg2(rv[0]);
+      if (t < L - 1) {
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+            double go[K];
+#pragma unroll
+            for (int u = 0; u < K; ++u) go[u] = Gout[i][u] - off;
+            st_vec_d<K>(vd + sg * K, go);
+          }
+        }
+      }
+      if (tb == 0) {
+        sm_lam[t] = lamt;
+        sm_ws[t] = wst;
+        if (valid && a.w_soft) a.w_soft[bb * L + t] = wst;
+      }
+      gws_prev = gt * wst;
+      lam_est = lamt - off + mBt;
+      __syncthreads();
+    }
+
+    // ------------------------------------------------------------------ S2
+    if constexpr (DC) {
+#pragma unroll
+      for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
+    }
+    for (int i = tb; i < GS; i += TPB) vf0[i] = 0.f;
+    __syncthreads();
+    const float invT = a.invT;
+    float xbar = 0.f;
+    for (int64_t t = L - 1; t >= 0; --t) {
+      const float wtf = wb[t];
+      const double wt = (double)wtf;
+      const float gt = gb[t];
+      const float wst = sm_ws[t];
+      const double lamt = sm_lam[t];
+      float* cur = ((L - 1 - t) & 1) ? vf1 : vf0;
+      float* nxt = ((L - 1 - t) & 1) ? vf0 : vf1;
+      float rv[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          float Bin[K], At[K];
+          double Hin[K], Gt[K];
+#pragma unroll
+          for (int b = 0; b < K; ++b) Bin[b] = cur[sg * K + b];
+          ld_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+          ld_vec_d<K>(hG + t * GS + ((i * TPB) << KB) + toK, Gt);
+          ld_vec<K>(hA + t * GS + ((i * TPB) << KB) + toK, At);
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            float cc[K];
+            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+            double x[K];
+            float y[K], cw[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const double d = wt - (double)cc[b];
+              x[b] = Hin[b] - d * d * k2;
+              cw[b] = cc[b] - wst;
+              y[b] = fmaf(gt, cw[b], Bin[b]);
+            }
+            const double m = max_of<K>(x);
+            float E[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) E[b] = ex2((float)(x[b] - m));
+            float s, sy, scw, scwy;
+            group_sums<K>(E, y, cw, s, sy, scw, scwy);
+            nxt[j * NSG + sg] = sy * rcp(s);
+            const float fac = ex2((float)(Gt[j] + m - lamt));
+            rv[0] = fmaf(fac, fmaf(At[j], scw, scwy), rv[0]);
+            rv[1] = fmaf(fac, fmaf(At[j], s, sy), rv[1]);
+            rv[2] = fmaf(fac, s, rv[2]);
+            if constexpr (DC) {
+#pragma unroll
+              for (int b = 0; b < K; ++b) {
+                const float p = E[b] * fac;
+                const float X = y[b] + At[j];
+                dcacc[(i * K + j) * K + b] += p * fmaf((wtf - cc[b]) * (X - xbar), invT, gt);
+              }
+            }
+          }
+          sg_fence();
+        }
+      }
+      red_pre<3, 0u>(rv, rc);
+      __syncthreads();
+      red_post<3, 0u>(rv, rc);
+      const float rinv = 1.f / rv[2];
+      xbar = rv[1] * rinv;
+      if (tb == 0 && valid && a.dW) a.dW[bb * L + t] = rv[0] * rinv * invT;
+    }
+    if constexpr (DC) {
+      if (valid) {
+        const bool first = base == (int64_t)blockIdx.x * BPW;
+        double* part = a.dc_part + slot * ((int64_t)1 << n);
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
+              if (first) {
+#pragma unroll
+                for (int b = 0; b < K; ++b) pj[b] = (double)dcacc[(i * K + j) * K + b];
+              } else {
+#pragma unroll
+                for (int b = 0; b < K; ++b) pj[b] += (double)dcacc[(i * K + j) * K + b];
+              }
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 

@@ -182,7 +182,7 @@ def test_config4_full_batch_sampled():
 
 
 # ---------------------------------------------------------------- config 5
-@pytest.mark.parametrize("call", [0, 7])
+@pytest.mark.parametrize("call", [0, 2, 3, 5, 7])
 def test_config5_anneal_subset_with_dcodebook(call):
     wl = WL.workload(5)
     c = WL.codebook(5)
@@ -212,6 +212,24 @@ def test_shapes_and_ragged_batches(n, k, B, L):
     rst, _ = O.viterbi(w, c, n, k)
     np.testing.assert_array_equal(host(st), rst)
     np.testing.assert_array_equal(host(wh), c[rst])
+
+
+@pytest.mark.parametrize("n,k,B,L", [
+    (4, 2, 3, 16), (8, 2, 5, 40), (12, 2, 3, 30), (13, 2, 2, 12), (14, 2, 2, 10), (15, 2, 2, 9),
+    (16, 2, 2, 12), (6, 1, 9, 21), (14, 1, 2, 6), (8, 3, 3, 9),
+])
+def test_low_temperature_fp64_path(n, k, B, L):
+    """T below the switch (log2(e)/2T > 30) runs the fp64 log-vector kernel."""
+    w, c, g = WL.random_case(5000 + 100 * n + k, B, L, n)
+    full_check(w, c, n, k, 0.003, g, True, f"lowT n={n} k={k}")
+    full_check(w, c, n, k, 0.003, g, False, f"lowT n={n} k={k} no-dc")
+
+
+@pytest.mark.parametrize("T", [0.0235, 0.0245])
+def test_precision_switch_boundary(T):
+    """Both sides of the fp32 / fp64 switch at S = 65536."""
+    w, c, g = WL.random_case(31, 3, 64, 16)
+    full_check(w, c, 16, 2, T, g, True, f"switch T={T}")
 
 
 @pytest.mark.parametrize("n", [8, 12, 16])
