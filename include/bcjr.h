@@ -33,9 +33,10 @@
  *     that may run concurrently.
  *   - Calls are asynchronous on `stream`; the returned status covers argument
  *     validation and launch errors only.  No exception crosses the ABI.
- *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12)
- *     (k = 1: 2..14, k = 2: 4..16, k = 3: 6..16).  Other valid (state_bits, k)
- *     return BCJR_ERR_UNSUPPORTED.
+ *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12),
+ *     and for k = 3 also state_bits <= 14 (k = 1: 2..14, k = 2: 4..16,
+ *     k = 3: 6..14).  Other valid (state_bits, k) return
+ *     BCJR_ERR_UNSUPPORTED.
  *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
  *   - Non-finite w or codebook values give non-finite outputs; they are not
  *     checked.

@@ -57,20 +57,25 @@ Family family(int n, int k, bool dc) {
 }
 
 // The VJP switches to fp64 log vectors when the field scale log2(e)/(2T)
-// exceeds this value (T < 0.024 for unit-variance data): below it the states
-// that carry the posterior sit hundreds of log2 units from the per-step
-// maximum and fp32 storage no longer keeps the VJP within 1e-4.
-constexpr double kHighPrecisionK2 = 30.0;
+// exceeds this value (T < 0.040 for unit-variance data).  The log values of
+// the states that carry the posterior sit ~(field scale) x O(1) below the
+// per-step maximum, and fp32 storage of them costs VJP accuracy roughly in
+// proportion to 1/T (dCodebook error 2e-5 at T = 0.05, 5e-5 at 0.0245,
+// 1.3e-4 at 0.014 for S = 65536); the switch keeps the fp32 path at >= 3x
+// margin below the 1e-4 tolerance.
+constexpr double kHighPrecisionK2 = 18.0;
 
 bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
 
-Family family_hp(int n, int k) {
+Family family_hp(int n, int k, bool dc) {
   Family f;
   const int nsg = 1 << (n - 2 * k);
   if (nsg <= 256) {
     f.nt = 256; f.sgmax = 1; f.sgt = 1; f.occ_est = 8;
   } else if (nsg <= 2048) {
     f.nt = 256; f.sgt = nsg / 256; f.sgmax = f.sgt; f.occ_est = 4;
+  } else if (!dc) {
+    f.nt = 1024; f.sgt = nsg / 1024; f.sgmax = f.sgt; f.occ_est = 1;
   } else {
     f.nt = 512; f.sgt = nsg / 512; f.sgmax = f.sgt; f.occ_est = 1;
   }
@@ -92,7 +97,7 @@ HpLayout hp_layout(int64_t L, int n, int k) {
   l.histH = align_up((size_t)L * gs * sizeof(double));
   l.histG = align_up((size_t)L * gs * sizeof(double));
   l.histA = align_up((size_t)L * gs * sizeof(float));
-  l.xA = align_up(2 * gs * sizeof(float));
+  l.xA = align_up(4 * gs * sizeof(float));
   l.small = align_up((size_t)3 * L * sizeof(double));
   l.dc = align_up(((size_t)1 << n) * sizeof(double));
   l.slot = l.histH + l.histG + l.histA + l.xA + l.small + l.dc;
@@ -176,7 +181,7 @@ FbFn hp_pick_kb(int n, const Family& f, bool dc) {
     if (n == n512 + 2)
       return dc ? fb_kernel_hp<KB, n512 + 2, 8, 256, true> : fb_kernel_hp<KB, n512 + 2, 8, 256, false>;
     if (n == n512 + 3)
-      return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 8, 512, false>;
+      return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 4, 1024, false>;
   }
   return nullptr;
 }
@@ -269,7 +274,7 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
               const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
               void* workspace, size_t ws_bytes, hipStream_t stream) {
   const bool dc = dCodebook != nullptr;
-  const Family f = family_hp(n, k);
+  const Family f = family_hp(n, k, dc);
   const HpLayout lay = hp_layout(L, n, k);
   FbFn fn = hp_pick(n, k, f, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
@@ -373,7 +378,7 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
   size_t bytes = (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
-    const Family fh = family_hp(state_bits, k);
+    const Family fh = family_hp(state_bits, k, true);
     const int64_t gh = std::min<int64_t>(ceil_div(B, fh.bpw), (int64_t)kDeviceCUs * fh.occ_est);
     bytes = std::max(bytes, (size_t)(gh * fh.bpw) * hp_layout(L, state_bits, k).slot);
   }

@@ -26,7 +26,7 @@ struct FbArgs {
   double* histHd;      // [slots][L][S/K] fp64
   double* histGd;      // [slots][L][S/K] fp64
   float* histA;        // [slots][L][S/K]
-  float* xA;           // [slots][2][S/K] exchange buffer of the A tangent
+  float* xA;           // [slots][4][S/K] exchange buffers: A partials [2], c* [2]
   double* smalld;      // [slots][3][L]   shifts of H, lambda_t (fp64), w_soft_t (fp32)
 };
 

@@ -69,6 +69,21 @@ __device__ __forceinline__ T max_of(const T (&x)[K]) {
   return m;
 }
 
+// Maximum of al[] and the codeword of the first predecessor attaining it
+// (the dominant predecessor c* of the group).
+template <int K, class T>
+__device__ __forceinline__ T max_arg_c(const T (&al)[K], const float (&cc)[K][K], int u, float& cst) {
+  T m = al[0];
+  cst = cc[0][u];
+#pragma unroll
+  for (int j = 1; j < K; ++j) {
+    const bool gt = al[j] > m;
+    m = gt ? al[j] : m;
+    cst = gt ? cc[j][u] : cst;
+  }
+  return m;
+}
+
 // s = sum E, sy = sum E y, scw = sum E cw, scwy = sum E cw y
 template <int K>
 __device__ __forceinline__ void group_sums(const float (&E)[K], const float (&y)[K],
@@ -404,7 +419,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             rv[1] += fac * s;
             rv[2] += fac * sc;
             if constexpr (VJP) {
-              // E-weighted mean of g_t c + A_t over the K predecessors
+              // E-weighted mean of g_t c + A_t over the K predecessors; the
+              // centring g_t w_soft_t is subtracted at write time
               float num = E[0] * Ain[0];
 #pragma unroll
               for (int j = 1; j < K; ++j) num = fmaf(E[j], Ain[j], num);
@@ -422,7 +438,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       const float wst = rv[2] / rv[1];
       const float lamt = lam_est + lg2(rv[1]);
       if (t < L - 1) {
-        const float gws = gt * wst;
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
@@ -434,7 +449,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             if constexpr (VJP) {
               float ao[K];
 #pragma unroll
-              for (int u = 0; u < K; ++u) ao[u] = Aout[i][u] - gws;
+              for (int u = 0; u < K; ++u) ao[u] = fmaf(-gt, wst, Aout[i][u]);
               st_vec<K>(v1 + sg * K, ao);
             }
           }
@@ -515,6 +530,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
                   const float X = y[b] + At[j];
                   dcacc[(i * K + j) * K + b] += p * fmaf((wt - cc[b]) * (X - xbar), invT, gt);
                 }
+                sg_fence();
               }
             }
             sg_fence();
@@ -565,8 +581,13 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 // the tangents stay fp32 (they are well conditioned).  Structure:
 //   S0: H (fp64) in LDS, in place (reads, barrier, writes, barrier);
 //   S1: G (fp64) in LDS in place; the A tangent travels through a per-slot
-//       global double buffer (L2 resident), written uncentred and centred on
-//       the soft codeword when read back;
+//       global double buffer (L2 resident).  Each output state stores its
+//       tangent centred on the codeword c* of its dominant predecessor
+//       (the one with the largest log weight) together with c*; the reader
+//       adds g_prev (c* - w_soft_prev) once w_soft of that step is known.
+//       With fp32 softmax weights this keeps the stored value small where
+//       the posterior has crystallised, which the plain centring on w_soft
+//       (not yet known at write time) cannot;
 //   S2: as in fb_kernel (B in LDS, ping-pong), with H, G read in fp64.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void lse_pair_d(double& m, float& s, double mo, float so) {
@@ -670,7 +691,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     double* hH = a.histHd + slot * L * GS;
     double* hG = a.histGd + slot * L * GS;
     float* hA = a.histA + slot * L * GS;
-    float* gA = a.xA + slot * 2 * GS;
+    float* gA = a.xA + slot * 4 * GS;  // A partials [2][S/K], then c* [2][S/K]
+    float* gC = gA + 2 * GS;
     double* sm_mB = a.smalld + slot * 3 * L;
     double* sm_lam = sm_mB + L;
     float* sm_ws = reinterpret_cast<float*>(sm_lam + L);
@@ -786,10 +808,11 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     for (int i = tb; i < GS; i += TPB) {
       vd[i] = 0.0;
       gA[i] = 0.f;
+      gC[i] = 0.f;
     }
     __syncthreads();
     double lam_est = lam0;
-    float gws_prev = 0.f;  // centring of the A values read this step
+    float gprev = 0.f, wsprev = 0.f;  // g and w_soft of the step that wrote A
     for (int64_t t = 0; t < L; ++t) {
       const double wt = (double)wb[t];
       const float wtf = wb[t];
@@ -797,6 +820,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       const double mBt = sm_mB[t];
       const float* Acur = gA + (t & 1) * GS;
       float* Anext = gA + ((t + 1) & 1) * GS;
+      const float* Ccur = gC + (t & 1) * GS;
+      float* Cnext = gC + ((t + 1) & 1) * GS;
       double Gout[SGMAX][K];
       double vmax[1] = {-INFINITY};
       float rv[2] = {0.f, 0.f};  // sum p, sum p c
@@ -809,7 +834,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             Gin[j] = vd[j * NSG + sg];
-            Ain[j] = Acur[j * NSG + sg] - gws_prev;
+            Ain[j] = fmaf(gprev, Ccur[j * NSG + sg] - wsprev, Acur[j * NSG + sg]);
           }
           st_vec_d<K>(hG + t * GS + ((i * TPB) << KB) + toK, Gin);
           st_vec<K>(hA + t * GS + ((i * TPB) << KB) + toK, Ain);
@@ -818,7 +843,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           float cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
-          float ao[K];
+          float ao[K], co[K];
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             double al[K];
@@ -827,25 +852,29 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
               const double d = wt - (double)cc[j][u];
               al[j] = Gin[j] - d * d * k2;
             }
-            const double m = max_of<K>(al);
+            float cst;
+            const double m = max_arg_c<K>(al, cc, u, cst);
             float E[K];
 #pragma unroll
             for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
-            float s = E[0], sc = E[0] * cc[0][u], num = E[0] * Ain[0];
+            float s = E[0], sc = E[0] * cc[0][u], num = E[0] * Ain[0], sd = E[0] * (cc[0][u] - cst);
 #pragma unroll
             for (int j = 1; j < K; ++j) {
               s += E[j];
               sc = fmaf(E[j], cc[j][u], sc);
               num = fmaf(E[j], Ain[j], num);
+              sd = fmaf(E[j], cc[j][u] - cst, sd);
             }
+            co[u] = cst;
             Gout[i][u] = m + (double)lg2(s);
             vmax[0] = fmax(vmax[0], Gout[i][u]);
             const float fac = ex2((float)(m + Hc[u] - lam_est));
             rv[0] = fmaf(fac, s, rv[0]);
             rv[1] = fmaf(fac, sc, rv[1]);
-            ao[u] = fmaf(gt, sc, num) * rcp(s);  // uncentred A_{t+1}
+            ao[u] = fmaf(gt, sd, num) * rcp(s);  // A_{t+1} - g_t (c* - w_soft_t)
           }
           st_vec<K>(Anext + ((i * TPB) << KB) + toK, ao);
+          st_vec<K>(Cnext + ((i * TPB) << KB) + toK, co);
           (void)wtf;
           sg_fence();
         }
@@ -875,7 +904,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         sm_ws[t] = wst;
         if (valid && a.w_soft) a.w_soft[bb * L + t] = wst;
       }
-      gws_prev = gt * wst;
+      gprev = gt;
+      wsprev = wst;
       lam_est = lamt - off + mBt;
       __syncthreads();
     }
@@ -940,6 +970,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
                 const float X = y[b] + At[j];
                 dcacc[(i * K + j) * K + b] += p * fmaf((wtf - cc[b]) * (X - xbar), invT, gt);
               }
+              sg_fence();
             }
           }
           sg_fence();
@@ -969,6 +1000,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
                 for (int b = 0; b < K; ++b) pj[b] += (double)dcacc[(i * K + j) * K + b];
               }
+              sg_fence();
             }
           }
         }
