@@ -84,7 +84,7 @@ Family family_hp(int n, int k, bool dc) {
 }
 
 struct FbLayout {
-  size_t histH, histGA, small, dc, slot;
+  size_t hist, small, dc, slot;
 };
 
 struct HpLayout {
@@ -106,17 +106,17 @@ HpLayout hp_layout(int64_t L, int n, int k) {
 
 size_t hp_lds_bytes(const Family& f, int n, int k) {
   const size_t gs = (size_t)1 << (n - k);
-  return (size_t)f.bpw * gs * sizeof(double) + (size_t)(f.nt / 64) * 4 * (sizeof(double) + sizeof(float));
+  return (size_t)f.bpw * gs * sizeof(double) +
+         (size_t)(f.nt / 64) * (4 * sizeof(double) + kRed * sizeof(float));
 }
 
 FbLayout fb_layout(int64_t L, int n, int k, bool vjp) {
   const size_t gs = (size_t)1 << (n - k);
   FbLayout l;
-  l.histH = align_up((size_t)L * gs * sizeof(float));
-  l.histGA = vjp ? align_up((size_t)L * 2 * gs * sizeof(float)) : 0;
-  l.small = align_up((size_t)4 * L * sizeof(float));
+  l.hist = align_up((size_t)L * (vjp ? 2 : 1) * gs * sizeof(float));
+  l.small = align_up((size_t)L * sizeof(float));
   l.dc = vjp ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
-  l.slot = l.histH + l.histGA + l.small + l.dc;
+  l.slot = l.hist + l.small + l.dc;
   return l;
 }
 
@@ -128,7 +128,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 size_t fb_lds_bytes(const Family& f, int n, int k) {
   const size_t gs = (size_t)1 << (n - k);
-  return (size_t)f.bpw * 2 * gs * sizeof(float) + (size_t)(f.nt / 64) * 4 * sizeof(float);
+  return (size_t)f.bpw * 2 * gs * sizeof(float) + (size_t)(f.nt / 64) * kRed * sizeof(float);
 }
 
 size_t vit_lds_bytes(const Family& f, int n, int k) {
@@ -335,11 +335,10 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
   a.invT = (float)(1.0 / Td);
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
-  a.histH = reinterpret_cast<float*>(base);
-  a.histGA = vjp ? reinterpret_cast<float*>(base + slots * lay.histH) : nullptr;
-  a.small = reinterpret_cast<float*>(base + slots * (lay.histH + lay.histGA));
-  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.histH + lay.histGA + lay.small))
-                 : nullptr;
+  a.histH = vjp ? nullptr : reinterpret_cast<float*>(base);
+  a.histHB = vjp ? reinterpret_cast<float*>(base) : nullptr;
+  a.small = reinterpret_cast<float*>(base + slots * lay.hist);
+  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.small)) : nullptr;
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {

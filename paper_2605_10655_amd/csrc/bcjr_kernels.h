@@ -32,16 +32,17 @@
 // VJP (the paper's Sec. 3.5 gives no formula; it follows from Eq. boltzmann).
 //   With F = sum_t g_t c(s_t):  dW_tau = Cov(F, c(s_tau)) / T and
 //   dc_sig = sum_t p_t(sig)[g_t + (w_t - c_sig)(E[F|s_t=sig] - E[F]) / T].
-//   E[F | s_t = s] = A_t(s) + B_t(s) with forward / backward tangent
-//   recursions that reuse the alpha / beta softmax weights.  Both tangents are
-//   centred on the soft codeword: they accumulate g_t (c(s_t) - w_soft_t), so
-//   E_p[A_t + B_t] = 0 and the tangents stay small exactly where p is large
-//   (fp32 keeps relative precision at low T).  That needs w_soft before the
-//   forward tangent runs, so the VJP is three sweeps per block:
-//     S0 backward: H only (stored per step);
-//     S1 forward:  G, marginals -> w_soft_t, lambda_t; A centred at write time;
-//     S2 backward: H read back from S0, B tangent, combine -> dW_t, dc.
-//   The soft codeword alone is S0 + S1.
+//   E[F | s_t = s] = g_t c(s) + A_t(s) + B_t(s) with forward / backward
+//   tangent recursions that reuse the alpha / beta softmax weights.  Each
+//   tangent is kept small by subtracting a per-step constant from every
+//   summand (covariances ignore such constants): the backward tangent
+//   accumulates g_t (c(s_t) - w_t), the forward one g_t (c(s_t) - w_soft_t),
+//   so fp32 keeps their differences accurate.  fb_kernel does two sweeps:
+//     S0 backward: H and B (both stored per step);
+//     S1 forward:  G, marginals -> w_soft_t, A, and the combine -> dW_t, dc.
+//   The soft codeword alone is S0 (H only) + S1 (no tangents).
+//   fb_kernel_hp (fp64 log vectors, low temperatures) centres both tangents
+//   on w_soft and therefore needs a third sweep.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -148,11 +149,13 @@ __device__ __forceinline__ void st_vec(float* p, const float (&v)[N]) {
 // waves, combined through a small LDS area after the caller's barrier.
 // xor butterflies give every lane bitwise-identical results.
 // ---------------------------------------------------------------------------
+constexpr int kRed = 8;  // floats per wave in the cross-wave reduction area
+
 struct RedCtx {
   int width;     // lanes combined inside a wave: min(TPB, 64)
   int rw;        // waves per block (1 when TPB <= 64)
   int lane, wave;
-  float* red;    // [waves][4] floats
+  float* red;    // [waves][kRed] floats
 };
 
 template <int NQ, unsigned MAXMASK>
@@ -165,7 +168,7 @@ __device__ __forceinline__ void red_pre(float (&v)[NQ], const RedCtx& r) {
     }
   if (r.rw > 1 && r.lane == 0) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) r.red[r.wave * 4 + q] = v[q];
+    for (int q = 0; q < NQ; ++q) r.red[r.wave * kRed + q] = v[q];
   }
 }
 
@@ -176,9 +179,9 @@ __device__ __forceinline__ void red_post(float (&v)[NQ], const RedCtx& r) {
     const int first = (r.wave / r.rw) * r.rw;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      float acc = r.red[first * 4 + q];
+      float acc = r.red[first * kRed + q];
       for (int i = 1; i < r.rw; ++i) {
-        const float o = r.red[(first + i) * 4 + q];
+        const float o = r.red[(first + i) * kRed + q];
         acc = ((MAXMASK >> q) & 1u) ? fmaxf(acc, o) : acc + o;
       }
       v[q] = acc;
@@ -200,17 +203,52 @@ __device__ __forceinline__ void lse_pre(float& m, float& s, const RedCtx& r) {
     lse_pair(m, s, mo, so);
   }
   if (r.rw > 1 && r.lane == 0) {
-    r.red[r.wave * 4 + 0] = m;
-    r.red[r.wave * 4 + 1] = s;
+    r.red[r.wave * kRed + 0] = m;
+    r.red[r.wave * kRed + 1] = s;
   }
 }
 
 __device__ __forceinline__ void lse_post(float& m, float& s, const RedCtx& r) {
   if (r.rw > 1) {
     const int first = (r.wave / r.rw) * r.rw;
-    m = r.red[first * 4 + 0];
-    s = r.red[first * 4 + 1];
-    for (int i = 1; i < r.rw; ++i) lse_pair(m, s, r.red[(first + i) * 4 + 0], r.red[(first + i) * 4 + 1]);
+    m = r.red[first * kRed + 0];
+    s = r.red[first * kRed + 1];
+    for (int i = 1; i < r.rw; ++i) lse_pair(m, s, r.red[(first + i) * kRed + 0], r.red[(first + i) * kRed + 1]);
+  }
+}
+
+// (max, scaled sum, scaled weighted sum) triples, combined like lse_pair
+__device__ __forceinline__ void lse3_pair(float& m, float& s, float& y, float mo, float so, float yo) {
+  const float M = fmaxf(m, mo);
+  const float f = ex2(m - M), fo = ex2(mo - M);
+  s = s * f + so * fo;
+  y = y * f + yo * fo;
+  m = M;
+}
+
+__device__ __forceinline__ void lse3_pre(float& m, float& s, float& y, const RedCtx& r) {
+  for (int off = 1; off < r.width; off <<= 1) {
+    const float mo = __shfl_xor(m, off);
+    const float so = __shfl_xor(s, off);
+    const float yo = __shfl_xor(y, off);
+    lse3_pair(m, s, y, mo, so, yo);
+  }
+  if (r.rw > 1 && r.lane == 0) {
+    r.red[r.wave * kRed + 0] = m;
+    r.red[r.wave * kRed + 1] = s;
+    r.red[r.wave * kRed + 2] = y;
+  }
+}
+
+__device__ __forceinline__ void lse3_post(float& m, float& s, float& y, const RedCtx& r) {
+  if (r.rw > 1) {
+    const int first = (r.wave / r.rw) * r.rw;
+    m = r.red[first * kRed + 0];
+    s = r.red[first * kRed + 1];
+    y = r.red[first * kRed + 2];
+    for (int i = 1; i < r.rw; ++i)
+      lse3_pair(m, s, y, r.red[(first + i) * kRed + 0], r.red[(first + i) * kRed + 1],
+                r.red[(first + i) * kRed + 2]);
   }
 }
 
@@ -263,37 +301,53 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
     const float* wb = a.w + bb * L;
     const float* gb = VJP ? a.g + bb * L : nullptr;
-    float* hH = a.histH + slot * L * GS;
-    float* hGA = VJP ? a.histGA + slot * L * 2 * GS : nullptr;
-    float* sm_mB = a.small + slot * 4 * L;  // shift applied to H_t
-    float* sm_lam = sm_mB + L;              // lambda_t
-    float* sm_ws = sm_lam + L;              // w_soft_t
+    float* hH = VJP ? nullptr : a.histH + slot * L * GS;       // [L][S/K]: H_t
+    float* hHB = VJP ? a.histHB + slot * L * 2 * GS : nullptr;  // [L][S/K/K][2K]: H_t, B_t
+    float* sm_mB = a.small + slot * L;                          // shift applied to H_t
 
     // ------------------------------------------------------------------ S0
-    // Backward sweep for H alone.  v0 / v1 alternate as the H_t being read and
-    // the H_{t-1} being written, so one barrier per step suffices; the shift
-    // of H_{t-1} (floor of its max, known after the barrier) is subtracted
-    // when it is read back.
-    for (int i = tb; i < GS; i += TPB) v0[i] = 0.f;
+    // Backward sweep.  Soft codeword alone: H only, v0 / v1 alternating as the
+    // H_t being read and the H_{t-1} being written (one barrier per step; the
+    // shift of H_{t-1}, known after the barrier, is subtracted when it is read
+    // back).  With the VJP: H in v0 and the backward tangent B in v1, updated
+    // in place (reads, barrier, writes, barrier).  B_t(s) = E[sum_{tau > t}
+    // g_tau (c(s_tau) - w_tau) | s_t = s] is centred on the input weights, so
+    // it stays O(quantisation error) in size.  Each thread stores the values
+    // its super-groups read (H_t, and B_t for the VJP) as the step's history.
+    for (int i = tb; i < GS; i += TPB) {
+      v0[i] = 0.f;
+      if (VJP) v1[i] = 0.f;
+    }
     __syncthreads();
     double shiftB = 0.0;  // sum of the integer shifts of H (exact)
     float lam0 = 0.f;
-    float offc = 0.f;     // shift of the H vector being read
+    float xbar = 0.f;     // VJP: E_p[X_0], see S1
+    float offc = 0.f;     // soft codeword alone: shift of the H vector being read
     for (int64_t t = L - 1;; --t) {
       const float wt = wb[t];
-      float* cur = ((L - 1 - t) & 1) ? v1 : v0;
+      const float gt = VJP ? gb[t] : 0.f;
+      float* cur = (!VJP && ((L - 1 - t) & 1)) ? v1 : v0;
       float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
       if (t == 0) {
-        // lambda_0 = LSE_s [h_0(s) + H_0(s & (S/K-1))]  (log2 alpha_0 = h_0)
-        float lm = -INFINITY, ls = 0.f;
+        // lambda_0 = LSE_s [h_0(s) + H_0(s & (S/K-1))]  (log2 alpha_0 = h_0);
+        // with the VJP also E_p[g_0 c(s_0) + B_0(s_0)], the mean of X_0
+        float lm = -INFINITY, ls = 0.f, ly = 0.f;
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
             const int sg = tb + i * TPB;
-            float Hin[K];
+            float Hin[K], Bin[K];
 #pragma unroll
-            for (int b = 0; b < K; ++b) Hin[b] = cur[sg * K + b] - offc;
-            st_vec<K>(hH + ((i * TPB) << KB) + toK, Hin);
+            for (int b = 0; b < K; ++b) {
+              Hin[b] = cur[sg * K + b] - offc;
+              Bin[b] = VJP ? v1[sg * K + b] : 0.f;
+            }
+            if constexpr (VJP) {
+              st_vec<K>(hHB + ((i * TPB) << (KB + 1)) + 2 * toK, Hin);
+              st_vec<K>(hHB + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bin);
+            } else {
+              st_vec<K>(hH + ((i * TPB) << KB) + toK, Hin);
+            }
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               float cc[K];
@@ -305,50 +359,92 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
                 x[b] = Hin[b] - d * d * k2;
               }
               const float m = max_of<K>(x);
-              float s = ex2(x[0] - m);
+              float E[K];
 #pragma unroll
-              for (int b = 1; b < K; ++b) s += ex2(x[b] - m);
-              lse_pair(lm, ls, m, s);
+              for (int b = 0; b < K; ++b) E[b] = ex2(x[b] - m);
+              float s = E[0];
+#pragma unroll
+              for (int b = 1; b < K; ++b) s += E[b];
+              if constexpr (VJP) {
+                float sy = E[0] * fmaf(gt, cc[0], Bin[0]);
+#pragma unroll
+                for (int b = 1; b < K; ++b) sy = fmaf(E[b], fmaf(gt, cc[b], Bin[b]), sy);
+                lse3_pair(lm, ls, ly, m, s, sy);
+              } else {
+                lse_pair(lm, ls, m, s);
+              }
             }
             sg_fence();
           }
         }
-        lse_pre(lm, ls, rc);
+        if constexpr (VJP) {
+          lse3_pre(lm, ls, ly, rc);
+        } else {
+          lse_pre(lm, ls, rc);
+        }
         if (tb == 0) sm_mB[L - 1] = 0.f;
         __syncthreads();
-        lse_post(lm, ls, rc);
+        if constexpr (VJP) {
+          lse3_post(lm, ls, ly, rc);
+          xbar = ly / ls;
+        } else {
+          lse_post(lm, ls, rc);
+        }
         lam0 = lm + lg2(ls);
         if (tb == 0 && valid && a.logZ)
           a.logZ[bb] = (float)((shiftB + (double)lam0) * 0.69314718055994530942);
         __syncthreads();
         break;
       }
+      float Hout[VJP ? SGMAX : 1][K], Bout[VJP ? SGMAX : 1][K];
       float vmax[1] = {-INFINITY};
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
           const int sg = tb + i * TPB;
-          float Hin[K];
+          float Hin[K], Bin[K];
 #pragma unroll
-          for (int b = 0; b < K; ++b) Hin[b] = cur[sg * K + b] - offc;
-          st_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+          for (int b = 0; b < K; ++b) {
+            Hin[b] = cur[sg * K + b] - offc;
+            Bin[b] = VJP ? v1[sg * K + b] : 0.f;
+          }
+          if constexpr (VJP) {
+            st_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Hin);
+            st_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bin);
+          } else {
+            st_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+          }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             float cc[K];
             ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-            float x[K];
+            float x[K], d[K];
 #pragma unroll
             for (int b = 0; b < K; ++b) {
-              const float d = wt - cc[b];
-              x[b] = Hin[b] - d * d * k2;
+              d[b] = wt - cc[b];
+              x[b] = Hin[b] - d[b] * d[b] * k2;
             }
             const float m = max_of<K>(x);
-            float s = ex2(x[0] - m);
+            float E[K];
 #pragma unroll
-            for (int b = 1; b < K; ++b) s += ex2(x[b] - m);
+            for (int b = 0; b < K; ++b) E[b] = ex2(x[b] - m);
+            float s = E[0];
+#pragma unroll
+            for (int b = 1; b < K; ++b) s += E[b];
             const float h = m + lg2(s);
-            nxt[j * NSG + sg] = h;
             vmax[0] = fmaxf(vmax[0], h);
+            if constexpr (VJP) {
+              // B_{t-1} = E-weighted mean of g_t (c - w_t) + B_t over the K successors
+              float num = E[0] * fmaf(-gt, d[0], Bin[0]);
+#pragma unroll
+              for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(-gt, d[b], Bin[b]), num);
+              Hout[i][j] = h;
+              pin(Hout[i][j]);
+              Bout[i][j] = num * rcp(s);
+              pin(Bout[i][j]);
+            } else {
+              nxt[j * NSG + sg] = h;
+            }
           }
           sg_fence();
         }
@@ -356,17 +452,50 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       red_pre<1, 1u>(vmax, rc);
       __syncthreads();
       red_post<1, 1u>(vmax, rc);
-      offc = floorf(vmax[0]);
-      shiftB += (double)offc;
-      if (tb == 0) sm_mB[t - 1] = offc;
+      const float off = floorf(vmax[0]);
+      shiftB += (double)off;
+      if (tb == 0) sm_mB[t - 1] = off;
+      if constexpr (VJP) {
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i) {
+          if (i < SGT) {
+            const int sg = tb + i * TPB;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              v0[j * NSG + sg] = Hout[i][j] - off;
+              v1[j * NSG + sg] = Bout[i][j];
+            }
+          }
+        }
+        __syncthreads();
+      } else {
+        offc = off;
+      }
     }
 
     // ------------------------------------------------------------------ S1
+    // Forward sweep: G (and the forward tangent A) in v0 (v1), in place: all
+    // reads, barrier, writes, barrier; outputs are held in registers across
+    // the first barrier.  For each output group the K-way LSE gives G_{t+1};
+    // its softmax weights E_j times one exponential 2^(m + H_t - lambda_t) are
+    // the marginals p_t of the group's K states.  With the VJP:
+    //   A_t(s) = E[sum_{tau < t} g_tau (c(s_tau) - w_soft_tau) | s_t = s]
+    //   (centred on the soft codeword at write time),
+    //   X_t(s) = g_t c(s) + A_t(s) + B_t(s) - xbar_t = E[F | s_t = s] - const,
+    // where xbar_t predicts E_p[X_t] (exact at t = 0 from S0, then carried by
+    // the known change of the centring constants and re-anchored each step),
+    // so that dW_t = (sum p c X - w_soft_t sum p X) / (T sum p) and the
+    // dCodebook summands p (g + (w - c) X / T) see a nearly centred X.
     for (int i = tb; i < GS; i += TPB) {
       v0[i] = 0.f;
       if (VJP) v1[i] = 0.f;
     }
+    if constexpr (DC) {
+#pragma unroll
+      for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
+    }
     __syncthreads();
+    const float invT = a.invT;
     float lam_est = lam0;
     for (int64_t t = 0; t < L; ++t) {
       const float wt = wb[t];
@@ -374,7 +503,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       const float mBt = sm_mB[t];
       float Gout[SGMAX][K];
       float Aout[VJP ? SGMAX : 1][K];
-      float rv[3] = {-INFINITY, 0.f, 0.f};  // max G_{t+1}, sum p, sum p*c
+      // max G_{t+1}, sum p, sum p c, and with the VJP sum p X, sum p c X
+      float rv[VJP ? 5 : 3];
+      rv[0] = -INFINITY;
+#pragma unroll
+      for (int q = 1; q < (VJP ? 5 : 3); ++q) rv[q] = 0.f;
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
@@ -385,12 +518,13 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             Gin[j] = v0[j * NSG + sg];
             Ain[j] = VJP ? v1[j * NSG + sg] : 0.f;
           }
-          if (VJP) {
-            st_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Gin);
-            st_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Ain);
+          float Hc[K], Bc[K];
+          if constexpr (VJP) {
+            ld_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Hc);
+            ld_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bc);
+          } else {
+            ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
           }
-          float Hc[K];
-          ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
           float cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
@@ -406,36 +540,56 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             float E[K];
 #pragma unroll
             for (int j = 0; j < K; ++j) E[j] = ex2(al[j] - m);
-            float s = E[0], sc = E[0] * cc[0][u];
+            float s = E[0], ec = E[0] * cc[0][u], sc = ec;
+            float y = 0.f, sy = 0.f, scy = 0.f;
+            if constexpr (VJP) {
+              y = fmaf(gt, cc[0][u], Ain[0]);
+              sy = E[0] * y;
+              scy = ec * y;
+            }
 #pragma unroll
             for (int j = 1; j < K; ++j) {
               s += E[j];
-              sc = fmaf(E[j], cc[j][u], sc);
+              ec = E[j] * cc[j][u];
+              sc += ec;
+              if constexpr (VJP) {
+                y = fmaf(gt, cc[j][u], Ain[j]);
+                sy = fmaf(E[j], y, sy);
+                scy = fmaf(ec, y, scy);
+              }
             }
             Gout[i][u] = m + lg2(s);
             pin(Gout[i][u]);
             rv[0] = fmaxf(rv[0], Gout[i][u]);
             const float fac = ex2(m + Hc[u] - lam_est);
-            rv[1] += fac * s;
-            rv[2] += fac * sc;
+            rv[1] = fmaf(fac, s, rv[1]);
+            rv[2] = fmaf(fac, sc, rv[2]);
             if constexpr (VJP) {
-              // E-weighted mean of g_t c + A_t over the K predecessors; the
-              // centring g_t w_soft_t is subtracted at write time
-              float num = E[0] * Ain[0];
-#pragma unroll
-              for (int j = 1; j < K; ++j) num = fmaf(E[j], Ain[j], num);
-              Aout[i][u] = fmaf(gt, sc, num) * rcp(s);
+              // X = y_j + bx over the group's states, bx = B_t - xbar
+              const float bx = Bc[u] - xbar;
+              rv[3] = fmaf(fac, fmaf(s, bx, sy), rv[3]);
+              rv[4] = fmaf(fac, fmaf(sc, bx, scy), rv[4]);
+              Aout[i][u] = sy * rcp(s);
               pin(Aout[i][u]);
+              if constexpr (DC) {
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                  const float X = fmaf(gt, cc[j][u], Ain[j]) + bx;
+                  dcacc[(i * K + j) * K + u] =
+                      fmaf(E[j] * fac, fmaf((wt - cc[j][u]) * X, invT, gt), dcacc[(i * K + j) * K + u]);
+                }
+              }
             }
           }
           sg_fence();
         }
       }
-      red_pre<3, 1u>(rv, rc);
+      red_pre<VJP ? 5 : 3, 1u>(rv, rc);
       __syncthreads();
-      red_post<3, 1u>(rv, rc);
+      red_post<VJP ? 5 : 3, 1u>(rv, rc);
       const float off = floorf(rv[0]);
-      const float wst = rv[2] / rv[1];
+      const float r1 = 1.f / rv[1];
+      const float wst = rv[2] * r1;
       const float lamt = lam_est + lg2(rv[1]);
       if (t < L - 1) {
 #pragma unroll
@@ -455,118 +609,40 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
         }
       }
-      if (tb == 0) {
-        sm_lam[t] = lamt;
-        sm_ws[t] = wst;
-        if (valid && a.w_soft) a.w_soft[bb * L + t] = wst;
+      if (tb == 0 && valid) {
+        if (a.w_soft) a.w_soft[bb * L + t] = wst;
+        if (VJP && a.dW) a.dW[bb * L + t] = (rv[VJP ? 4 : 0] - wst * rv[VJP ? 3 : 0]) * r1 * invT;
       }
       lam_est = lamt - off + mBt;
+      if constexpr (VJP) {
+        // E_p[X_t] = xbar + sum p X / sum p; X_{t+1} drops g_t w_soft_t (A is
+        // centred) and gains g_{t+1} w_{t+1} (B_{t+1} no longer holds step t+1)
+        if (t < L - 1) xbar = fmaf(rv[3], r1, xbar) - gt * wst + gb[t + 1] * wb[t + 1];
+      }
       __syncthreads();
     }
 
-    // ------------------------------------------------------------------ S2
-    // Backward sweep for the B tangent and the combine.  H_t is read back from
-    // S0's history (the exact values S1 used), so only B lives in LDS, again
-    // alternating between v0 and v1 with one barrier per step.
-    if constexpr (VJP) {
-      if constexpr (DC) {
-#pragma unroll
-        for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
-      }
-      for (int i = tb; i < GS; i += TPB) v0[i] = 0.f;
-      __syncthreads();
-      const float invT = a.invT;
-      float xbar = 0.f;  // E_p[X] of the previous step (lagged mean removal)
-      for (int64_t t = L - 1; t >= 0; --t) {
-        const float wt = wb[t];
-        const float gt = gb[t];
-        const float wst = sm_ws[t];
-        const float lamt = sm_lam[t];
-        float* cur = ((L - 1 - t) & 1) ? v1 : v0;
-        float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
-        float rv[3] = {0.f, 0.f, 0.f};  // sum p (c - ws) X, sum p X, sum p
+    if constexpr (DC) {
+      if (valid) {
+        const bool first = base == (int64_t)blockIdx.x * BPW;
+        double* part = a.dc_part + slot * ((int64_t)1 << n);
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
-            const int sg = tb + i * TPB;
-            float Hin[K], Bin[K], Gt[K], At[K];
-#pragma unroll
-            for (int b = 0; b < K; ++b) Bin[b] = cur[sg * K + b];
-            ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
-            ld_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Gt);
-            ld_vec<K>(hGA + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, At);
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              float cc[K];
-              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-              // per state: x = h + log beta (beta-side LSE term), cw = c - w_soft,
-              // y = g (c - w_soft) + B_t (the B-tangent summand); X = y + A_t.
-              float x[K], y[K], cw[K];
+              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
+              if (first) {
 #pragma unroll
-              for (int b = 0; b < K; ++b) {
-                const float d = wt - cc[b];
-                x[b] = Hin[b] - d * d * k2;
-                cw[b] = cc[b] - wst;
-                y[b] = fmaf(gt, cw[b], Bin[b]);
-              }
-              const float m = max_of<K>(x);
-              // marginals of the K states: p_b = E_b * fac; group sums give
-              //   sum p = fac s, sum p X = fac (sy + A s),
-              //   sum p (c - w_soft) X = fac (scwy + A scw)
-              float E[K];
+                for (int u = 0; u < K; ++u) pj[u] = (double)dcacc[(i * K + j) * K + u];
+              } else {
 #pragma unroll
-              for (int b = 0; b < K; ++b) E[b] = ex2(x[b] - m);
-              float s, sy, scw, scwy;
-              group_sums<K>(E, y, cw, s, sy, scw, scwy);
-              nxt[j * NSG + sg] = sy * rcp(s);  // B_{t-1}; unused after t = 0
-              const float fac = ex2(Gt[j] + m - lamt);
-              rv[0] = fmaf(fac, fmaf(At[j], scw, scwy), rv[0]);
-              rv[1] = fmaf(fac, fmaf(At[j], s, sy), rv[1]);
-              rv[2] = fmaf(fac, s, rv[2]);
-              if constexpr (DC) {
-#pragma unroll
-                for (int b = 0; b < K; ++b) {
-                  const float p = E[b] * fac;
-                  const float X = y[b] + At[j];
-                  dcacc[(i * K + j) * K + b] += p * fmaf((wt - cc[b]) * (X - xbar), invT, gt);
-                }
-                sg_fence();
-              }
-            }
-            sg_fence();
-          }
-        }
-        red_pre<3, 0u>(rv, rc);
-        __syncthreads();
-        red_post<3, 0u>(rv, rc);
-        const float rinv = 1.f / rv[2];
-        xbar = rv[1] * rinv;
-        if (tb == 0 && valid && a.dW) a.dW[bb * L + t] = rv[0] * rinv * invT;
-      }
-      if constexpr (DC) {
-        if (valid) {
-          const bool first = base == (int64_t)blockIdx.x * BPW;
-          double* part = a.dc_part + slot * ((int64_t)1 << n);
-#pragma unroll
-          for (int i = 0; i < SGMAX; ++i) {
-            if (i < SGT) {
-              const int sg = tb + i * TPB;
-#pragma unroll
-              for (int j = 0; j < K; ++j) {
-                double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
-                if (first) {
-#pragma unroll
-                  for (int b = 0; b < K; ++b) pj[b] = (double)dcacc[(i * K + j) * K + b];
-                } else {
-#pragma unroll
-                  for (int b = 0; b < K; ++b) pj[b] += (double)dcacc[(i * K + j) * K + b];
-                }
+                for (int u = 0; u < K; ++u) pj[u] += (double)dcacc[(i * K + j) * K + u];
               }
             }
           }
         }
       }
-      __syncthreads();
     }
   }
 }
@@ -675,7 +751,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   rc.wave = tid >> 6;
   double* vd = ldsh + (size_t)bw * GS;                              // G or H (fp64)
   double* redd = ldsh + (size_t)BPW * GS;                           // [waves][4] fp64
-  rc.red = reinterpret_cast<float*>(redd + (NT / 64) * 4);          // [waves][4] fp32
+  rc.red = reinterpret_cast<float*>(redd + (NT / 64) * 4);          // [waves][kRed] fp32
   float* vf0 = reinterpret_cast<float*>(vd);                        // S2: B ping-pong
   float* vf1 = vf0 + GS;
 
@@ -746,15 +822,15 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         }
         if (rc.rw > 1 && rc.lane == 0) {
           redd[rc.wave * 4 + 0] = lm;
-          rc.red[rc.wave * 4 + 0] = ls;
+          rc.red[rc.wave * kRed + 0] = ls;
         }
         if (tb == 0) sm_mB[L - 1] = 0.0;
         __syncthreads();
         if (rc.rw > 1) {
           const int first = (rc.wave / rc.rw) * rc.rw;
           lm = redd[first * 4];
-          ls = rc.red[first * 4];
-          for (int q = 1; q < rc.rw; ++q) lse_pair_d(lm, ls, redd[(first + q) * 4], rc.red[(first + q) * 4]);
+          ls = rc.red[first * kRed];
+          for (int q = 1; q < rc.rw; ++q) lse_pair_d(lm, ls, redd[(first + q) * 4], rc.red[(first + q) * kRed]);
         }
         lam0 = lm + (double)lg2(ls);
         if (tb == 0 && valid && a.logZ)
