@@ -35,8 +35,10 @@
  *     validation and launch errors only.  No exception crosses the ABI.
  *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12),
  *     and for k = 3 also state_bits <= 14 (k = 1: 2..14, k = 2: 4..16,
- *     k = 3: 6..14).  Other valid (state_bits, k) return
- *     BCJR_ERR_UNSUPPORTED.
+ *     k = 3: 6..14), and L small enough that one workgroup's histories
+ *     stay below 2 GiB (L <= 16383 at state_bits = 16, k = 2; at least
+ *     16383 for every supported shape).  Other valid shapes return
+ *     BCJR_ERR_UNSUPPORTED and a workspace size of 0.
  *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
  *   - Non-finite w or codebook values give non-finite outputs; they are not
  *     checked.

@@ -83,6 +83,17 @@ Family family_hp(int n, int k, bool dc) {
   return f;
 }
 
+// The histories of one workgroup's blocks are addressed with 32-bit byte
+// offsets: blocks per workgroup x L x S/K x 8 bytes must stay below 2^31.
+bool length_ok(int64_t L, int n, int k) {
+  for (int dc = 0; dc < 2; ++dc) {
+    const Family f = family(n, k, dc != 0);
+    const int64_t per_step = (int64_t)f.bpw * 8 * ((int64_t)1 << (n - k));
+    if (L > 0x7FFFFFFF / per_step) return false;
+  }
+  return true;
+}
+
 struct FbLayout {
   size_t hist, small, dc, slot;
 };
@@ -231,7 +242,7 @@ int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, i
   if (B > 0 && (!w || !codebook)) return BCJR_ERR_INVALID_ARG;
   if (codebook && ((uintptr_t)codebook & 15u)) return BCJR_ERR_INVALID_ARG;
   if (w && ((uintptr_t)w & 3u)) return BCJR_ERR_INVALID_ARG;
-  if (!supported(n, k)) return BCJR_ERR_UNSUPPORTED;
+  if (!supported(n, k) || !length_ok(L, n, k)) return BCJR_ERR_UNSUPPORTED;
   return BCJR_OK;
 }
 
@@ -360,7 +371,7 @@ extern "C" {
 
 size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op) {
   if (B < 0 || L < 1 || k < 1 || state_bits < k || state_bits > 16) return 0;
-  if (!supported(state_bits, k)) return 0;
+  if (!supported(state_bits, k) || !length_ok(L, state_bits, k)) return 0;
   if (B == 0) return 0;
   if (op == BCJR_OP_VITERBI) {
     const Family f = family(state_bits, k, false);

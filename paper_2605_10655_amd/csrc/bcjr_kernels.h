@@ -144,10 +144,87 @@ __device__ __forceinline__ void st_vec(float* p, const float (&v)[N]) {
 }
 
 // ---------------------------------------------------------------------------
+// Buffer-resource access.  A descriptor (4 SGPRs) holds the array's base and
+// size; every access gives a per-thread byte offset (one VGPR, fixed for the
+// whole call) and a block-uniform byte offset (an SGPR).  This keeps the
+// per-super-group addresses out of vector registers.
+// ---------------------------------------------------------------------------
+using rsrc_t = __amdgpu_buffer_rsrc_t;
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRsrcFlags = 0x00020000;  // raw (unswizzled) buffer, 32-bit elements
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kRsrcFlags);
+}
+
+// Vector elements are moved through plain scalars: a bit cast applied to an
+// element expression (x.y) reads element 0 with this compiler.
+__device__ __forceinline__ float as_f(unsigned u) { return __uint_as_float(u); }
+__device__ __forceinline__ unsigned as_u(float f) { return __float_as_uint(f); }
+
+template <int N>
+__device__ __forceinline__ void buf_ld(rsrc_t r, uint32_t voff, uint32_t soff, float (&v)[N]) {
+  static_assert(N == 1 || N == 2 || N % 4 == 0, "vector width");
+  if constexpr (N == 1) {
+    v[0] = as_f(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+  } else if constexpr (N == 2) {
+    const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+    const unsigned x0 = x.x, x1 = x.y;
+    v[0] = as_f(x0);
+    v[1] = as_f(x1);
+  } else {
+#pragma unroll
+    for (int q = 0; q < N / 4; ++q) {
+      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)(soff + 16u * q), 0);
+      const unsigned x0 = x.x, x1 = x.y, x2 = x.z, x3 = x.w;
+      v[4 * q + 0] = as_f(x0);
+      v[4 * q + 1] = as_f(x1);
+      v[4 * q + 2] = as_f(x2);
+      v[4 * q + 3] = as_f(x3);
+    }
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void buf_st(rsrc_t r, uint32_t voff, uint32_t soff, const float (&v)[N]) {
+  static_assert(N == 1 || N == 2 || N % 4 == 0, "vector width");
+  if constexpr (N == 1) {
+    __builtin_amdgcn_raw_buffer_store_b32(as_u(v[0]), r, (int)voff, (int)soff, 0);
+  } else if constexpr (N == 2) {
+    const u32x2 x = {as_u(v[0]), as_u(v[1])};
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)voff, (int)soff, 0);
+  } else {
+#pragma unroll
+    for (int q = 0; q < N / 4; ++q) {
+      const u32x4 x = {as_u(v[4 * q + 0]), as_u(v[4 * q + 1]), as_u(v[4 * q + 2]), as_u(v[4 * q + 3])};
+      __builtin_amdgcn_raw_buffer_store_b128(x, r, (int)voff, (int)(soff + 16u * q), 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void pin_u(uint32_t& x) { asm volatile("" : "+v"(x)); }
+
+__device__ __forceinline__ float read_lane(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// One row of a block (w or g) is read 64 entries at a time: lane l of the
+// wave holds row[base + l] (0 past the end); a step takes its entry with a
+// lane read into a scalar register.
+__device__ __forceinline__ float row_chunk(const float* row, int64_t base, int64_t L) {
+  const int64_t i = base + (threadIdx.x & 63);
+  return i < L ? row[i] : 0.f;
+}
+
+// ---------------------------------------------------------------------------
 // Reductions over the TPB threads that own one block.  TPB is a power of two.
 // Below 64 the threads are an aligned lane segment of one wave; above, whole
 // waves, combined through a small LDS area after the caller's barrier.
-// xor butterflies give every lane bitwise-identical results.
+// Within a wave the tree uses DPP lane permutations (quad xor 1, quad xor 2,
+// half-row mirror, row mirror), then the four 16-lane rows are combined in a
+// fixed order; every lane ends with bitwise-identical results.
 // ---------------------------------------------------------------------------
 constexpr int kRed = 8;  // floats per wave in the cross-wave reduction area
 
@@ -158,33 +235,49 @@ struct RedCtx {
   float* red;    // [waves][kRed] floats
 };
 
+template <bool MAX>
+__device__ __forceinline__ float red_op(float a, float b) { return MAX ? fmaxf(a, b) : a + b; }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// all-reduce over aligned segments of `width` lanes (a power of two <= 64)
+template <bool MAX>
+__device__ __forceinline__ float seg_reduce(float v, int width) {
+  if (width >= 2) v = red_op<MAX>(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  if (width >= 4) v = red_op<MAX>(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  if (width >= 8) v = red_op<MAX>(v, dpp<0x141>(v));  // row_half_mirror
+  if (width >= 16) v = red_op<MAX>(v, dpp<0x140>(v)); // row_mirror
+  if (width == 32) v = red_op<MAX>(v, __shfl_xor(v, 16));
+  if (width == 64)
+    v = red_op<MAX>(red_op<MAX>(read_lane(v, 0), read_lane(v, 16)),
+                    red_op<MAX>(read_lane(v, 32), read_lane(v, 48)));
+  return v;
+}
+
 template <int NQ, unsigned MAXMASK>
 __device__ __forceinline__ void red_pre(float (&v)[NQ], const RedCtx& r) {
 #pragma unroll
   for (int q = 0; q < NQ; ++q)
-    for (int off = 1; off < r.width; off <<= 1) {
-      const float o = __shfl_xor(v[q], off);
-      v[q] = ((MAXMASK >> q) & 1u) ? fmaxf(v[q], o) : v[q] + o;
-    }
+    v[q] = ((MAXMASK >> q) & 1u) ? seg_reduce<true>(v[q], r.width) : seg_reduce<false>(v[q], r.width);
   if (r.rw > 1 && r.lane == 0) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) r.red[r.wave * kRed + q] = v[q];
   }
 }
 
-// call after a barrier that follows red_pre
+// call after a barrier that follows red_pre: lane l reads the partial of
+// wave (l mod rw) of its block, and the partials are reduced like a segment
 template <int NQ, unsigned MAXMASK>
 __device__ __forceinline__ void red_post(float (&v)[NQ], const RedCtx& r) {
   if (r.rw > 1) {
-    const int first = (r.wave / r.rw) * r.rw;
+    const int src = (r.wave / r.rw) * r.rw + (r.lane & (r.rw - 1));
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      float acc = r.red[first * kRed + q];
-      for (int i = 1; i < r.rw; ++i) {
-        const float o = r.red[(first + i) * kRed + q];
-        acc = ((MAXMASK >> q) & 1u) ? fmaxf(acc, o) : acc + o;
-      }
-      v[q] = acc;
+      const float x = r.red[src * kRed + q];
+      v[q] = ((MAXMASK >> q) & 1u) ? seg_reduce<true>(x, r.rw) : seg_reduce<false>(x, r.rw);
     }
   }
 }
@@ -278,9 +371,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const int tb = BPW == 1 ? tid : tid - bw * TPB;
   const int64_t L = a.L;
   const float k2 = a.k2;
-  // Addresses are written as (block-uniform base) + (32-bit thread offset) so
-  // that the loads use a scalar base and a single offset register.
-  const uint32_t toK = (uint32_t)tb << KB;  // thread's first super-group * K
 
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
@@ -289,8 +379,26 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   rc.wave = tid >> 6;
   rc.red = lds + (size_t)BPW * 2 * GS;
 
-  float* v0 = lds + (size_t)bw * 2 * GS;  // G (forward) or H (backward)
-  float* v1 = v0 + GS;                    // A or B tangent
+  // LDS: the block's two group vectors v0 = lds[vb ..), v1 = lds[vb + GS ..).
+  // A super-group sg = tb + i*TPB reads / writes two patterns:
+  //   column form  v[j*NSG + sg]  = lds[col + j*NSG + i*TPB]
+  //   row form     v[sg*K + u]    = lds[row + i*TPB*K + u]
+  // col / row (and their +GS twins) are re-pinned every step so the compiler
+  // keeps one base register each and folds the rest into the instruction.
+  const uint32_t vb = (uint32_t)bw * 2 * GS;
+  const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;
+
+  // Codebook row j of super-group i: byte offset (j*S/K + i*TPB*K)*4 + tb*K*4.
+  const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
+  const uint32_t voK = (uint32_t)tb << (KB + 2);
+  // Histories: one descriptor per workgroup over its BPW slots; the block's
+  // slot and the thread's super-group row go into the per-thread offset.
+  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per super-group row
+  const uint32_t hstep = (uint32_t)GS * (VJP ? 2 : 1);   // floats per step
+  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * hrow) * 4u;
+  // w and g of the step: when a block spans whole waves every lane needs the
+  // same value, read 64 steps at a time and taken with a lane read
+  const bool lane_rows = TPB >= 64;
 
   float dcacc[DC ? SGMAX * K * K : 1];
 
@@ -301,9 +409,12 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
     const float* wb = a.w + bb * L;
     const float* gb = VJP ? a.g + bb * L : nullptr;
-    float* hH = VJP ? nullptr : a.histH + slot * L * GS;       // [L][S/K]: H_t
-    float* hHB = VJP ? a.histHB + slot * L * 2 * GS : nullptr;  // [L][S/K/K][2K]: H_t, B_t
-    float* sm_mB = a.small + slot * L;                          // shift applied to H_t
+    // history of each block: soft codeword alone [L][S/K] (H_t); with the VJP
+    // [L][S/K/K][2K] (H_t, B_t of each super-group)
+    const int64_t slot0 = (int64_t)blockIdx.x * BPW;
+    const rsrc_t hist = make_rsrc(VJP ? a.histHB + slot0 * L * hstep : a.histH + slot0 * L * hstep,
+                                  (uint32_t)BPW * (uint32_t)L * hstep * 4u);
+    float* sm_mB = a.small + slot * L;  // shift applied to H_t
 
     // ------------------------------------------------------------------ S0
     // Backward sweep.  Soft codeword alone: H only, v0 / v1 alternating as the
@@ -315,19 +426,43 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // it stays O(quantisation error) in size.  Each thread stores the values
     // its super-groups read (H_t, and B_t for the VJP) as the step's history.
     for (int i = tb; i < GS; i += TPB) {
-      v0[i] = 0.f;
-      if (VJP) v1[i] = 0.f;
+      lds[vb + i] = 0.f;
+      if (VJP) lds[vb + GS + i] = 0.f;
     }
     __syncthreads();
     double shiftB = 0.0;  // sum of the integer shifts of H (exact)
     float lam0 = 0.f;
     float xbar = 0.f;     // VJP: E_p[X_0], see S1
     float offc = 0.f;     // soft codeword alone: shift of the H vector being read
+    float wch = 0.f, gch = 0.f;
+    int64_t cbase = 0;
     for (int64_t t = L - 1;; --t) {
-      const float wt = wb[t];
-      const float gt = VJP ? gb[t] : 0.f;
-      float* cur = (!VJP && ((L - 1 - t) & 1)) ? v1 : v0;
-      float* nxt = ((L - 1 - t) & 1) ? v0 : v1;
+      float wt, gt = 0.f;
+      if (lane_rows) {
+        if (t == L - 1 || (t & 63) == 63) {
+          cbase = t & ~(int64_t)63;
+          wch = row_chunk(wb, cbase, L);
+          if (VJP) gch = row_chunk(gb, cbase, L);
+        }
+        wt = read_lane(wch, (int)(t - cbase));
+        if (VJP) gt = read_lane(gch, (int)(t - cbase));
+      } else {
+        wt = wb[t];
+        if (VJP) gt = gb[t];
+      }
+      // read side: the vector holding H_t (row form); write side: column form
+      const bool odd = !VJP && ((L - 1 - t) & 1);
+      uint32_t rrow = row0 + (odd ? GS : 0), rrowB = row0 + GS;
+      uint32_t wcol = col0 + (odd ? 0 : GS), wcolB = col0 + GS;
+      pin_u(rrow);
+      pin_u(wcol);
+      if (VJP) {
+        pin_u(rrowB);
+        wcol = col0;
+        pin_u(wcol);
+        pin_u(wcolB);
+      }
+      const uint32_t soH = (uint32_t)t * hstep * 4u;
       if (t == 0) {
         // lambda_0 = LSE_s [h_0(s) + H_0(s & (S/K-1))]  (log2 alpha_0 = h_0);
         // with the VJP also E_p[g_0 c(s_0) + B_0(s_0)], the mean of X_0
@@ -335,23 +470,22 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
-            const int sg = tb + i * TPB;
             float Hin[K], Bin[K];
 #pragma unroll
             for (int b = 0; b < K; ++b) {
-              Hin[b] = cur[sg * K + b] - offc;
-              Bin[b] = VJP ? v1[sg * K + b] : 0.f;
+              Hin[b] = lds[rrow + i * TPB * K + b] - offc;
+              Bin[b] = VJP ? lds[rrowB + i * TPB * K + b] : 0.f;
             }
             if constexpr (VJP) {
-              st_vec<K>(hHB + ((i * TPB) << (KB + 1)) + 2 * toK, Hin);
-              st_vec<K>(hHB + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bin);
+              buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)), Hin);
+              buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)) + 4 * K, Bin);
             } else {
-              st_vec<K>(hH + ((i * TPB) << KB) + toK, Hin);
+              buf_st<K>(hist, voH, ((i * TPB) << (KB + 2)), Hin);
             }
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               float cc[K];
-              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+              buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
               float x[K];
 #pragma unroll
               for (int b = 0; b < K; ++b) {
@@ -401,23 +535,22 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
-          const int sg = tb + i * TPB;
           float Hin[K], Bin[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) {
-            Hin[b] = cur[sg * K + b] - offc;
-            Bin[b] = VJP ? v1[sg * K + b] : 0.f;
+            Hin[b] = lds[rrow + i * TPB * K + b] - offc;
+            Bin[b] = VJP ? lds[rrowB + i * TPB * K + b] : 0.f;
           }
           if constexpr (VJP) {
-            st_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Hin);
-            st_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bin);
+            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)), Hin);
+            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bin);
           } else {
-            st_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
+            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 2)), Hin);
           }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             float cc[K];
-            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
+            buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
             float x[K], d[K];
 #pragma unroll
             for (int b = 0; b < K; ++b) {
@@ -443,7 +576,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               Bout[i][j] = num * rcp(s);
               pin(Bout[i][j]);
             } else {
-              nxt[j * NSG + sg] = h;
+              lds[wcol + j * NSG + i * TPB] = h;
             }
           }
           sg_fence();
@@ -459,11 +592,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
-            const int sg = tb + i * TPB;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              v0[j * NSG + sg] = Hout[i][j] - off;
-              v1[j * NSG + sg] = Bout[i][j];
+              lds[wcol + j * NSG + i * TPB] = Hout[i][j] - off;
+              lds[wcolB + j * NSG + i * TPB] = Bout[i][j];
             }
           }
         }
@@ -487,8 +619,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // so that dW_t = (sum p c X - w_soft_t sum p X) / (T sum p) and the
     // dCodebook summands p (g + (w - c) X / T) see a nearly centred X.
     for (int i = tb; i < GS; i += TPB) {
-      v0[i] = 0.f;
-      if (VJP) v1[i] = 0.f;
+      lds[vb + i] = 0.f;
+      if (VJP) lds[vb + GS + i] = 0.f;
     }
     if constexpr (DC) {
 #pragma unroll
@@ -498,9 +630,29 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     const float invT = a.invT;
     float lam_est = lam0;
     for (int64_t t = 0; t < L; ++t) {
-      const float wt = wb[t];
-      const float gt = VJP ? gb[t] : 0.f;
+      float wt, gt = 0.f;
+      if (lane_rows) {
+        if ((t & 63) == 0) {
+          cbase = t;
+          wch = row_chunk(wb, cbase, L);
+          if (VJP) gch = row_chunk(gb, cbase, L);
+        }
+        wt = read_lane(wch, (int)(t - cbase));
+        if (VJP) gt = read_lane(gch, (int)(t - cbase));
+      } else {
+        wt = wb[t];
+        if (VJP) gt = gb[t];
+      }
+      if (VJP && t > 0) xbar = fmaf(gt, wt, xbar);  // B_t no longer holds step t
       const float mBt = sm_mB[t];
+      uint32_t rcol = col0, rcolA = col0 + GS, wrow = row0, wrowA = row0 + GS;
+      pin_u(rcol);
+      pin_u(wrow);
+      if (VJP) {
+        pin_u(rcolA);
+        pin_u(wrowA);
+      }
+      const uint32_t soH = (uint32_t)t * hstep * 4u;
       float Gout[SGMAX][K];
       float Aout[VJP ? SGMAX : 1][K];
       // max G_{t+1}, sum p, sum p c, and with the VJP sum p X, sum p c X
@@ -511,23 +663,22 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
-          const int sg = tb + i * TPB;
           float Gin[K], Ain[K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            Gin[j] = v0[j * NSG + sg];
-            Ain[j] = VJP ? v1[j * NSG + sg] : 0.f;
+            Gin[j] = lds[rcol + j * NSG + i * TPB];
+            Ain[j] = VJP ? lds[rcolA + j * NSG + i * TPB] : 0.f;
           }
           float Hc[K], Bc[K];
           if constexpr (VJP) {
-            ld_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + 2 * toK, Hc);
-            ld_vec<K>(hHB + t * 2 * GS + ((i * TPB) << (KB + 1)) + K + 2 * toK, Bc);
+            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 3)), Hc);
+            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bc);
           } else {
-            ld_vec<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
+            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 2)), Hc);
           }
           float cc[K][K];
 #pragma unroll
-          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
+          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             float al[K];
@@ -595,16 +746,15 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
-            const int sg = tb + i * TPB;
             float go[K];
 #pragma unroll
             for (int u = 0; u < K; ++u) go[u] = Gout[i][u] - off;
-            st_vec<K>(v0 + sg * K, go);
+            st_vec<K>(lds + wrow + i * TPB * K, go);
             if constexpr (VJP) {
               float ao[K];
 #pragma unroll
               for (int u = 0; u < K; ++u) ao[u] = fmaf(-gt, wst, Aout[i][u]);
-              st_vec<K>(v1 + sg * K, ao);
+              st_vec<K>(lds + wrowA + i * TPB * K, ao);
             }
           }
         }
@@ -614,11 +764,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         if (VJP && a.dW) a.dW[bb * L + t] = (rv[VJP ? 4 : 0] - wst * rv[VJP ? 3 : 0]) * r1 * invT;
       }
       lam_est = lamt - off + mBt;
-      if constexpr (VJP) {
-        // E_p[X_t] = xbar + sum p X / sum p; X_{t+1} drops g_t w_soft_t (A is
-        // centred) and gains g_{t+1} w_{t+1} (B_{t+1} no longer holds step t+1)
-        if (t < L - 1) xbar = fmaf(rv[3], r1, xbar) - gt * wst + gb[t + 1] * wb[t + 1];
-      }
+      // E_p[X_t] = xbar + sum p X / sum p; X_{t+1} drops g_t w_soft_t (A is
+      // centred); it gains g_{t+1} w_{t+1} at the top of the next step
+      if (VJP) xbar = fmaf(rv[VJP ? 3 : 0], r1, xbar) - gt * wst;
       __syncthreads();
     }
 
@@ -631,7 +779,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           if (i < SGT) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
+              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + ((uint32_t)tb << KB);
               if (first) {
 #pragma unroll
                 for (int u = 0; u < K; ++u) pj[u] = (double)dcacc[(i * K + j) * K + u];
