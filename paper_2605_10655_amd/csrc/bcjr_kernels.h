@@ -204,6 +204,14 @@ __device__ __forceinline__ void buf_st(rsrc_t r, uint32_t voff, uint32_t soff, c
   }
 }
 
+// History row of one super-group: H (and B after it with the VJP).
+template <int K, bool VJP>
+__device__ __forceinline__ void hist_row(rsrc_t h, uint32_t voff, uint32_t step_off, uint32_t sg_off,
+                                         uint32_t, float (&H)[K], float (&B)[K]) {
+  buf_ld<K>(h, voff, step_off + sg_off, H);
+  if constexpr (VJP) buf_ld<K>(h, voff, step_off + sg_off + 4 * K, B);
+}
+
 __device__ __forceinline__ void pin_u(uint32_t& x) { asm volatile("" : "+v"(x)); }
 
 __device__ __forceinline__ float read_lane(float v, int lane) {
@@ -535,6 +543,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
+          float cc[K][K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
           float Hin[K], Bin[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) {
@@ -549,12 +560,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            float cc[K];
-            buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
             float x[K], d[K];
 #pragma unroll
             for (int b = 0; b < K; ++b) {
-              d[b] = wt - cc[b];
+              d[b] = wt - cc[j][b];
               x[b] = Hin[b] - d[b] * d[b] * k2;
             }
             const float m = max_of<K>(x);
@@ -629,6 +638,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     __syncthreads();
     const float invT = a.invT;
     float lam_est = lam0;
+    // The history row of the next super-group is loaded one super-group
+    // ahead (the last super-group of a step fetches the first of the next
+    // step, so that HBM read is in flight across the barriers).
+    float pH[K], pB[K];
+    hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
     for (int64_t t = 0; t < L; ++t) {
       float wt, gt = 0.f;
       if (lane_rows) {
@@ -652,7 +666,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         pin_u(rcolA);
         pin_u(wrowA);
       }
-      const uint32_t soH = (uint32_t)t * hstep * 4u;
       float Gout[SGMAX][K];
       float Aout[VJP ? SGMAX : 1][K];
       // max G_{t+1}, sum p, sum p c, and with the VJP sum p X, sum p c X
@@ -669,16 +682,19 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             Gin[j] = lds[rcol + j * NSG + i * TPB];
             Ain[j] = VJP ? lds[rcolA + j * NSG + i * TPB] : 0.f;
           }
-          float Hc[K], Bc[K];
-          if constexpr (VJP) {
-            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 3)), Hc);
-            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bc);
-          } else {
-            buf_ld<K>(hist, voH, soH + ((i * TPB) << (KB + 2)), Hc);
+          float Hc[K], Bc[K], cc[K][K];
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            Hc[u] = pH[u];
+            Bc[u] = VJP ? pB[u] : 0.f;
           }
-          float cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
+          // (a select, not a branch: at t = L - 1 it re-reads row t, unused)
+          const bool last = i + 1 >= SGT;
+          const int64_t tn = last && t + 1 < L ? t + 1 : t;
+          hist_row<K, VJP>(hist, voH, (uint32_t)tn * hstep * 4u,
+                           last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, hstep, pH, pB);
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             float al[K];
@@ -731,6 +747,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
                 }
               }
             }
+            __builtin_amdgcn_sched_barrier(0);  // one output group at a time
           }
           sg_fence();
         }
