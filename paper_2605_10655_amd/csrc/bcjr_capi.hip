@@ -94,6 +94,10 @@ bool length_ok(int64_t L, int n, int k) {
   return true;
 }
 
+// The fp32 forward-backward path keeps the scaled codebook at the front of
+// its workspace.
+size_t cs_bytes(int n) { return align_up(((size_t)4) << n); }
+
 struct FbLayout {
   size_t hist, small, dc, slot;
 };
@@ -335,17 +339,27 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (!fn) return BCJR_ERR_UNSUPPORTED;
   const size_t lds = fb_lds_bytes(f, n, k);
   int herr = 0;
-  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, lay.slot, &herr);
+  if (ws_bytes < cs_bytes(n)) return BCJR_ERR_WORKSPACE;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes - cs_bytes(n), lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
   const int64_t slots = grid * f.bpw;
-  char* base = static_cast<char*>(workspace);
+  const int64_t S = (int64_t)1 << n;
+  // [scaled codebook][slots: histories][slots: shifts][slots: dCodebook partials]
+  float* cs = static_cast<float*>(workspace);
+  char* base = static_cast<char*>(workspace) + cs_bytes(n);
   FbArgs a = {};
-  a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
+  a.w = w; a.g = g; a.c = codebook; a.cs = cs; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   const double Td = (double)T;
   a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
   a.invT = (float)(1.0 / Td);
+  a.kap = (float)std::sqrt(1.4426950408889634074 / (2.0 * Td));
+  a.inv_kap = (float)(1.0 / (double)a.kap);
+  a.dws = (float)(1.0 / ((double)a.kap * (double)a.kap * Td));
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  hipLaunchKernelGGL(scale_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, codebook,
+                     a.kap, cs, S);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   a.histH = vjp ? nullptr : reinterpret_cast<float*>(base);
   a.histHB = vjp ? reinterpret_cast<float*>(base) : nullptr;
   a.small = reinterpret_cast<float*>(base + slots * lay.hist);
@@ -353,7 +367,6 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {
-    const int64_t S = (int64_t)1 << n;
     const int64_t used = slots < B ? slots : B;
     hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
                        a.dc_part, used, S, dCodebook);
@@ -386,7 +399,7 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
   const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
-  size_t bytes = (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
+  size_t bytes = cs_bytes(state_bits) + (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
     const Family fh = family_hp(state_bits, k, true);
     const int64_t gh = std::min<int64_t>(ceil_div(B, fh.bpw), (int64_t)kDeviceCUs * fh.occ_est);

@@ -9,11 +9,14 @@ struct FbArgs {
   const float* w;      // [B, L]
   const float* g;      // [B, L] upstream gradient (VJP only)
   const float* c;      // [S] codebook
+  const float* cs;     // [S] codebook times kappa (fp32 forward-backward kernel)
   int64_t B, L;
   int n;               // state bits
   int sgt;             // super-groups per thread
   float k2;            // log2(e) / (2T): h_t(s) in log2 units = -(w_t - c(s))^2 * k2
   float invT;          // 1 / T
+  float kap, inv_kap;  // kappa = sqrt(k2) and 1 / kappa
+  float dws;           // 1 / (kappa^2 T)
   float* w_soft;       // [B, L] or null
   float* logZ;         // [B] or null
   float* dW;           // [B, L] or null

@@ -378,7 +378,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const int bw = BPW == 1 ? 0 : tid / TPB;
   const int tb = BPW == 1 ? tid : tid - bw * TPB;
   const int64_t L = a.L;
-  const float k2 = a.k2;
+  // Emissions use the codebook scaled by kappa = sqrt(log2(e) / (2T)):
+  // h_t(s) in log2 units is -(w'_t - c'(s))^2 with w' = kappa w, c' = kappa c.
+  // Soft codeword and tangents are carried in scaled units as well.
+  const float kap = a.kap;
 
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
@@ -397,7 +400,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;
 
   // Codebook row j of super-group i: byte offset (j*S/K + i*TPB*K)*4 + tb*K*4.
-  const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
+  const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)4 << n);
   const uint32_t voK = (uint32_t)tb << (KB + 2);
   // Histories: one descriptor per workgroup over its BPW slots; the block's
   // slot and the thread's super-group row go into the per-thread offset.
@@ -458,6 +461,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         wt = wb[t];
         if (VJP) gt = gb[t];
       }
+      wt *= kap;
       // read side: the vector holding H_t (row form); write side: column form
       const bool odd = !VJP && ((L - 1 - t) & 1);
       uint32_t rrow = row0 + (odd ? GS : 0), rrowB = row0 + GS;
@@ -478,12 +482,16 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
-            float Hin[K], Bin[K];
+            float Hin[K], Bin[K];  // row form: one 16-byte LDS read per K floats
+            ld_vec<K>(lds + rrow + i * TPB * K, Hin);
+            if constexpr (VJP) {
+              ld_vec<K>(lds + rrowB + i * TPB * K, Bin);
+            } else {
 #pragma unroll
-            for (int b = 0; b < K; ++b) {
-              Hin[b] = lds[rrow + i * TPB * K + b] - offc;
-              Bin[b] = VJP ? lds[rrowB + i * TPB * K + b] : 0.f;
+              for (int b = 0; b < K; ++b) Bin[b] = 0.f;
             }
+#pragma unroll
+            for (int b = 0; b < K; ++b) Hin[b] -= offc;
             if constexpr (VJP) {
               buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)), Hin);
               buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)) + 4 * K, Bin);
@@ -498,7 +506,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
               for (int b = 0; b < K; ++b) {
                 const float d = wt - cc[b];
-                x[b] = Hin[b] - d * d * k2;
+                x[b] = fmaf(-d, d, Hin[b]);
               }
               const float m = max_of<K>(x);
               float E[K];
@@ -546,12 +554,16 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           float cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
-          float Hin[K], Bin[K];
+          float Hin[K], Bin[K];  // row form: one 16-byte LDS read per K floats
+          ld_vec<K>(lds + rrow + i * TPB * K, Hin);
+          if constexpr (VJP) {
+            ld_vec<K>(lds + rrowB + i * TPB * K, Bin);
+          } else {
 #pragma unroll
-          for (int b = 0; b < K; ++b) {
-            Hin[b] = lds[rrow + i * TPB * K + b] - offc;
-            Bin[b] = VJP ? lds[rrowB + i * TPB * K + b] : 0.f;
+            for (int b = 0; b < K; ++b) Bin[b] = 0.f;
           }
+#pragma unroll
+          for (int b = 0; b < K; ++b) Hin[b] -= offc;
           if constexpr (VJP) {
             buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)), Hin);
             buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bin);
@@ -564,7 +576,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
             for (int b = 0; b < K; ++b) {
               d[b] = wt - cc[j][b];
-              x[b] = Hin[b] - d[b] * d[b] * k2;
+              x[b] = fmaf(-d[b], d[b], Hin[b]);
             }
             const float m = max_of<K>(x);
             float E[K];
@@ -626,7 +638,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // where xbar_t predicts E_p[X_t] (exact at t = 0 from S0, then carried by
     // the known change of the centring constants and re-anchored each step),
     // so that dW_t = (sum p c X - w_soft_t sum p X) / (T sum p) and the
-    // dCodebook summands p (g + (w - c) X / T) see a nearly centred X.
+    // dCodebook summands p (g + (w - c) X / T) see a nearly centred X.  In
+    // the scaled units used here c, w_soft and X carry a factor kappa, hence
+    // the 1 / (kappa^2 T) of both formulas.
     for (int i = tb; i < GS; i += TPB) {
       lds[vb + i] = 0.f;
       if (VJP) lds[vb + GS + i] = 0.f;
@@ -636,7 +650,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
     }
     __syncthreads();
-    const float invT = a.invT;
+    const float dws = a.dws;  // 1 / (kappa^2 T): scaled covariances -> dW, dCodebook
     float lam_est = lam0;
     // The history row of the next super-group is loaded one super-group
     // ahead (the last super-group of a step fetches the first of the next
@@ -657,6 +671,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         wt = wb[t];
         if (VJP) gt = gb[t];
       }
+      wt *= kap;
       if (VJP && t > 0) xbar = fmaf(gt, wt, xbar);  // B_t no longer holds step t
       const float mBt = sm_mB[t];
       uint32_t rcol = col0, rcolA = col0 + GS, wrow = row0, wrowA = row0 + GS;
@@ -701,7 +716,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               const float d = wt - cc[j][u];
-              al[j] = Gin[j] - d * d * k2;
+              al[j] = fmaf(-d, d, Gin[j]);
             }
             const float m = max_of<K>(al);
             float E[K];
@@ -743,7 +758,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
                 for (int j = 0; j < K; ++j) {
                   const float X = fmaf(gt, cc[j][u], Ain[j]) + bx;
                   dcacc[(i * K + j) * K + u] =
-                      fmaf(E[j] * fac, fmaf((wt - cc[j][u]) * X, invT, gt), dcacc[(i * K + j) * K + u]);
+                      fmaf(E[j] * fac, fmaf((wt - cc[j][u]) * X, dws, gt), dcacc[(i * K + j) * K + u]);
                 }
               }
             }
@@ -777,8 +792,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         }
       }
       if (tb == 0 && valid) {
-        if (a.w_soft) a.w_soft[bb * L + t] = wst;
-        if (VJP && a.dW) a.dW[bb * L + t] = (rv[VJP ? 4 : 0] - wst * rv[VJP ? 3 : 0]) * r1 * invT;
+        if (a.w_soft) a.w_soft[bb * L + t] = wst * a.inv_kap;
+        if (VJP && a.dW) a.dW[bb * L + t] = (rv[VJP ? 4 : 0] - wst * rv[VJP ? 3 : 0]) * r1 * dws;
       }
       lam_est = lamt - off + mBt;
       // E_p[X_t] = xbar + sum p X / sum p; X_{t+1} drops g_t w_soft_t (A is
@@ -1258,6 +1273,12 @@ __global__ void dc_reduce_kernel(const double* part, int64_t nslots, int64_t S, 
   double acc = 0.0;
   for (int64_t q = 0; q < nslots; ++q) acc += part[q * S + s];
   out[s] = (float)acc;
+}
+
+// c'(s) = kappa c(s): the codebook in the scaled units of fb_kernel.
+__global__ void scale_kernel(const float* c, float kap, float* cs, int64_t S) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < S) cs[i] = c[i] * kap;
 }
 
 __global__ void fill_kernel(float* out, int64_t count, float v) {
