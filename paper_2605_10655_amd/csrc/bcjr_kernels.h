@@ -415,6 +415,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   // w and g of the step: when a block spans whole waves every lane needs the
   // same value, read 64 steps at a time and taken with a lane read
   const bool lane_rows = TPB >= 64;
+  constexpr bool PF = !DC;  // forward-sweep prefetches
 
   float dcacc[DC ? SGMAX * K * K : 1];
 
@@ -675,11 +676,14 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // The history row of the next super-group is loaded one super-group
     // ahead (the last super-group of a step fetches the first of the next
     // step, so that HBM read is in flight across the barriers).
+    // (not with dCodebook, whose per-state accumulators need the registers)
     float pH[K], pB[K];
-    hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
     float p0[K][K];  // codebook rows of the first super-group, fetched a step ahead
+    if constexpr (PF) {
+      hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
 #pragma unroll
-    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+      for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+    }
     for (int64_t t = 0; t < L; ++t) {
       float wt, gt = 0.f;
       if (lane_rows) {
@@ -721,12 +725,17 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             Ain[j] = VJP ? lds[rcolA + j * NSG + i * TPB] : 0.f;
           }
           float Hc[K], Bc[K], cc[K][K];
+          if constexpr (PF) {
 #pragma unroll
-          for (int u = 0; u < K; ++u) {
-            Hc[u] = pH[u];
-            Bc[u] = VJP ? pB[u] : 0.f;
+            for (int u = 0; u < K; ++u) {
+              Hc[u] = pH[u];
+              Bc[u] = VJP ? pB[u] : 0.f;
+            }
+          } else {
+            hist_row<K, VJP>(hist, voH, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u, hstep,
+                             Hc, Bc);
           }
-          if (i == 0) {
+          if (PF && i == 0) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
 #pragma unroll
@@ -736,15 +745,17 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
           }
-          if (i + 1 >= SGT) {
+          if constexpr (PF) {
+            if (i + 1 >= SGT) {
 #pragma unroll
-            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+              for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+            }
+            // (a select, not a branch: at t = L - 1 it re-reads row t, unused)
+            const bool last = i + 1 >= SGT;
+            const int64_t tn = last && t + 1 < L ? t + 1 : t;
+            hist_row<K, VJP>(hist, voH, (uint32_t)tn * hstep * 4u,
+                             last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, hstep, pH, pB);
           }
-          // (a select, not a branch: at t = L - 1 it re-reads row t, unused)
-          const bool last = i + 1 >= SGT;
-          const int64_t tn = last && t + 1 < L ? t + 1 : t;
-          hist_row<K, VJP>(hist, voH, (uint32_t)tn * hstep * 4u,
-                           last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, hstep, pH, pB);
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             float al[K];
