@@ -44,13 +44,10 @@ Family family(int n, int k, bool dc) {
     f.nt = 256; f.sgmax = 1; f.sgt = 1; f.occ_est = 8;
   } else if (nsg <= 2048) {
     f.nt = 256; f.sgt = nsg / 256; f.sgmax = f.sgt; f.occ_est = 4;
-  } else if (!dc) {
-    f.nt = 1024; f.sgt = nsg / 1024; f.sgmax = f.sgt; f.occ_est = 1;
   } else {
-    // 4 KB super-groups with per-state dCodebook accumulators: 512 threads
-    // (two waves per SIMD) leave room for 8 x K^2 accumulators per thread
-    f.nt = 512; f.sgt = nsg / 512; f.sgmax = f.sgt; f.occ_est = 1;
+    f.nt = 1024; f.sgt = nsg / 1024; f.sgmax = f.sgt; f.occ_est = 1;
   }
+  (void)dc;  // dCodebook runs as a separate sweep: same family
   const int tpb = nsg / f.sgt;
   f.bpw = f.nt / tpb;
   return f;
@@ -99,7 +96,7 @@ bool length_ok(int64_t L, int n, int k) {
 size_t cs_bytes(int n) { return align_up(((size_t)4) << n); }
 
 struct FbLayout {
-  size_t hist, small, dc, slot;
+  size_t hist, histGA, small, dc, slot;
 };
 
 struct HpLayout {
@@ -125,13 +122,14 @@ size_t hp_lds_bytes(const Family& f, int n, int k) {
          (size_t)(f.nt / 64) * (4 * sizeof(double) + kRed * sizeof(float));
 }
 
-FbLayout fb_layout(int64_t L, int n, int k, bool vjp) {
+FbLayout fb_layout(int64_t L, int n, int k, bool vjp, bool dc) {
   const size_t gs = (size_t)1 << (n - k);
   FbLayout l;
   l.hist = align_up((size_t)L * (vjp ? 2 : 1) * gs * sizeof(float));
-  l.small = align_up((size_t)L * sizeof(float));
-  l.dc = vjp ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
-  l.slot = l.hist + l.small + l.dc;
+  l.histGA = dc ? align_up((size_t)L * 2 * gs * sizeof(float)) : 0;
+  l.small = align_up((size_t)3 * L * sizeof(float));
+  l.dc = dc ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
+  l.slot = l.hist + l.histGA + l.small + l.dc;
   return l;
 }
 
@@ -169,18 +167,14 @@ template <int KB>
 FbFn fb_pick_kb(int n, const Family& f, bool vjp, bool dc) {
   if (f.sgmax == 1) return fb_variant<KB, 0, 1, 256>(vjp, dc);
   if constexpr (KB < 3) {
-    // nsg = 2^(n - 2KB): 512, 1024, 2048 -> 256 threads; 4096 -> 1024, or
-    // 512 with dCodebook
+    // nsg = 2^(n - 2KB): 512, 1024, 2048 -> 256 threads; 4096 -> 1024
     constexpr int n512 = 2 * KB + 9;
     if (f.nt == 256) {
       if (n == n512) return fb_variant<KB, n512, 2, 256>(vjp, dc);
       if (n == n512 + 1) return fb_variant<KB, n512 + 1, 4, 256>(vjp, dc);
       if (n == n512 + 2) return fb_variant<KB, n512 + 2, 8, 256>(vjp, dc);
     }
-    if (n == n512 + 3) {
-      if (f.nt == 1024) return fb_variant<KB, n512 + 3, 4, 1024>(vjp, dc);
-      if (f.nt == 512 && dc) return fb_kernel<KB, n512 + 3, 8, 512, true, true>;
-    }
+    if (n == n512 + 3 && f.nt == 1024) return fb_variant<KB, n512 + 3, 4, 1024>(vjp, dc);
   }
   return nullptr;
 }
@@ -334,7 +328,7 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
   const Family f = family(n, k, dc);
-  const FbLayout lay = fb_layout(L, n, k, vjp);
+  const FbLayout lay = fb_layout(L, n, k, vjp, dc);
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
   const size_t lds = fb_lds_bytes(f, n, k);
@@ -362,8 +356,10 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   a.histH = vjp ? nullptr : reinterpret_cast<float*>(base);
   a.histHB = vjp ? reinterpret_cast<float*>(base) : nullptr;
-  a.small = reinterpret_cast<float*>(base + slots * lay.hist);
-  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.small)) : nullptr;
+  a.histGA = dc ? reinterpret_cast<float*>(base + slots * lay.hist) : nullptr;
+  a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
+  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
+                 : nullptr;
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {
@@ -399,7 +395,7 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
   const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
-  size_t bytes = cs_bytes(state_bits) + (size_t)slots * fb_layout(L, state_bits, k, vjp).slot;
+  size_t bytes = cs_bytes(state_bits) + (size_t)slots * fb_layout(L, state_bits, k, vjp, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
     const Family fh = family_hp(state_bits, k, true);
     const int64_t gh = std::min<int64_t>(ceil_div(B, fh.bpw), (int64_t)kDeviceCUs * fh.occ_est);

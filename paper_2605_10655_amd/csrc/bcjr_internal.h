@@ -23,7 +23,8 @@ struct FbArgs {
   double* dc_part;     // [slots][S] fp64 partial sums of dCodebook, or null
   float* histH;        // [slots][L][S/K]   H_t as read by each super-group (soft codeword)
   float* histHB;       // [slots][L][2 S/K] H_t and the B tangent per super-group (VJP)
-  float* small;        // [slots][L]        shifts of H
+  float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group (dCodebook)
+  float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
   // high-precision variant (fp64 log vectors)
   double k2d;          // log2(e) / (2T) in fp64
   double* histHd;      // [slots][L][S/K] fp64

@@ -415,9 +415,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   // w and g of the step: when a block spans whole waves every lane needs the
   // same value, read 64 steps at a time and taken with a lane read
   const bool lane_rows = TPB >= 64;
-  constexpr bool PF = !DC;  // forward-sweep prefetches
+  constexpr bool PF = true;  // forward-sweep prefetches
 
-  float dcacc[DC ? SGMAX * K * K : 1];
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
     const int64_t blk = base + bw;
@@ -431,7 +430,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     const int64_t slot0 = (int64_t)blockIdx.x * BPW;
     const rsrc_t hist = make_rsrc(VJP ? a.histHB + slot0 * L * hstep : a.histH + slot0 * L * hstep,
                                   (uint32_t)BPW * (uint32_t)L * hstep * 4u);
-    float* sm_mB = a.small + slot * L;  // shift applied to H_t
+    float* sm_mB = a.small + slot * 3 * L;  // shift applied to H_t
+    float* sm_lam = sm_mB + L;              // dCodebook: lambda_t
+    float* sm_xb = sm_lam + L;              // dCodebook: E_p[X_t]
+    const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * L * hstep : a.histHB,
+                                 DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
 
     // ------------------------------------------------------------------ S0
     // Backward sweep.  Soft codeword alone: H only, v0 / v1 alternating as the
@@ -666,17 +669,12 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       lds[vb + i] = 0.f;
       if (VJP) lds[vb + GS + i] = 0.f;
     }
-    if constexpr (DC) {
-#pragma unroll
-      for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
-    }
     __syncthreads();
     const float dws = a.dws;  // 1 / (kappa^2 T): scaled covariances -> dW, dCodebook
     float lam_est = lam0;
     // The history row of the next super-group is loaded one super-group
     // ahead (the last super-group of a step fetches the first of the next
     // step, so that HBM read is in flight across the barriers).
-    // (not with dCodebook, whose per-state accumulators need the registers)
     float pH[K], pB[K];
     float p0[K][K];  // codebook rows of the first super-group, fetched a step ahead
     if constexpr (PF) {
@@ -723,6 +721,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           for (int j = 0; j < K; ++j) {
             Gin[j] = lds[rcol + j * NSG + i * TPB];
             Ain[j] = VJP ? lds[rcolA + j * NSG + i * TPB] : 0.f;
+          }
+          if constexpr (DC) {  // (G_t, A_t) row of the super-group for the dCodebook sweep
+            const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
+            buf_st<K>(hga, voH, so, Gin);
+            buf_st<K>(hga, voH, so + 4 * K, Ain);
           }
           float Hc[K], Bc[K], cc[K][K];
           if constexpr (PF) {
@@ -799,14 +802,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               rv[4] = fmaf(fac, fmaf(sc, bx, scy), rv[4]);
               Aout[i][u] = sy * rcp(s);
               pin(Aout[i][u]);
-              if constexpr (DC) {
-#pragma unroll
-                for (int j = 0; j < K; ++j) {
-                  const float X = fmaf(gt, cc[j][u], Ain[j]) + bx;
-                  dcacc[(i * K + j) * K + u] =
-                      fmaf(E[j] * fac, fmaf((wt - cc[j][u]) * X, dws, gt), dcacc[(i * K + j) * K + u]);
-                }
-              }
             }
             __builtin_amdgcn_sched_barrier(0);  // one output group at a time
           }
@@ -837,6 +832,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
         }
       }
+      if (DC && tb == 0) {
+        sm_lam[t] = lamt;
+        sm_xb[t] = fmaf(rv[VJP ? 3 : 0], r1, xbar);
+      }
       if (tb == 0 && valid) {
         if (a.w_soft) a.w_soft[bb * L + t] = wst * a.inv_kap;
         if (VJP && a.dW) a.dW[bb * L + t] = (rv[VJP ? 4 : 0] - wst * rv[VJP ? 3 : 0]) * r1 * dws;
@@ -848,28 +847,97 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       __syncthreads();
     }
 
+    // ------------------------------------------------------------------ S2
+    // dCodebook: dc(s) = sum_t p_t(s) [g_t + (w_t - c(s)) (X_t(s) - E_p[X_t]) / T].
+    // No recursion is left, so each thread runs super-group by super-group
+    // over all steps with 16 accumulators: p_t(s) = 2^(G_t + h_t + H_t -
+    // lambda_t) per state from the (G, A) and (H, B) histories, with the exact
+    // lambda_t and E_p[X_t] recorded by S1.
     if constexpr (DC) {
-      if (valid) {
-        const bool first = base == (int64_t)blockIdx.x * BPW;
-        double* part = a.dc_part + slot * ((int64_t)1 << n);
+      __syncthreads();  // S1's per-step scalars
+      const bool first = base == (int64_t)blockIdx.x * BPW;
+      double* part = a.dc_part + slot * ((int64_t)1 << n);
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        float cc[K][K], acc[K][K];
 #pragma unroll
-        for (int i = 0; i < SGMAX; ++i) {
-          if (i < SGT) {
+        for (int j = 0; j < K; ++j) {
+          buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
+#pragma unroll
+          for (int u = 0; u < K; ++u) acc[j][u] = 0.f;
+        }
+        float lch = 0.f, xch = 0.f;
+        // the four history rows of a step, loaded one step ahead
+        float nH[K], nB[K], nG[K], nA[K];
+        {
+          const uint32_t so = (uint32_t)i * TPB * hrow * 4u;
+          buf_ld<K>(hist, voH, so, nH);
+          buf_ld<K>(hist, voH, so + 4 * K, nB);
+          buf_ld<K>(hga, voH, so, nG);
+          buf_ld<K>(hga, voH, so + 4 * K, nA);
+        }
+#pragma unroll 1
+        for (int64_t t = 0; t < L; ++t) {
+          float wt, gt, lt, xt;
+          if (lane_rows) {
+            if ((t & 63) == 0) {
+              cbase = t;
+              wch = row_chunk(wb, cbase, L);
+              gch = row_chunk(gb, cbase, L);
+              lch = row_chunk(sm_lam, cbase, L);
+              xch = row_chunk(sm_xb, cbase, L);
+            }
+            const int ln = (int)(t - cbase);
+            wt = read_lane(wch, ln);
+            gt = read_lane(gch, ln);
+            lt = read_lane(lch, ln);
+            xt = read_lane(xch, ln);
+          } else {
+            wt = wb[t];
+            gt = gb[t];
+            lt = sm_lam[t];
+            xt = sm_xb[t];
+          }
+          wt *= kap;
+          float H[K], Bv[K], G[K], A[K];
+#pragma unroll
+          for (int q = 0; q < K; ++q) {
+            H[q] = nH[q];
+            Bv[q] = nB[q];
+            G[q] = nG[q];
+            A[q] = nA[q];
+          }
+          {  // (a select, not a branch: the last step re-reads its own rows)
+            const int64_t tn = t + 1 < L ? t + 1 : t;
+            const uint32_t so = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
+            buf_ld<K>(hist, voH, so, nH);
+            buf_ld<K>(hist, voH, so + 4 * K, nB);
+            buf_ld<K>(hga, voH, so, nG);
+            buf_ld<K>(hga, voH, so + 4 * K, nA);
+          }
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            const float hb = H[u] - lt, bx = Bv[u] - xt;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + ((uint32_t)tb << KB);
-              if (first) {
-#pragma unroll
-                for (int u = 0; u < K; ++u) pj[u] = (double)dcacc[(i * K + j) * K + u];
-              } else {
-#pragma unroll
-                for (int u = 0; u < K; ++u) pj[u] += (double)dcacc[(i * K + j) * K + u];
-              }
+              const float d = wt - cc[j][u];
+              const float p = ex2(fmaf(-d, d, G[j]) + hb);
+              const float X = fmaf(gt, cc[j][u], A[j]) + bx;
+              acc[j][u] = fmaf(p, fmaf(d * X, dws, gt), acc[j][u]);
             }
+          }
+        }
+        if (valid) {
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + ((uint32_t)tb << KB);
+#pragma unroll
+            for (int u = 0; u < K; ++u) pj[u] = first ? (double)acc[j][u] : pj[u] + (double)acc[j][u];
           }
         }
       }
     }
+
   }
 }
 
