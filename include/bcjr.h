@@ -36,8 +36,9 @@
  *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12),
  *     and for k = 3 also state_bits <= 14 (k = 1: 2..14, k = 2: 4..16,
  *     k = 3: 6..14), and L small enough that one workgroup's histories
- *     stay below 2 GiB (L <= 16383 at state_bits = 16, k = 2; at least
- *     16383 for every supported shape).  Other valid shapes return
+ *     stay below 2 GiB: the soft codeword and Viterbi take L <= 16383 at
+ *     state_bits = 16, k = 2 (at least 16383 for every supported shape),
+ *     the VJP L <= 10922 (at least 10922).  Other valid shapes return
  *     BCJR_ERR_UNSUPPORTED and a workspace size of 0.
  *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
  *   - Non-finite w or codebook values give non-finite outputs; they are not

@@ -64,31 +64,13 @@ constexpr double kHighPrecisionK2 = 18.0;
 
 bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
 
-Family family_hp(int n, int k, bool dc) {
-  Family f;
-  const int nsg = 1 << (n - 2 * k);
-  if (nsg <= 256) {
-    f.nt = 256; f.sgmax = 1; f.sgt = 1; f.occ_est = 8;
-  } else if (nsg <= 2048) {
-    f.nt = 256; f.sgt = nsg / 256; f.sgmax = f.sgt; f.occ_est = 4;
-  } else if (!dc) {
-    f.nt = 1024; f.sgt = nsg / 1024; f.sgmax = f.sgt; f.occ_est = 1;
-  } else {
-    f.nt = 512; f.sgt = nsg / 512; f.sgmax = f.sgt; f.occ_est = 1;
-  }
-  f.bpw = f.nt / (nsg / f.sgt);
-  return f;
-}
-
 // The histories of one workgroup's blocks are addressed with 32-bit byte
-// offsets: blocks per workgroup x L x S/K x 8 bytes must stay below 2^31.
-bool length_ok(int64_t L, int n, int k) {
-  for (int dc = 0; dc < 2; ++dc) {
-    const Family f = family(n, k, dc != 0);
-    const int64_t per_step = (int64_t)f.bpw * 8 * ((int64_t)1 << (n - k));
-    if (L > 0x7FFFFFFF / per_step) return false;
-  }
-  return true;
+// offsets: blocks per workgroup x L x S/K x (8 bytes, 12 for the VJP, whose
+// low-temperature variant keeps three words per group) below 2^31.
+bool length_ok(int64_t L, int n, int k, bool vjp) {
+  const Family f = family(n, k, false);
+  const int64_t per_step = (int64_t)f.bpw * (vjp ? 12 : 8) * ((int64_t)1 << (n - k));
+  return L <= 0x7FFFFFFF / per_step;
 }
 
 // The fp32 forward-backward path keeps the scaled codebook at the front of
@@ -100,27 +82,31 @@ struct FbLayout {
 };
 
 struct HpLayout {
-  size_t histH, histG, histA, xA, small, dc, slot;
+  size_t hist, histGA, xA, small, dc, slot;
 };
 
-HpLayout hp_layout(int64_t L, int n, int k) {
+HpLayout hp_layout(int64_t L, int n, int k, bool dc) {
   const size_t gs = (size_t)1 << (n - k);
   HpLayout l;
-  l.histH = align_up((size_t)L * gs * sizeof(double));
-  l.histG = align_up((size_t)L * gs * sizeof(double));
-  l.histA = align_up((size_t)L * gs * sizeof(float));
+  l.hist = align_up((size_t)L * 3 * gs * sizeof(float));
+  l.histGA = dc ? align_up((size_t)L * 3 * gs * sizeof(float)) : 0;
   l.xA = align_up(4 * gs * sizeof(float));
-  l.small = align_up((size_t)3 * L * sizeof(double));
-  l.dc = align_up(((size_t)1 << n) * sizeof(double));
-  l.slot = l.histH + l.histG + l.histA + l.xA + l.small + l.dc;
+  l.small = align_up((size_t)4 * L * sizeof(float));
+  l.dc = dc ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
+  l.slot = l.hist + l.histGA + l.xA + l.small + l.dc;
   return l;
 }
 
 size_t hp_lds_bytes(const Family& f, int n, int k) {
   const size_t gs = (size_t)1 << (n - k);
-  return (size_t)f.bpw * gs * sizeof(double) +
-         (size_t)(f.nt / 64) * (4 * sizeof(double) + kRed * sizeof(float));
+  return (size_t)f.bpw * 2 * gs * sizeof(float) +
+         (size_t)(f.nt / 64) * (2 * kRed * sizeof(float) + sizeof(double));
 }
+
+// The low-temperature VJP first decodes the minimum-distortion path (its
+// codewords centre the backward tangent): [w_hard B*L f32][states B*L i32]
+// [slots: Viterbi digits, then reused by the VJP kernel].
+size_t hp_prefix_bytes(int64_t B, int64_t L) { return 2 * align_up((size_t)B * L * 4); }
 
 FbLayout fb_layout(int64_t L, int n, int k, bool vjp, bool dc) {
   const size_t gs = (size_t)1 << (n - k);
@@ -141,7 +127,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 size_t fb_lds_bytes(const Family& f, int n, int k) {
   const size_t gs = (size_t)1 << (n - k);
-  return (size_t)f.bpw * 2 * gs * sizeof(float) + (size_t)(f.nt / 64) * kRed * sizeof(float);
+  return (size_t)f.bpw * 2 * gs * sizeof(float) + (size_t)(f.nt / 64) * 2 * kRed * sizeof(float);
 }
 
 size_t vit_lds_bytes(const Family& f, int n, int k) {
@@ -190,7 +176,7 @@ FbFn hp_pick_kb(int n, const Family& f, bool dc) {
     if (n == n512 + 2)
       return dc ? fb_kernel_hp<KB, n512 + 2, 8, 256, true> : fb_kernel_hp<KB, n512 + 2, 8, 256, false>;
     if (n == n512 + 3)
-      return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 4, 1024, false>;
+      return dc ? fb_kernel_hp<KB, n512 + 3, 4, 1024, true> : fb_kernel_hp<KB, n512 + 3, 4, 1024, false>;
   }
   return nullptr;
 }
@@ -235,12 +221,13 @@ VitFn vit_pick(int n, int k, const Family& f) {
   }
 }
 
-int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k) {
+int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
+                  bool vjp) {
   if (B < 0 || L < 1 || k < 1 || n < k || n > 16) return BCJR_ERR_INVALID_ARG;
   if (B > 0 && (!w || !codebook)) return BCJR_ERR_INVALID_ARG;
   if (codebook && ((uintptr_t)codebook & 15u)) return BCJR_ERR_INVALID_ARG;
   if (w && ((uintptr_t)w & 3u)) return BCJR_ERR_INVALID_ARG;
-  if (!supported(n, k) || !length_ok(L, n, k)) return BCJR_ERR_UNSUPPORTED;
+  if (!supported(n, k) || !length_ok(L, n, k, vjp)) return BCJR_ERR_UNSUPPORTED;
   return BCJR_OK;
 }
 
@@ -279,21 +266,52 @@ int fill_zero(float* p, int64_t count, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
+                int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
+                hipStream_t stream) {
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  const Family f = family(n, k, false);
+  VitFn fn = vit_pick(n, k, f);
+  if (!fn) return BCJR_ERR_UNSUPPORTED;
+  const size_t lds = vit_lds_bytes(f, n, k);
+  const size_t slot = vit_slot_bytes(L, n, k);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  VitArgs a;
+  a.w = w; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
+  a.states = states; a.w_hard = w_hard;
+  a.bp = static_cast<uint8_t*>(workspace);
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
 int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
               const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
               void* workspace, size_t ws_bytes, hipStream_t stream) {
   const bool dc = dCodebook != nullptr;
-  const Family f = family_hp(n, k, dc);
-  const HpLayout lay = hp_layout(L, n, k);
+  const Family f = family(n, k, false);
+  const HpLayout lay = hp_layout(L, n, k, dc);
   FbFn fn = hp_pick(n, k, f, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
+  const size_t pre = hp_prefix_bytes(B, L);
+  if (ws_bytes <= pre) return BCJR_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  float* w_hard = reinterpret_cast<float*>(ws);
+  int32_t* states = reinterpret_cast<int32_t*>(ws + pre / 2);
+  char* rest = ws + pre;
+  const size_t rest_bytes = ws_bytes - pre;
+  // the minimum-distortion codewords, which centre the backward tangent
+  int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream);
+  if (st != BCJR_OK) return st;
   const size_t lds = hp_lds_bytes(f, n, k);
   int herr = 0;
-  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, lay.slot, &herr);
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, rest_bytes, lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
   const int64_t slots = grid * f.bpw;
-  char* p = static_cast<char*>(workspace);
+  char* p = rest;
   FbArgs a = {};
   a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   const double Td = (double)T;
@@ -301,11 +319,11 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.k2d = 1.4426950408889634074 / (2.0 * Td);
   a.invT = (float)(1.0 / Td);
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
-  a.histHd = reinterpret_cast<double*>(p);            p += slots * lay.histH;
-  a.histGd = reinterpret_cast<double*>(p);            p += slots * lay.histG;
-  a.histA = reinterpret_cast<float*>(p);              p += slots * lay.histA;
+  a.bref = w_hard;
+  a.histHB = reinterpret_cast<float*>(p);             p += slots * lay.hist;
+  a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;  p += slots * lay.histGA;
   a.xA = reinterpret_cast<float*>(p);                 p += slots * lay.xA;
-  a.smalld = reinterpret_cast<double*>(p);            p += slots * lay.small;
+  a.small = reinterpret_cast<float*>(p);              p += slots * lay.small;
   a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
@@ -380,7 +398,8 @@ extern "C" {
 
 size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op) {
   if (B < 0 || L < 1 || k < 1 || state_bits < k || state_bits > 16) return 0;
-  if (!supported(state_bits, k) || !length_ok(L, state_bits, k)) return 0;
+  if (!supported(state_bits, k) || !length_ok(L, state_bits, k, op != BCJR_OP_FWD && op != BCJR_OP_VITERBI))
+    return 0;
   if (B == 0) return 0;
   if (op == BCJR_OP_VITERBI) {
     const Family f = family(state_bits, k, false);
@@ -397,9 +416,9 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
   size_t bytes = cs_bytes(state_bits) + (size_t)slots * fb_layout(L, state_bits, k, vjp, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
-    const Family fh = family_hp(state_bits, k, true);
-    const int64_t gh = std::min<int64_t>(ceil_div(B, fh.bpw), (int64_t)kDeviceCUs * fh.occ_est);
-    bytes = std::max(bytes, (size_t)(gh * fh.bpw) * hp_layout(L, state_bits, k).slot);
+    const size_t vit = (size_t)(g2 * f2.bpw) * vit_slot_bytes(L, state_bits, k);
+    const size_t hp = (size_t)(g2 * f2.bpw) * hp_layout(L, state_bits, k, true).slot;
+    bytes = std::max(bytes, hp_prefix_bytes(B, L) + std::max(vit, hp));
   }
   return bytes;
 }
@@ -407,7 +426,7 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
 int bcjr_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,
                        int k, float T, float* w_soft, float* logZ, void* workspace,
                        size_t ws_bytes, hipStream_t stream) {
-  int st = common_checks(w, B, L, codebook, state_bits, k);
+  int st = common_checks(w, B, L, codebook, state_bits, k, false);
   if (st != BCJR_OK) return st;
   if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
   if (B > 0 && !w_soft) return BCJR_ERR_INVALID_ARG;
@@ -420,7 +439,7 @@ int bcjr_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const float
                                int state_bits, int k, float T, const float* grad_w_soft,
                                float* w_soft, float* logZ, float* dW, float* dCodebook,
                                void* workspace, size_t ws_bytes, hipStream_t stream) {
-  int st = common_checks(w, B, L, codebook, state_bits, k);
+  int st = common_checks(w, B, L, codebook, state_bits, k, true);
   if (st != BCJR_OK) return st;
   if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
   if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
@@ -442,26 +461,11 @@ int bcjr_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* co
 int viterbi_decode(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,
                    int k, int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
                    hipStream_t stream) {
-  int st = common_checks(w, B, L, codebook, state_bits, k);
+  int st = common_checks(w, B, L, codebook, state_bits, k, false);
   if (st != BCJR_OK) return st;
   if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
   if (B == 0) return BCJR_OK;
-  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
-  const Family f = family(state_bits, k, false);
-  VitFn fn = vit_pick(state_bits, k, f);
-  if (!fn) return BCJR_ERR_UNSUPPORTED;
-  const size_t lds = vit_lds_bytes(f, state_bits, k);
-  const size_t slot = vit_slot_bytes(L, state_bits, k);
-  int herr = 0;
-  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, slot, &herr);
-  if (herr) return BCJR_ERR_HIP;
-  if (grid < 1) return BCJR_ERR_WORKSPACE;
-  VitArgs a;
-  a.w = w; a.c = codebook; a.B = B; a.L = L; a.n = state_bits; a.sgt = f.sgt;
-  a.states = states; a.w_hard = w_hard;
-  a.bp = static_cast<uint8_t*>(workspace);
-  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
-  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+  return run_viterbi(w, B, L, codebook, state_bits, k, states, w_hard, workspace, ws_bytes, stream);
 }
 
 const char* bcjr_status_string(int status) {

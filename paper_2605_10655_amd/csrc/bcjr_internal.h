@@ -25,13 +25,11 @@ struct FbArgs {
   float* histHB;       // [slots][L][2 S/K] H_t and the B tangent per super-group (VJP)
   float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group (dCodebook)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
-  // high-precision variant (fp64 log vectors)
+  // low-temperature variant (double-float log vectors); histHB and histGA
+  // then hold rows of 3K floats (hi, lo, tangent) and small [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
-  double* histHd;      // [slots][L][S/K] fp64
-  double* histGd;      // [slots][L][S/K] fp64
-  float* histA;        // [slots][L][S/K]
-  float* xA;           // [slots][4][S/K] exchange buffers: A partials [2], c* [2]
-  double* smalld;      // [slots][3][L]   shifts of H, lambda_t (fp64), w_soft_t (fp32)
+  const float* bref;   // [B, L] centring reference of the backward tangent
+  float* xA;           // [slots][4][S/K] exchange: lo words [2], tangents [2]
 };
 
 struct VitArgs {

@@ -70,41 +70,6 @@ __device__ __forceinline__ T max_of(const T (&x)[K]) {
   return m;
 }
 
-// Maximum of al[] and the codeword of the first predecessor attaining it
-// (the dominant predecessor c* of the group).
-template <int K, class T>
-__device__ __forceinline__ T max_arg_c(const T (&al)[K], const float (&cc)[K][K], int u, float& cst) {
-  T m = al[0];
-  cst = cc[0][u];
-#pragma unroll
-  for (int j = 1; j < K; ++j) {
-    const bool gt = al[j] > m;
-    m = gt ? al[j] : m;
-    cst = gt ? cc[j][u] : cst;
-  }
-  return m;
-}
-
-// s = sum E, sy = sum E y, scw = sum E cw, scwy = sum E cw y
-template <int K>
-__device__ __forceinline__ void group_sums(const float (&E)[K], const float (&y)[K],
-                                           const float (&cw)[K], float& s, float& sy, float& scw,
-                                           float& scwy) {
-  s = E[0];
-  sy = E[0] * y[0];
-  float e = E[0] * cw[0];
-  scw = e;
-  scwy = e * y[0];
-#pragma unroll
-  for (int b = 1; b < K; ++b) {
-    s += E[b];
-    sy = fmaf(E[b], y[b], sy);
-    e = E[b] * cw[b];
-    scw += e;
-    scwy = fmaf(e, y[b], scwy);
-  }
-}
-
 // Keeps the scheduler from hoisting the next super-group's loads above the
 // current one: that hoisting multiplies the live registers by SGMAX.
 __device__ __forceinline__ void sg_fence() {
@@ -393,7 +358,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   rc.rw = TPB > 64 ? TPB / 64 : 1;
   rc.lane = tid & 63;
   rc.wave = tid >> 6;
-  rc.red = lds + (size_t)BPW * 2 * GS;
+  // cross-wave partials, [2 parities][waves][kRed]: a sweep with one barrier
+  // per step alternates them, so a fast wave's next partial never overwrites
+  // one a slow wave is still reading
+  float* const red0 = lds + (size_t)BPW * 2 * GS;
+  rc.red = red0;
 
   // LDS: the block's two group vectors v0 = lds[vb ..), v1 = lds[vb + GS ..).
   // A super-group sg = tb + i*TPB reads / writes two patterns:
@@ -460,6 +429,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
     for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, q0[j]);
     for (int64_t t = L - 1;; --t) {
+      rc.red = red0 + ((L - 1 - t) & 1) * (NT / 64) * kRed;
       float wt, gt = 0.f;
       if (lane_rows) {
         if (t == L - 1 || (t & 63) == 63) {
@@ -670,6 +640,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       if (VJP) lds[vb + GS + i] = 0.f;
     }
     __syncthreads();
+    rc.red = red0;
     const float dws = a.dws;  // 1 / (kappa^2 T): scaled covariances -> dW, dCodebook
     float lam_est = lam0;
     // The history row of the next super-group is loaded one super-group
@@ -942,23 +913,26 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// High-precision VJP kernel for low temperatures.  At small T the log-domain
-// values of the states that carry the posterior lie hundreds of log2 units
-// from the per-step maximum (|h_t| ~ (w - c)^2 / 2T), so fp32 storage of G
-// and H rounds them at ~1e-5 and the VJP loses its 1e-4 relative accuracy.
-// Here the field, the K-way maxima, the LSE results and their storage (LDS
-// and histories) are fp64; only the normalised exponentials, their sums and
-// the tangents stay fp32 (they are well conditioned).  Structure:
-//   S0: H (fp64) in LDS, in place (reads, barrier, writes, barrier);
-//   S1: G (fp64) in LDS in place; the A tangent travels through a per-slot
-//       global double buffer (L2 resident).  Each output state stores its
-//       tangent centred on the codeword c* of its dominant predecessor
-//       (the one with the largest log weight) together with c*; the reader
-//       adds g_prev (c* - w_soft_prev) once w_soft of that step is known.
-//       With fp32 softmax weights this keeps the stored value small where
-//       the posterior has crystallised, which the plain centring on w_soft
-//       (not yet known at write time) cannot;
-//   S2: as in fb_kernel (B in LDS, ping-pong), with H, G read in fp64.
+// Low-temperature VJP kernel.  At small T the log-domain values of the states
+// that carry the posterior lie hundreds of log2 units from the per-step
+// maximum (|h_t| ~ (w - c)^2 / 2T), so fp32 log vectors round them at ~1e-5
+// and the VJP loses its 1e-4 relative accuracy.  Here G and H are carried as
+// double-float pairs (hi + lo, two fp32 words, ~48 bits) with fp64 LSE
+// arithmetic; softmax weights and tangents stay fp32.
+//   Exchange between threads: the hi words ping-pong in LDS (2 x S/K fp32,
+//   the footprint of fb_kernel), the lo words and the tangent ping-pong in
+//   a per-slot global buffer (L2-resident), so every step needs a single
+//   barrier and no output is held across it.  For that the integer shift of
+//   a step is the floor of the previous step's maximum (the stored maxima
+//   stay within the per-step drift of 0), and the forward tangent is
+//   centred on w_soft when it is read, one step later (the same arithmetic
+//   as centring before the write).  The backward tangent is centred on a
+//   reference path given per block (the minimum-distortion codewords),
+//   which the posterior follows at low temperature.
+//   S0 backward: H and B, history rows (H hi, H lo, B);
+//   S1 forward:  G and A, marginals, w_soft, dW; with dCodebook also the
+//                rows (G hi, G lo, A) and the exact lambda_t, E_p[X_t];
+//   S2 dCodebook as in fb_kernel, with p from the fp64 sums.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void lse_pair_d(double& m, float& s, double mo, float so) {
   const double M = fmax(m, mo);
@@ -966,65 +940,52 @@ __device__ __forceinline__ void lse_pair_d(double& m, float& s, double mo, float
   m = M;
 }
 
-template <int NQ, unsigned MAXMASK>
-__device__ __forceinline__ void red_pre_d(double (&v)[NQ], const RedCtx& r, double* redd) {
-#pragma unroll
-  for (int q = 0; q < NQ; ++q)
-    for (int off = 1; off < r.width; off <<= 1) {
-      const double o = __shfl_xor(v[q], off);
-      v[q] = ((MAXMASK >> q) & 1u) ? fmax(v[q], o) : v[q] + o;
-    }
+__device__ __forceinline__ void lse3_pair_d(double& m, float& s, float& y, double mo, float so,
+                                            float yo) {
+  const double M = fmax(m, mo);
+  const float f = ex2((float)(m - M)), fo = ex2((float)(mo - M));
+  s = s * f + so * fo;
+  y = y * f + yo * fo;
+  m = M;
+}
+
+// (max, sum, weighted sum) over the block with a double max; redd holds
+// [waves] doubles, r.red the floats
+__device__ __forceinline__ void lse3d_pre(double& m, float& s, float& y, const RedCtx& r, double* redd) {
+  for (int off = 1; off < r.width; off <<= 1) {
+    const double mo = __shfl_xor(m, off);
+    const float so = __shfl_xor(s, off);
+    const float yo = __shfl_xor(y, off);
+    lse3_pair_d(m, s, y, mo, so, yo);
+  }
   if (r.rw > 1 && r.lane == 0) {
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) redd[r.wave * 4 + q] = v[q];
+    redd[r.wave] = m;
+    r.red[r.wave * kRed + 0] = s;
+    r.red[r.wave * kRed + 1] = y;
   }
 }
 
-template <int NQ, unsigned MAXMASK>
-__device__ __forceinline__ void red_post_d(double (&v)[NQ], const RedCtx& r, const double* redd) {
+__device__ __forceinline__ void lse3d_post(double& m, float& s, float& y, const RedCtx& r,
+                                           const double* redd) {
   if (r.rw > 1) {
     const int first = (r.wave / r.rw) * r.rw;
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      double acc = redd[first * 4 + q];
-      for (int i = 1; i < r.rw; ++i) {
-        const double o = redd[(first + i) * 4 + q];
-        acc = ((MAXMASK >> q) & 1u) ? fmax(acc, o) : acc + o;
-      }
-      v[q] = acc;
-    }
+    m = redd[first];
+    s = r.red[first * kRed + 0];
+    y = r.red[first * kRed + 1];
+    for (int i = 1; i < r.rw; ++i)
+      lse3_pair_d(m, s, y, redd[first + i], r.red[(first + i) * kRed + 0], r.red[(first + i) * kRed + 1]);
   }
 }
 
-template <int K>
-__device__ __forceinline__ void ld_vec_d(const double* p, double (&v)[K]) {
-  if constexpr (K == 1) {
-    v[0] = p[0];
-  } else {
-#pragma unroll
-    for (int q = 0; q < K / 2; ++q) {
-      const double2 t = reinterpret_cast<const double2*>(p)[q];
-      v[2 * q] = t.x;
-      v[2 * q + 1] = t.y;
-    }
-  }
-}
-
-template <int K>
-__device__ __forceinline__ void st_vec_d(double* p, const double (&v)[K]) {
-  if constexpr (K == 1) {
-    p[0] = v[0];
-  } else {
-#pragma unroll
-    for (int q = 0; q < K / 2; ++q)
-      reinterpret_cast<double2*>(p)[q] = make_double2(v[2 * q], v[2 * q + 1]);
-  }
+__device__ __forceinline__ void split_df(double v, float& hi, float& lo) {
+  hi = (float)v;
+  lo = (float)(v - (double)hi);
 }
 
 template <int KB, int NB, int SGMAX, int NT, bool DC>
 __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   constexpr int K = 1 << KB;
-  extern __shared__ double ldsh[];
+  extern __shared__ float lds[];
   const int n = NB ? NB : a.n;
   const int GS = 1 << (n - KB);
   const int NSG = 1 << (n - 2 * KB);
@@ -1034,344 +995,384 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   const int tid = threadIdx.x;
   const int bw = BPW == 1 ? 0 : tid / TPB;
   const int tb = BPW == 1 ? tid : tid - bw * TPB;
-  const uint32_t toK = (uint32_t)tb << KB;
   const int64_t L = a.L;
-  const double k2 = (double)a.k2d;
+  const double k2 = a.k2d;
+  const float invT = a.invT;
 
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
   rc.lane = tid & 63;
   rc.wave = tid >> 6;
-  double* vd = ldsh + (size_t)bw * GS;                              // G or H (fp64)
-  double* redd = ldsh + (size_t)BPW * GS;                           // [waves][4] fp64
-  rc.red = reinterpret_cast<float*>(redd + (NT / 64) * 4);          // [waves][kRed] fp32
-  float* vf0 = reinterpret_cast<float*>(vd);                        // S2: B ping-pong
-  float* vf1 = vf0 + GS;
+  // [2 parities][waves][kRed] floats, then [waves] doubles
+  float* red0 = lds + (size_t)BPW * 2 * GS;
+  double* redd = reinterpret_cast<double*>(red0 + 2 * (NT / 64) * kRed);
 
-  float dcacc[DC ? SGMAX * K * K : 1];
+  const uint32_t vb = (uint32_t)bw * 2 * GS;
+  const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;
+  const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
+  const uint32_t voK = (uint32_t)tb << (KB + 2);
+  const uint32_t hrow = 3 * K;                    // floats per history row: hi, lo, tangent
+  const uint32_t hstep = (uint32_t)GS * 3;        // floats per history step
+  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * hrow) * 4u;
+  const bool lane_rows = TPB >= 64;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
     const int64_t blk = base + bw;
     const bool valid = blk < a.B;
     const int64_t bb = valid ? blk : a.B - 1;
     const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const int64_t slot0 = (int64_t)blockIdx.x * BPW;
     const float* wb = a.w + bb * L;
     const float* gb = a.g + bb * L;
-    double* hH = a.histHd + slot * L * GS;
-    double* hG = a.histGd + slot * L * GS;
-    float* hA = a.histA + slot * L * GS;
-    float* gA = a.xA + slot * 4 * GS;  // A partials [2][S/K], then c* [2][S/K]
-    float* gC = gA + 2 * GS;
-    double* sm_mB = a.smalld + slot * 3 * L;
-    double* sm_lam = sm_mB + L;
-    float* sm_ws = reinterpret_cast<float*>(sm_lam + L);
+    const float* rb = a.bref + bb * L;
+    const rsrc_t hist = make_rsrc(a.histHB + slot0 * L * hstep, (uint32_t)BPW * (uint32_t)L * hstep * 4u);
+    const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * L * hstep : a.histHB,
+                                 DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
+    // exchange buffer of the slot: [2][S/K] lo words, then [2][S/K] tangents
+    float* xlo = a.xA + slot * 4 * GS;
+    float* xtg = xlo + 2 * GS;
+    float* sm_mB = a.small + slot * 4 * L;   // shift applied to H_t (integer)
+    float* sm_xb = sm_mB + L;                // dCodebook: E_p[X_t]
+    double* sm_lam = reinterpret_cast<double*>(sm_xb + L);  // dCodebook: lambda_t (fp64)
 
     // ------------------------------------------------------------------ S0
-    for (int i = tb; i < GS; i += TPB) vd[i] = 0.0;
+    for (int i = tb; i < GS; i += TPB) {
+      lds[vb + i] = 0.f;
+      xlo[i] = 0.f;
+      xtg[i] = 0.f;
+    }
     __syncthreads();
     double shiftB = 0.0;
     double lam0 = 0.0;
+    float xbar = 0.f;
+    float dlag = 0.f;   // shift applied to the values written this step
+    float wch = 0.f, gch = 0.f, rch = 0.f;
+    int64_t cbase = 0;
     for (int64_t t = L - 1;; --t) {
-      const double wt = (double)wb[t];
-      double Hin[SGMAX][K];
-#pragma unroll
-      for (int i = 0; i < SGMAX; ++i) {
-        if (i < SGT) {
-          const int sg = tb + i * TPB;
-#pragma unroll
-          for (int b = 0; b < K; ++b) Hin[i][b] = vd[sg * K + b];
-          st_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin[i]);
+      const int par = (int)((L - 1 - t) & 1);
+      rc.red = red0 + par * (NT / 64) * kRed;
+      float wf, gt, rt;
+      if (lane_rows) {
+        if (t == L - 1 || (t & 63) == 63) {
+          cbase = t & ~(int64_t)63;
+          wch = row_chunk(wb, cbase, L);
+          gch = row_chunk(gb, cbase, L);
+          rch = row_chunk(rb, cbase, L);
         }
+        wf = read_lane(wch, (int)(t - cbase));
+        gt = read_lane(gch, (int)(t - cbase));
+        rt = read_lane(rch, (int)(t - cbase));
+      } else {
+        wf = wb[t];
+        gt = gb[t];
+        rt = rb[t];
       }
+      const double wt = (double)wf;
+      uint32_t rrow = row0 + (par ? GS : 0), wcol = col0 + (par ? 0 : GS);
+      pin_u(rrow);
+      pin_u(wcol);
+      const float* xlo_r = xlo + (par ? GS : 0);
+      const float* xtg_r = xtg + (par ? GS : 0);
+      float* xlo_w = xlo + (par ? 0 : GS);
+      float* xtg_w = xtg + (par ? 0 : GS);
+      const uint32_t soH = (uint32_t)t * hstep * 4u;
       if (t == 0) {
+        // lambda_0 = LSE_s [h_0(s) + H_0] and E_p[g_0 c + B_0]
         double lm = -INFINITY;
-        float ls = 0.f;
+        float ls = 0.f, ly = 0.f;
+#pragma unroll 1
+        for (int i = 0; i < SGT; ++i) {
+          float Hh[K], Hl[K], Bin[K];
+          ld_vec<K>(lds + rrow + i * TPB * K, Hh);
+          ld_vec<K>(xlo_r + (i * TPB + tb) * K, Hl);
+          ld_vec<K>(xtg_r + (i * TPB + tb) * K, Bin);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
 #pragma unroll
-        for (int i = 0; i < SGMAX; ++i) {
-          if (i < SGT) {
+          for (int j = 0; j < K; ++j) {
+            float cc[K];
+            buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
+            double x[K];
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-              float cc[K];
-              ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-              double x[K];
-#pragma unroll
-              for (int b = 0; b < K; ++b) {
-                const double d = wt - (double)cc[b];
-                x[b] = Hin[i][b] - d * d * k2;
-              }
-              const double m = max_of<K>(x);
-              float s = ex2((float)(x[0] - m));
-#pragma unroll
-              for (int b = 1; b < K; ++b) s += ex2((float)(x[b] - m));
-              lse_pair_d(lm, ls, m, s);
+            for (int b = 0; b < K; ++b) {
+              const double d = wt - (double)cc[b];
+              x[b] = fma(-d * k2, d, (double)Hh[b] + (double)Hl[b]);
             }
-            sg_fence();
+            const double m = max_of<K>(x);
+            float s = 0.f, sy = 0.f;
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const float E = ex2((float)(x[b] - m));
+              s += E;
+              sy = fmaf(E, fmaf(gt, cc[b], Bin[b]), sy);
+            }
+            lse3_pair_d(lm, ls, ly, m, s, sy);
           }
         }
-        for (int off = 1; off < rc.width; off <<= 1) {
-          const double mo = __shfl_xor(lm, off);
-          const float so = __shfl_xor(ls, off);
-          lse_pair_d(lm, ls, mo, so);
-        }
-        if (rc.rw > 1 && rc.lane == 0) {
-          redd[rc.wave * 4 + 0] = lm;
-          rc.red[rc.wave * kRed + 0] = ls;
-        }
-        if (tb == 0) sm_mB[L - 1] = 0.0;
+        lse3d_pre(lm, ls, ly, rc, redd);
+        if (tb == 0) sm_mB[L - 1] = 0.f;
         __syncthreads();
-        if (rc.rw > 1) {
-          const int first = (rc.wave / rc.rw) * rc.rw;
-          lm = redd[first * 4];
-          ls = rc.red[first * kRed];
-          for (int q = 1; q < rc.rw; ++q) lse_pair_d(lm, ls, redd[(first + q) * 4], rc.red[(first + q) * kRed]);
-        }
+        lse3d_post(lm, ls, ly, rc, redd);
+        xbar = ly / ls;
         lam0 = lm + (double)lg2(ls);
         if (tb == 0 && valid && a.logZ)
           a.logZ[bb] = (float)((shiftB + lam0) * 0.69314718055994530942);
         __syncthreads();
         break;
       }
-      double Hout[SGMAX][K];
-      double vmax[1] = {-INFINITY};
+      float vmax[1] = {-INFINITY};
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        float Hh[K], Hl[K], Bin[K];
+        ld_vec<K>(lds + rrow + i * TPB * K, Hh);
+        ld_vec<K>(xlo_r + (i * TPB + tb) * K, Hl);
+        ld_vec<K>(xtg_r + (i * TPB + tb) * K, Bin);
+        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
+        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
+        double H[K];
 #pragma unroll
-      for (int i = 0; i < SGMAX; ++i) {
-        if (i < SGT) {
+        for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
 #pragma unroll
-          for (int j = 0; j < K; ++j) {
-            float cc[K];
-            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-            double x[K];
+        for (int j = 0; j < K; ++j) {
+          float cc[K];
+          buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
+          double x[K];
 #pragma unroll
-            for (int b = 0; b < K; ++b) {
-              const double d = wt - (double)cc[b];
-              x[b] = Hin[i][b] - d * d * k2;
-            }
-            const double m = max_of<K>(x);
-            float s = ex2((float)(x[0] - m));
-#pragma unroll
-            for (int b = 1; b < K; ++b) s += ex2((float)(x[b] - m));
-            Hout[i][j] = m + (double)lg2(s);
-            vmax[0] = fmax(vmax[0], Hout[i][j]);
+          for (int b = 0; b < K; ++b) {
+            const double d = wt - (double)cc[b];
+            x[b] = fma(-d * k2, d, H[b]);
           }
-          sg_fence();
-        }
-      }
-      red_pre_d<1, 1u>(vmax, rc, redd);
-      __syncthreads();
-      red_post_d<1, 1u>(vmax, rc, redd);
-      const double off = floor(vmax[0]);
+          const double m = max_of<K>(x);
+          float E[K];
 #pragma unroll
-      for (int i = 0; i < SGMAX; ++i) {
-        if (i < SGT) {
-          const int sg = tb + i * TPB;
+          for (int b = 0; b < K; ++b) E[b] = ex2((float)(x[b] - m));
+          float s = E[0];
 #pragma unroll
-          for (int j = 0; j < K; ++j) vd[j * NSG + sg] = Hout[i][j] - off;
+          for (int b = 1; b < K; ++b) s += E[b];
+          // B_{t-1}: E-weighted mean of g_t (c - r_t) + B_t over the K successors
+          float num = E[0] * fmaf(gt, cc[0] - rt, Bin[0]);
+#pragma unroll
+          for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[b] - rt, Bin[b]), num);
+          const double h = m + (double)lg2(s) - (double)dlag;
+          float hi, lo;
+          split_df(h, hi, lo);
+          vmax[0] = fmaxf(vmax[0], hi);
+          lds[wcol + j * NSG + i * TPB] = hi;
+          xlo_w[j * NSG + i * TPB + tb] = lo;
+          xtg_w[j * NSG + i * TPB + tb] = num * rcp(s);
         }
+        sg_fence();
       }
-      shiftB += off;
-      if (tb == 0) sm_mB[t - 1] = off;
+      shiftB += (double)dlag;
+      if (tb == 0) sm_mB[t - 1] = dlag;
+      red_pre<1, 1u>(vmax, rc);
       __syncthreads();
+      {
+        float vm[1] = {vmax[0]};
+        red_post<1, 1u>(vm, rc);
+        dlag = floorf(vm[0]);
+      }
     }
 
     // ------------------------------------------------------------------ S1
     for (int i = tb; i < GS; i += TPB) {
-      vd[i] = 0.0;
-      gA[i] = 0.f;
-      gC[i] = 0.f;
+      lds[vb + i] = 0.f;
+      xlo[i] = 0.f;
+      xtg[i] = 0.f;
     }
     __syncthreads();
     double lam_est = lam0;
-    float gprev = 0.f, wsprev = 0.f;  // g and w_soft of the step that wrote A
+    float cprev = 0.f;  // g_{t-1} w_soft_{t-1}: the forward tangent's centring, applied on read
+    dlag = 0.f;
     for (int64_t t = 0; t < L; ++t) {
-      const double wt = (double)wb[t];
-      const float wtf = wb[t];
-      const float gt = gb[t];
-      const double mBt = sm_mB[t];
-      const float* Acur = gA + (t & 1) * GS;
-      float* Anext = gA + ((t + 1) & 1) * GS;
-      const float* Ccur = gC + (t & 1) * GS;
-      float* Cnext = gC + ((t + 1) & 1) * GS;
-      double Gout[SGMAX][K];
-      double vmax[1] = {-INFINITY};
-      float rv[2] = {0.f, 0.f};  // sum p, sum p c
+      const int par = (int)(t & 1);
+      rc.red = red0 + par * (NT / 64) * kRed;
+      float wf, gt, rt;
+      if (lane_rows) {
+        if ((t & 63) == 0) {
+          cbase = t;
+          wch = row_chunk(wb, cbase, L);
+          gch = row_chunk(gb, cbase, L);
+          rch = row_chunk(rb, cbase, L);
+        }
+        wf = read_lane(wch, (int)(t - cbase));
+        gt = read_lane(gch, (int)(t - cbase));
+        rt = read_lane(rch, (int)(t - cbase));
+      } else {
+        wf = wb[t];
+        gt = gb[t];
+        rt = rb[t];
+      }
+      if (t > 0) xbar = fmaf(gt, rt, xbar);  // B_t no longer holds step t
+      const double wt = (double)wf;
+      const double mBt = (double)sm_mB[t];
+      uint32_t rcol = col0 + (par ? GS : 0), wrow = row0 + (par ? 0 : GS);
+      pin_u(rcol);
+      pin_u(wrow);
+      const float* xlo_r = xlo + (par ? GS : 0);
+      const float* xtg_r = xtg + (par ? GS : 0);
+      float* xlo_w = xlo + (par ? 0 : GS);
+      float* xtg_w = xtg + (par ? 0 : GS);
+      const uint32_t soH = (uint32_t)t * hstep * 4u;
+      // max G_{t+1}, sum p, sum p c, sum p X, sum p c X
+      float rv[5] = {-INFINITY, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        float Gh[K], Gl[K], Ar[K];
 #pragma unroll
-      for (int i = 0; i < SGMAX; ++i) {
-        if (i < SGT) {
-          const int sg = tb + i * TPB;
-          double Gin[K];
-          float Ain[K];
+        for (int j = 0; j < K; ++j) {
+          Gh[j] = lds[rcol + j * NSG + i * TPB];
+          Gl[j] = xlo_r[j * NSG + i * TPB + tb];
+          Ar[j] = xtg_r[j * NSG + i * TPB + tb] - cprev;
+        }
+        if constexpr (DC) {
+          const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
+          buf_st<K>(hga, voH, so, Gh);
+          buf_st<K>(hga, voH, so + 4 * K, Gl);
+          buf_st<K>(hga, voH, so + 8 * K, Ar);
+        }
+        double G[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
+        float Hh[K], Hl[K], Bc[K];
+        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
+        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bc);
+        float cc[K][K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
+        float go_hi[K], go_lo[K], ao[K];
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+          double al[K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            Gin[j] = vd[j * NSG + sg];
-            Ain[j] = fmaf(gprev, Ccur[j * NSG + sg] - wsprev, Acur[j * NSG + sg]);
+            const double d = wt - (double)cc[j][u];
+            al[j] = fma(-d * k2, d, G[j]);
           }
-          st_vec_d<K>(hG + t * GS + ((i * TPB) << KB) + toK, Gin);
-          st_vec<K>(hA + t * GS + ((i * TPB) << KB) + toK, Ain);
-          double Hc[K];
-          ld_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hc);
-          float cc[K][K];
+          const double m = max_of<K>(al);
+          float E[K];
 #pragma unroll
-          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
-          float ao[K], co[K];
+          for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
+          // X is centred per state before the sums: at low T the moments of
+          // an uncentred X cancel only to its rounding, amplified by 1/T
+          const float bx = Bc[u] - xbar;
+          float s = E[0], ec = E[0] * cc[0][u], sc = ec;
+          float x = fmaf(gt, cc[0][u], Ar[0]) + bx;
+          float sx = E[0] * x, scx = ec * x;
 #pragma unroll
-          for (int u = 0; u < K; ++u) {
-            double al[K];
-#pragma unroll
-            for (int j = 0; j < K; ++j) {
-              const double d = wt - (double)cc[j][u];
-              al[j] = Gin[j] - d * d * k2;
-            }
-            float cst;
-            const double m = max_arg_c<K>(al, cc, u, cst);
-            float E[K];
-#pragma unroll
-            for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
-            float s = E[0], sc = E[0] * cc[0][u], num = E[0] * Ain[0], sd = E[0] * (cc[0][u] - cst);
-#pragma unroll
-            for (int j = 1; j < K; ++j) {
-              s += E[j];
-              sc = fmaf(E[j], cc[j][u], sc);
-              num = fmaf(E[j], Ain[j], num);
-              sd = fmaf(E[j], cc[j][u] - cst, sd);
-            }
-            co[u] = cst;
-            Gout[i][u] = m + (double)lg2(s);
-            vmax[0] = fmax(vmax[0], Gout[i][u]);
-            const float fac = ex2((float)(m + Hc[u] - lam_est));
-            rv[0] = fmaf(fac, s, rv[0]);
-            rv[1] = fmaf(fac, sc, rv[1]);
-            ao[u] = fmaf(gt, sd, num) * rcp(s);  // A_{t+1} - g_t (c* - w_soft_t)
+          for (int j = 1; j < K; ++j) {
+            s += E[j];
+            ec = E[j] * cc[j][u];
+            sc += ec;
+            x = fmaf(gt, cc[j][u], Ar[j]) + bx;
+            sx = fmaf(E[j], x, sx);
+            scx = fmaf(ec, x, scx);
           }
-          st_vec<K>(Anext + ((i * TPB) << KB) + toK, ao);
-          st_vec<K>(Cnext + ((i * TPB) << KB) + toK, co);
-          (void)wtf;
-          sg_fence();
+          const double gout = m + (double)lg2(s) - (double)dlag;
+          split_df(gout, go_hi[u], go_lo[u]);
+          rv[0] = fmaxf(rv[0], go_hi[u]);
+          const float fac = ex2((float)(m + ((double)Hh[u] + (double)Hl[u]) - lam_est));
+          rv[1] = fmaf(fac, s, rv[1]);
+          rv[2] = fmaf(fac, sc, rv[2]);
+          rv[3] = fmaf(fac, sx, rv[3]);
+          rv[4] = fmaf(fac, scx, rv[4]);
+          ao[u] = fmaf(sx, rcp(s), -bx);  // E-weighted mean of g c + A
         }
+        st_vec<K>(lds + wrow + i * TPB * K, go_hi);
+        st_vec<K>(xlo_w + (i * TPB + tb) * K, go_lo);
+        st_vec<K>(xtg_w + (i * TPB + tb) * K, ao);
+        sg_fence();
       }
-      red_pre_d<1, 1u>(vmax, rc, redd);
-      red_pre<2, 0u>(rv, rc);
+      red_pre<5, 1u>(rv, rc);
       __syncthreads();
-      red_post_d<1, 1u>(vmax, rc, redd);
-      red_post<2, 0u>(rv, rc);
-      const double off = floor(vmax[0]);
-      const float wst = rv[1] / rv[0];
-      const double lamt = lam_est + (double)lg2(rv[0]);
-      if (t < L - 1) {
-#pragma unroll
-        for (int i = 0; i < SGMAX; ++i) {
-          if (i < SGT) {
-            const int sg = tb + i * TPB;
-            double go[K];
-#pragma unroll
-            for (int u = 0; u < K; ++u) go[u] = Gout[i][u] - off;
-            st_vec_d<K>(vd + sg * K, go);
-          }
-        }
-      }
+      red_post<5, 1u>(rv, rc);
+      const float r1 = 1.f / rv[1];
+      const float wst = rv[2] * r1;
+      const double lamt = lam_est + (double)lg2(rv[1]);
+      const float xbe = fmaf(rv[3], r1, xbar);
       if (tb == 0) {
-        sm_lam[t] = lamt;
-        sm_ws[t] = wst;
-        if (valid && a.w_soft) a.w_soft[bb * L + t] = wst;
+        if (DC) {
+          sm_lam[t] = lamt;
+          sm_xb[t] = xbe;
+        }
+        if (valid) {
+          if (a.w_soft) a.w_soft[bb * L + t] = wst;
+          if (a.dW) a.dW[bb * L + t] = (rv[4] - wst * rv[3]) * r1 * invT;
+        }
       }
-      gprev = gt;
-      wsprev = wst;
-      lam_est = lamt - off + mBt;
-      __syncthreads();
+      lam_est = lamt - (double)dlag + mBt;
+      dlag = floorf(rv[0]);
+      cprev = gt * wst;
+      xbar = xbe - cprev;
     }
 
     // ------------------------------------------------------------------ S2
     if constexpr (DC) {
-#pragma unroll
-      for (int q = 0; q < SGMAX * K * K; ++q) dcacc[q] = 0.f;
-    }
-    for (int i = tb; i < GS; i += TPB) vf0[i] = 0.f;
-    __syncthreads();
-    const float invT = a.invT;
-    float xbar = 0.f;
-    for (int64_t t = L - 1; t >= 0; --t) {
-      const float wtf = wb[t];
-      const double wt = (double)wtf;
-      const float gt = gb[t];
-      const float wst = sm_ws[t];
-      const double lamt = sm_lam[t];
-      float* cur = ((L - 1 - t) & 1) ? vf1 : vf0;
-      float* nxt = ((L - 1 - t) & 1) ? vf0 : vf1;
-      float rv[3] = {0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < SGMAX; ++i) {
-        if (i < SGT) {
-          const int sg = tb + i * TPB;
-          float Bin[K], At[K];
-          double Hin[K], Gt[K];
-#pragma unroll
-          for (int b = 0; b < K; ++b) Bin[b] = cur[sg * K + b];
-          ld_vec_d<K>(hH + t * GS + ((i * TPB) << KB) + toK, Hin);
-          ld_vec_d<K>(hG + t * GS + ((i * TPB) << KB) + toK, Gt);
-          ld_vec<K>(hA + t * GS + ((i * TPB) << KB) + toK, At);
-#pragma unroll
-          for (int j = 0; j < K; ++j) {
-            float cc[K];
-            ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc);
-            double x[K];
-            float y[K], cw[K];
-#pragma unroll
-            for (int b = 0; b < K; ++b) {
-              const double d = wt - (double)cc[b];
-              x[b] = Hin[b] - d * d * k2;
-              cw[b] = cc[b] - wst;
-              y[b] = fmaf(gt, cw[b], Bin[b]);
-            }
-            const double m = max_of<K>(x);
-            float E[K];
-#pragma unroll
-            for (int b = 0; b < K; ++b) E[b] = ex2((float)(x[b] - m));
-            float s, sy, scw, scwy;
-            group_sums<K>(E, y, cw, s, sy, scw, scwy);
-            nxt[j * NSG + sg] = sy * rcp(s);
-            const float fac = ex2((float)(Gt[j] + m - lamt));
-            rv[0] = fmaf(fac, fmaf(At[j], scw, scwy), rv[0]);
-            rv[1] = fmaf(fac, fmaf(At[j], s, sy), rv[1]);
-            rv[2] = fmaf(fac, s, rv[2]);
-            if constexpr (DC) {
-#pragma unroll
-              for (int b = 0; b < K; ++b) {
-                const float p = E[b] * fac;
-                const float X = y[b] + At[j];
-                dcacc[(i * K + j) * K + b] += p * fmaf((wtf - cc[b]) * (X - xbar), invT, gt);
-              }
-              sg_fence();
-            }
-          }
-          sg_fence();
-        }
-      }
-      red_pre<3, 0u>(rv, rc);
       __syncthreads();
-      red_post<3, 0u>(rv, rc);
-      const float rinv = 1.f / rv[2];
-      xbar = rv[1] * rinv;
-      if (tb == 0 && valid && a.dW) a.dW[bb * L + t] = rv[0] * rinv * invT;
-    }
-    if constexpr (DC) {
-      if (valid) {
-        const bool first = base == (int64_t)blockIdx.x * BPW;
-        double* part = a.dc_part + slot * ((int64_t)1 << n);
+      const bool first = base == (int64_t)blockIdx.x * BPW;
+      double* part = a.dc_part + slot * ((int64_t)1 << n);
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        float cc[K][K], acc[K][K];
 #pragma unroll
-        for (int i = 0; i < SGMAX; ++i) {
-          if (i < SGT) {
+        for (int j = 0; j < K; ++j) {
+          buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
+#pragma unroll
+          for (int u = 0; u < K; ++u) acc[j][u] = 0.f;
+        }
+        float xch = 0.f;
+#pragma unroll 1
+        for (int64_t t = 0; t < L; ++t) {
+          float wf, gt, xt;
+          if (lane_rows) {
+            if ((t & 63) == 0) {
+              cbase = t;
+              wch = row_chunk(wb, cbase, L);
+              gch = row_chunk(gb, cbase, L);
+              xch = row_chunk(sm_xb, cbase, L);
+            }
+            const int ln = (int)(t - cbase);
+            wf = read_lane(wch, ln);
+            gt = read_lane(gch, ln);
+            xt = read_lane(xch, ln);
+          } else {
+            wf = wb[t];
+            gt = gb[t];
+            xt = sm_xb[t];
+          }
+          const double lt = sm_lam[t];
+          const double wt = (double)wf;
+          const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
+          float Hh[K], Hl[K], Bv[K], Gh[K], Gl[K], A[K];
+          buf_ld<K>(hist, voH, so, Hh);
+          buf_ld<K>(hist, voH, so + 4 * K, Hl);
+          buf_ld<K>(hist, voH, so + 8 * K, Bv);
+          buf_ld<K>(hga, voH, so, Gh);
+          buf_ld<K>(hga, voH, so + 4 * K, Gl);
+          buf_ld<K>(hga, voH, so + 8 * K, A);
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            const double hb = ((double)Hh[u] + (double)Hl[u]) - lt;
+            const float bx = Bv[u] - xt;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + toK;
-              if (first) {
-#pragma unroll
-                for (int b = 0; b < K; ++b) pj[b] = (double)dcacc[(i * K + j) * K + b];
-              } else {
-#pragma unroll
-                for (int b = 0; b < K; ++b) pj[b] += (double)dcacc[(i * K + j) * K + b];
-              }
-              sg_fence();
+              const double d = wt - (double)cc[j][u];
+              const float p = ex2((float)(fma(-d * k2, d, (double)Gh[j] + (double)Gl[j]) + hb));
+              const float X = fmaf(gt, cc[j][u], A[j]) + bx;
+              acc[j][u] = fmaf(p, fmaf((wf - cc[j][u]) * X, invT, gt), acc[j][u]);
             }
+          }
+        }
+        if (valid) {
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + ((uint32_t)tb << KB);
+#pragma unroll
+            for (int u = 0; u < K; ++u) pj[u] = first ? (double)acc[j][u] : pj[u] + (double)acc[j][u];
           }
         }
       }
@@ -1380,7 +1381,6 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   }
 }
 
-// dCodebook[s] = sum over used slots of the fp64 partials, in slot order.
 __global__ void dc_reduce_kernel(const double* part, int64_t nslots, int64_t S, float* out) {
   const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (s >= S) return;

@@ -64,11 +64,15 @@ def test_workspace_bytes_host_arithmetic(lib):
         assert ws(100, 32, n, k, P.OP_VITERBI) > 0
     assert ws(100, 32, 15, 3, P.OP_FWD) == 0           # k = 3 stops at 14 state bits
     # 32-bit history offsets: one workgroup's histories below 2 GiB
-    assert ws(4, 16383, 16, 2, P.OP_FWD_VJP) > 0
-    assert ws(4, 16384, 16, 2, P.OP_FWD_VJP) == 0
+    assert ws(4, 16383, 16, 2, P.OP_FWD) > 0
+    assert ws(4, 16383, 16, 2, P.OP_VITERBI) > 0
+    assert ws(4, 16384, 16, 2, P.OP_FWD) == 0
     assert ws(4, 16384, 16, 2, P.OP_VITERBI) == 0
+    assert ws(4, 10922, 16, 2, P.OP_FWD_VJP) > 0
+    assert ws(4, 10923, 16, 2, P.OP_FWD_VJP) == 0
     for n, k in [(4, 2), (8, 2), (12, 2), (16, 2), (2, 1), (14, 1), (6, 3), (14, 3)]:
-        assert ws(4, 16383, n, k, P.OP_FWD_VJP) > 0, (n, k)
+        assert ws(4, 16383, n, k, P.OP_FWD) > 0, (n, k)
+        assert ws(4, 10922, n, k, P.OP_FWD_VJP) > 0, (n, k)
     # the S = 65536 histories: per block L * S/K * (4 + 8) bytes plus small arrays
     B, L = 16384, 256
     per_slot = L * (1 << 14) * 12
