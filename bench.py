@@ -9,6 +9,12 @@ seeded synthetic data resident in HBM before timing starts.
 
 A step is one such call over the whole matrix.  Edges per step are
 B * L * S * 2^k.  Prints one JSON line.
+
+--path ste times the BCJR-STE training step on the same matrix instead: the
+hard Viterbi forward (viterbi_decode) followed by its backward pass
+(bcjr_ste_vjp, dW only); the roofline then covers the VJP launch.  --T
+overrides the temperature (below 0.04 the VJP runs its double-float variant,
+whose roofline is not the one reported here).
 """
 from __future__ import annotations
 
@@ -36,7 +42,7 @@ EDGES_PER_GROUP = 16.0           # K^2
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map a plain 1 GiB
 # device copy's readings to its 1 GiB read and written), keyed by a digest of
 # the kernel sources they were taken on.  Any other source reports null.
-MEASURED_TRAFFIC = {"930ca5a2d8179972": 2.68949e8 * 1024 * 2.0 + 5.37672e8 * 1024 * 1.0}
+MEASURED_TRAFFIC = {"e945d33e8277e7a4": 2.68937e8 * 1024 * 2.0 + 5.37660e8 * 1024 * 1.0}
 KERNEL_SOURCES = ("bcjr_kernels.h", "bcjr_capi.hip", "bcjr_internal.h")
 
 
@@ -93,6 +99,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=("fwd_vjp", "ste"), default="fwd_vjp")
+    ap.add_argument("--T", type=float, default=None)
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes (the "
                          "reference kernel for scaling FETCH_SIZE / WRITE_SIZE counters)")
@@ -121,7 +129,8 @@ def main():
         return
     P.load_library()
     wl = WL.workload(4)
-    n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0]
+    n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0] if args.T is None else args.T
+    ste = args.path == "ste"
     dev = torch.device("cuda:0")
     w = torch.from_numpy(WL.weights(4)).to(dev)
     c = torch.from_numpy(WL.codebook(4)).to(dev)
@@ -130,13 +139,24 @@ def main():
     w_soft = torch.empty_like(w)
     logZ = torch.empty(B, dtype=torch.float32, device=dev)
     dW = torch.empty_like(w)
-    ws = torch.empty(P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP), dtype=torch.uint8,
-                     device=dev)
+    states = torch.empty((B, L), dtype=torch.int32, device=dev) if ste else None
+    ws_bytes = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
+    if ste:
+        ws_bytes = max(ws_bytes, P.bcjr_workspace_bytes(B, L, n, k, P.OP_VITERBI))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step():
-        P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
-                                     want_dCodebook=False, workspace=ws, stream=stream)
+    def step(mid=None):
+        if ste:
+            P.viterbi_decode(w, c, n, k, states=states, w_hard=w_soft, workspace=ws,
+                             stream=stream)
+            if mid is not None:
+                mid.record(stream)
+            P.bcjr_ste_vjp(w, c, n, k, T, w_soft, g, dW=dW, want_dCodebook=False, workspace=ws,
+                           stream=stream)
+        else:
+            P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
+                                         want_dCodebook=False, workspace=ws, stream=stream)
 
     for i in range(args.warmup):
         step()
@@ -144,17 +164,18 @@ def main():
         print(f"warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
 
     # events recorded on the stream the kernels are launched on
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    # (the STE step's VJP launch starts at the event recorded after its decode)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         ev[i][0].record(stream)
-        step()
+        step(ev[i][2] if ste else None)
         ev[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kernel_ms = [a.elapsed_time(b) for a, b in ev]
+    kernel_ms = [(m if ste else a).elapsed_time(b) for a, b, m in ev]
     ms_per_step = wall * 1e3 / args.steps
     edges = wl.edges
     value = edges / (ms_per_step / 1e3)
@@ -164,8 +185,14 @@ def main():
     print(f"timed {args.steps} steps: {ms_per_step:.1f} ms/step (events avg {kern_avg_s * 1e3:.1f} ms)",
           file=sys.stderr, flush=True)
 
+    if ste:
+        metric = "trellis edge-updates/s BCJR-STE step (Viterbi fwd + VJP) at S=65536,k=2,L=256"
+        what = "BCJR-STE step: viterbi_decode + bcjr_ste_vjp (dW)"
+    else:
+        metric = "trellis edge-updates/s fwd+VJP at S=65536,k=2,L=256; % VALU roofline"
+        what = "fused w_soft+logZ+dW"
     rec = {
-        "metric": "trellis edge-updates/s fwd+VJP at S=65536,k=2,L=256; % VALU roofline",
+        "metric": metric,
         "value": value,
         "unit": "edge-updates/s",
         "n_gpus": 1,
@@ -178,15 +205,16 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "2048x2048 N(0,1) weights as 16384 blocks of L=256; S=65536, k=2, "
-                               "T=0.05; fused w_soft+logZ+dW",
+                               f"T={T}; {what}",
                    "B": B, "L": L, "S": wl.S, "k": k, "T": T},
         "blocks_per_s": B / (ms_per_step / 1e3),
         "roofline": {"bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
                      "unit": "Gedge/s", "frac": achieved / peak,
-                     "traffic": MEASURED_TRAFFIC.get(kernel_source_digest()),
+                     "traffic": None if (ste or args.T is not None)
+                     else MEASURED_TRAFFIC.get(kernel_source_digest()),
                      "kernel_ms": kern_avg_s * 1e3},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not ste and args.T is None:
         print("timing the oracle on the host cores ...", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)

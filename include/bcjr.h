@@ -17,7 +17,8 @@
  *   g: dW = d<g, w_soft>/dw per block and dCodebook = d<g, w_soft>/dc summed
  *   over the call's blocks.  T is a constant of the call (no dT).
  *   viterbi_decode returns the minimum-distortion path (Sec. 3.2), the
- *   T -> 0 limit of the soft codeword (Sec. 3.3).
+ *   T -> 0 limit of the soft codeword (Sec. 3.3).  bcjr_ste_vjp is the
+ *   backward pass of the BCJR-STE variant, whose forward pass is that path.
  *
  * Conventions for every entry point:
  *   - w, grad_w_soft, w_soft, dW, w_hard are row-major [B, L] float32; block
@@ -98,6 +99,21 @@ int bcjr_soft_codeword_fwd_vjp(const float *w, int64_t B, int64_t L, const float
                                int state_bits, int k, float T, const float *grad_w_soft,
                                float *w_soft, float *logZ, float *dW, float *dCodebook,
                                void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Backward pass of BCJR-STE (Sec. 3.5 and Sec. "BCJR-STE variant"): the
+ * variant's forward output is the hard Viterbi codeword w_hard (viterbi_decode)
+ * and its backward pass is the VJP of the soft codeword at temperature T, so
+ * dW and dCodebook are those of bcjr_soft_codeword_vjp for the same w,
+ * codebook, T and grad_w_soft.  w_hard[B*L] (required) is the forward output;
+ * below T = 0.04 the VJP centres its backward tangent on it rather than
+ * decoding the path again, so this call skips the Viterbi pass that
+ * bcjr_soft_codeword_vjp runs there.  Any finite w_hard gives the same
+ * result up to rounding; the accuracy stated for the VJP holds when it is
+ * viterbi_decode's output for the same w and codebook.  Workspace: as for
+ * BCJR_OP_VJP.  dW and dCodebook may each be NULL. */
+int bcjr_ste_vjp(const float *w, int64_t B, int64_t L, const float *codebook, int state_bits,
+                 int k, float T, const float *w_hard, const float *grad_w_soft, float *dW,
+                 float *dCodebook, void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /* Minimum-distortion path, sum_t (w_t - c(s_t))^2 evaluated in fp64 with the
  * product and the sum rounded separately (Sec. 3.2).  Ties go to the

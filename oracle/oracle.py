@@ -120,6 +120,17 @@ def viterbi(w, c, n, k, nthreads=None):
     return st, cost
 
 
+def ste(w, c, n, k, T, g, want_dc=True, nthreads=None):
+    """BCJR-STE (paper Sec. 3.5 and Sec. "BCJR-STE variant"): the forward
+    output is the hard codeword c(s_t) of the minimum-distortion path
+    (Sec. 3.2) and the backward pass is the VJP of the temperature-T soft
+    codeword (Sec. 3.5), not an identity.  Returns (w_hard[B, L], dW[B, L],
+    dc[S] or None) in float64."""
+    st, _ = viterbi(w, c, n, k, nthreads)
+    _, _, dW, dc = soft_codeword_vjp(w, c, n, k, T, g, want_dc, nthreads)
+    return _d(c)[st], dW, dc
+
+
 def block_tables(w_block, c, n, k, T, g_block=None):
     """One block: (log alpha[L, S], log beta[L, S], A[L, S] | None, B[L, S] | None)."""
     w = _d(w_block).reshape(-1)

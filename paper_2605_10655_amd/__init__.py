@@ -6,10 +6,14 @@ computation runs in the library's HIP kernels; this module only checks
 tensor shapes, allocates outputs and the workspace through PyTorch, and
 passes raw device pointers and the current HIP stream.
 
+The autograd layer (``BcjrQuant``, soft or BCJR-STE forward) is in
+``paper_2605_10655_amd.autograd``.
+
 Functions keep the C names:
     bcjr_soft_codeword(w, codebook, state_bits, k, T)            -> (w_soft, logZ)
     bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, g)     -> (dW, dCodebook)
     bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, g) -> (w_soft, logZ, dW, dCodebook)
+    bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, g)       -> (dW, dCodebook)
     viterbi_decode(w, codebook, state_bits, k)                   -> (states, w_hard)
     bcjr_workspace_bytes(B, L, state_bits, k, op)                -> int
 """
@@ -21,7 +25,7 @@ import os
 __all__ = [
     "BcjrError", "OP_FWD", "OP_VJP", "OP_FWD_VJP", "OP_VITERBI", "library_path", "load_library",
     "bcjr_workspace_bytes", "bcjr_status_string", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
-    "bcjr_soft_codeword_fwd_vjp", "viterbi_decode",
+    "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode",
 ]
 
 OP_FWD, OP_VJP, OP_FWD_VJP, OP_VITERBI = 0, 1, 2, 3
@@ -61,9 +65,10 @@ def load_library():
     L.bcjr_soft_codeword_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, sz, vp]
     L.bcjr_soft_codeword_fwd_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, vp,
                                              sz, vp]
+    L.bcjr_ste_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
     L.viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, vp, vp, vp, sz, vp]
     for f in (L.bcjr_soft_codeword, L.bcjr_soft_codeword_vjp, L.bcjr_soft_codeword_fwd_vjp,
-              L.viterbi_decode):
+              L.bcjr_ste_vjp, L.viterbi_decode):
         f.restype = ci
     _lib = L
     return L
@@ -192,6 +197,30 @@ def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, wa
                                         _ptr(dCodebook), _ptr(ws), ws.numel(), _stream(stream))
     _raise("bcjr_soft_codeword_fwd_vjp", rc)
     return w_soft, logZ, dW, dCodebook
+
+
+def bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, grad_w_soft, *, want_dW=True,
+                 want_dCodebook=True, dW=None, dCodebook=None, workspace=None, stream=None):
+    """Backward pass of BCJR-STE: the VJP of <grad_w_soft, w_soft> at temperature T,
+    given the forward pass's Viterbi codewords w_hard[B, L] (the centring
+    reference of the low-temperature variant).  (dW or None, dCodebook or None)."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _check_in("codebook", codebook, (1 << state_bits,))
+    _check_in("w_hard", w_hard, (B, L))
+    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    if dW is None and want_dW:
+        dW = torch.empty_like(w)
+    if dCodebook is None and want_dCodebook:
+        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=w.device)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, w.device)
+    rc = lib.bcjr_ste_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T), _ptr(w_hard),
+                          _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws), ws.numel(),
+                          _stream(stream))
+    _raise("bcjr_ste_vjp", rc)
+    return dW, dCodebook
 
 
 def viterbi_decode(w, codebook, state_bits, k, *, want_w_hard=True, states=None, w_hard=None,

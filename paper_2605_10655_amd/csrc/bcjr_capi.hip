@@ -287,24 +287,31 @@ int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+// `ref` is the centring reference of the backward tangent ([B, L]); when it
+// is null the minimum-distortion codewords are decoded into the front of the
+// workspace first.
 int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
-              const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
-              void* workspace, size_t ws_bytes, hipStream_t stream) {
+              const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
+              float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const bool dc = dCodebook != nullptr;
   const Family f = family(n, k, false);
   const HpLayout lay = hp_layout(L, n, k, dc);
   FbFn fn = hp_pick(n, k, f, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
-  const size_t pre = hp_prefix_bytes(B, L);
-  if (ws_bytes <= pre) return BCJR_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
-  float* w_hard = reinterpret_cast<float*>(ws);
-  int32_t* states = reinterpret_cast<int32_t*>(ws + pre / 2);
-  char* rest = ws + pre;
-  const size_t rest_bytes = ws_bytes - pre;
-  // the minimum-distortion codewords, which centre the backward tangent
-  int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream);
-  if (st != BCJR_OK) return st;
+  char* rest = ws;
+  size_t rest_bytes = ws_bytes;
+  if (!ref) {
+    const size_t pre = hp_prefix_bytes(B, L);
+    if (ws_bytes <= pre) return BCJR_ERR_WORKSPACE;
+    float* w_hard = reinterpret_cast<float*>(ws);
+    int32_t* states = reinterpret_cast<int32_t*>(ws + pre / 2);
+    rest = ws + pre;
+    rest_bytes = ws_bytes - pre;
+    int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream);
+    if (st != BCJR_OK) return st;
+    ref = w_hard;
+  }
   const size_t lds = hp_lds_bytes(f, n, k);
   int herr = 0;
   const int64_t grid = grid_size((const void*)fn, f, lds, B, rest_bytes, lay.slot, &herr);
@@ -319,7 +326,7 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.k2d = 1.4426950408889634074 / (2.0 * Td);
   a.invT = (float)(1.0 / Td);
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
-  a.bref = w_hard;
+  a.bref = ref;
   a.histHB = reinterpret_cast<float*>(p);             p += slots * lay.hist;
   a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;  p += slots * lay.histGA;
   a.xA = reinterpret_cast<float*>(p);                 p += slots * lay.xA;
@@ -338,11 +345,11 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
 }
 
 int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
-           const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
-           void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
+           const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
+           float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
   if (vjp && use_high_precision(T))
-    return run_fb_hp(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace,
+    return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
   const Family f = family(n, k, dc);
@@ -389,6 +396,21 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   return BCJR_OK;
 }
 
+int fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits, int k,
+            float T, const float* grad_w_soft, const float* ref, float* w_soft, float* logZ,
+            float* dW, float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  int st = common_checks(w, B, L, codebook, state_bits, k, true);
+  if (st != BCJR_OK) return st;
+  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
+  if (grad_w_soft && ((uintptr_t)grad_w_soft & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (ref && ((uintptr_t)ref & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return fill_zero(dCodebook, (int64_t)1 << state_bits, stream);
+  if (!w_soft && !logZ && !dW && !dCodebook) return BCJR_OK;
+  return run_fb(w, B, L, codebook, state_bits, k, T, grad_w_soft, ref, w_soft, logZ, dW,
+                dCodebook, workspace, ws_bytes, stream, true);
+}
+
 }  // namespace
 }  // namespace bcjr
 
@@ -431,23 +453,16 @@ int bcjr_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebo
   if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
   if (B > 0 && !w_soft) return BCJR_ERR_INVALID_ARG;
   if (B == 0) return BCJR_OK;
-  return run_fb(w, B, L, codebook, state_bits, k, T, nullptr, w_soft, logZ, nullptr, nullptr,
-                workspace, ws_bytes, stream, false);
+  return run_fb(w, B, L, codebook, state_bits, k, T, nullptr, nullptr, w_soft, logZ, nullptr,
+                nullptr, workspace, ws_bytes, stream, false);
 }
 
 int bcjr_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
                                int state_bits, int k, float T, const float* grad_w_soft,
                                float* w_soft, float* logZ, float* dW, float* dCodebook,
                                void* workspace, size_t ws_bytes, hipStream_t stream) {
-  int st = common_checks(w, B, L, codebook, state_bits, k, true);
-  if (st != BCJR_OK) return st;
-  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
-  if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
-  if (grad_w_soft && ((uintptr_t)grad_w_soft & 3u)) return BCJR_ERR_INVALID_ARG;
-  if (B == 0) return fill_zero(dCodebook, (int64_t)1 << state_bits, stream);
-  if (!w_soft && !logZ && !dW && !dCodebook) return BCJR_OK;
-  return run_fb(w, B, L, codebook, state_bits, k, T, grad_w_soft, w_soft, logZ, dW, dCodebook,
-                workspace, ws_bytes, stream, true);
+  return fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, nullptr, w_soft, logZ, dW,
+                 dCodebook, workspace, ws_bytes, stream);
 }
 
 int bcjr_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
@@ -456,6 +471,14 @@ int bcjr_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* co
                            hipStream_t stream) {
   return bcjr_soft_codeword_fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, nullptr,
                                     nullptr, dW, dCodebook, workspace, ws_bytes, stream);
+}
+
+int bcjr_ste_vjp(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,
+                 int k, float T, const float* w_hard, const float* grad_w_soft, float* dW,
+                 float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (B > 0 && !w_hard) return BCJR_ERR_INVALID_ARG;
+  return fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, w_hard, nullptr, nullptr, dW,
+                 dCodebook, workspace, ws_bytes, stream);
 }
 
 int viterbi_decode(const float* w, int64_t B, int64_t L, const float* codebook, int state_bits,

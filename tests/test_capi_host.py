@@ -35,7 +35,8 @@ def lib():
 def test_library_exports_every_declared_function(lib):
     names = header_functions()
     assert set(names) >= {"bcjr_workspace_bytes", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
-                          "bcjr_soft_codeword_fwd_vjp", "viterbi_decode", "bcjr_status_string"}
+                          "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode",
+                          "bcjr_status_string"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -119,6 +120,15 @@ def test_vjp_and_viterbi_argument_validation(lib):
     v = lib.bcjr_soft_codeword_vjp
     assert v(FAKE, 4, 8, FAKE, 4, 2, 1.0, None, FAKE, None, None, 0, None) == -1
     assert v(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, None, None, None, 0, None) == 0
+    st = lib.bcjr_ste_vjp
+    assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, None, FAKE, FAKE, None, None, 0, None) == -1  # w_hard
+    assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE + 2, FAKE, FAKE, None, None, 0, None) == -1
+    assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, None, FAKE, None, None, 0, None) == -1  # grad
+    assert st(FAKE, 4, 8, FAKE, 4, 2, -1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -1
+    assert st(FAKE, 4, 8, FAKE, 3, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -2
+    assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -3
+    assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, FAKE, None, None, None, 0, None) == 0
+    assert st(FAKE, 0, 8, FAKE, 4, 2, 1.0, None, None, None, None, None, 0, None) == 0
     vd = lib.viterbi_decode
     assert vd(FAKE, 4, 8, FAKE, 4, 2, None, None, FAKE, 1 << 20, None) == -1
     assert vd(FAKE, 4, 8, FAKE, 4, 2, FAKE, None, None, 0, None) == -3
@@ -132,3 +142,16 @@ def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(P, "library_path", lambda: str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         P.load_library()
+
+
+def test_autograd_layer_refuses_host_tensors(lib):
+    """The autograd node has no CPU path: host tensors are an error."""
+    torch = pytest.importorskip("torch")
+    from paper_2605_10655_amd.autograd import BcjrQuant, bcjr_quant
+    w = torch.zeros(2, 8, requires_grad=True)
+    c = torch.zeros(16)
+    for hard in (False, True):
+        with pytest.raises(TypeError):
+            BcjrQuant.apply(w, c, 4, 2, 0.5, hard)
+    with pytest.raises(ValueError):
+        bcjr_quant(torch.zeros(3, 5), c, 4, 2, 0.5, block=4)

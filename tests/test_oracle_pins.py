@@ -310,3 +310,33 @@ def test_oracle_rejects_bad_arguments():
         O.soft_codeword(w, c, 4, 2, 0.0)     # T <= 0
     with pytest.raises(RuntimeError):
         O.soft_codeword(w, c, 4, 2, float("nan"))
+
+
+@pytest.mark.parametrize("n,k,L", [(4, 2, 5), (3, 1, 8), (5, 2, 4), (6, 3, 3)])
+@pytest.mark.parametrize("T", [0.7, 0.1])
+def test_ste_matches_enumeration(n, k, L, T):
+    """BCJR-STE: forward = codeword of the enumerated minimum-distortion path
+    (independent of T); backward = enumerated path covariances at T."""
+    for seed in range(3):
+        w, c, g = _case(n, k, L, 4242 + 31 * seed + n)
+        wh, dW, dc = O.ste(w[None], c, n, k, T, g[None])
+        p, _ = bf.viterbi(w, c, n, k)
+        np.testing.assert_array_equal(wh[0], c[p])
+        ref = bf.expectations(w, c, n, k, T, g)
+        np.testing.assert_allclose(dW[0], ref["dW"], rtol=0, atol=1e-10 * max(1, abs(ref["dW"]).max()))
+        np.testing.assert_allclose(dc, ref["dc"], rtol=0, atol=1e-10 * max(1, abs(ref["dc"]).max()))
+
+
+def test_ste_gradient_couples_neighbours():
+    """The STE backward is the trellis-coupled gradient, not the identity:
+    a unit upstream gradient at step t moves dW at other steps, and its own
+    entry is Var(c(s_t))/T, not 1."""
+    n, k, L, T = 4, 2, 8, 0.3       # 16 * 4^7 enumerated paths
+    w, c, _ = _case(n, k, L, 77)
+    t = 4
+    g = np.zeros(L); g[t] = 1.0
+    _, dW, _ = O.ste(w[None], c, n, k, T, g[None], want_dc=False)
+    ref = bf.expectations(w, c, n, k, T)
+    var_t = (ref["marg"][t] * c * c).sum() - ref["w_soft"][t] ** 2
+    assert abs(dW[0, t] - var_t / T) <= 1e-10 * max(1.0, var_t / T)
+    assert abs(dW[0, t - 1]) > 1e-6 and abs(dW[0, t + 1]) > 1e-6
