@@ -26,6 +26,12 @@
  *     follow recursions with the same weights as the alpha / beta sums;
  *   - Viterbi (Sec. 3.2): min-sum dynamic programming with backtrack.
  * The first state s_1 carries no prior weight: alpha_1(s) = exp(h_1(s)).
+ *
+ * Vector emission (Sec. 3.1, S = 2^{k+V}; Sec. 4.1, the V = 2 trellis): each
+ * step emits V consecutive weights, the codeword c(s) is a V-vector stored at
+ * c[s*V .. s*V+V-1], the step's energy is ||w_t - c(s)||^2 / 2 and F becomes
+ * sum_t <g_t, c(s_t)>; every formula above holds per component.  A block of
+ * L weights then has L/V steps.  V = 1 is the scalar case.
  */
 #include "bcjr_oracle.h"
 
@@ -35,8 +41,9 @@
 #include <string.h>
 
 static int bad_args(int64_t B, int64_t L, const void *w, const void *c, int n,
-                    int k, double T) {
+                    int k, int V, double T) {
   if (B < 0 || L < 1 || !w || !c) return 1;
+  if (V < 1 || V > 8 || L % V) return 1;
   if (k < 1 || n < k || n > 16) return 1;
   if (!(T > 0.0) || !isfinite(T)) return 1;
   return 0;
@@ -50,9 +57,21 @@ static double log_add_exp(double a, double b) {
   return m + log1p(exp(-fabs(a - b)));
 }
 
-static double field(double w, double c, double T) {
-  double d = w - c;
-  return -(d * d) / (2.0 * T);
+/* h_t(s) = -||w_t - c(s)||^2 / (2T) over the V components of step t */
+static double field(const double *w, const double *c, int V, double T) {
+  double e = 0.0;
+  for (int a = 0; a < V; ++a) {
+    double d = w[a] - c[a];
+    e += d * d;
+  }
+  return -e / (2.0 * T);
+}
+
+/* <g_t, c(s)> */
+static double dotv(const double *g, const double *c, int V) {
+  double r = 0.0;
+  for (int a = 0; a < V; ++a) r += g[a] * c[a];
+  return r;
 }
 
 /* ------------------------------------------------------------------ */
@@ -105,12 +124,12 @@ static void work_free(work_t *wk) {
  * w_1..w_t]: A_1(s) = g_1 c(s);
  * A_t(s) = g_t c(s) + sum_{s'->s} alpha_{t-1}(s') A_{t-1}(s') / sum_{s'->s} alpha_{t-1}(s'). */
 static void forward_sweep(const double *w, int64_t L, const double *c, int n,
-                          int k, double T, const double *g, work_t *wk) {
+                          int k, int V, double T, const double *g, work_t *wk) {
   const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
   double *alpha = wk->alpha, *A = wk->A, *acc = wk->acc, *num = wk->num;
   for (int64_t s = 0; s < S; ++s) {
-    alpha[s] = field(w[0], c[s], T);
-    if (g) A[s] = g[0] * c[s];
+    alpha[s] = field(w, c + s * V, V, T);
+    if (g) A[s] = dotv(g, c + s * V, V);
   }
   for (int64_t t = 1; t < L; ++t) {
     const double *ap = alpha + (t - 1) * S;
@@ -122,7 +141,7 @@ static void forward_sweep(const double *w, int64_t L, const double *c, int n,
         int64_t d = ((sp << k) | b) & mask;
         acc[d] = log_add_exp(acc[d], ap[sp]);
       }
-    for (int64_t s = 0; s < S; ++s) at[s] = field(w[t], c[s], T) + acc[s];
+    for (int64_t s = 0; s < S; ++s) at[s] = field(w + t * V, c + s * V, V, T) + acc[s];
     if (g) {
       const double *Ap = A + (t - 1) * S;
       double *At = A + t * S;
@@ -132,7 +151,7 @@ static void forward_sweep(const double *w, int64_t L, const double *c, int n,
           int64_t d = ((sp << k) | b) & mask;
           num[d] += exp(ap[sp] - acc[d]) * Ap[sp];
         }
-      for (int64_t s = 0; s < S; ++s) At[s] = g[t] * c[s] + num[s];
+      for (int64_t s = 0; s < S; ++s) At[s] = dotv(g + t * V, c + s * V, V) + num[s];
     }
   }
 }
@@ -152,21 +171,21 @@ static double lse_row(const double *x, int64_t S) {
  * Eq. beta), and, when g != NULL, the backward conditional expectation
  * B_{t-1}(s) = E[sum_{tau>=t} g_tau c(s_tau) | s_{t-1} = s, w_t..w_L]. */
 static void backward_step(const double *w, int64_t t, const double *c, int n,
-                          int k, double T, const double *g, work_t *wk) {
+                          int k, int V, double T, const double *g, work_t *wk) {
   const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
   for (int64_t s = 0; s < S; ++s) {
     double acc = -INFINITY;
     for (int64_t b = 0; b < K; ++b) {
       int64_t d = ((s << k) | b) & mask;
-      acc = log_add_exp(acc, field(w[t], c[d], T) + wk->beta[d]);
+      acc = log_add_exp(acc, field(w + t * V, c + d * V, V, T) + wk->beta[d]);
     }
     wk->betap[s] = acc;
     if (g) {
       double sum = 0.0;
       for (int64_t b = 0; b < K; ++b) {
         int64_t d = ((s << k) | b) & mask;
-        double r = exp(field(w[t], c[d], T) + wk->beta[d] - acc);
-        sum += r * (g[t] * c[d] + wk->Bc[d]);
+        double r = exp(field(w + t * V, c + d * V, V, T) + wk->beta[d] - acc);
+        sum += r * (dotv(g + t * V, c + d * V, V) + wk->Bc[d]);
       }
       wk->Bp[s] = sum;
     }
@@ -179,40 +198,42 @@ static void backward_step(const double *w, int64_t t, const double *c, int n,
   wk->Bp = tmp;
 }
 
+/* One block of L weights = N = L / V steps.  w_soft, dW: [L]; dc: [S*V]. */
 static void block_run(const double *w, int64_t L, const double *c, int n,
-                      int k, double T, const double *g, double *w_soft,
+                      int k, int V, double T, const double *g, double *w_soft,
                       double *logZ_out, double *dW, double *dc, work_t *wk) {
-  const int64_t S = (int64_t)1 << n;
-  forward_sweep(w, L, c, n, k, T, g, wk);
-  const double *aL = wk->alpha + (L - 1) * S;
-  const double logZ = lse_row(aL, S); /* Z = sum_s alpha_L(s), beta_L = 1 */
+  const int64_t S = (int64_t)1 << n, N = L / V;
+  forward_sweep(w, N, c, n, k, V, T, g, wk);
+  const double *aL = wk->alpha + (N - 1) * S;
+  const double logZ = lse_row(aL, S); /* Z = sum_s alpha_N(s), beta_N = 1 */
   if (logZ_out) *logZ_out = logZ;
-  double EF = 0.0; /* E[F] = sum_s p_L(s) A_L(s) */
+  double EF = 0.0; /* E[F] = sum_s p_N(s) A_N(s) */
   if (g)
-    for (int64_t s = 0; s < S; ++s) EF += exp(aL[s] - logZ) * wk->A[(L - 1) * S + s];
+    for (int64_t s = 0; s < S; ++s) EF += exp(aL[s] - logZ) * wk->A[(N - 1) * S + s];
   for (int64_t s = 0; s < S; ++s) {
-    wk->beta[s] = 0.0; /* log beta_L = 0 */
-    wk->Bc[s] = 0.0;   /* B_L = 0 */
+    wk->beta[s] = 0.0; /* log beta_N = 0 */
+    wk->Bc[s] = 0.0;   /* B_N = 0 */
   }
-  for (int64_t t = L - 1; t >= 0; --t) {
+  for (int64_t t = N - 1; t >= 0; --t) {
     const double *at = wk->alpha + t * S;
-    double ws = 0.0;
-    for (int64_t s = 0; s < S; ++s) {
-      wk->p[s] = exp(at[s] + wk->beta[s] - logZ); /* Eq. marginal */
-      ws += c[s] * wk->p[s];                       /* Eq. soft-codeword */
-    }
-    if (w_soft) w_soft[t] = ws;
-    if (g) {
-      const double *At = wk->A + t * S;
-      double cov = 0.0;
-      for (int64_t s = 0; s < S; ++s) {
-        double X = At[s] + wk->Bc[s] - EF; /* E[F | s_t = s] - E[F] */
-        cov += wk->p[s] * (c[s] - ws) * X;
-        if (dc) dc[s] += wk->p[s] * (g[t] + (w[t] - c[s]) * X / T);
+    for (int64_t s = 0; s < S; ++s) wk->p[s] = exp(at[s] + wk->beta[s] - logZ); /* Eq. marginal */
+    for (int a = 0; a < V; ++a) {
+      double ws = 0.0;
+      for (int64_t s = 0; s < S; ++s) ws += c[s * V + a] * wk->p[s]; /* Eq. soft-codeword */
+      if (w_soft) w_soft[t * V + a] = ws;
+      if (g) {
+        const double *At = wk->A + t * S;
+        double cov = 0.0;
+        for (int64_t s = 0; s < S; ++s) {
+          double X = At[s] + wk->Bc[s] - EF; /* E[F | s_t = s] - E[F] */
+          cov += wk->p[s] * (c[s * V + a] - ws) * X;
+          if (dc)
+            dc[s * V + a] += wk->p[s] * (g[t * V + a] + (w[t * V + a] - c[s * V + a]) * X / T);
+        }
+        if (dW) dW[t * V + a] = cov / T;
       }
-      if (dW) dW[t] = cov / T;
     }
-    if (t > 0) backward_step(w, t, c, n, k, T, g, wk);
+    if (t > 0) backward_step(w, t, c, n, k, V, T, g, wk);
   }
 }
 
@@ -223,7 +244,7 @@ static void block_run(const double *w, int64_t L, const double *c, int n,
 typedef struct {
   const double *w, *c, *g;
   int64_t B, L;
-  int n, k;
+  int n, k, V;
   double T;
   double *w_soft, *logZ, *dW;
   double *dc_part; /* [S] private to this thread, or NULL */
@@ -235,13 +256,13 @@ static void *job_main(void *arg) {
   job_t *j = (job_t *)arg;
   const int64_t S = (int64_t)1 << j->n;
   work_t wk;
-  if (work_alloc(&wk, j->L, S, j->g != NULL) != 0) {
+  if (work_alloc(&wk, j->L / j->V, S, j->g != NULL) != 0) {
     work_free(&wk);
     j->status = -2;
     return NULL;
   }
   for (int64_t b = j->tid; b < j->B; b += j->nthreads) {
-    block_run(j->w + b * j->L, j->L, j->c, j->n, j->k, j->T, j->g ? j->g + b * j->L : NULL,
+    block_run(j->w + b * j->L, j->L, j->c, j->n, j->k, j->V, j->T, j->g ? j->g + b * j->L : NULL,
               j->w_soft ? j->w_soft + b * j->L : NULL, j->logZ ? j->logZ + b : NULL,
               j->dW ? j->dW + b * j->L : NULL, j->dc_part, &wk);
   }
@@ -251,9 +272,9 @@ static void *job_main(void *arg) {
 }
 
 static int run_jobs(const double *w, int64_t B, int64_t L, const double *c,
-                    int n, int k, double T, const double *g, double *w_soft,
+                    int n, int k, int V, double T, const double *g, double *w_soft,
                     double *logZ, double *dW, double *dc, int nthreads) {
-  const int64_t S = (int64_t)1 << n;
+  const int64_t S = ((int64_t)1 << n) * V;  /* dCodebook entries */
   if (nthreads < 1) nthreads = 1;
   if ((int64_t)nthreads > B && B > 0) nthreads = (int)B;
   if (dc)
@@ -270,7 +291,7 @@ static int run_jobs(const double *w, int64_t B, int64_t L, const double *c,
   }
   for (int i = 0; i < nthreads; ++i) {
     job_t *j = &jobs[i];
-    j->w = w; j->c = c; j->g = g; j->B = B; j->L = L; j->n = n; j->k = k;
+    j->w = w; j->c = c; j->g = g; j->B = B; j->L = L; j->n = n; j->k = k; j->V = V;
     j->T = T; j->w_soft = w_soft; j->logZ = logZ; j->dW = dW;
     j->dc_part = dc ? parts + (int64_t)i * S : NULL;
     j->tid = i; j->nthreads = nthreads; j->status = -3;
@@ -290,46 +311,65 @@ static int run_jobs(const double *w, int64_t B, int64_t L, const double *c,
   return status;
 }
 
+int oracle_soft_codeword_v(const double *w, int64_t B, int64_t L, const double *c,
+                           int n, int k, int V, double T, double *w_soft, double *logZ,
+                           int nthreads) {
+  if (bad_args(B, L, w, c, n, k, V, T)) return -1;
+  return run_jobs(w, B, L, c, n, k, V, T, NULL, w_soft, logZ, NULL, NULL, nthreads);
+}
+
 int oracle_soft_codeword(const double *w, int64_t B, int64_t L, const double *c,
                          int n, int k, double T, double *w_soft, double *logZ,
                          int nthreads) {
-  if (bad_args(B, L, w, c, n, k, T)) return -1;
-  return run_jobs(w, B, L, c, n, k, T, NULL, w_soft, logZ, NULL, NULL, nthreads);
+  return oracle_soft_codeword_v(w, B, L, c, n, k, 1, T, w_soft, logZ, nthreads);
+}
+
+int oracle_soft_codeword_vjp_v(const double *w, int64_t B, int64_t L,
+                               const double *c, int n, int k, int V, double T,
+                               const double *g, double *w_soft, double *logZ,
+                               double *dW, double *dc, int nthreads) {
+  if (bad_args(B, L, w, c, n, k, V, T) || !g) return -1;
+  return run_jobs(w, B, L, c, n, k, V, T, g, w_soft, logZ, dW, dc, nthreads);
 }
 
 int oracle_soft_codeword_vjp(const double *w, int64_t B, int64_t L,
                              const double *c, int n, int k, double T,
                              const double *g, double *w_soft, double *logZ,
                              double *dW, double *dc, int nthreads) {
-  if (bad_args(B, L, w, c, n, k, T) || !g) return -1;
-  return run_jobs(w, B, L, c, n, k, T, g, w_soft, logZ, dW, dc, nthreads);
+  return oracle_soft_codeword_vjp_v(w, B, L, c, n, k, 1, T, g, w_soft, logZ, dW, dc, nthreads);
+}
+
+int oracle_block_tables_v(const double *w, int64_t L, const double *c, int n,
+                          int k, int V, double T, const double *g, double *alpha,
+                          double *beta, double *A, double *Bt) {
+  if (bad_args(1, L, w, c, n, k, V, T) || !alpha || !beta) return -1;
+  if (g && (!A || !Bt)) return -1;
+  const int64_t S = (int64_t)1 << n, N = L / V;
+  work_t wk;
+  if (work_alloc(&wk, N, S, g != NULL) != 0) {
+    work_free(&wk);
+    return -2;
+  }
+  forward_sweep(w, N, c, n, k, V, T, g, &wk);
+  memcpy(alpha, wk.alpha, sizeof(double) * (size_t)(N * S));
+  if (g) memcpy(A, wk.A, sizeof(double) * (size_t)(N * S));
+  for (int64_t s = 0; s < S; ++s) {
+    wk.beta[s] = 0.0;
+    wk.Bc[s] = 0.0;
+  }
+  for (int64_t t = N - 1; t >= 0; --t) {
+    memcpy(beta + t * S, wk.beta, sizeof(double) * (size_t)S);
+    if (g) memcpy(Bt + t * S, wk.Bc, sizeof(double) * (size_t)S);
+    if (t > 0) backward_step(w, t, c, n, k, V, T, g, &wk);
+  }
+  work_free(&wk);
+  return 0;
 }
 
 int oracle_block_tables(const double *w, int64_t L, const double *c, int n,
                         int k, double T, const double *g, double *alpha,
                         double *beta, double *A, double *Bt) {
-  if (bad_args(1, L, w, c, n, k, T) || !alpha || !beta) return -1;
-  if (g && (!A || !Bt)) return -1;
-  const int64_t S = (int64_t)1 << n;
-  work_t wk;
-  if (work_alloc(&wk, L, S, g != NULL) != 0) {
-    work_free(&wk);
-    return -2;
-  }
-  forward_sweep(w, L, c, n, k, T, g, &wk);
-  memcpy(alpha, wk.alpha, sizeof(double) * (size_t)(L * S));
-  if (g) memcpy(A, wk.A, sizeof(double) * (size_t)(L * S));
-  for (int64_t s = 0; s < S; ++s) {
-    wk.beta[s] = 0.0;
-    wk.Bc[s] = 0.0;
-  }
-  for (int64_t t = L - 1; t >= 0; --t) {
-    memcpy(beta + t * S, wk.beta, sizeof(double) * (size_t)S);
-    if (g) memcpy(Bt + t * S, wk.Bc, sizeof(double) * (size_t)S);
-    if (t > 0) backward_step(w, t, c, n, k, T, g, &wk);
-  }
-  work_free(&wk);
-  return 0;
+  return oracle_block_tables_v(w, L, c, n, k, 1, T, g, alpha, beta, A, Bt);
 }
 
 /* ------------------------------------------------------------------ */
@@ -339,24 +379,32 @@ int oracle_block_tables(const double *w, int64_t L, const double *c, int n,
 typedef struct {
   const double *w, *c;
   int64_t B, L;
-  int n, k;
+  int n, k, V;
   int32_t *states;
   double *cost;
   int tid, nthreads, status;
 } vjob_t;
 
-/* squared distortion, multiply and add rounded separately (no fused ops;
- * the file is compiled with -ffp-contract=off) */
-static double sqdist(double w, double c) {
-  double d = w - c;
-  return d * d;
+/* squared distortion of one step, ||w_t - c(s)||^2: each square rounded,
+ * then added in component order (no fused ops; the file is compiled with
+ * -ffp-contract=off).  For V = 1 it is the plain (w - c)^2. */
+static double sqdist(const double *w, const double *c, int V) {
+  double d = w[0] - c[0];
+  double e = d * d;
+  for (int a = 1; a < V; ++a) {
+    double da = w[a] - c[a];
+    e = e + da * da;
+  }
+  return e;
 }
 
+/* One block of L weights, N = L / V steps; states[N]. */
 static void viterbi_block(const double *w, int64_t L, const double *c, int n,
-                          int k, int32_t *states, double *cost, double *m,
+                          int k, int V, int32_t *states, double *cost, double *m,
                           double *mn, double *best, int32_t *from) {
   const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
-  for (int64_t s = 0; s < S; ++s) m[s] = sqdist(w[0], c[s]);
+  L /= V;
+  for (int64_t s = 0; s < S; ++s) m[s] = sqdist(w, c + s * V, V);
   for (int64_t t = 1; t < L; ++t) {
     int32_t *ft = from + t * S;
     for (int64_t s = 0; s < S; ++s) {
@@ -373,7 +421,7 @@ static void viterbi_block(const double *w, int64_t L, const double *c, int n,
           ft[d] = (int32_t)sp;
         }
       }
-    for (int64_t s = 0; s < S; ++s) mn[s] = sqdist(w[t], c[s]) + best[s];
+    for (int64_t s = 0; s < S; ++s) mn[s] = sqdist(w + t * V, c + s * V, V) + best[s];
     double *tmp = m;
     m = mn;
     mn = tmp;
@@ -392,12 +440,12 @@ static void *vjob_main(void *arg) {
   double *m = (double *)malloc(sizeof(double) * (size_t)S);
   double *mn = (double *)malloc(sizeof(double) * (size_t)S);
   double *best = (double *)malloc(sizeof(double) * (size_t)S);
-  int32_t *from = (int32_t *)malloc(sizeof(int32_t) * (size_t)(j->L * S));
+  int32_t *from = (int32_t *)malloc(sizeof(int32_t) * (size_t)(j->L / j->V * S));
   if (!m || !mn || !best || !from) {
     j->status = -2;
   } else {
     for (int64_t b = j->tid; b < j->B; b += j->nthreads)
-      viterbi_block(j->w + b * j->L, j->L, j->c, j->n, j->k, j->states + b * j->L,
+      viterbi_block(j->w + b * j->L, j->L, j->c, j->n, j->k, j->V, j->states + b * (j->L / j->V),
                     j->cost ? j->cost + b : NULL, m, mn, best, from);
     j->status = 0;
   }
@@ -408,9 +456,9 @@ static void *vjob_main(void *arg) {
   return NULL;
 }
 
-int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
-                   int n, int k, int32_t *states, double *cost, int nthreads) {
-  if (bad_args(B, L, w, c, n, k, 1.0) || !states) return -1;
+int oracle_viterbi_v(const double *w, int64_t B, int64_t L, const double *c,
+                     int n, int k, int V, int32_t *states, double *cost, int nthreads) {
+  if (bad_args(B, L, w, c, n, k, V, 1.0) || !states) return -1;
   if (B == 0) return 0;
   if (nthreads < 1) nthreads = 1;
   if ((int64_t)nthreads > B) nthreads = (int)B;
@@ -423,7 +471,7 @@ int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
   }
   for (int i = 0; i < nthreads; ++i) {
     vjob_t *j = &jobs[i];
-    j->w = w; j->c = c; j->B = B; j->L = L; j->n = n; j->k = k;
+    j->w = w; j->c = c; j->B = B; j->L = L; j->n = n; j->k = k; j->V = V;
     j->states = states; j->cost = cost; j->tid = i; j->nthreads = nthreads;
     j->status = -3;
   }
@@ -436,4 +484,9 @@ int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
   free(jobs);
   free(th);
   return status;
+}
+
+int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
+                   int n, int k, int32_t *states, double *cost, int nthreads) {
+  return oracle_viterbi_v(w, B, L, c, n, k, 1, states, cost, nthreads);
 }

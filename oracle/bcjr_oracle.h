@@ -59,6 +59,27 @@ int oracle_block_tables(const double *w, int64_t L, const double *c, int n,
                         int k, double T, const double *g, double *alpha,
                         double *beta, double *A, double *Bt);
 
+/* Vector emission (Sec. 3.1, S = 2^{k+V}; the V = 2 trellis of Sec. 4.1):
+ * the same four functions with V weights per step.  L counts weights and
+ * must be a multiple of V (L / V steps); the codebook is c[S*V] with the
+ * V-vector of state s at c[s*V ..]; dc is [S*V]; states is [B*(L/V)];
+ * alpha, beta, A, Bt are [(L/V)*S].  Energy ||w_t - c(s)||^2 / 2 per step;
+ * the Viterbi step distortion adds the V rounded squares in component
+ * order.  The functions above are these with V = 1. */
+int oracle_soft_codeword_v(const double *w, int64_t B, int64_t L, const double *c,
+                           int n, int k, int V, double T, double *w_soft,
+                           double *logZ, int nthreads);
+int oracle_soft_codeword_vjp_v(const double *w, int64_t B, int64_t L,
+                               const double *c, int n, int k, int V, double T,
+                               const double *g, double *w_soft, double *logZ,
+                               double *dW, double *dc, int nthreads);
+int oracle_viterbi_v(const double *w, int64_t B, int64_t L, const double *c,
+                     int n, int k, int V, int32_t *states, double *cost,
+                     int nthreads);
+int oracle_block_tables_v(const double *w, int64_t L, const double *c, int n,
+                          int k, int V, double T, const double *g, double *alpha,
+                          double *beta, double *A, double *Bt);
+
 #ifdef __cplusplus
 }
 #endif

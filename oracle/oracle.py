@@ -46,8 +46,14 @@ def lib():
         L.oracle_soft_codeword_vjp.argtypes = [dp, i64, i64, dp, ci, ci, cd, dp, dp, dp, dp, dp, ci]
         L.oracle_viterbi.argtypes = [dp, i64, i64, dp, ci, ci, ip, dp, ci]
         L.oracle_block_tables.argtypes = [dp, i64, dp, ci, ci, cd, dp, dp, dp, dp, dp]
+        L.oracle_soft_codeword_v.argtypes = [dp, i64, i64, dp, ci, ci, ci, cd, dp, dp, ci]
+        L.oracle_soft_codeword_vjp_v.argtypes = [dp, i64, i64, dp, ci, ci, ci, cd, dp, dp, dp, dp,
+                                                 dp, ci]
+        L.oracle_viterbi_v.argtypes = [dp, i64, i64, dp, ci, ci, ci, ip, dp, ci]
+        L.oracle_block_tables_v.argtypes = [dp, i64, dp, ci, ci, ci, cd, dp, dp, dp, dp, dp]
         for f in (L.oracle_soft_codeword, L.oracle_soft_codeword_vjp, L.oracle_viterbi,
-                  L.oracle_block_tables):
+                  L.oracle_block_tables, L.oracle_soft_codeword_v, L.oracle_soft_codeword_vjp_v,
+                  L.oracle_viterbi_v, L.oracle_block_tables_v):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -75,77 +81,90 @@ def _check(rc, name):
         raise RuntimeError(f"{name} failed with status {rc}")
 
 
-def soft_codeword(w, c, n, k, T, nthreads=None):
-    """w[B, L] -> (w_soft[B, L] float64, logZ[B] float64)."""
+def _codebook(c, n, V):
+    """Codebook as a flat float64 array of S*V values (state-major)."""
+    c = _d(c).reshape(-1)
+    if c.size != (1 << n) * V:
+        raise ValueError(f"codebook must hold {1 << n} x {V} values, got {c.size}")
+    return c
+
+
+def soft_codeword(w, c, n, k, T, nthreads=None, V=1):
+    """w[B, L] -> (w_soft[B, L] float64, logZ[B] float64).  With V > 1 each
+    step emits V consecutive weights and c is [S, V] (or flat, state-major)."""
     w = _d(w)
-    c = _d(c)
+    c = _codebook(c, n, V)
     B, L = w.shape
     ws = np.empty((B, L), np.float64)
     lz = np.empty((B,), np.float64)
-    rc = lib().oracle_soft_codeword(_ptr(w), B, L, _ptr(c), n, k, float(T), _ptr(ws),
-                                    _ptr(lz), nthreads or default_threads())
-    _check(rc, "oracle_soft_codeword")
+    rc = lib().oracle_soft_codeword_v(_ptr(w), B, L, _ptr(c), n, k, V, float(T), _ptr(ws),
+                                      _ptr(lz), nthreads or default_threads())
+    _check(rc, "oracle_soft_codeword_v")
     return ws, lz
 
 
-def soft_codeword_vjp(w, c, n, k, T, g, want_dc=True, nthreads=None):
+def soft_codeword_vjp(w, c, n, k, T, g, want_dc=True, nthreads=None, V=1):
     """Returns (w_soft, logZ, dW, dc) in float64; dc is summed over blocks
-    (None when want_dc is False)."""
+    (None when want_dc is False) and has the codebook's shape."""
+    shape = np.shape(c)
     w = _d(w)
-    c = _d(c)
+    c = _codebook(c, n, V)
     g = _d(g)
     B, L = w.shape
     assert g.shape == (B, L)
     ws = np.empty((B, L), np.float64)
     lz = np.empty((B,), np.float64)
     dW = np.empty((B, L), np.float64)
-    dc = np.empty((1 << n,), np.float64) if want_dc else None
-    rc = lib().oracle_soft_codeword_vjp(_ptr(w), B, L, _ptr(c), n, k, float(T), _ptr(g),
-                                        _ptr(ws), _ptr(lz), _ptr(dW), _ptr(dc),
-                                        nthreads or default_threads())
-    _check(rc, "oracle_soft_codeword_vjp")
-    return ws, lz, dW, dc
+    dc = np.empty(c.size, np.float64) if want_dc else None
+    rc = lib().oracle_soft_codeword_vjp_v(_ptr(w), B, L, _ptr(c), n, k, V, float(T), _ptr(g),
+                                          _ptr(ws), _ptr(lz), _ptr(dW), _ptr(dc),
+                                          nthreads or default_threads())
+    _check(rc, "oracle_soft_codeword_vjp_v")
+    return ws, lz, dW, (dc.reshape(shape) if want_dc else None)
 
 
-def viterbi(w, c, n, k, nthreads=None):
-    """w[B, L] -> (states[B, L] int32, cost[B] float64)."""
+def viterbi(w, c, n, k, nthreads=None, V=1):
+    """w[B, L] -> (states[B, L // V] int32, cost[B] float64)."""
     w = _d(w)
-    c = _d(c)
+    c = _codebook(c, n, V)
     B, L = w.shape
-    st = np.empty((B, L), np.int32)
+    st = np.empty((B, L // V), np.int32)
     cost = np.empty((B,), np.float64)
-    rc = lib().oracle_viterbi(_ptr(w), B, L, _ptr(c), n, k, _ptr(st, ctypes.c_int32),
-                              _ptr(cost), nthreads or default_threads())
-    _check(rc, "oracle_viterbi")
+    rc = lib().oracle_viterbi_v(_ptr(w), B, L, _ptr(c), n, k, V, _ptr(st, ctypes.c_int32),
+                                _ptr(cost), nthreads or default_threads())
+    _check(rc, "oracle_viterbi_v")
     return st, cost
 
 
-def ste(w, c, n, k, T, g, want_dc=True, nthreads=None):
+def ste(w, c, n, k, T, g, want_dc=True, nthreads=None, V=1):
     """BCJR-STE (paper Sec. 3.5 and Sec. "BCJR-STE variant"): the forward
     output is the hard codeword c(s_t) of the minimum-distortion path
     (Sec. 3.2) and the backward pass is the VJP of the temperature-T soft
     codeword (Sec. 3.5), not an identity.  Returns (w_hard[B, L], dW[B, L],
     dc[S] or None) in float64."""
-    st, _ = viterbi(w, c, n, k, nthreads)
-    _, _, dW, dc = soft_codeword_vjp(w, c, n, k, T, g, want_dc, nthreads)
-    return _d(c)[st], dW, dc
+    st, _ = viterbi(w, c, n, k, nthreads, V)
+    _, _, dW, dc = soft_codeword_vjp(w, c, n, k, T, g, want_dc, nthreads, V)
+    wh = _codebook(c, n, V).reshape(-1, V)[st].reshape(np.shape(w))
+    return wh, dW, dc
 
 
-def block_tables(w_block, c, n, k, T, g_block=None):
-    """One block: (log alpha[L, S], log beta[L, S], A[L, S] | None, B[L, S] | None)."""
+def block_tables(w_block, c, n, k, T, g_block=None, V=1):
+    """One block: (log alpha[N, S], log beta[N, S], A[N, S] | None, B[N, S] | None),
+    N = L / V steps."""
     w = _d(w_block).reshape(-1)
-    c = _d(c)
+    c = _codebook(c, n, V)
     L = w.shape[0]
+    N = L // V
     S = 1 << n
-    al = np.empty((L, S), np.float64)
-    be = np.empty((L, S), np.float64)
+    al = np.empty((N, S), np.float64)
+    be = np.empty((N, S), np.float64)
     A = Bt = None
     g = None
     if g_block is not None:
         g = _d(g_block).reshape(-1)
-        A = np.empty((L, S), np.float64)
-        Bt = np.empty((L, S), np.float64)
-    rc = lib().oracle_block_tables(_ptr(w), L, _ptr(c), n, k, float(T), _ptr(g), _ptr(al),
-                                   _ptr(be), _ptr(A), _ptr(Bt))
-    _check(rc, "oracle_block_tables")
+        A = np.empty((N, S), np.float64)
+        Bt = np.empty((N, S), np.float64)
+    rc = lib().oracle_block_tables_v(_ptr(w), L, _ptr(c), n, k, V, float(T), _ptr(g), _ptr(al),
+                                     _ptr(be), _ptr(A), _ptr(Bt))
+    _check(rc, "oracle_block_tables_v")
     return al, be, A, Bt

@@ -340,3 +340,119 @@ def test_ste_gradient_couples_neighbours():
     var_t = (ref["marg"][t] * c * c).sum() - ref["w_soft"][t] ** 2
     assert abs(dW[0, t] - var_t / T) <= 1e-10 * max(1.0, var_t / T)
     assert abs(dW[0, t - 1]) > 1e-6 and abs(dW[0, t + 1]) > 1e-6
+
+
+# ---------------------------------------------------------------- V = 2
+# Vector emission (Sec. 3.1 with V = 2; the kV = 4, 16-predecessor trellis of
+# Sec. 4.1 is (n, k) = (16, 4)).  (n, k, L weights): K = 16 cases keep the
+# enumeration small (S * 16^(N-1) paths).
+VEC = [(8, 4, 4), (6, 4, 6), (4, 4, 6), (4, 2, 8), (3, 1, 10), (5, 2, 6)]
+
+
+def _vcase(n, L, seed, V=2):
+    r = np.random.default_rng(seed)
+    return r.standard_normal(L), r.standard_normal((1 << n, V)), r.standard_normal(L)
+
+
+@pytest.mark.parametrize("n,k,L", VEC)
+@pytest.mark.parametrize("T", [1.0, 0.2])
+def test_vector_emission_matches_enumeration(n, k, L, T):
+    for seed in range(2):
+        w, c, g = _vcase(n, L, 900 + 17 * seed + n * k)
+        ws, lz, dW, dc = O.soft_codeword_vjp(w[None], c, n, k, T, g[None], V=2)
+        ref = bf.expectations(w, c, n, k, T, g, V=2)
+        tol = lambda a: 1e-10 * max(1.0, np.abs(a).max())
+        assert abs(lz[0] - ref["logZ"]) <= 1e-10 * max(1.0, abs(ref["logZ"]))
+        np.testing.assert_allclose(ws[0], ref["w_soft"], rtol=0, atol=1e-11)
+        np.testing.assert_allclose(dW[0], ref["dW"], rtol=0, atol=tol(ref["dW"]))
+        np.testing.assert_allclose(dc, ref["dc"], rtol=0, atol=tol(ref["dc"]))
+        al, be, _, _ = O.block_tables(w, c, n, k, T, V=2)
+        marg = np.exp(al + be - lz[0])
+        np.testing.assert_allclose(marg, ref["marg"], rtol=0, atol=1e-11)
+
+
+@pytest.mark.parametrize("n,k,T", [(8, 4, 0.3), (6, 2, 0.5)])
+def test_vector_vjp_matches_finite_differences(n, k, T):
+    B, L, h = 2, 12, 1e-5
+    r = np.random.default_rng(31 * n + k)
+    c = r.standard_normal((1 << n, 2))
+    w = r.standard_normal((B, L))
+    g = r.standard_normal((B, L))
+    _, _, dW, dc = O.soft_codeword_vjp(w, c, n, k, T, g, V=2)
+
+    def gdot(w_, c_):
+        return (O.soft_codeword(w_, c_, n, k, T, V=2)[0] * g).sum()
+
+    for b in range(B):
+        for t in range(L):
+            wp = w.copy(); wp[b, t] += h
+            wm = w.copy(); wm[b, t] -= h
+            fd = (gdot(wp, c) - gdot(wm, c)) / (2 * h)
+            assert abs(dW[b, t] - fd) <= 2e-7 * max(1, abs(fd)), (b, t, dW[b, t], fd)
+    for s in r.choice(1 << n, size=8, replace=False):
+        for comp in range(2):
+            cp = c.copy(); cp[s, comp] += h
+            cm = c.copy(); cm[s, comp] -= h
+            fd = (gdot(w, cp) - gdot(w, cm)) / (2 * h)
+            assert abs(dc[s, comp] - fd) <= 2e-7 * max(1, abs(fd)), (s, comp, dc[s, comp], fd)
+
+
+def test_vector_emission_with_constant_component_reduces_to_scalar():
+    """c(s) = (c0(s), const): the second weights of every step see the same
+    energy on every path, so the distribution is the scalar trellis on the
+    first weights; the second components' soft codeword is the constant and
+    their dW is 0."""
+    n, k, L, T = 8, 4, 16, 0.25
+    r = np.random.default_rng(5)
+    c0 = r.standard_normal(1 << n)
+    c = np.stack([c0, np.full(1 << n, 0.375)], axis=1)
+    w = r.standard_normal((3, L))
+    g = r.standard_normal((3, L))
+    ws, lz, dW, dc = O.soft_codeword_vjp(w, c, n, k, T, g, V=2)
+    ws1, lz1, dW1, dc1 = O.soft_codeword_vjp(w[:, 0::2], c0, n, k, T, g[:, 0::2])
+    np.testing.assert_allclose(ws[:, 0::2], ws1, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ws[:, 1::2], 0.375, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dW[:, 0::2], dW1, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dW[:, 1::2], 0.0, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dc[:, 0], dc1, rtol=0, atol=1e-11)
+    # logZ differs by the constant energy of the second weights
+    shift = -(((w[:, 1::2] - 0.375) ** 2).sum(1)) / (2 * T)
+    np.testing.assert_allclose(lz, lz1 + shift, rtol=0, atol=1e-10)
+    # dc of the constant component: sum over steps of g_t,1 + (w_t,1 - c)(...)
+    # only its total over states is fixed: sum_s p_t(s) = 1 at every step
+    np.testing.assert_allclose(dc[:, 1].sum(), g[:, 1::2].sum(), rtol=0, atol=1e-9)
+
+
+@pytest.mark.parametrize("n,k,L", [(8, 4, 6), (4, 4, 8), (5, 2, 10), (3, 1, 12)])
+def test_vector_viterbi_matches_enumeration(n, k, L):
+    r = np.random.default_rng(n * 13 + L)
+    for _ in range(3):
+        w, c, _ = _vcase(n, L, int(r.integers(1 << 30)))
+        st, cost = O.viterbi(w[None], c, n, k, V=2)
+        p, best = bf.viterbi_vec(w, c, n, k, 2)
+        np.testing.assert_array_equal(st[0], p)
+        assert cost[0] == best
+
+
+@pytest.mark.parametrize("n,k,L", [(8, 4, 6), (4, 2, 8)])
+def test_vector_viterbi_tie_break_rule(n, k, L):
+    """Dyadic values (every sum exact): many exact ties, resolved to the
+    reverse-lexicographically smallest optimal path."""
+    r = np.random.default_rng(n + k + L + 1)
+    for _ in range(4):
+        c = r.integers(-3, 4, (1 << n, 2)) / 4.0
+        w = r.integers(-6, 7, L) / 8.0
+        st, cost = O.viterbi(w[None], c, n, k, V=2)
+        p, best = bf.viterbi_vec(w, c, n, k, 2)
+        np.testing.assert_array_equal(st[0], p)
+        assert cost[0] == best
+
+
+def test_vector_ste_composition():
+    n, k, L, T = 6, 4, 6, 0.4
+    w, c, g = _vcase(n, L, 4711)
+    wh, dW, dc = O.ste(w[None], c, n, k, T, g[None], V=2)
+    p, _ = bf.viterbi_vec(w, c, n, k, 2)
+    np.testing.assert_array_equal(wh[0], c[p].reshape(-1))
+    ref = bf.expectations(w, c, n, k, T, g, V=2)
+    np.testing.assert_allclose(dW[0], ref["dW"], rtol=0, atol=1e-10 * max(1, abs(ref["dW"]).max()))
