@@ -124,6 +124,46 @@ int viterbi_decode(const float *w, int64_t B, int64_t L, const float *codebook,
                    int state_bits, int k, int32_t *states, float *w_hard, void *workspace,
                    size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------
+ * Vector emission (Sec. 3.1: S = 2^{k+V} with V weights per step; Sec. 4.1
+ * and Sec. 4.4 use V = 2 with 4 bits per step, i.e. 16 predecessors per
+ * state and 128 steps per 256-weight block).  Each step emits V consecutive
+ * weights of the block and each state a V-vector codeword:
+ *     h_t(s) = -||w_t - c(s)||^2 / (2T),   w_t = w[t*V .. t*V + V-1],
+ * and k here is the number of bits shifted per step.  L counts weights and
+ * must be a multiple of V (L / V steps).  codebook and dCodebook are
+ * [S*V], the V-vector of state s at [s*V ..]; w_soft, dW, w_hard are
+ * [B*L]; states is [B*(L/V)].  The Viterbi step distortion adds the V
+ * rounded squares in component order.
+ *
+ * V = 1 calls the scalar entry points above with the same arguments.
+ * V = 2 supports k = 4 and 8 <= state_bits <= 16 (L/2 steps up to 65535 at
+ * state_bits 16); other shapes return BCJR_ERR_UNSUPPORTED.  The V = 2 VJP
+ * runs in fp32 and accepts T >= 0.04 (the double-float variant of the
+ * scalar trellis is not built for it): below, BCJR_ERR_UNSUPPORTED.  The
+ * soft codeword and Viterbi take any T > 0.  Workspace: as reported by
+ * bcjr_vec_workspace_bytes for the same op codes.  All other conventions
+ * are those of the scalar entry points. */
+size_t bcjr_vec_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int V, int op);
+
+int bcjr_vec_soft_codeword(const float *w, int64_t B, int64_t L, const float *codebook,
+                           int state_bits, int k, int V, float T, float *w_soft, float *logZ,
+                           void *workspace, size_t ws_bytes, hipStream_t stream);
+
+int bcjr_vec_soft_codeword_vjp(const float *w, int64_t B, int64_t L, const float *codebook,
+                               int state_bits, int k, int V, float T, const float *grad_w_soft,
+                               float *dW, float *dCodebook, void *workspace, size_t ws_bytes,
+                               hipStream_t stream);
+
+int bcjr_vec_soft_codeword_fwd_vjp(const float *w, int64_t B, int64_t L, const float *codebook,
+                                   int state_bits, int k, int V, float T, const float *grad_w_soft,
+                                   float *w_soft, float *logZ, float *dW, float *dCodebook,
+                                   void *workspace, size_t ws_bytes, hipStream_t stream);
+
+int bcjr_vec_viterbi_decode(const float *w, int64_t B, int64_t L, const float *codebook,
+                            int state_bits, int k, int V, int32_t *states, float *w_hard,
+                            void *workspace, size_t ws_bytes, hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char *bcjr_status_string(int status);
 

@@ -16,6 +16,12 @@ Functions keep the C names:
     bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, g)       -> (dW, dCodebook)
     viterbi_decode(w, codebook, state_bits, k)                   -> (states, w_hard)
     bcjr_workspace_bytes(B, L, state_bits, k, op)                -> int
+and the vector-emission forms (V weights per step, codebook [S, V]):
+    bcjr_vec_soft_codeword(w, codebook, state_bits, k, V, T)          -> (w_soft, logZ)
+    bcjr_vec_soft_codeword_vjp(w, codebook, state_bits, k, V, T, g)   -> (dW, dCodebook)
+    bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, g)
+    bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V)            -> (states, w_hard)
+    bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op)              -> int
 """
 from __future__ import annotations
 
@@ -25,7 +31,9 @@ import os
 __all__ = [
     "BcjrError", "OP_FWD", "OP_VJP", "OP_FWD_VJP", "OP_VITERBI", "library_path", "load_library",
     "bcjr_workspace_bytes", "bcjr_status_string", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
-    "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode",
+    "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode", "bcjr_vec_workspace_bytes",
+    "bcjr_vec_soft_codeword", "bcjr_vec_soft_codeword_vjp", "bcjr_vec_soft_codeword_fwd_vjp",
+    "bcjr_vec_viterbi_decode",
 ]
 
 OP_FWD, OP_VJP, OP_FWD_VJP, OP_VITERBI = 0, 1, 2, 3
@@ -67,8 +75,18 @@ def load_library():
                                              sz, vp]
     L.bcjr_ste_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
     L.viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, vp, vp, vp, sz, vp]
+    L.bcjr_vec_workspace_bytes.argtypes = [i64, i64, ci, ci, ci, ci]
+    L.bcjr_vec_workspace_bytes.restype = sz
+    L.bcjr_vec_soft_codeword.argtypes = [vp, i64, i64, vp, ci, ci, ci, cf, vp, vp, vp, sz, vp]
+    L.bcjr_vec_soft_codeword_vjp.argtypes = [vp, i64, i64, vp, ci, ci, ci, cf, vp, vp, vp, vp, sz,
+                                             vp]
+    L.bcjr_vec_soft_codeword_fwd_vjp.argtypes = [vp, i64, i64, vp, ci, ci, ci, cf, vp, vp, vp, vp,
+                                                 vp, vp, sz, vp]
+    L.bcjr_vec_viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, ci, vp, vp, vp, sz, vp]
     for f in (L.bcjr_soft_codeword, L.bcjr_soft_codeword_vjp, L.bcjr_soft_codeword_fwd_vjp,
-              L.bcjr_ste_vjp, L.viterbi_decode):
+              L.bcjr_ste_vjp, L.viterbi_decode, L.bcjr_vec_soft_codeword,
+              L.bcjr_vec_soft_codeword_vjp, L.bcjr_vec_soft_codeword_fwd_vjp,
+              L.bcjr_vec_viterbi_decode):
         f.restype = ci
     _lib = L
     return L
@@ -239,4 +257,105 @@ def viterbi_decode(w, codebook, state_bits, k, *, want_w_hard=True, states=None,
     rc = lib.viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, _ptr(states),
                             _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
     _raise("viterbi_decode", rc)
+    return states, w_hard
+
+
+# ---------------------------------------------------------------- vector emission
+def bcjr_vec_workspace_bytes(B: int, L: int, state_bits: int, k: int, V: int, op: int) -> int:
+    return int(load_library().bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op))
+
+
+def _vec_codebook(codebook, state_bits, V):
+    S = 1 << state_bits
+    if codebook.numel() != S * V:
+        raise ValueError(f"codebook must hold {S} x {V} values, got {tuple(codebook.shape)}")
+    _check_in("codebook", codebook)
+
+
+def _vec_workspace(workspace, B, L, state_bits, k, V, op, device):
+    torch = _torch()
+    if workspace is not None:
+        return workspace
+    nbytes = bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op)
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def bcjr_vec_soft_codeword(w, codebook, state_bits, k, V, T, *, w_soft=None, logZ=None,
+                           want_logZ=True, workspace=None, stream=None):
+    """Soft codeword w_soft[B, L] and logZ[B] with V weights per step."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _vec_codebook(codebook, state_bits, V)
+    if w_soft is None:
+        w_soft = torch.empty_like(w)
+    if logZ is None and want_logZ:
+        logZ = torch.empty(B, dtype=torch.float32, device=w.device)
+    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_FWD, w.device)
+    rc = lib.bcjr_vec_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, float(T),
+                                    _ptr(w_soft), _ptr(logZ), _ptr(ws), ws.numel(), _stream(stream))
+    _raise("bcjr_vec_soft_codeword", rc)
+    return w_soft, logZ
+
+
+def bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, grad_w_soft, *,
+                                   want_w_soft=True, want_logZ=True, want_dW=True,
+                                   want_dCodebook=True, w_soft=None, logZ=None, dW=None,
+                                   dCodebook=None, workspace=None, stream=None):
+    """(w_soft, logZ, dW, dCodebook) with V weights per step; dCodebook has
+    the codebook's shape."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _vec_codebook(codebook, state_bits, V)
+    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    dev = w.device
+    if w_soft is None and want_w_soft:
+        w_soft = torch.empty_like(w)
+    if logZ is None and want_logZ:
+        logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    if dW is None and want_dW:
+        dW = torch.empty_like(w)
+    if dCodebook is None and want_dCodebook:
+        dCodebook = torch.empty_like(codebook)
+    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_FWD_VJP, dev)
+    rc = lib.bcjr_vec_soft_codeword_fwd_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, V,
+                                            float(T), _ptr(grad_w_soft), _ptr(w_soft), _ptr(logZ),
+                                            _ptr(dW), _ptr(dCodebook), _ptr(ws), ws.numel(),
+                                            _stream(stream))
+    _raise("bcjr_vec_soft_codeword_fwd_vjp", rc)
+    return w_soft, logZ, dW, dCodebook
+
+
+def bcjr_vec_soft_codeword_vjp(w, codebook, state_bits, k, V, T, grad_w_soft, *, want_dW=True,
+                               want_dCodebook=True, dW=None, dCodebook=None, workspace=None,
+                               stream=None):
+    """(dW or None, dCodebook or None) with V weights per step."""
+    out = bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, grad_w_soft,
+                                         want_w_soft=False, want_logZ=False, want_dW=want_dW,
+                                         want_dCodebook=want_dCodebook, dW=dW, dCodebook=dCodebook,
+                                         workspace=workspace, stream=stream)
+    return out[2], out[3]
+
+
+def bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V, *, want_w_hard=True, states=None,
+                            w_hard=None, workspace=None, stream=None):
+    """(states[B, L // V] int32, w_hard[B, L] or None) with V weights per step."""
+    torch = _torch()
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    _vec_codebook(codebook, state_bits, V)
+    if L % V:
+        raise ValueError(f"L = {L} is not a multiple of V = {V}")
+    if states is None:
+        states = torch.empty((B, L // V), dtype=torch.int32, device=w.device)
+    if w_hard is None and want_w_hard:
+        w_hard = torch.empty_like(w)
+    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_VITERBI, w.device)
+    rc = lib.bcjr_vec_viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, _ptr(states),
+                                     _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
+    _raise("bcjr_vec_viterbi_decode", rc)
     return states, w_hard

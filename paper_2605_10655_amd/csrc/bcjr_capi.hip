@@ -10,6 +10,7 @@
 #include "bcjr.h"
 #include "bcjr_internal.h"
 #include "bcjr_kernels.h"
+#include "bcjr_vec_kernels.h"
 
 namespace bcjr {
 namespace {
@@ -411,6 +412,162 @@ int fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook, int sta
                 dCodebook, workspace, ws_bytes, stream, true);
 }
 
+// ------------------------------------------------------------ vector emission
+// k = 4 bits and V = 2 weights per step (16 predecessors per state).  One
+// tile of 16 x 16 states per 16 lanes; 1024 threads per workgroup.
+bool vec_supported(int n, int k, int V) { return V == 2 && k == 4 && n >= 8 && n <= 16; }
+
+struct VecFamily {
+  int nt = 1024, tpb = 0, sgt = 0, bpw = 0, occ_est = 1;
+};
+
+VecFamily vec_family(int n) {
+  VecFamily f;
+  const int lanes = 16 << (n - 8);
+  f.tpb = std::min(lanes, f.nt);
+  f.sgt = lanes / f.tpb;
+  f.bpw = f.nt / f.tpb;
+  return f;
+}
+
+size_t vec_vsz(int n) { return ((size_t)1 << (n - 4)) + ((n - 8) >= 4 ? 64 : 0); }
+
+size_t fbv_lds_bytes(const VecFamily& f, int n) {
+  return (size_t)f.bpw * 4 * vec_vsz(n) * sizeof(float) + (size_t)(f.nt / 64) * 2 * kRed * sizeof(float);
+}
+
+size_t vitv_lds_bytes(const VecFamily& f, int n) {
+  return (size_t)f.bpw * 2 * vec_vsz(n) * sizeof(double) +
+         (size_t)(f.nt / 64) * (sizeof(double) + sizeof(int));
+}
+
+// One workgroup's histories are addressed with 32-bit byte offsets: blocks
+// per workgroup x N steps x S/16 groups x 8 bytes (4 for the soft codeword
+// alone) below 2^31.
+bool vec_length_ok(int64_t N, int n, bool vjp) {
+  const VecFamily f = vec_family(n);
+  const int64_t per_step = (int64_t)f.bpw * (vjp ? 8 : 4) * ((int64_t)1 << (n - 4));
+  return N >= 1 && N <= 0x7FFFFFFF / per_step;
+}
+
+size_t vec_cs_bytes(int n) { return align_up(((size_t)8) << n); }
+
+FbLayout fbv_layout(int64_t N, int n, bool vjp, bool dc) {
+  const size_t gs = (size_t)1 << (n - 4);
+  FbLayout l;
+  l.hist = align_up((size_t)N * (vjp ? 2 : 1) * gs * sizeof(float));
+  l.histGA = dc ? align_up((size_t)N * 2 * gs * sizeof(float)) : 0;
+  l.small = align_up((size_t)4 * N * sizeof(float));
+  l.dc = dc ? align_up(((size_t)2 << n) * sizeof(double)) : 0;
+  l.slot = l.hist + l.histGA + l.small + l.dc;
+  return l;
+}
+
+size_t vitv_slot_bytes(int64_t N, int n) { return align_up((size_t)N * ((size_t)1 << (n - 4))); }
+
+using FbvFn = void (*)(FbvArgs);
+using VitvFn = void (*)(VitvArgs);
+
+template <int NB, int SGM>
+FbvFn fbv_variant(bool vjp, bool dc) {
+  if (!vjp) return fbv_kernel<NB, SGM, 1024, false, false>;
+  if (!dc) return fbv_kernel<NB, SGM, 1024, true, false>;
+  return fbv_kernel<NB, SGM, 1024, true, true>;
+}
+
+FbvFn fbv_pick(int n, bool vjp, bool dc) {
+  if (n == 16) return fbv_variant<16, 4>(vjp, dc);
+  return fbv_variant<0, 4>(vjp, dc);
+}
+
+VitvFn vitv_pick(int n) {
+  if (n == 16) return vitv_kernel<16, 4, 1024>;
+  return vitv_kernel<0, 4, 1024>;
+}
+
+int vec_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, int V,
+               bool vjp) {
+  if (B < 0 || L < 1 || k < 1 || n < k || n > 16 || V < 1) return BCJR_ERR_INVALID_ARG;
+  if (L % V) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && (!w || !codebook)) return BCJR_ERR_INVALID_ARG;
+  if (codebook && ((uintptr_t)codebook & 15u)) return BCJR_ERR_INVALID_ARG;
+  if (w && ((uintptr_t)w & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (!vec_supported(n, k, V) || !vec_length_ok(L / V, n, vjp)) return BCJR_ERR_UNSUPPORTED;
+  return BCJR_OK;
+}
+
+int run_vitv(const float* w, int64_t B, int64_t L, const float* codebook, int n, int32_t* states,
+             float* w_hard, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  const VecFamily f = vec_family(n);
+  const int64_t N = L / 2;
+  VitvFn fn = vitv_pick(n);
+  const size_t lds = vitv_lds_bytes(f, n);
+  Family ff;
+  ff.nt = f.nt; ff.bpw = f.bpw;
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, ff, lds, B, ws_bytes, vitv_slot_bytes(N, n), &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  VitvArgs a;
+  a.w = w; a.c = codebook; a.B = B; a.N = N; a.n = n; a.sgt = f.sgt;
+  a.states = states; a.w_hard = w_hard;
+  a.bp = static_cast<uint8_t*>(workspace);
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+int run_fbv(const float* w, int64_t B, int64_t L, const float* codebook, int n, float T,
+            const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
+            void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
+  if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  // the fp32 VJP of this trellis holds its accuracy above T = 0.04 (the
+  // double-float variant exists for the scalar trellis only)
+  if (vjp && use_high_precision(T)) return BCJR_ERR_UNSUPPORTED;
+  const bool dc = vjp && dCodebook != nullptr;
+  const VecFamily f = vec_family(n);
+  const int64_t N = L / 2;
+  const FbLayout lay = fbv_layout(N, n, vjp, dc);
+  FbvFn fn = fbv_pick(n, vjp, dc);
+  const size_t lds = fbv_lds_bytes(f, n);
+  if (ws_bytes < vec_cs_bytes(n)) return BCJR_ERR_WORKSPACE;
+  Family ff;
+  ff.nt = f.nt; ff.bpw = f.bpw;
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, ff, lds, B, ws_bytes - vec_cs_bytes(n), lay.slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const int64_t slots = grid * f.bpw;
+  const int64_t S2 = (int64_t)2 << n;  // codebook floats
+  // [scaled codebook][slots: histories][slots: (G, A) histories][slots: scalars][slots: dCodebook]
+  float* cs = static_cast<float*>(workspace);
+  char* base = static_cast<char*>(workspace) + vec_cs_bytes(n);
+  FbvArgs a = {};
+  a.w = w; a.g = g; a.cs = cs; a.B = B; a.N = N; a.n = n; a.sgt = f.sgt;
+  const double Td = (double)T;
+  a.kap = (float)std::sqrt(1.4426950408889634074 / (2.0 * Td));
+  a.inv_kap = (float)(1.0 / (double)a.kap);
+  a.dws = (float)(1.0 / ((double)a.kap * (double)a.kap * Td));
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  hipLaunchKernelGGL(scale_kernel, dim3((unsigned)ceil_div(S2, 256)), dim3(256), 0, stream, codebook,
+                     a.kap, cs, S2);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  a.hist = reinterpret_cast<float*>(base);
+  a.histGA = dc ? reinterpret_cast<float*>(base + slots * lay.hist) : nullptr;
+  a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
+  a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
+                 : nullptr;
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dc) {
+    const int64_t used = slots < B ? slots : B;
+    hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S2, 256)), dim3(256), 0, stream,
+                       a.dc_part, used, S2, dCodebook);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
 }  // namespace
 }  // namespace bcjr
 
@@ -489,6 +646,73 @@ int viterbi_decode(const float* w, int64_t B, int64_t L, const float* codebook, 
   if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
   if (B == 0) return BCJR_OK;
   return run_viterbi(w, B, L, codebook, state_bits, k, states, w_hard, workspace, ws_bytes, stream);
+}
+
+size_t bcjr_vec_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int V, int op) {
+  if (V == 1) return bcjr_workspace_bytes(B, L, state_bits, k, op);
+  const bool vjp = op == BCJR_OP_VJP || op == BCJR_OP_FWD_VJP;
+  if (op != BCJR_OP_FWD && !vjp && op != BCJR_OP_VITERBI) return 0;
+  if (B <= 0 || vec_checks(nullptr, 0, L, nullptr, state_bits, k, V, vjp) != BCJR_OK) return 0;
+  const VecFamily f = vec_family(state_bits);
+  const int64_t N = L / V;
+  const int64_t slots = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est) * f.bpw;
+  if (op == BCJR_OP_VITERBI) return (size_t)slots * vitv_slot_bytes(N, state_bits);
+  return vec_cs_bytes(state_bits) + (size_t)slots * fbv_layout(N, state_bits, vjp, vjp).slot;
+}
+
+int bcjr_vec_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebook,
+                           int state_bits, int k, int V, float T, float* w_soft, float* logZ,
+                           void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (V == 1)
+    return bcjr_soft_codeword(w, B, L, codebook, state_bits, k, T, w_soft, logZ, workspace, ws_bytes,
+                              stream);
+  int st = vec_checks(w, B, L, codebook, state_bits, k, V, false);
+  if (st != BCJR_OK) return st;
+  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && !w_soft) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return BCJR_OK;
+  return run_fbv(w, B, L, codebook, state_bits, T, nullptr, w_soft, logZ, nullptr, nullptr, workspace,
+                 ws_bytes, stream, false);
+}
+
+int bcjr_vec_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
+                                   int state_bits, int k, int V, float T, const float* grad_w_soft,
+                                   float* w_soft, float* logZ, float* dW, float* dCodebook,
+                                   void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (V == 1)
+    return bcjr_soft_codeword_fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, w_soft, logZ,
+                                      dW, dCodebook, workspace, ws_bytes, stream);
+  int st = vec_checks(w, B, L, codebook, state_bits, k, V, true);
+  if (st != BCJR_OK) return st;
+  if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
+  if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
+  if (grad_w_soft && ((uintptr_t)grad_w_soft & 3u)) return BCJR_ERR_INVALID_ARG;
+  if (use_high_precision(T)) return BCJR_ERR_UNSUPPORTED;
+  if (B == 0) return fill_zero(dCodebook, (int64_t)V << state_bits, stream);
+  if (!w_soft && !logZ && !dW && !dCodebook) return BCJR_OK;
+  return run_fbv(w, B, L, codebook, state_bits, T, grad_w_soft, w_soft, logZ, dW, dCodebook,
+                 workspace, ws_bytes, stream, true);
+}
+
+int bcjr_vec_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
+                               int state_bits, int k, int V, float T, const float* grad_w_soft,
+                               float* dW, float* dCodebook, void* workspace, size_t ws_bytes,
+                               hipStream_t stream) {
+  return bcjr_vec_soft_codeword_fwd_vjp(w, B, L, codebook, state_bits, k, V, T, grad_w_soft, nullptr,
+                                        nullptr, dW, dCodebook, workspace, ws_bytes, stream);
+}
+
+int bcjr_vec_viterbi_decode(const float* w, int64_t B, int64_t L, const float* codebook,
+                            int state_bits, int k, int V, int32_t* states, float* w_hard,
+                            void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (V == 1)
+    return viterbi_decode(w, B, L, codebook, state_bits, k, states, w_hard, workspace, ws_bytes,
+                          stream);
+  int st = vec_checks(w, B, L, codebook, state_bits, k, V, false);
+  if (st != BCJR_OK) return st;
+  if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
+  if (B == 0) return BCJR_OK;
+  return run_vitv(w, B, L, codebook, state_bits, states, w_hard, workspace, ws_bytes, stream);
 }
 
 const char* bcjr_status_string(int status) {

@@ -32,6 +32,37 @@ struct FbArgs {
   float* xA;           // [slots][4][S/K] exchange: lo words [2], tangents [2]
 };
 
+// Vector-emission trellis: k = 4 bits per step (K = 16), V = 2 weights per
+// step.  Blocks hold L = 2 N weights.
+struct FbvArgs {
+  const float* w;      // [B, 2N]
+  const float* g;      // [B, 2N] upstream gradient (VJP only)
+  const float* cs;     // [S][2] codebook times kappa
+  int64_t B, N;        // blocks, steps per block
+  int n;               // state bits
+  int sgt;             // tiles per thread
+  float kap, inv_kap;  // kappa = sqrt(log2(e) / (2T)) and 1 / kappa
+  float dws;           // 1 / (kappa^2 T)
+  float* w_soft;       // [B, 2N] or null
+  float* logZ;         // [B] or null
+  float* dW;           // [B, 2N] or null
+  double* dc_part;     // [slots][S][2] fp64 partial sums of dCodebook, or null
+  float* hist;         // [slots][N][S/16] H_t, or [slots][N][S/16][2] (H_t, B_t) with the VJP
+  float* histGA;       // [slots][N][S/16][2] (G_t, A_t) (dCodebook)
+  float* small;        // [slots][4][N] shifts of H, lambda_t, E_p[X_t], A centring
+};
+
+struct VitvArgs {
+  const float* w;      // [B, 2N]
+  const float* c;      // [S][2]
+  int64_t B, N;
+  int n;
+  int sgt;
+  int32_t* states;     // [B, N]
+  float* w_hard;       // [B, 2N] or null
+  uint8_t* bp;         // [slots][N][S/16] winning predecessor digit
+};
+
 struct VitArgs {
   const float* w;
   const float* c;

@@ -155,3 +155,33 @@ def test_autograd_layer_refuses_host_tensors(lib):
             BcjrQuant.apply(w, c, 4, 2, 0.5, hard)
     with pytest.raises(ValueError):
         bcjr_quant(torch.zeros(3, 5), c, 4, 2, 0.5, block=4)
+
+
+def test_vector_emission_host_checks(lib):
+    ws = P.bcjr_vec_workspace_bytes
+    assert ws(16, 256, 16, 4, 2, P.OP_FWD) > 0
+    assert ws(16, 256, 16, 4, 2, P.OP_VJP) > ws(16, 256, 16, 4, 2, P.OP_FWD)
+    assert ws(16, 256, 16, 4, 2, P.OP_VITERBI) > 0
+    assert ws(16, 255, 16, 4, 2, P.OP_FWD) == 0          # L not a multiple of V
+    assert ws(16, 256, 16, 2, 2, P.OP_FWD) == 0          # only k = 4 with V = 2
+    assert ws(16, 256, 7, 4, 2, P.OP_FWD) == 0           # state_bits >= 8
+    assert ws(16, 256, 16, 4, 3, P.OP_FWD) == 0
+    assert ws(16, 256, 16, 2, 1, P.OP_FWD) == P.bcjr_workspace_bytes(16, 256, 16, 2, P.OP_FWD)
+    # 32-bit history offsets: N = L / 2 steps, 8 bytes per group with the VJP
+    assert ws(4, 2 * 65535, 16, 4, 2, P.OP_FWD_VJP) > 0
+    assert ws(4, 2 * 65536, 16, 4, 2, P.OP_FWD_VJP) == 0
+    f = lib.bcjr_vec_soft_codeword
+    assert f(FAKE, 4, 8, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -3
+    assert f(FAKE, 4, 7, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -1  # L % V
+    assert f(FAKE, 4, 8, FAKE, 8, 4, 2, 0.0, FAKE, None, None, 0, None) == -1
+    assert f(FAKE, 4, 8, FAKE, 8, 3, 2, 1.0, FAKE, None, None, 0, None) == -2
+    assert f(FAKE, 4, 8, MISALIGNED, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -1
+    assert f(FAKE, 0, 8, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == 0
+    v = lib.bcjr_vec_soft_codeword_fwd_vjp
+    assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.03, FAKE, FAKE, None, None, None, None, 0, None) == -2
+    assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.5, None, FAKE, None, None, None, None, 0, None) == -1
+    assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.5, FAKE, FAKE, None, None, None, None, 0, None) == -3
+    vd = lib.bcjr_vec_viterbi_decode
+    assert vd(FAKE, 4, 8, FAKE, 8, 4, 2, None, None, FAKE, 1 << 20, None) == -1
+    assert vd(FAKE, 4, 8, FAKE, 8, 4, 2, FAKE, None, None, 0, None) == -3
+    assert vd(FAKE, 0, 8, FAKE, 8, 4, 2, None, None, None, 0, None) == 0

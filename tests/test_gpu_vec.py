@@ -1,0 +1,217 @@
+"""GPU parity of the vector-emission trellis (V = 2 weights per step, k = 4
+bits per step: 16 predecessors per state) against the fp64 oracle.
+
+Tolerances as for the scalar trellis: w_soft |gpu - ref| <= 2e-5, logZ
+1e-4 relative, dW and dCodebook 1e-4 of max(|ref_i|, rms(ref)), Viterbi
+states bit-exact and w_hard == codebook[states].
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2605_10655_amd as P
+from paper_2605_10655_amd import workloads as WL
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+TOL_WS = 2e-5
+TOL_LOGZ = 1e-4
+TOL_GRAD = 1e-4
+K_BITS, V = 4, 2
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    P.load_library()
+    yield
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def host(t):
+    return None if t is None else t.detach().cpu().numpy()
+
+
+def case(seed, B, L, n):
+    r = np.random.Generator(np.random.PCG64(seed))
+    c = r.standard_normal((1 << n, V)).astype(np.float32)
+    w = r.standard_normal((B, L)).astype(np.float32)
+    g = r.standard_normal((B, L)).astype(np.float32)
+    return w, c, g
+
+
+def grad_err(gpu, ref, what):
+    ref = np.asarray(ref, np.float64)
+    rms = np.sqrt(np.mean(ref * ref))
+    scale = np.maximum(np.abs(ref), rms)
+    err = (np.abs(gpu.astype(np.float64) - ref) / np.where(scale > 0, scale, 1.0)).max()
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite"
+    assert err <= TOL_GRAD, f"{what}: gradient err {err:.3e} (rms {rms:.3e})"
+    return err
+
+
+def full_check(w, c, n, T, g, want_dc=True, what=""):
+    _say(f"[vec] {what} B={w.shape[0]} L={w.shape[1]} n={n} T={T} dc={want_dc}")
+    ws, lz, dW, dc = P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), n, K_BITS, V, T, dev(g),
+                                                      want_dCodebook=want_dc)
+    torch.cuda.synchronize()
+    ws, lz, dW, dc = host(ws), host(lz), host(dW), host(dc)
+    rws, rlz, rdW, rdc = O.soft_codeword_vjp(w, c, n, K_BITS, float(np.float32(T)), g,
+                                             want_dc=want_dc, V=V)
+    e_ws = np.abs(ws.astype(np.float64) - rws).max()
+    e_lz = (np.abs(lz.astype(np.float64) - rlz) / np.abs(rlz)).max()
+    assert e_ws <= TOL_WS, f"{what}: w_soft err {e_ws:.3e}"
+    assert e_lz <= TOL_LOGZ, f"{what}: logZ err {e_lz:.3e}"
+    e = [e_ws, e_lz, grad_err(dW, rdW, what + " dW")]
+    if want_dc:
+        e.append(grad_err(dc, rdc, what + " dc"))
+    _say(f"[vec] {what} errors {['%.2e' % x for x in e]}")
+    return ws, lz, dW, dc
+
+
+def viterbi_check(w, c, n, what=""):
+    _say(f"[vec viterbi] {what} B={w.shape[0]} L={w.shape[1]} n={n}")
+    st, wh = P.bcjr_vec_viterbi_decode(dev(w), dev(c), n, K_BITS, V)
+    torch.cuda.synchronize()
+    rst, _ = O.viterbi(w, c, n, K_BITS, V=V)
+    np.testing.assert_array_equal(host(st), rst)
+    np.testing.assert_array_equal(host(wh), c[rst].reshape(w.shape))
+
+
+@pytest.mark.parametrize("n,B,L", [
+    (8, 1, 2), (8, 3, 4), (8, 70, 34), (9, 5, 18), (10, 9, 66), (11, 3, 40), (12, 5, 64),
+    (13, 3, 30), (14, 2, 24), (15, 2, 20), (16, 2, 16),
+])
+def test_shapes_and_ragged_batches(n, B, L):
+    w, c, g = case(100 * n + B, B, L, n)
+    full_check(w, c, n, 0.3, g, True, f"shape n={n}")
+    full_check(w, c, n, 0.3, g, False, f"shape n={n} no-dc")
+    viterbi_check(w, c, n, f"shape n={n}")
+
+
+@pytest.mark.parametrize("T", [1.0, 0.1, 0.05, 0.0405])
+def test_temperatures_mid_trellis(T):
+    w, c, g = case(7, 6, 96, 12)
+    full_check(w, c, 12, T, g, True, f"T={T}")
+
+
+@pytest.mark.parametrize("T", [0.1, 0.05])
+def test_full_trellis_subset(T):
+    """S = 65536 (the paper's 16-predecessor trellis), blocks of 256 weights."""
+    w, c, g = case(11, 4, 256, 16)
+    full_check(w, c, 16, T, g, True, f"S=65536 T={T}")
+
+
+def test_full_trellis_viterbi():
+    w, c, _ = case(12, 4, 256, 16)
+    viterbi_check(w, c, 16, "S=65536")
+
+
+def test_full_batch_sampled():
+    """The benchmark's launch: a 2048 x 2048 N(0,1) matrix as 16384 blocks of
+    256 weights, S = 65536, T = 0.05, fwd + logZ + dW, checked on sampled
+    blocks."""
+    n, T = 16, 0.05
+    r = np.random.Generator(np.random.PCG64(2605))
+    c = r.standard_normal((1 << n, V)).astype(np.float32)
+    w = r.standard_normal((16384, 256)).astype(np.float32)
+    g = r.standard_normal((16384, 256)).astype(np.float32)
+    _say("[vec] full batch B=16384")
+    ws, lz, dW, _ = P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), n, K_BITS, V, T, dev(g),
+                                                     want_dCodebook=False)
+    torch.cuda.synchronize()
+    idx = np.sort(r.choice(16384, size=6, replace=False))
+    rws, rlz, rdW, _ = O.soft_codeword_vjp(w[idx], c, n, K_BITS, float(np.float32(T)), g[idx],
+                                           want_dc=False, V=V)
+    assert np.abs(host(ws)[idx] - rws).max() <= TOL_WS
+    assert (np.abs(host(lz)[idx] - rlz) / np.abs(rlz)).max() <= TOL_LOGZ
+    grad_err(host(dW)[idx], rdW, "full dW")
+
+
+def test_soft_codeword_low_temperature():
+    """The soft codeword alone runs at any T; the V = 2 VJP stops at 0.04."""
+    w, c, g = case(13, 3, 64, 12)
+    T = 0.001
+    ws, lz = P.bcjr_vec_soft_codeword(dev(w), dev(c), 12, K_BITS, V, T)
+    torch.cuda.synchronize()
+    rws, rlz = O.soft_codeword(w, c, 12, K_BITS, float(np.float32(T)), V=V)
+    assert np.abs(host(ws) - rws).max() <= TOL_WS
+    assert (np.abs(host(lz) - rlz) / np.abs(rlz)).max() <= TOL_LOGZ
+    with pytest.raises(P.BcjrError) as e:
+        P.bcjr_vec_soft_codeword_vjp(dev(w), dev(c), 12, K_BITS, V, T, dev(g))
+    assert e.value.status == -2
+
+
+def test_entry_points_agree_and_deterministic():
+    n, T = 12, 0.2
+    w, c, g = case(14, 9, 48, n)
+    a = P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), n, K_BITS, V, T, dev(g))
+    b = P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), n, K_BITS, V, T, dev(g))
+    fws, flz = P.bcjr_vec_soft_codeword(dev(w), dev(c), n, K_BITS, V, T)
+    vdW, vdc = P.bcjr_vec_soft_codeword_vjp(dev(w), dev(c), n, K_BITS, V, T, dev(g))
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(host(x), host(y))
+    np.testing.assert_allclose(host(fws), host(a[0]), rtol=0, atol=1e-6)
+    np.testing.assert_allclose(host(flz), host(a[1]), rtol=1e-6)
+    np.testing.assert_array_equal(host(vdW), host(a[2]))
+    np.testing.assert_array_equal(host(vdc), host(a[3]))
+
+
+def test_small_workspace_runs_persistent_loop():
+    n, T, B, L = 12, 0.2, 24, 40
+    w, c, g = case(15, B, L, n)
+    full = [host(t) for t in P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), n, K_BITS, V, T,
+                                                               dev(g))]
+    big = P.bcjr_vec_workspace_bytes(B, L, n, K_BITS, V, P.OP_FWD_VJP)
+    out = None
+    for nb in range(1, B + 1):
+        try:
+            ws = torch.empty(big * nb // B, dtype=torch.uint8, device="cuda:0")
+            out = [host(t) for t in P.bcjr_vec_soft_codeword_fwd_vjp(
+                dev(w), dev(c), n, K_BITS, V, T, dev(g), workspace=ws)]
+            break
+        except P.BcjrError as e:
+            assert e.status == -3
+    assert out is not None
+    for x, y in zip(full, out):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_scalar_emission_delegates():
+    """V = 1 through the vector entry points is the scalar trellis."""
+    r = np.random.Generator(np.random.PCG64(16))
+    c = r.standard_normal(256).astype(np.float32)
+    w = r.standard_normal((5, 20)).astype(np.float32)
+    g = r.standard_normal((5, 20)).astype(np.float32)
+    a = P.bcjr_vec_soft_codeword_fwd_vjp(dev(w), dev(c), 8, 2, 1, 0.2, dev(g))
+    b = P.bcjr_soft_codeword_fwd_vjp(dev(w), dev(c), 8, 2, 0.2, dev(g))
+    sa, _ = P.bcjr_vec_viterbi_decode(dev(w), dev(c), 8, 2, 1)
+    sb, _ = P.viterbi_decode(dev(w), dev(c), 8, 2)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(host(x), host(y))
+    np.testing.assert_array_equal(host(sa), host(sb))
+
+
+def test_empty_batch_zeroes_dcodebook():
+    c = dev(np.ones((256, 2), np.float32))
+    w = torch.empty((0, 8), dtype=torch.float32, device="cuda:0")
+    dc = torch.full((256, 2), 7.0, device="cuda:0")
+    P.bcjr_vec_soft_codeword_vjp(w, c, 8, K_BITS, V, 0.5, w.clone(), want_dW=False, dCodebook=dc,
+                                 workspace=torch.empty(256, dtype=torch.uint8, device="cuda:0"))
+    torch.cuda.synchronize()
+    assert float(dc.abs().max()) == 0.0
