@@ -10,6 +10,11 @@ seeded synthetic data resident in HBM before timing starts.
 A step is one such call over the whole matrix.  Edges per step are
 B * L * S * 2^k.  Prints one JSON line.
 
+--path vec times the paper's own trellis shape on the same matrix: V = 2
+weights and 4 bits per step (16 predecessors per state, 128 steps per
+256-weight block), a [65536, 2] N(0,1) codebook, fused w_soft + logZ + dW
+(bcjr_vec_soft_codeword_fwd_vjp); edges per step B * (L/2) * S * 16.
+
 --path ste times the BCJR-STE training step on the same matrix instead: the
 hard Viterbi forward (viterbi_decode) followed by its backward pass
 (bcjr_ste_vjp, dW only); the roofline then covers the VJP launch.  --T
@@ -36,6 +41,13 @@ TRANS_LANES_PER_CLK = 32         # per CU: v_exp/v_log/v_rcp at half rate (measu
 ALG_VALU_PER_GROUP = 97.0
 ALG_TRANS_PER_GROUP = 11.0
 EDGES_PER_GROUP = 16.0           # K^2
+# vector-emission trellis (K = 16, V = 2): algorithmic work per state-step,
+# fwd + w_soft + logZ + dW (backward row: 10 VALU + 1 exp per state, 4 VALU and
+# a log and a reciprocal per row; forward column: 15 VALU + 1 exp per state,
+# 17 VALU and a log, an exp and a reciprocal per column of 16 states)
+ALG_VEC_VALU_PER_STATE = 25.0 + (4.0 + 17.0) / 16.0
+ALG_VEC_TRANS_PER_STATE = 2.0 + 5.0 / 16.0
+EDGES_PER_STATE_VEC = 16.0
 
 
 # HBM bytes per launch of the timed kernel, from two rocprofv3 --pmc passes
@@ -63,6 +75,12 @@ def kernel_source_digest() -> str:
 def roofline_edges_per_s() -> float:
     t_group = (ALG_VALU_PER_GROUP / VALU_LANES_PER_CLK + ALG_TRANS_PER_GROUP / TRANS_LANES_PER_CLK)
     return EDGES_PER_GROUP * CUS * CLOCK_HZ / t_group
+
+
+def roofline_vec_edges_per_s() -> float:
+    t_state = (ALG_VEC_VALU_PER_STATE / VALU_LANES_PER_CLK
+               + ALG_VEC_TRANS_PER_STATE / TRANS_LANES_PER_CLK)
+    return EDGES_PER_STATE_VEC * CUS * CLOCK_HZ / t_state
 
 
 def cpu_baseline(target_s: float = 15.0):
@@ -99,7 +117,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=("fwd_vjp", "ste"), default="fwd_vjp")
+    ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec"), default="fwd_vjp")
     ap.add_argument("--T", type=float, default=None)
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes (the "
@@ -131,16 +149,20 @@ def main():
     wl = WL.workload(4)
     n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0] if args.T is None else args.T
     ste = args.path == "ste"
+    vec = args.path == "vec"
     dev = torch.device("cuda:0")
     w = torch.from_numpy(WL.weights(4)).to(dev)
-    c = torch.from_numpy(WL.codebook(4)).to(dev)
+    c = torch.from_numpy(WL.codebook_vec(4) if vec else WL.codebook(4)).to(dev)
     g = torch.from_numpy(WL.upstream(4)).to(dev)
     B = w.shape[0]
     w_soft = torch.empty_like(w)
     logZ = torch.empty(B, dtype=torch.float32, device=dev)
     dW = torch.empty_like(w)
     states = torch.empty((B, L), dtype=torch.int32, device=dev) if ste else None
-    ws_bytes = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
+    if vec:
+        k = 4
+    ws_bytes = (P.bcjr_vec_workspace_bytes(B, L, n, k, 2, P.OP_FWD_VJP) if vec
+                else P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP))
     if ste:
         ws_bytes = max(ws_bytes, P.bcjr_workspace_bytes(B, L, n, k, P.OP_VITERBI))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -154,6 +176,9 @@ def main():
                 mid.record(stream)
             P.bcjr_ste_vjp(w, c, n, k, T, w_soft, g, dW=dW, want_dCodebook=False, workspace=ws,
                            stream=stream)
+        elif vec:
+            P.bcjr_vec_soft_codeword_fwd_vjp(w, c, n, k, 2, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
+                                             want_dCodebook=False, workspace=ws, stream=stream)
         else:
             P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
                                          want_dCodebook=False, workspace=ws, stream=stream)
@@ -177,15 +202,19 @@ def main():
     wall = time.perf_counter() - t0
     kernel_ms = [(m if ste else a).elapsed_time(b) for a, b, m in ev]
     ms_per_step = wall * 1e3 / args.steps
-    edges = wl.edges
+    edges = B * (L // 2) * wl.S * 16 if vec else wl.edges
     value = edges / (ms_per_step / 1e3)
     kern_avg_s = float(np.mean(kernel_ms)) / 1e3
     achieved = edges / kern_avg_s
-    peak = roofline_edges_per_s()
+    peak = roofline_vec_edges_per_s() if vec else roofline_edges_per_s()
     print(f"timed {args.steps} steps: {ms_per_step:.1f} ms/step (events avg {kern_avg_s * 1e3:.1f} ms)",
           file=sys.stderr, flush=True)
 
-    if ste:
+    if vec:
+        metric = ("trellis edge-updates/s fwd+VJP at S=65536, 16 predecessors (4 bits/step), "
+                  "V=2, 256-weight blocks")
+        what = "V=2, 4 bits per step (128 steps per block), [65536,2] N(0,1) codebook; fused w_soft+logZ+dW"
+    elif ste:
         metric = "trellis edge-updates/s BCJR-STE step (Viterbi fwd + VJP) at S=65536,k=2,L=256"
         what = "BCJR-STE step: viterbi_decode + bcjr_ste_vjp (dW)"
     else:
@@ -204,17 +233,17 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "2048x2048 N(0,1) weights as 16384 blocks of L=256; S=65536, k=2, "
+        "config": {"workload": f"2048x2048 N(0,1) weights as 16384 blocks of L=256; S=65536, k={k}, "
                                f"T={T}; {what}",
-                   "B": B, "L": L, "S": wl.S, "k": k, "T": T},
+                   "B": B, "L": L, "S": wl.S, "k": k, "V": 2 if vec else 1, "T": T},
         "blocks_per_s": B / (ms_per_step / 1e3),
         "roofline": {"bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
                      "unit": "Gedge/s", "frac": achieved / peak,
-                     "traffic": None if (ste or args.T is not None)
+                     "traffic": None if (ste or vec or args.T is not None)
                      else MEASURED_TRAFFIC.get(kernel_source_digest()),
                      "kernel_ms": kern_avg_s * 1e3},
     }
-    if not args.no_cpu_baseline and not ste and args.T is None:
+    if not args.no_cpu_baseline and not ste and not vec and args.T is None:
         print("timing the oracle on the host cores ...", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)

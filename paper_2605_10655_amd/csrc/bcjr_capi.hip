@@ -414,11 +414,13 @@ int fwd_vjp(const float* w, int64_t B, int64_t L, const float* codebook, int sta
 
 // ------------------------------------------------------------ vector emission
 // k = 4 bits and V = 2 weights per step (16 predecessors per state).  One
-// tile of 16 x 16 states per 16 lanes; 1024 threads per workgroup.
+// tile of 16 x 16 states per 16 lanes; 512 threads per workgroup, so that
+// at S = 65536 two blocks (two workgroups, 66 KiB of LDS each) share a CU
+// and one's barriers overlap the other's arithmetic.
 bool vec_supported(int n, int k, int V) { return V == 2 && k == 4 && n >= 8 && n <= 16; }
 
 struct VecFamily {
-  int nt = 1024, tpb = 0, sgt = 0, bpw = 0, occ_est = 1;
+  int nt = 512, tpb = 0, sgt = 0, bpw = 0, occ_est = 2;
 };
 
 VecFamily vec_family(int n) {
@@ -470,19 +472,19 @@ using VitvFn = void (*)(VitvArgs);
 
 template <int NB, int SGM>
 FbvFn fbv_variant(bool vjp, bool dc) {
-  if (!vjp) return fbv_kernel<NB, SGM, 1024, false, false>;
-  if (!dc) return fbv_kernel<NB, SGM, 1024, true, false>;
-  return fbv_kernel<NB, SGM, 1024, true, true>;
+  if (!vjp) return fbv_kernel<NB, SGM, 512, false, false>;
+  if (!dc) return fbv_kernel<NB, SGM, 512, true, false>;
+  return fbv_kernel<NB, SGM, 512, true, true>;
 }
 
 FbvFn fbv_pick(int n, bool vjp, bool dc) {
-  if (n == 16) return fbv_variant<16, 4>(vjp, dc);
-  return fbv_variant<0, 4>(vjp, dc);
+  if (n == 16) return fbv_variant<16, 8>(vjp, dc);
+  return fbv_variant<0, 8>(vjp, dc);
 }
 
 VitvFn vitv_pick(int n) {
-  if (n == 16) return vitv_kernel<16, 4, 1024>;
-  return vitv_kernel<0, 4, 1024>;
+  if (n == 16) return vitv_kernel<16, 8, 512>;
+  return vitv_kernel<0, 8, 512>;
 }
 
 int vec_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, int V,

@@ -42,6 +42,12 @@ namespace {
 struct VecGeom {
   int n, GS, NSG, lgNSG, pad, VSZ;
   __device__ __forceinline__ int phys(int v) const { return v + pad * (v >> lgNSG); }
+  // the same positions written per field: column-form entry r * NSG + m
+  // (m < NSG) and the start of row-form run m * 16 + (0..15)
+  __device__ __forceinline__ int col(int r, int m) const { return r * (NSG + pad) + m; }
+  __device__ __forceinline__ int row(int m) const {
+    return m * 16 + (pad ? pad * (m >> (lgNSG - 4)) : 0);
+  }
 };
 
 __device__ __forceinline__ VecGeom vec_geom(int n) {
@@ -173,12 +179,12 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
 #pragma unroll
             for (int u4 = 0; u4 < 8; ++u4) {
               float t4[4];
-              ld_vec<4>(cur + 2 * q.phys(m * 16) + 4 * u4, t4);
+              ld_vec<4>(cur + 2 * q.row(m) + 4 * u4, t4);
 #pragma unroll
               for (int e = 0; e < 4; ++e) hb[4 * u4 + e] = t4[e];
             }
             float own[2];
-            ld_vec<2>(cur + 2 * q.phys(m * 16 + tl), own);
+            ld_vec<2>(cur + 2 * (q.row(m) + tl), own);
             if constexpr (VJP) {
               buf_st<2>(hist, voH, soH + (uint32_t)i * tileH, own);
             } else {
@@ -235,12 +241,12 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
 #pragma unroll
           for (int u4 = 0; u4 < 8; ++u4) {
             float t4[4];
-            ld_vec<4>(cur + 2 * q.phys(m * 16) + 4 * u4, t4);
+            ld_vec<4>(cur + 2 * q.row(m) + 4 * u4, t4);
 #pragma unroll
             for (int e = 0; e < 4; ++e) hb[4 * u4 + e] = t4[e];
           }
           float own[2];
-          ld_vec<2>(cur + 2 * q.phys(m * 16 + tl), own);
+          ld_vec<2>(cur + 2 * (q.row(m) + tl), own);
           if constexpr (VJP) {
             buf_st<2>(hist, voH, soH + (uint32_t)i * tileH, own);
           } else {
@@ -267,7 +273,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
           const float Hn = M + lg2(s) - dl;
           vmax[0] = fmaxf(vmax[0], Hn);
           float o[2] = {Hn, VJP ? sy * rcp(s) : 0.f};
-          st_vec<2>(nxt + 2 * q.phys(tl * NSG + m), o);
+          st_vec<2>(nxt + 2 * q.col(tl, m), o);
           sg_fence();
         }
       }
@@ -332,7 +338,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
             buf_ld<2>(cbk, voC1, (uint32_t)r * (uint32_t)GS * 8u + (uint32_t)i * tileC, cv);
             c0[r] = cv[0];
             c1[r] = cv[1];
-            ld_vec<2>(cur + 2 * q.phys(r * NSG + m), ga);
+            ld_vec<2>(cur + 2 * q.col(r, m), ga);
             G[r] = ga[0];
             A[r] = ga[1];
           }
@@ -376,7 +382,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
           }
           if (t < N - 1) {
             float o[2] = {Gn, An};
-            st_vec<2>(nxt + 2 * q.phys(m * 16 + tl), o);
+            st_vec<2>(nxt + 2 * (q.row(m) + tl), o);
             // (G_{t+1}, A_{t+1}) as the next step reads them, for the dCodebook sweep
             if constexpr (DC) buf_st<2>(hga, voH, soH + hstep + (uint32_t)i * tileH, o);
           }
@@ -540,7 +546,7 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
             const float2 cv = c2[s];
             const double d0 = w0 - (double)cv.x, d1 = w1 - (double)cv.y;
             const double e = __dadd_rn(__dmul_rn(d0, d0), __dmul_rn(d1, d1));
-            const double v = __dadd_rn(e, cur[q.phys(r * NSG + m)]);
+            const double v = __dadd_rn(e, cur[q.col(r, m)]);
             if (t < N - 1) {
               if (r == 0 || v < best) {
                 best = v;
@@ -552,7 +558,7 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
             }
           }
           if (t < N - 1) {
-            nxt[q.phys(m * 16 + tl)] = best;
+            nxt[(q.row(m) + tl)] = best;
             bp[(t + 1) * GS + m * 16 + tl] = (uint8_t)br;
           }
         }

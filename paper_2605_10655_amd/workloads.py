@@ -11,7 +11,7 @@ for incoherence-processed (approximately iid Gaussian) Llama-3.2-1B
 projection weights; none of the paper's models or datasets are used.
 
 Seeds: 1000 * cfg + {0: codebook, 1: weights, 2 + call: upstream gradient,
-900: parity subset}.
+500: [S, 2] codebook of the vector-emission trellis, 900: parity subset}.
 """
 from __future__ import annotations
 
@@ -99,6 +99,13 @@ def weights(cfg: int, rows: int | None = None) -> np.ndarray:
     if wl.weights == "normal_rms_block":
         W = W / np.sqrt((W * W).mean(axis=1, keepdims=True))
     return np.ascontiguousarray(W, dtype=np.float32)
+
+
+def codebook_vec(cfg: int, V: int = 2) -> np.ndarray:
+    """A [S, V] N(0,1) codebook for the vector-emission trellis (seed
+    1000 * cfg + 500)."""
+    wl = WORKLOADS[cfg]
+    return _rng(1000 * cfg + 500).standard_normal((wl.S, V)).astype(np.float32)
 
 
 def upstream(cfg: int, call: int = 0, B: int | None = None) -> np.ndarray:
