@@ -452,7 +452,8 @@ bool vec_length_ok(int64_t N, int n, bool vjp) {
   return N >= 1 && N <= 0x7FFFFFFF / per_step;
 }
 
-size_t vec_cs_bytes(int n) { return align_up(((size_t)8) << n); }
+// the scaled codebook and its transposed copy
+size_t vec_cs_bytes(int n) { return 2 * align_up(((size_t)8) << n); }
 
 FbLayout fbv_layout(int64_t N, int n, bool vjp, bool dc) {
   const size_t gs = (size_t)1 << (n - 4);
@@ -551,8 +552,9 @@ int run_fbv(const float* w, int64_t B, int64_t L, const float* codebook, int n, 
   a.inv_kap = (float)(1.0 / (double)a.kap);
   a.dws = (float)(1.0 / ((double)a.kap * (double)a.kap * Td));
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
-  hipLaunchKernelGGL(scale_kernel, dim3((unsigned)ceil_div(S2, 256)), dim3(256), 0, stream, codebook,
-                     a.kap, cs, S2);
+  a.csT = cs + S2;
+  hipLaunchKernelGGL(scale_vec_kernel, dim3((unsigned)ceil_div((int64_t)1 << n, 256)), dim3(256), 0,
+                     stream, codebook, a.kap, cs, const_cast<float*>(a.csT), n);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   a.hist = reinterpret_cast<float*>(base);
   a.histGA = dc ? reinterpret_cast<float*>(base + slots * lay.hist) : nullptr;

@@ -38,6 +38,7 @@ struct FbvArgs {
   const float* w;      // [B, 2N]
   const float* g;      // [B, 2N] upstream gradient (VJP only)
   const float* cs;     // [S][2] codebook times kappa
+  const float* csT;    // the same, transposed: entry (s mod (S/16)) * 16 + s / (S/16)
   int64_t B, N;        // blocks, steps per block
   int n;               // state bits
   int sgt;             // tiles per thread

@@ -84,6 +84,31 @@ __device__ __forceinline__ void pair_at(const float* row, int64_t t, int64_t L, 
   }
 }
 
+// The 16 codewords of one tile row (backward sweep) from the transposed
+// scaled codebook: cc[2u], cc[2u + 1] = c'(r * GS + m * 16 + u).
+__device__ __forceinline__ void row_codewords(rsrc_t cT, uint32_t voff, uint32_t soff, float (&cc)[32]) {
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    float v[2];
+    buf_ld<2>(cT, voff, soff + (uint32_t)u * 128u, v);
+    cc[2 * u] = v[0];
+    cc[2 * u + 1] = v[1];
+  }
+}
+
+// History entry of one lane: H, and B after it with the VJP (HW = 2).
+template <int HW>
+__device__ __forceinline__ void hist_entry(rsrc_t h, uint32_t voff, uint32_t soff, float (&e)[2]) {
+  if constexpr (HW == 2) {
+    buf_ld<2>(h, voff, soff, e);
+  } else {
+    float e1[1];
+    buf_ld<1>(h, voff, soff, e1);
+    e[0] = e1[0];
+    e[1] = 0.f;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Soft codeword, logZ and the VJP (dW, and dCodebook with DC).  NB > 0 fixes
 // the state bits at compile time (then SGT = SGMAX).
@@ -120,10 +145,14 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
   float* const vec1 = vec0 + 2 * q.VSZ;
 
   const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)8 << n);
+  const rsrc_t cbkT = make_rsrc(a.csT, (uint32_t)8 << n);
   // forward sweep: column tl of tile m reads states r * GS + m * 16 + tl
   const uint32_t voC1 = ((uint32_t)tq * 16 + tl) * 8u;
-  // backward sweep: row tl of tile m reads states tl * GS + m * 16 + (0..15)
-  const uint32_t voC0 = ((uint32_t)tl * GS + (uint32_t)tq * 16) * 8u;
+  // backward sweep: row tl of tile m reads states tl * GS + m * 16 + u, u < 16,
+  // from the transposed copy, entry (m * 16 + u) * 16 + tl: for each u the
+  // 16 rows of a tile are one contiguous 128-byte line
+  const uint32_t voC0 = ((uint32_t)tq * 256 + tl) * 8u;
+  const uint32_t tileCT = (uint32_t)TQ * 2048u;        // transposed-copy bytes between tile slots
   const uint32_t tileC = (uint32_t)TQ * 128u;          // codebook bytes between tile slots
   const uint32_t hstep = (uint32_t)GS * HW * 4u;       // history bytes per step
   const uint32_t voH = (uint32_t)bw * (uint32_t)N * hstep + ((uint32_t)tq * 16 + tl) * HW * 4u;
@@ -175,7 +204,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
           {
             const int m = tq + i * TQ;
             float cc[32], hb[32];
-            buf_ld<32>(cbk, voC0, (uint32_t)i * tileC, cc);
+            row_codewords(cbkT, voC0, (uint32_t)i * tileCT, cc);
 #pragma unroll
             for (int u4 = 0; u4 < 8; ++u4) {
               float t4[4];
@@ -237,7 +266,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
         {
           const int m = tq + i * TQ;
           float cc[32], hb[32];
-          buf_ld<32>(cbk, voC0, (uint32_t)i * tileC, cc);
+          row_codewords(cbkT, voC0, (uint32_t)i * tileCT, cc);
 #pragma unroll
           for (int u4 = 0; u4 < 8; ++u4) {
             float t4[4];
@@ -298,6 +327,11 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
     float lam = lam0;
     float dlG = 0.f;   // shift for the G values written this step
     float cprev = 0.f; // <g_{t-1}, w_soft_{t-1}>: centring of the A being read
+    // The history entry of the next tile is loaded one tile ahead (the last
+    // tile of a step fetches the first of the next step), so its HBM latency
+    // overlaps the current tile's arithmetic.
+    float pH[2] = {0.f, 0.f};
+    hist_entry<HW>(hist, voH, 0u, pH);
     for (int64_t t = 0; t < N; ++t) {
       const int par = (int)(t & 1);
       rc.red = red0 + par * (NT / 64) * kRed;
@@ -323,14 +357,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
       for (int i = 0; i < SGT; ++i) {
         {
           const int m = tq + i * TQ;
-          float hu[2] = {0.f, 0.f};
-          if constexpr (VJP) {
-            buf_ld<2>(hist, voH, soH + (uint32_t)i * tileH, hu);
-          } else {
-            float h1[1];
-            buf_ld<1>(hist, voH, soH + (uint32_t)i * tileH, h1);
-            hu[0] = h1[0];
-          }
+          const float hu[2] = {pH[0], pH[1]};
           float c0[16], c1[16], G[16], A[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
@@ -341,6 +368,12 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
             ld_vec<2>(cur + 2 * q.col(r, m), ga);
             G[r] = ga[0];
             A[r] = ga[1];
+          }
+          {
+            // (a select, not a branch: at t = N - 1 it re-reads an entry of step t, unused)
+            const bool last = i + 1 >= SGT;
+            const int64_t tn = last && t + 1 < N ? t + 1 : t;
+            hist_entry<HW>(hist, voH, (uint32_t)tn * hstep + (last ? 0u : (uint32_t)(i + 1) * tileH), pH);
           }
           // in place: G[r] <- log2 alpha_t of the column's states, A[r] <- y_r =
           // <g_t, c> + A_t (raw) of the same states
@@ -614,6 +647,21 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
     }
     __syncthreads();
   }
+}
+
+// Scaled codebook of the vector-emission kernels in two layouts: cs[s] =
+// kappa c(s) (2-vectors, state order) and csT[(s mod GS) * 16 + s / GS], the
+// transposed copy read by the backward sweep.
+__global__ void scale_vec_kernel(const float* c, float kap, float* cs, float* csT, int n) {
+  const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= ((int64_t)1 << n)) return;
+  const int64_t gs = (int64_t)1 << (n - 4);
+  const float c0 = c[2 * s] * kap, c1 = c[2 * s + 1] * kap;
+  cs[2 * s] = c0;
+  cs[2 * s + 1] = c1;
+  const int64_t j = (s & (gs - 1)) * 16 + (s >> (n - 4));
+  csT[2 * j] = c0;
+  csT[2 * j + 1] = c1;
 }
 
 }  // namespace
