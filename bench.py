@@ -15,6 +15,10 @@ weights and 4 bits per step (16 predecessors per state, 128 steps per
 256-weight block), a [65536, 2] N(0,1) codebook, fused w_soft + logZ + dW
 (bcjr_vec_soft_codeword_fwd_vjp); edges per step B * (L/2) * S * 16.
 
+--op soft | dc | viterbi times another call on the same data (the soft
+codeword alone, the fused call with dCodebook, the Viterbi decode); those
+lines carry no roofline.
+
 --path ste times the BCJR-STE training step on the same matrix instead: the
 hard Viterbi forward (viterbi_decode) followed by its backward pass
 (bcjr_ste_vjp, dW only); the roofline then covers the VJP launch.  --T
@@ -54,8 +58,11 @@ EDGES_PER_STATE_VEC = 16.0
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map a plain 1 GiB
 # device copy's readings to its 1 GiB read and written), keyed by a digest of
 # the kernel sources they were taken on.  Any other source reports null.
-MEASURED_TRAFFIC = {"e945d33e8277e7a4": 2.68937e8 * 1024 * 2.0 + 5.37660e8 * 1024 * 1.0}
-KERNEL_SOURCES = ("bcjr_kernels.h", "bcjr_capi.hip", "bcjr_internal.h")
+# Keyed by (path, digest).
+MEASURED_TRAFFIC = {
+    ("vec", "47570edd27ed8bc3"): 3.37972e7 * 1024 * 2.0 + 6.74007e7 * 1024 * 1.0,
+}
+KERNEL_SOURCES = ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_capi.hip", "bcjr_internal.h")
 
 
 def kernel_source_digest() -> str:
@@ -119,6 +126,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec"), default="fwd_vjp")
     ap.add_argument("--T", type=float, default=None)
+    ap.add_argument("--op", choices=("fwd_vjp", "soft", "dc", "viterbi"), default="fwd_vjp",
+                    help="call timed on the fwd_vjp and vec paths: the fused w_soft+logZ+dW call "
+                         "(default), the soft codeword + logZ alone, w_soft+logZ+dW+dCodebook, or "
+                         "the Viterbi decode; only the default carries a roofline")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes (the "
                          "reference kernel for scaling FETCH_SIZE / WRITE_SIZE counters)")
@@ -168,8 +179,38 @@ def main():
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
+    op = "fwd_vjp" if ste else args.op
+    dc_out = torch.empty_like(c) if op == "dc" else None
+    vstates = torch.empty((B, L // 2 if vec else L), dtype=torch.int32, device=dev)
+    if op == "viterbi":
+        ws_bytes = (P.bcjr_vec_workspace_bytes(B, L, n, k, 2, P.OP_VITERBI) if vec
+                    else P.bcjr_workspace_bytes(B, L, n, k, P.OP_VITERBI))
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
     def step(mid=None):
-        if ste:
+        if op == "soft":
+            if vec:
+                P.bcjr_vec_soft_codeword(w, c, n, k, 2, T, w_soft=w_soft, logZ=logZ, workspace=ws,
+                                         stream=stream)
+            else:
+                P.bcjr_soft_codeword(w, c, n, k, T, w_soft=w_soft, logZ=logZ, workspace=ws,
+                                     stream=stream)
+        elif op == "viterbi":
+            if vec:
+                P.bcjr_vec_viterbi_decode(w, c, n, k, 2, states=vstates, w_hard=w_soft,
+                                          workspace=ws, stream=stream)
+            else:
+                P.viterbi_decode(w, c, n, k, states=vstates, w_hard=w_soft, workspace=ws,
+                                 stream=stream)
+        elif op == "dc":
+            if vec:
+                P.bcjr_vec_soft_codeword_fwd_vjp(w, c, n, k, 2, T, g, w_soft=w_soft, logZ=logZ,
+                                                 dW=dW, dCodebook=dc_out, workspace=ws,
+                                                 stream=stream)
+            else:
+                P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
+                                             dCodebook=dc_out, workspace=ws, stream=stream)
+        elif ste:
             P.viterbi_decode(w, c, n, k, states=states, w_hard=w_soft, workspace=ws,
                              stream=stream)
             if mid is not None:
@@ -210,16 +251,23 @@ def main():
     print(f"timed {args.steps} steps: {ms_per_step:.1f} ms/step (events avg {kern_avg_s * 1e3:.1f} ms)",
           file=sys.stderr, flush=True)
 
+    op_what = {"fwd_vjp": "fused w_soft+logZ+dW", "soft": "soft codeword + logZ",
+               "dc": "fused w_soft+logZ+dW+dCodebook", "viterbi": "Viterbi decode"}[op]
+    op_metric = {"fwd_vjp": "fwd+VJP", "soft": "soft codeword", "dc": "fwd+VJP incl. dCodebook",
+                 "viterbi": "Viterbi"}[op]
     if vec:
-        metric = ("trellis edge-updates/s fwd+VJP at S=65536, 16 predecessors (4 bits/step), "
+        metric = (f"trellis edge-updates/s {op_metric} at S=65536, 16 predecessors (4 bits/step), "
                   "V=2, 256-weight blocks")
-        what = "V=2, 4 bits per step (128 steps per block), [65536,2] N(0,1) codebook; fused w_soft+logZ+dW"
+        what = f"V=2, 4 bits per step (128 steps per block), [65536,2] N(0,1) codebook; {op_what}"
     elif ste:
         metric = "trellis edge-updates/s BCJR-STE step (Viterbi fwd + VJP) at S=65536,k=2,L=256"
         what = "BCJR-STE step: viterbi_decode + bcjr_ste_vjp (dW)"
-    else:
+    elif op == "fwd_vjp":
         metric = "trellis edge-updates/s fwd+VJP at S=65536,k=2,L=256; % VALU roofline"
         what = "fused w_soft+logZ+dW"
+    else:
+        metric = f"trellis edge-updates/s {op_metric} at S=65536,k=2,L=256"
+        what = op_what
     rec = {
         "metric": metric,
         "value": value,
@@ -237,13 +285,16 @@ def main():
                                f"T={T}; {what}",
                    "B": B, "L": L, "S": wl.S, "k": k, "V": 2 if vec else 1, "T": T},
         "blocks_per_s": B / (ms_per_step / 1e3),
-        "roofline": {"bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
-                     "unit": "Gedge/s", "frac": achieved / peak,
-                     "traffic": None if (ste or vec or args.T is not None)
-                     else MEASURED_TRAFFIC.get(kernel_source_digest()),
-                     "kernel_ms": kern_avg_s * 1e3},
+        "roofline": None if op != "fwd_vjp" else {
+            "bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
+            "unit": "Gedge/s", "frac": achieved / peak,
+            "traffic": None if (ste or args.T is not None)
+            else MEASURED_TRAFFIC.get((args.path, kernel_source_digest())),
+            "kernel_ms": kern_avg_s * 1e3},
     }
-    if not args.no_cpu_baseline and not ste and not vec and args.T is None:
+    if op != "fwd_vjp":
+        rec["kernel_ms"] = kern_avg_s * 1e3
+    if not args.no_cpu_baseline and not ste and not vec and args.T is None and op == "fwd_vjp":
         print("timing the oracle on the host cores ...", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)
