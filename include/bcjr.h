@@ -164,6 +164,40 @@ int bcjr_vec_viterbi_decode(const float *w, int64_t B, int64_t L, const float *c
                             int state_bits, int k, int V, int32_t *states, float *w_hard,
                             void *workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------
+ * Quantisation-aware training helpers.
+ *
+ * Computed Gaussian codebook (Sec. 3.1: c(s) = Phi^{-1}((s + 1/2) / S) under an
+ * incoherent permutation of the states).  Writes codebook[S*V], component a
+ * of state s at [s*V + a]:
+ *     codebook[s*V + a] = Phi^{-1}((pi_a(s) + 1/2) / S)   rounded to fp32,
+ * where pi_a is a bijection of the state_bits-bit integers: with h =
+ * ceil(state_bits / 2) and arithmetic mod 2^state_bits,
+ *     x = s * A1_a + B_a;  x ^= x >> h;  x = x * A2_a;  x ^= x >> h,
+ * and (A1_a | 1, B_a, A2_a | 1) for a = 0, 1, ... are consecutive draws of
+ * SplitMix64 started from `seed`.  Each component is therefore an exact
+ * permutation of the S Gaussian quantiles.  1 <= state_bits <= 24,
+ * 1 <= V <= 8; codebook is a device pointer (4-byte aligned) owned by the
+ * caller.  Asynchronous on stream. */
+int bcjr_gaussian_codebook(float *codebook, int state_bits, int V, uint64_t seed,
+                           hipStream_t stream);
+
+/* One Adam step (Kingma & Ba) of the annealing loop (Sec. 3.6 and the
+ * BCJR-QAT algorithm), elementwise over count values, in place on param, m
+ * and v (device pointers, caller-owned; m and v start at zero):
+ *     g = clamp(grad, -grad_clip, grad_clip)   (no clipping when grad_clip == 0)
+ *     m = beta1 m + (1 - beta1) g,   v = beta2 v + (1 - beta2) g^2
+ *     param -= lr * (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * step >= 1 counts the calls.  The clip is the max-norm bound g_max of the
+ * drift budget. */
+int qat_adam_step(float *param, const float *grad, float *m, float *v, int64_t count, float lr,
+                  float beta1, float beta2, float eps, int64_t step, float grad_clip,
+                  hipStream_t stream);
+
+/* Plain gradient step with the same clipping: param -= lr * clamp(grad). */
+int qat_sgd_step(float *param, const float *grad, int64_t count, float lr, float grad_clip,
+                 hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char *bcjr_status_string(int status);
 

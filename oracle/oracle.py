@@ -168,3 +168,53 @@ def block_tables(w_block, c, n, k, T, g_block=None, V=1):
                                      _ptr(be), _ptr(A), _ptr(Bt))
     _check(rc, "oracle_block_tables_v")
     return al, be, A, Bt
+
+
+# ---------------------------------------------------------------- computed codebook
+_M64 = (1 << 64) - 1
+
+
+def splitmix64(state: int):
+    """SplitMix64 (Steele, Lea and Flood, 2014): returns (new state, output)."""
+    state = (state + 0x9E3779B97F4A7C15) & _M64
+    z = state
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return state, z ^ (z >> 31)
+
+
+def state_permutation(n: int, V: int, seed: int):
+    """The V component permutations of the n-bit states: pi_a(s) with
+    x = s * A1 + B, x ^= x >> h, x = x * A2, x ^= x >> h (mod 2^n,
+    h = ceil(n / 2)), (A1 | 1, B, A2 | 1) consecutive SplitMix64 draws from
+    seed.  Returns an int64 array [S, V]."""
+    S = 1 << n
+    mask = S - 1
+    h = (n + 1) // 2
+    st = seed & _M64
+    s = np.arange(S, dtype=np.uint64)
+    out = np.empty((S, V), np.int64)
+    for a in range(V):
+        st, a1 = splitmix64(st)
+        st, b = splitmix64(st)
+        st, a2 = splitmix64(st)
+        a1 |= 1
+        a2 |= 1
+        with np.errstate(over="ignore"):
+            x = (s * np.uint64(a1) + np.uint64(b)) & np.uint64(mask)
+            x ^= x >> np.uint64(h)
+            x = (x * np.uint64(a2)) & np.uint64(mask)
+            x ^= x >> np.uint64(h)
+        out[:, a] = x.astype(np.int64)
+    return out
+
+
+def gaussian_codebook(n: int, V: int, seed: int):
+    """Computed Gaussian emission (paper Sec. 3.1): c_a(s) = Phi^{-1}((pi_a(s) +
+    1/2) / S) under the incoherent permutation above.  float64 [S, V]
+    (V = 1: [S])."""
+    from scipy.special import ndtri
+    S = 1 << n
+    pi = state_permutation(n, V, seed)
+    c = ndtri((pi.astype(np.float64) + 0.5) / S)
+    return c[:, 0] if V == 1 else c

@@ -22,6 +22,10 @@ and the vector-emission forms (V weights per step, codebook [S, V]):
     bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, g)
     bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V)            -> (states, w_hard)
     bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op)              -> int
+and the training helpers:
+    bcjr_gaussian_codebook(state_bits, V, seed)                       -> codebook [S] or [S, V]
+    qat_adam_step(param, grad, m, v, lr, beta1, beta2, eps, step, grad_clip)   (in place)
+    qat_sgd_step(param, grad, lr, grad_clip)                          (in place)
 """
 from __future__ import annotations
 
@@ -33,7 +37,7 @@ __all__ = [
     "bcjr_workspace_bytes", "bcjr_status_string", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
     "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode", "bcjr_vec_workspace_bytes",
     "bcjr_vec_soft_codeword", "bcjr_vec_soft_codeword_vjp", "bcjr_vec_soft_codeword_fwd_vjp",
-    "bcjr_vec_viterbi_decode",
+    "bcjr_vec_viterbi_decode", "bcjr_gaussian_codebook", "qat_adam_step", "qat_sgd_step",
 ]
 
 OP_FWD, OP_VJP, OP_FWD_VJP, OP_VITERBI = 0, 1, 2, 3
@@ -83,10 +87,15 @@ def load_library():
     L.bcjr_vec_soft_codeword_fwd_vjp.argtypes = [vp, i64, i64, vp, ci, ci, ci, cf, vp, vp, vp, vp,
                                                  vp, vp, sz, vp]
     L.bcjr_vec_viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, ci, vp, vp, vp, sz, vp]
+    u64 = ctypes.c_uint64
+    L.bcjr_gaussian_codebook.argtypes = [vp, ci, ci, u64, vp]
+    L.qat_adam_step.argtypes = [vp, vp, vp, vp, i64, cf, cf, cf, cf, i64, cf, vp]
+    L.qat_sgd_step.argtypes = [vp, vp, i64, cf, cf, vp]
     for f in (L.bcjr_soft_codeword, L.bcjr_soft_codeword_vjp, L.bcjr_soft_codeword_fwd_vjp,
               L.bcjr_ste_vjp, L.viterbi_decode, L.bcjr_vec_soft_codeword,
               L.bcjr_vec_soft_codeword_vjp, L.bcjr_vec_soft_codeword_fwd_vjp,
-              L.bcjr_vec_viterbi_decode):
+              L.bcjr_vec_viterbi_decode, L.bcjr_gaussian_codebook, L.qat_adam_step,
+              L.qat_sgd_step):
         f.restype = ci
     _lib = L
     return L
@@ -359,3 +368,42 @@ def bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V, *, want_w_hard=True, 
                                      _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
     _raise("bcjr_vec_viterbi_decode", rc)
     return states, w_hard
+
+
+# ---------------------------------------------------------------- training helpers
+def bcjr_gaussian_codebook(state_bits, V=1, seed=0, *, out=None, device="cuda", stream=None):
+    """Computed Gaussian codebook: [S] (V = 1) or [S, V] float32 on the device."""
+    torch = _torch()
+    lib = load_library()
+    S = 1 << state_bits
+    if out is None:
+        out = torch.empty((S,) if V == 1 else (S, V), dtype=torch.float32, device=device)
+    _check_in("out", out)
+    if out.numel() != S * V:
+        raise ValueError(f"out must hold {S} x {V} values")
+    rc = lib.bcjr_gaussian_codebook(_ptr(out), state_bits, V, int(seed) & ((1 << 64) - 1),
+                                    _stream(stream))
+    _raise("bcjr_gaussian_codebook", rc)
+    return out
+
+
+def qat_adam_step(param, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, step=1, grad_clip=0.0,
+                  stream=None):
+    """One Adam step in place on param, m, v (same shape, float32, device)."""
+    lib = load_library()
+    for name, t in (("param", param), ("grad", grad), ("m", m), ("v", v)):
+        _check_in(name, t, tuple(param.shape))
+    rc = lib.qat_adam_step(_ptr(param), _ptr(grad), _ptr(m), _ptr(v), param.numel(), float(lr),
+                           float(beta1), float(beta2), float(eps), int(step), float(grad_clip),
+                           _stream(stream))
+    _raise("qat_adam_step", rc)
+
+
+def qat_sgd_step(param, grad, lr, grad_clip=0.0, stream=None):
+    """param -= lr * clamp(grad, -grad_clip, grad_clip), in place."""
+    lib = load_library()
+    _check_in("param", param)
+    _check_in("grad", grad, tuple(param.shape))
+    rc = lib.qat_sgd_step(_ptr(param), _ptr(grad), param.numel(), float(lr), float(grad_clip),
+                          _stream(stream))
+    _raise("qat_sgd_step", rc)

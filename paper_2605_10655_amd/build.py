@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libbcjr.so")
 SOURCES = [os.path.join(CSRC, "bcjr_capi.hip")]
-DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_internal.h")] + [
+DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_qat.h", "bcjr_internal.h")] + [
     os.path.join(INCLUDE, "bcjr.h")]
 
 

@@ -11,6 +11,7 @@
 #include "bcjr_internal.h"
 #include "bcjr_kernels.h"
 #include "bcjr_vec_kernels.h"
+#include "bcjr_qat.h"
 
 namespace bcjr {
 namespace {
@@ -717,6 +718,42 @@ int bcjr_vec_viterbi_decode(const float* w, int64_t B, int64_t L, const float* c
   if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
   if (B == 0) return BCJR_OK;
   return run_vitv(w, B, L, codebook, state_bits, states, w_hard, workspace, ws_bytes, stream);
+}
+
+int bcjr_gaussian_codebook(float* codebook, int state_bits, int V, uint64_t seed,
+                           hipStream_t stream) {
+  if (!codebook || state_bits < 1 || state_bits > 24 || V < 1 || V > kMaxV)
+    return BCJR_ERR_INVALID_ARG;
+  if ((uintptr_t)codebook & 3u) return BCJR_ERR_INVALID_ARG;
+  const int64_t count = (int64_t)V << state_bits;
+  hipLaunchKernelGGL(gauss_codebook_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, stream,
+                     codebook, state_bits, V, perm_set(seed, V));
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+int qat_adam_step(float* param, const float* grad, float* m, float* v, int64_t count, float lr,
+                  float beta1, float beta2, float eps, int64_t step, float grad_clip,
+                  hipStream_t stream) {
+  if (count < 0 || step < 1 || !(lr >= 0.f) || !(beta1 >= 0.f && beta1 < 1.f) ||
+      !(beta2 >= 0.f && beta2 < 1.f) || !(eps > 0.f) || !(grad_clip >= 0.f))
+    return BCJR_ERR_INVALID_ARG;
+  if (count == 0) return BCJR_OK;
+  if (!param || !grad || !m || !v) return BCJR_ERR_INVALID_ARG;
+  const float c1 = (float)(1.0 / (1.0 - std::pow((double)beta1, (double)step)));
+  const float c2 = (float)(1.0 / (1.0 - std::pow((double)beta2, (double)step)));
+  hipLaunchKernelGGL(adam_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, stream, param,
+                     grad, m, v, count, lr, beta1, beta2, eps, c1, c2, grad_clip);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+int qat_sgd_step(float* param, const float* grad, int64_t count, float lr, float grad_clip,
+                 hipStream_t stream) {
+  if (count < 0 || !(lr >= 0.f) || !(grad_clip >= 0.f)) return BCJR_ERR_INVALID_ARG;
+  if (count == 0) return BCJR_OK;
+  if (!param || !grad) return BCJR_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, stream, param,
+                     grad, count, lr, grad_clip);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
 const char* bcjr_status_string(int status) {

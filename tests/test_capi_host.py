@@ -185,3 +185,22 @@ def test_vector_emission_host_checks(lib):
     assert vd(FAKE, 4, 8, FAKE, 8, 4, 2, None, None, FAKE, 1 << 20, None) == -1
     assert vd(FAKE, 4, 8, FAKE, 8, 4, 2, FAKE, None, None, 0, None) == -3
     assert vd(FAKE, 0, 8, FAKE, 8, 4, 2, None, None, None, 0, None) == 0
+
+
+def test_training_helpers_argument_validation(lib):
+    g = lib.bcjr_gaussian_codebook
+    assert g(None, 8, 1, 0, None) == -1
+    assert g(FAKE, 0, 1, 0, None) == -1
+    assert g(FAKE, 25, 1, 0, None) == -1
+    assert g(FAKE, 8, 9, 0, None) == -1
+    assert g(FAKE + 2, 8, 1, 0, None) == -1
+    a = lib.qat_adam_step
+    assert a(None, None, None, None, 0, 1e-3, 0.9, 0.999, 1e-8, 1, 0.0, None) == 0  # empty
+    assert a(FAKE, FAKE, FAKE, FAKE, 4, 1e-3, 0.9, 0.999, 1e-8, 0, 0.0, None) == -1  # step 0
+    assert a(FAKE, FAKE, FAKE, FAKE, 4, 1e-3, 1.0, 0.999, 1e-8, 1, 0.0, None) == -1  # beta1
+    assert a(FAKE, FAKE, FAKE, FAKE, 4, 1e-3, 0.9, 0.999, 0.0, 1, 0.0, None) == -1   # eps
+    assert a(FAKE, None, FAKE, FAKE, 4, 1e-3, 0.9, 0.999, 1e-8, 1, 0.0, None) == -1
+    s = lib.qat_sgd_step
+    assert s(None, None, 0, 0.1, 0.0, None) == 0
+    assert s(FAKE, FAKE, 4, -0.1, 0.0, None) == -1
+    assert s(FAKE, FAKE, 4, 0.1, -1.0, None) == -1

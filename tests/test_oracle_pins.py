@@ -456,3 +456,42 @@ def test_vector_ste_composition():
     np.testing.assert_array_equal(wh[0], c[p].reshape(-1))
     ref = bf.expectations(w, c, n, k, T, g, V=2)
     np.testing.assert_allclose(dW[0], ref["dW"], rtol=0, atol=1e-10 * max(1, abs(ref["dW"]).max()))
+
+
+
+# ---------------------------------------------------------------- computed codebook
+def test_splitmix64_reference_outputs():
+    """The first outputs of SplitMix64 started from state 0, as printed by its
+    reference C implementation (Vigna)."""
+    st, out = 0, []
+    for _ in range(3):
+        st, z = O.splitmix64(st)
+        out.append(z)
+    assert out == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+@pytest.mark.parametrize("n,V", [(1, 1), (4, 2), (8, 1), (12, 2), (16, 2), (17, 3)])
+def test_state_permutation_is_a_bijection(n, V):
+    pi = O.state_permutation(n, V, 20260510)
+    for a in range(V):
+        assert np.array_equal(np.sort(pi[:, a]), np.arange(1 << n))
+    if n >= 8:  # incoherent: neighbouring states land far apart
+        d = np.abs(np.diff(pi[:, 0]))
+        assert np.median(d) > (1 << n) / 16
+
+
+@pytest.mark.parametrize("n,V", [(4, 1), (10, 2), (16, 2)])
+def test_gaussian_codebook_is_the_normal_quantiles(n, V):
+    """Sorted, each component is the S Gaussian quantiles: Phi(c_(i)) = (i + 1/2)/S
+    with Phi from the error function, and the quantiles are symmetric."""
+    import math
+    c = O.gaussian_codebook(n, V, 7).reshape(1 << n, V)
+    S = 1 << n
+    for a in range(V):
+        q = np.sort(c[:, a])
+        phi = np.array([0.5 * math.erfc(-x / math.sqrt(2.0)) for x in q])
+        np.testing.assert_allclose(phi, (np.arange(S) + 0.5) / S, rtol=1e-12, atol=0)
+        np.testing.assert_allclose(q, -q[::-1], rtol=0, atol=1e-12)
+    assert abs(c.mean()) < 1e-12
+    if n >= 10:
+        assert abs(c.var() - 1) < 0.01
