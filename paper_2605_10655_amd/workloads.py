@@ -11,7 +11,8 @@ for incoherence-processed (approximately iid Gaussian) Llama-3.2-1B
 projection weights; none of the paper's models or datasets are used.
 
 Seeds: 1000 * cfg + {0: codebook, 1: weights, 2 + call: upstream gradient,
-500: [S, 2] codebook of the vector-emission trellis, 900: parity subset}.
+500: [S, 2] codebook of the vector-emission trellis, 600: calibration inputs,
+900: parity subset}.
 """
 from __future__ import annotations
 
@@ -106,6 +107,17 @@ def codebook_vec(cfg: int, V: int = 2) -> np.ndarray:
     1000 * cfg + 500)."""
     wl = WORKLOADS[cfg]
     return _rng(1000 * cfg + 500).standard_normal((wl.S, V)).astype(np.float32)
+
+
+def calibration_inputs(cfg: int, n_x: int = 4096) -> np.ndarray:
+    """Synthetic layer inputs X [n_x, cols] for a proxy Hessian H = X^T X / n_x:
+    N(0,1) draws times per-column scales exp(N(0, 0.5^2)), the uneven input
+    channel energies of LLM activations (seed 1000 * cfg + 600)."""
+    wl = WORKLOADS[cfg]
+    r = _rng(1000 * cfg + 600)
+    scale = np.exp(0.5 * r.standard_normal(wl.cols)).astype(np.float32)
+    X = r.standard_normal((n_x, wl.cols), dtype=np.float32)
+    return X * scale[None, :]
 
 
 def upstream(cfg: int, call: int = 0, B: int | None = None) -> np.ndarray:
