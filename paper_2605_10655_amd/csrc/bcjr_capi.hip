@@ -445,11 +445,12 @@ size_t vitv_lds_bytes(const VecFamily& f, int n) {
 }
 
 // One workgroup's histories are addressed with 32-bit byte offsets: blocks
-// per workgroup x N steps x S/16 groups x 8 bytes (4 for the soft codeword
+// per workgroup x N steps x S/16 groups x 16 bytes (4 for the soft codeword
 // alone) below 2^31.
 bool vec_length_ok(int64_t N, int n, bool vjp) {
   const VecFamily f = vec_family(n);
-  const int64_t per_step = (int64_t)f.bpw * (vjp ? 8 : 4) * ((int64_t)1 << (n - 4));
+  // 16 bytes per group for the VJP (the low-temperature variant's entries)
+  const int64_t per_step = (int64_t)f.bpw * (vjp ? 16 : 4) * ((int64_t)1 << (n - 4));
   return N >= 1 && N <= 0x7FFFFFFF / per_step;
 }
 
@@ -469,6 +470,34 @@ FbLayout fbv_layout(int64_t N, int n, bool vjp, bool dc) {
 
 size_t vitv_slot_bytes(int64_t N, int n) { return align_up((size_t)N * ((size_t)1 << (n - 4))); }
 
+// Low-temperature V = 2 VJP: histories of (hi, lo, tangent, 0) entries, the
+// lo-word exchange buffer, the per-step scalars (with lambda_t in fp64).
+struct HpvLayout {
+  size_t hist, histGA, xlo, small, dc, slot;
+};
+
+HpvLayout fbv_hp_layout(int64_t N, int n, bool dc) {
+  const size_t gs = (size_t)1 << (n - 4);
+  HpvLayout l;
+  l.hist = align_up((size_t)N * gs * 16);
+  l.histGA = dc ? align_up((size_t)N * gs * 16) : 0;
+  l.xlo = align_up(2 * gs * sizeof(float));
+  l.small = align_up((size_t)6 * N * sizeof(float));
+  l.dc = dc ? align_up(((size_t)2 << n) * sizeof(double)) : 0;
+  l.slot = l.hist + l.histGA + l.xlo + l.small + l.dc;
+  return l;
+}
+
+// [w_hard B*L f32][states B*(L/2) i32]: the reference decode of the
+// low-temperature VJP
+size_t fbv_hp_prefix_bytes(int64_t B, int64_t L) {
+  return align_up((size_t)B * L * 4) + align_up((size_t)B * (L / 2) * 4);
+}
+
+size_t fbv_hp_lds_bytes(const VecFamily& f, int n) {
+  return fbv_lds_bytes(f, n) + (size_t)(f.nt / 64) * sizeof(double);
+}
+
 using FbvFn = void (*)(FbvArgs);
 using VitvFn = void (*)(VitvArgs);
 
@@ -482,6 +511,11 @@ FbvFn fbv_variant(bool vjp, bool dc) {
 FbvFn fbv_pick(int n, bool vjp, bool dc) {
   if (n == 16) return fbv_variant<16, 8>(vjp, dc);
   return fbv_variant<0, 8>(vjp, dc);
+}
+
+FbvFn fbv_hp_pick(int n, bool dc) {
+  if (n == 16) return dc ? fbv_kernel_hp<16, 8, 512, true> : fbv_kernel_hp<16, 8, 512, false>;
+  return dc ? fbv_kernel_hp<0, 8, 512, true> : fbv_kernel_hp<0, 8, 512, false>;
 }
 
 VitvFn vitv_pick(int n) {
@@ -521,13 +555,78 @@ int run_vitv(const float* w, int64_t B, int64_t L, const float* codebook, int n,
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+// `ref` is the centring reference of the backward tangent ([B, L]); when it
+// is null the minimum-distortion codewords are decoded into the workspace
+// first.
+int run_fbv_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, float T,
+               const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
+               float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  const bool dc = dCodebook != nullptr;
+  const VecFamily f = vec_family(n);
+  const int64_t N = L / 2;
+  const HpvLayout lay = fbv_hp_layout(N, n, dc);
+  FbvFn fn = fbv_hp_pick(n, dc);
+  const size_t cb = vec_cs_bytes(n);
+  if (ws_bytes <= cb) return BCJR_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  float* cs = reinterpret_cast<float*>(ws);
+  const int64_t S2 = (int64_t)2 << n;
+  char* rest = ws + cb;
+  size_t rest_bytes = ws_bytes - cb;
+  if (!ref) {
+    const size_t pre = fbv_hp_prefix_bytes(B, L);
+    if (rest_bytes <= pre) return BCJR_ERR_WORKSPACE;
+    float* w_hard = reinterpret_cast<float*>(rest);
+    int32_t* states = reinterpret_cast<int32_t*>(rest + align_up((size_t)B * L * 4));
+    rest += pre;
+    rest_bytes -= pre;
+    int st = run_vitv(w, B, L, codebook, n, states, w_hard, rest, rest_bytes, stream);
+    if (st != BCJR_OK) return st;
+    ref = w_hard;
+  }
+  const size_t lds = fbv_hp_lds_bytes(f, n);
+  Family ff;
+  ff.nt = f.nt; ff.bpw = f.bpw;
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, ff, lds, B, rest_bytes, lay.slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const int64_t slots = grid * f.bpw;
+  FbvArgs a = {};
+  a.w = w; a.g = g; a.cs = cs; a.csT = cs + S2; a.B = B; a.N = N; a.n = n; a.sgt = f.sgt;
+  const double Td = (double)T;
+  a.k2d = 1.4426950408889634074 / (2.0 * Td);
+  a.invT = (float)(1.0 / Td);
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  a.bref = ref;
+  // the unscaled codebook and its transposed copy
+  hipLaunchKernelGGL(scale_vec_kernel, dim3((unsigned)ceil_div((int64_t)1 << n, 256)), dim3(256), 0,
+                     stream, codebook, 1.0f, cs, const_cast<float*>(a.csT), n);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  char* p = rest;
+  a.hist = reinterpret_cast<float*>(p);                     p += slots * lay.hist;
+  a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;    p += slots * lay.histGA;
+  a.xlo = reinterpret_cast<float*>(p);                      p += slots * lay.xlo;
+  a.small = reinterpret_cast<float*>(p);                    p += slots * lay.small;
+  a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dc) {
+    const int64_t used = slots < B ? slots : B;
+    hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S2, 256)), dim3(256), 0, stream,
+                       a.dc_part, used, S2, dCodebook);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
 int run_fbv(const float* w, int64_t B, int64_t L, const float* codebook, int n, float T,
             const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
             void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
-  // the fp32 VJP of this trellis holds its accuracy above T = 0.04 (the
-  // double-float variant exists for the scalar trellis only)
-  if (vjp && use_high_precision(T)) return BCJR_ERR_UNSUPPORTED;
+  if (vjp && use_high_precision(T))
+    return run_fbv_hp(w, B, L, codebook, n, T, g, nullptr, w_soft, logZ, dW, dCodebook, workspace,
+                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
   const VecFamily f = vec_family(n);
   const int64_t N = L / 2;
@@ -662,7 +761,13 @@ size_t bcjr_vec_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int
   const int64_t N = L / V;
   const int64_t slots = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est) * f.bpw;
   if (op == BCJR_OP_VITERBI) return (size_t)slots * vitv_slot_bytes(N, state_bits);
-  return vec_cs_bytes(state_bits) + (size_t)slots * fbv_layout(N, state_bits, vjp, vjp).slot;
+  size_t bytes = vec_cs_bytes(state_bits) + (size_t)slots * fbv_layout(N, state_bits, vjp, vjp).slot;
+  if (vjp) {  // the temperature decides the variant at call time: cover both
+    const size_t vit = (size_t)slots * vitv_slot_bytes(N, state_bits);
+    const size_t hp = (size_t)slots * fbv_hp_layout(N, state_bits, true).slot;
+    bytes = std::max(bytes, vec_cs_bytes(state_bits) + fbv_hp_prefix_bytes(B, L) + std::max(vit, hp));
+  }
+  return bytes;
 }
 
 int bcjr_vec_soft_codeword(const float* w, int64_t B, int64_t L, const float* codebook,
@@ -692,7 +797,6 @@ int bcjr_vec_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const f
   if (!temperature_ok(T)) return BCJR_ERR_INVALID_ARG;
   if (B > 0 && !grad_w_soft) return BCJR_ERR_INVALID_ARG;
   if (grad_w_soft && ((uintptr_t)grad_w_soft & 3u)) return BCJR_ERR_INVALID_ARG;
-  if (use_high_precision(T)) return BCJR_ERR_UNSUPPORTED;
   if (B == 0) return fill_zero(dCodebook, (int64_t)V << state_bits, stream);
   if (!w_soft && !logZ && !dW && !dCodebook) return BCJR_OK;
   return run_fbv(w, B, L, codebook, state_bits, T, grad_w_soft, w_soft, logZ, dW, dCodebook,

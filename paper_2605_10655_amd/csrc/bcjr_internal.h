@@ -51,6 +51,13 @@ struct FbvArgs {
   float* hist;         // [slots][N][S/16] H_t, or [slots][N][S/16][2] (H_t, B_t) with the VJP
   float* histGA;       // [slots][N][S/16][2] (G_t, A_t) (dCodebook)
   float* small;        // [slots][4][N] shifts of H, lambda_t, E_p[X_t], A centring
+  // low-temperature variant (double-float log vectors, unscaled codebook in
+  // cs / csT): hist and histGA hold [slots][N][S/16][4] (hi, lo, tangent, 0),
+  // small [slots][6][N] (shift, E_p[X_t], A centring, -, lambda_t as fp64)
+  double k2d;          // log2(e) / (2T)
+  float invT;          // 1 / T
+  const float* bref;   // [B, 2N] centring reference of the backward tangent
+  float* xlo;          // [slots][2][S/16] lo words of the group vector being exchanged
 };
 
 struct VitvArgs {

@@ -521,6 +521,362 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Low-temperature VJP of the vector-emission trellis (T < 0.04).  As in the
+// scalar trellis's fb_kernel_hp, G and H are double-float pairs (an fp32 hi
+// word and an fp32 lo word) with the emission and the log-sum-exp in fp64;
+// softmax weights and tangents stay fp32.  The hi words and the tangent
+// ping-pong in LDS as (hi, tangent) pairs, the lo words in a per-slot global
+// buffer, one barrier per step.  The codebook is unscaled here (cs = c,
+// csT its transposed copy).  The backward tangent is centred on the
+// reference codewords bref (the minimum-distortion path, which the posterior
+// follows at low temperature), X is centred per state before the moment
+// sums, and the forward tangent is centred on <g_t, w_soft_t> when read.
+//   S0 backward: H, B; history entries (H hi, H lo, B, 0);
+//   S1 forward:  G, A, marginals, w_soft, dW; with DC the (G hi, G lo, A, 0)
+//                entries and the exact lambda_t, E_p[X_t], A centring;
+//   S2 (DC):     dCodebook per state over all steps.
+// ---------------------------------------------------------------------------
+template <int NB, int SGMAX, int NT, bool DC>
+__global__ void __launch_bounds__(NT) fbv_kernel_hp(FbvArgs a) {
+  extern __shared__ float lds[];
+  const int n = NB ? NB : a.n;
+  const VecGeom q = vec_geom(n);
+  const int GS = q.GS, NSG = q.NSG;
+  const int SGT = NB ? SGMAX : a.sgt;
+  const int TPB = 16 * NSG / SGT;
+  const int TQ = TPB / 16;
+  const int BPW = NT / TPB;
+  const int tid = threadIdx.x;
+  const int bw = BPW == 1 ? 0 : tid / TPB;
+  const int tb = BPW == 1 ? tid : tid - bw * TPB;
+  const int tq = tb >> 4, tl = tb & 15;
+  const int64_t N = a.N, L = 2 * a.N;
+  const double k2 = a.k2d;
+  const float invT = a.invT;
+
+  RedCtx rc;
+  rc.width = TPB < 64 ? TPB : 64;
+  rc.rw = TPB > 64 ? TPB / 64 : 1;
+  rc.lane = tid & 63;
+  rc.wave = tid >> 6;
+  float* const red0 = lds + (size_t)BPW * 4 * q.VSZ;  // [2 parities][waves][kRed] floats
+  double* const redd = reinterpret_cast<double*>(red0 + 2 * (NT / 64) * kRed);  // [waves]
+  rc.red = red0;
+  float* const vec0 = lds + (size_t)bw * 4 * q.VSZ;
+  float* const vec1 = vec0 + 2 * q.VSZ;
+
+  const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)8 << n);
+  const rsrc_t cbkT = make_rsrc(a.csT, (uint32_t)8 << n);
+  const uint32_t voC1 = ((uint32_t)tq * 16 + tl) * 8u;
+  const uint32_t tileC = (uint32_t)TQ * 128u;
+  const uint32_t voC0 = ((uint32_t)tq * 256 + tl) * 8u;
+  const uint32_t tileCT = (uint32_t)TQ * 2048u;
+  const uint32_t hstep = (uint32_t)GS * 16u;          // history bytes per step (4 floats per group)
+  const uint32_t voH = (uint32_t)bw * (uint32_t)N * hstep + ((uint32_t)tq * 16 + tl) * 16u;
+  const uint32_t tileH = (uint32_t)TQ * 16u * 16u;
+  const bool lane_rows = TPB >= 64;
+
+  for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    const int64_t blk = base + bw;
+    const bool valid = blk < a.B;
+    const int64_t bb = valid ? blk : a.B - 1;
+    const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const int64_t slot0 = (int64_t)blockIdx.x * BPW;
+    const float* wb = a.w + bb * L;
+    const float* gb = a.g + bb * L;
+    const float* rb = a.bref + bb * L;
+    const rsrc_t hist = make_rsrc(a.hist + slot0 * N * GS * 4, (uint32_t)BPW * (uint32_t)N * hstep);
+    const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * N * GS * 4 : a.hist,
+                                 DC ? (uint32_t)BPW * (uint32_t)N * hstep : 0u);
+    float* xlo0 = a.xlo + slot * 2 * GS;
+    float* xlo1 = xlo0 + GS;
+    float* sm_mB = a.small + slot * 6 * N;   // shift applied to H_t
+    float* sm_xb = sm_mB + N;                // dCodebook: E_p[X_t]
+    float* sm_cp = sm_xb + N;                // dCodebook: centring of A_t
+    double* sm_lam = reinterpret_cast<double*>(sm_mB + 4 * N);  // dCodebook: lambda_t
+
+    // ---------------------------------------------------------------- S0
+    for (int i = tb; i < 2 * q.VSZ; i += TPB) vec0[i] = 0.f;
+    for (int i = tb; i < GS; i += TPB) xlo0[i] = 0.f;
+    if (tb == 0) sm_mB[N - 1] = 0.f;
+    __syncthreads();
+    double shiftB = 0.0;
+    double lam0 = 0.0;
+    float xbar = 0.f;
+    float dlag = 0.f;
+    PairRows rw_, rg_, rr_;
+    for (int64_t t = N - 1;; --t) {
+      const int par = (int)((N - 1 - t) & 1);
+      rc.red = red0 + par * (NT / 64) * kRed;
+      float* cur = par ? vec1 : vec0;
+      float* nxt = par ? vec0 : vec1;
+      const float* xlo_r = par ? xlo1 : xlo0;
+      float* xlo_w = par ? xlo0 : xlo1;
+      const bool reload = t == N - 1 || (t & 31) == 31;
+      float w0f, w1f, g0, g1, r0, r1;
+      pair_at(wb, t, L, lane_rows, reload, rw_, w0f, w1f);
+      pair_at(gb, t, L, lane_rows, reload, rg_, g0, g1);
+      pair_at(rb, t, L, lane_rows, reload, rr_, r0, r1);
+      const double w0 = (double)w0f, w1 = (double)w1f;
+      const uint32_t soH = (uint32_t)t * hstep;
+      const bool first = t == 0;
+      double lm = -INFINITY;
+      float ls = 0.f, ly = 0.f;
+      float vmax[1] = {-INFINITY};
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        const int m = tq + i * TQ;
+        float cc[32], hb[32], hl[16];
+        row_codewords(cbkT, voC0, (uint32_t)i * tileCT, cc);
+#pragma unroll
+        for (int u4 = 0; u4 < 8; ++u4) {
+          float t4[4];
+          ld_vec<4>(cur + 2 * q.row(m) + 4 * u4, t4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) hb[4 * u4 + e] = t4[e];
+        }
+        ld_vec<16>(xlo_r + m * 16, hl);
+        {
+          float own[2];
+          ld_vec<2>(cur + 2 * (q.row(m) + tl), own);
+          const float ent[4] = {own[0], xlo_r[m * 16 + tl], own[1], 0.f};
+          buf_st<4>(hist, voH, soH + (uint32_t)i * tileH, ent);
+        }
+        double x[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const double d0 = w0 - (double)cc[2 * u], d1 = w1 - (double)cc[2 * u + 1];
+          x[u] = fma(-k2, fma(d0, d0, d1 * d1), (double)hb[2 * u] + (double)hl[u]);
+        }
+        const double M = max_of<16>(x);
+        float s = 0.f, sy = 0.f;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const float E = ex2((float)(x[u] - M));
+          s += E;
+          // first step: E_p[<g_0, c> + B_0]; otherwise the summand of B_{t-1},
+          // <g_t, c - r_t> + B_t
+          const float y = first ? fmaf(g1, cc[2 * u + 1], fmaf(g0, cc[2 * u], hb[2 * u + 1]))
+                                : fmaf(g1, cc[2 * u + 1] - r1, fmaf(g0, cc[2 * u] - r0, hb[2 * u + 1]));
+          sy = fmaf(E, y, sy);
+        }
+        if (first) {
+          lse3_pair_d(lm, ls, ly, M, s, sy);
+        } else {
+          const double h = M + (double)lg2(s) - (double)dlag;
+          float hi, lo;
+          split_df(h, hi, lo);
+          vmax[0] = fmaxf(vmax[0], hi);
+          const float o[2] = {hi, sy * rcp(s)};
+          st_vec<2>(nxt + 2 * q.col(tl, m), o);
+          xlo_w[tl * NSG + m] = lo;
+        }
+        sg_fence();
+      }
+      if (first) {
+        lse3d_pre(lm, ls, ly, rc, redd);
+        __syncthreads();
+        lse3d_post(lm, ls, ly, rc, redd);
+        xbar = ly / ls;
+        lam0 = lm + (double)lg2(ls);
+        if (tb == 0 && valid && a.logZ)
+          a.logZ[bb] = (float)((shiftB + lam0) * 0.69314718055994530942);
+        __syncthreads();
+        break;
+      }
+      shiftB += (double)dlag;
+      if (tb == 0) sm_mB[t - 1] = dlag;
+      red_pre<1, 1u>(vmax, rc);
+      __syncthreads();
+      red_post<1, 1u>(vmax, rc);
+      dlag = floorf(vmax[0]);
+    }
+
+    // ---------------------------------------------------------------- S1
+    for (int i = tb; i < 2 * q.VSZ; i += TPB) vec0[i] = 0.f;
+    for (int i = tb; i < GS; i += TPB) xlo0[i] = 0.f;
+    if constexpr (DC) {
+      const float z[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) buf_st<4>(hga, voH, (uint32_t)i * tileH, z);
+    }
+    __syncthreads();
+    double lam_est = lam0;
+    float cprev = 0.f;
+    dlag = 0.f;
+    float pH[4];
+    buf_ld<4>(hist, voH, 0u, pH);
+    for (int64_t t = 0; t < N; ++t) {
+      const int par = (int)(t & 1);
+      rc.red = red0 + par * (NT / 64) * kRed;
+      float* cur = par ? vec1 : vec0;
+      float* nxt = par ? vec0 : vec1;
+      const float* xlo_r = par ? xlo1 : xlo0;
+      float* xlo_w = par ? xlo0 : xlo1;
+      const bool reload = (t & 31) == 0;
+      float w0f, w1f, g0, g1, r0, r1;
+      pair_at(wb, t, L, lane_rows, reload, rw_, w0f, w1f);
+      pair_at(gb, t, L, lane_rows, reload, rg_, g0, g1);
+      pair_at(rb, t, L, lane_rows, reload, rr_, r0, r1);
+      const double w0 = (double)w0f, w1 = (double)w1f;
+      if (t > 0) xbar = fmaf(g1, r1, fmaf(g0, r0, xbar));  // B_t no longer holds step t
+      const double mBt = (double)sm_mB[t];
+      const uint32_t soH = (uint32_t)t * hstep;
+      float rv[7] = {-INFINITY, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        const int m = tq + i * TQ;
+        const float hu[4] = {pH[0], pH[1], pH[2], pH[3]};
+        float c0[16], c1[16], Ar[16];
+        double G[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float cv[2], ga[2];
+          buf_ld<2>(cbk, voC1, (uint32_t)r * (uint32_t)GS * 8u + (uint32_t)i * tileC, cv);
+          c0[r] = cv[0];
+          c1[r] = cv[1];
+          ld_vec<2>(cur + 2 * q.col(r, m), ga);
+          G[r] = (double)ga[0] + (double)xlo_r[r * NSG + m];
+          Ar[r] = ga[1] - cprev;
+        }
+        {
+          const bool last = i + 1 >= SGT;
+          const int64_t tn = last && t + 1 < N ? t + 1 : t;
+          buf_ld<4>(hist, voH, (uint32_t)tn * hstep + (last ? 0u : (uint32_t)(i + 1) * tileH), pH);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const double d0 = w0 - (double)c0[r], d1 = w1 - (double)c1[r];
+          G[r] = fma(-k2, fma(d0, d0, d1 * d1), G[r]);
+        }
+        const double M = max_of<16>(G);
+        // X is centred per state before the sums (at low T uncentred moments
+        // cancel only to X's rounding, amplified by 1/T)
+        const float bx = hu[2] - xbar;
+        float s = 0.f, e0 = 0.f, e1 = 0.f, sx = 0.f, sx0 = 0.f, sx1 = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float E = ex2((float)(G[r] - M));
+          const float X = fmaf(g1, c1[r], fmaf(g0, c0[r], Ar[r])) + bx;
+          const float EX = E * X;
+          s += E;
+          e0 = fmaf(E, c0[r], e0);
+          e1 = fmaf(E, c1[r], e1);
+          sx += EX;
+          sx0 = fmaf(EX, c0[r], sx0);
+          sx1 = fmaf(EX, c1[r], sx1);
+        }
+        const double gout = M + (double)lg2(s) - (double)dlag;
+        float hi, lo;
+        split_df(gout, hi, lo);
+        rv[0] = fmaxf(rv[0], hi);
+        const float f = ex2((float)(M + ((double)hu[0] + (double)hu[1]) - lam_est));
+        rv[1] = fmaf(f, s, rv[1]);
+        rv[2] = fmaf(f, e0, rv[2]);
+        rv[3] = fmaf(f, e1, rv[3]);
+        rv[4] = fmaf(f, sx, rv[4]);
+        rv[5] = fmaf(f, sx0, rv[5]);
+        rv[6] = fmaf(f, sx1, rv[6]);
+        const float An = fmaf(sx, rcp(s), -bx);  // E-weighted mean of <g_t, c> + A_t
+        if (t < N - 1) {
+          const float o[2] = {hi, An};
+          st_vec<2>(nxt + 2 * (q.row(m) + tl), o);
+          xlo_w[m * 16 + tl] = lo;
+          if constexpr (DC) {
+            const float ent[4] = {hi, lo, An, 0.f};
+            buf_st<4>(hga, voH, soH + hstep + (uint32_t)i * tileH, ent);
+          }
+        }
+        sg_fence();
+      }
+      red_pre<7, 1u>(rv, rc);
+      __syncthreads();
+      red_post<7, 1u>(rv, rc);
+      const float r1v = 1.f / rv[1];
+      const float ws0 = rv[2] * r1v, ws1 = rv[3] * r1v;
+      const double lamt = lam_est + (double)lg2(rv[1]);
+      const float xbe = fmaf(rv[4], r1v, xbar);
+      if (tb == 0) {
+        if (DC) {
+          sm_lam[t] = lamt;
+          sm_xb[t] = xbe;
+          sm_cp[t] = cprev;
+        }
+        if (valid) {
+          if (a.w_soft) {
+            a.w_soft[bb * L + 2 * t] = ws0;
+            a.w_soft[bb * L + 2 * t + 1] = ws1;
+          }
+          if (a.dW) {
+            a.dW[bb * L + 2 * t] = (rv[5] - ws0 * rv[4]) * r1v * invT;
+            a.dW[bb * L + 2 * t + 1] = (rv[6] - ws1 * rv[4]) * r1v * invT;
+          }
+        }
+      }
+      lam_est = lamt - (double)dlag + mBt;
+      dlag = floorf(rv[0]);
+      cprev = fmaf(g1, ws1, g0 * ws0);
+      xbar = xbe - cprev;
+    }
+
+    // ---------------------------------------------------------------- S2
+    if constexpr (DC) {
+      __syncthreads();
+      const bool first = base == (int64_t)blockIdx.x * BPW;
+      double* part = a.dc_part + slot * ((int64_t)2 << n);
+#pragma unroll 1
+      for (int i = 0; i < SGT; ++i) {
+        const int m = tq + i * TQ;
+        float c0[16], c1[16], acc0[16], acc1[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float cv[2];
+          buf_ld<2>(cbk, voC1, (uint32_t)r * (uint32_t)GS * 8u + (uint32_t)i * tileC, cv);
+          c0[r] = cv[0];
+          c1[r] = cv[1];
+          acc0[r] = 0.f;
+          acc1[r] = 0.f;
+        }
+        const uint32_t voGA = (uint32_t)bw * (uint32_t)N * hstep + (uint32_t)m * 16u;
+        PairRows cw, cg;
+        for (int64_t t = 0; t < N; ++t) {
+          const bool reload = (t & 31) == 0;
+          float w0f, w1f, g0, g1;
+          pair_at(wb, t, L, lane_rows, reload, cw, w0f, w1f);
+          pair_at(gb, t, L, lane_rows, reload, cg, g0, g1);
+          const double w0 = (double)w0f, w1 = (double)w1f;
+          const uint32_t soH = (uint32_t)t * hstep;
+          float hu[4];
+          buf_ld<4>(hist, voH, soH + (uint32_t)i * tileH, hu);
+          const double hl = ((double)hu[0] + (double)hu[1]) - sm_lam[t];
+          const float bq = hu[2] - sm_xb[t] - sm_cp[t];
+#pragma unroll 4
+          for (int r = 0; r < 16; ++r) {
+            float ga[4];
+            buf_ld<4>(hga, voGA, soH + (uint32_t)r * (uint32_t)NSG * 16u, ga);
+            const double d0 = w0 - (double)c0[r], d1 = w1 - (double)c1[r];
+            const float p = ex2((float)(fma(-k2, fma(d0, d0, d1 * d1), (double)ga[0] + (double)ga[1]) + hl));
+            const float X = fmaf(g1, c1[r], fmaf(g0, c0[r], ga[2] + bq));
+            const float pX = p * X * invT;
+            acc0[r] = fmaf(pX, w0f - c0[r], fmaf(p, g0, acc0[r]));
+            acc1[r] = fmaf(pX, w1f - c1[r], fmaf(p, g1, acc1[r]));
+          }
+        }
+        if (valid) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int64_t st = (int64_t)r * GS + m * 16 + tl;
+            part[2 * st] = (first ? 0.0 : part[2 * st]) + (double)acc0[r];
+            part[2 * st + 1] = (first ? 0.0 : part[2 * st + 1]) + (double)acc1[r];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Min-sum decode (paper Sec. 3.2) on the vector-emission trellis, fp64 path
 // metrics: Mn_{t+1}(m * 16 + u) = min_r [d_t(r, m, u) + Mn_t(r * NSG + m)],
 // d_t(s) = (w_t0 - c_0(s))^2 + (w_t1 - c_1(s))^2 (each square rounded, then

@@ -167,9 +167,10 @@ def test_vector_emission_host_checks(lib):
     assert ws(16, 256, 7, 4, 2, P.OP_FWD) == 0           # state_bits >= 8
     assert ws(16, 256, 16, 4, 3, P.OP_FWD) == 0
     assert ws(16, 256, 16, 2, 1, P.OP_FWD) == P.bcjr_workspace_bytes(16, 256, 16, 2, P.OP_FWD)
-    # 32-bit history offsets: N = L / 2 steps, 8 bytes per group with the VJP
-    assert ws(4, 2 * 65535, 16, 4, 2, P.OP_FWD_VJP) > 0
-    assert ws(4, 2 * 65536, 16, 4, 2, P.OP_FWD_VJP) == 0
+    # 32-bit history offsets: N = L / 2 steps, 16 bytes per group with the VJP
+    assert ws(4, 2 * 32767, 16, 4, 2, P.OP_FWD_VJP) > 0
+    assert ws(4, 2 * 32768, 16, 4, 2, P.OP_FWD_VJP) == 0
+    assert ws(4, 2 * 131071, 16, 4, 2, P.OP_FWD) > 0
     f = lib.bcjr_vec_soft_codeword
     assert f(FAKE, 4, 8, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -3
     assert f(FAKE, 4, 7, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -1  # L % V
@@ -178,7 +179,7 @@ def test_vector_emission_host_checks(lib):
     assert f(FAKE, 4, 8, MISALIGNED, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == -1
     assert f(FAKE, 0, 8, FAKE, 8, 4, 2, 1.0, FAKE, None, None, 0, None) == 0
     v = lib.bcjr_vec_soft_codeword_fwd_vjp
-    assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.03, FAKE, FAKE, None, None, None, None, 0, None) == -2
+    assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.03, FAKE, FAKE, None, None, None, None, 0, None) == -3
     assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.5, None, FAKE, None, None, None, None, 0, None) == -1
     assert v(FAKE, 4, 8, FAKE, 8, 4, 2, 0.5, FAKE, FAKE, None, None, None, None, 0, None) == -3
     vd = lib.bcjr_vec_viterbi_decode

@@ -142,7 +142,7 @@ def test_full_batch_sampled():
 
 
 def test_soft_codeword_low_temperature():
-    """The soft codeword alone runs at any T; the V = 2 VJP stops at 0.04."""
+    """The soft codeword alone stays fp32 at every T."""
     w, c, g = case(13, 3, 64, 12)
     T = 0.001
     ws, lz = P.bcjr_vec_soft_codeword(dev(w), dev(c), 12, K_BITS, V, T)
@@ -150,9 +150,29 @@ def test_soft_codeword_low_temperature():
     rws, rlz = O.soft_codeword(w, c, 12, K_BITS, float(np.float32(T)), V=V)
     assert np.abs(host(ws) - rws).max() <= TOL_WS
     assert (np.abs(host(lz) - rlz) / np.abs(rlz)).max() <= TOL_LOGZ
-    with pytest.raises(P.BcjrError) as e:
-        P.bcjr_vec_soft_codeword_vjp(dev(w), dev(c), 12, K_BITS, V, T, dev(g))
-    assert e.value.status == -2
+
+
+@pytest.mark.parametrize("n,B,L", [(8, 5, 24), (10, 9, 40), (12, 3, 64), (14, 2, 24), (15, 2, 20),
+                                   (16, 2, 32)])
+@pytest.mark.parametrize("T", [0.02, 0.003])
+def test_low_temperature_double_float_path(n, B, L, T):
+    """Below T = 0.04 the VJP runs the double-float kernel after a Viterbi
+    decode of the reference codewords."""
+    w, c, g = case(300 + 10 * n + B, B, L, n)
+    full_check(w, c, n, T, g, True, f"lowT n={n} T={T}")
+    full_check(w, c, n, T, g, False, f"lowT n={n} T={T} no-dc")
+
+
+@pytest.mark.parametrize("T", [0.0395, 0.0405])
+def test_precision_switch_boundary(T):
+    w, c, g = case(31, 3, 64, 16)
+    full_check(w, c, 16, T, g, True, f"switch T={T}")
+
+
+@pytest.mark.parametrize("T", [0.01, 1e-3])
+def test_full_trellis_low_temperature(T):
+    w, c, g = case(17, 3, 256, 16)
+    full_check(w, c, 16, T, g, True, f"S=65536 lowT T={T}")
 
 
 def test_entry_points_agree_and_deterministic():
