@@ -137,13 +137,13 @@ int viterbi_decode(const float *w, int64_t B, int64_t L, const float *codebook,
  * rounded squares in component order.
  *
  * V = 1 calls the scalar entry points above with the same arguments.
- * V = 2 supports k = 4 and 8 <= state_bits <= 16 (L/2 steps up to 65535 at
- * state_bits 16); other shapes return BCJR_ERR_UNSUPPORTED.  The V = 2 VJP
- * runs in fp32 and accepts T >= 0.04 (the double-float variant of the
- * scalar trellis is not built for it): below, BCJR_ERR_UNSUPPORTED.  The
- * soft codeword and Viterbi take any T > 0.  Workspace: as reported by
- * bcjr_vec_workspace_bytes for the same op codes.  All other conventions
- * are those of the scalar entry points. */
+ * V = 2 supports k = 4 and 8 <= state_bits <= 16 (at state_bits 16: L/2
+ * steps up to 131071 for the soft codeword and Viterbi, 32767 for the VJP);
+ * other shapes return BCJR_ERR_UNSUPPORTED.  As for the scalar trellis the
+ * VJP switches below T = 0.04 to double-float log vectors, after a Viterbi
+ * decode whose codewords centre the backward tangent.  Workspace: as
+ * reported by bcjr_vec_workspace_bytes for the same op codes.  All other
+ * conventions are those of the scalar entry points. */
 size_t bcjr_vec_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int V, int op);
 
 int bcjr_vec_soft_codeword(const float *w, int64_t B, int64_t L, const float *codebook,
