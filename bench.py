@@ -23,6 +23,9 @@ lines carry no roofline.
 of forward + VJP with dW and dCodebook + Adam, Viterbi snap) on the
 2048 x 8192 gate/up-projection shape; one run of the loop, no roofline.
 
+--path ldlq times BlockLDLQ Viterbi rounding (the Hessian-weighted PTQ
+reference) of the 2048 x 2048 matrix under a proxy Hessian; no roofline.
+
 --path ste times the BCJR-STE training step on the same matrix instead: the
 hard Viterbi forward (viterbi_decode) followed by its backward pass
 (bcjr_ste_vjp, dW only); the roofline then covers the VJP launch.  --T
@@ -178,13 +181,62 @@ def run_anneal(args):
     print(json.dumps(rec), flush=True)
 
 
+def run_ldlq(args):
+    """BlockLDLQ Viterbi rounding of the 2048 x 2048 N(0,1) matrix (S = 65536,
+    k = 2, blocks of 256 columns) under the proxy Hessian of synthetic
+    inputs: 8 column blocks, each one batched Viterbi call over the 2048 rows
+    plus the feedback GEMM.  Reports the time of the whole rounding and the
+    Hessian-weighted loss against the plain per-block Viterbi codeword."""
+    import numpy as np
+    import torch
+    import paper_2605_10655_amd as P
+    from paper_2605_10655_amd import workloads as WL
+    from paper_2605_10655_amd.ldlq import hw_loss, ldlq_viterbi
+    wl = WL.workload(4)
+    dev = torch.device("cuda:0")
+    rows, cols = wl.rows, wl.cols
+    W = torch.from_numpy(WL.weights(4)).to(dev).view(rows, cols)
+    c = torch.from_numpy(WL.codebook(4)).to(dev)
+    X = torch.from_numpy(WL.calibration_inputs(4)).to(dev)
+    H = (X.T @ X) / X.shape[0]
+    del X
+    for _ in range(args.warmup):
+        ldlq_viterbi(W, c, wl.state_bits, wl.k, H, block=wl.L)
+        torch.cuda.synchronize()
+    times = []
+    for _ in range(max(1, args.steps)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        Wh, _ = ldlq_viterbi(W, c, wl.state_bits, wl.k, H, block=wl.L)
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
+    _, plain = P.viterbi_decode(W.reshape(-1, wl.L), c, wl.state_bits, wl.k)
+    torch.cuda.synchronize()
+    sec = float(np.median(times))
+    B = rows * cols // wl.L
+    rec = {
+        "metric": "BlockLDLQ Viterbi rounding: trellis edge-updates/s (Viterbi) at S=65536,k=2,L=256",
+        "value": B * wl.L * wl.S * (1 << wl.k) / sec, "unit": "edge-updates/s", "n_gpus": 1,
+        "steps": len(times), "warmup": args.warmup, "ms_per_step": sec * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64 metrics",
+        "data": "synthetic",
+        "config": {"workload": "2048x2048 N(0,1) weights, S=65536, k=2, blocks of 256 columns; "
+                               "proxy Hessian H = X^T X / 4096 of synthetic inputs, damp 0.01",
+                   "B": B, "L": wl.L, "S": wl.S, "k": wl.k},
+        "roofline": None,
+        "hw_loss_ldlq": hw_loss(W, Wh, H) / W.numel(),
+        "hw_loss_plain_viterbi": hw_loss(W, plain.view(rows, cols), H) / W.numel(),
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec", "anneal"), default="fwd_vjp")
+    ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec", "anneal", "ldlq"), default="fwd_vjp")
     ap.add_argument("--T", type=float, default=None)
     ap.add_argument("--op", choices=("fwd_vjp", "soft", "dc", "viterbi"), default="fwd_vjp",
                     help="call timed on the fwd_vjp and vec paths: the fused w_soft+logZ+dW call "
@@ -219,6 +271,9 @@ def main():
     P.load_library()
     if args.path == "anneal":
         run_anneal(args)
+        return
+    if args.path == "ldlq":
+        run_ldlq(args)
         return
     wl = WL.workload(4)
     n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0] if args.T is None else args.T

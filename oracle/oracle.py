@@ -218,3 +218,49 @@ def gaussian_codebook(n: int, V: int, seed: int):
     pi = state_permutation(n, V, seed)
     c = ndtri((pi.astype(np.float64) + 0.5) / S)
     return c[:, 0] if V == 1 else c
+
+
+# ---------------------------------------------------------------- BlockLDLQ
+def block_ldl(H, block):
+    """H = M D M^T with M unit block-upper-triangular and D block-diagonal
+    (blocks of `block`), from the Cholesky factor of H with its index order
+    reversed (numpy, float64)."""
+    H = np.asarray(H, np.float64)
+    d = H.shape[0]
+    R = np.linalg.cholesky(H[::-1, ::-1])[::-1, ::-1]     # H = R R^T, R upper triangular
+    M = np.zeros_like(R)
+    D = np.zeros_like(R)
+    for k in range(0, d, block):
+        Rkk = R[k:k + block, k:k + block]
+        M[:, k:k + block] = R[:, k:k + block] @ np.linalg.inv(Rkk)
+        D[k:k + block, k:k + block] = Rkk @ Rkk.T
+    return M, D
+
+
+def ldlq_viterbi(W, c, n, k, H, block, V=1, damp=0.01, targets_from=None):
+    """BlockLDLQ rounding with the trellis quantiser (the PTQ reference of the
+    paper's Eq. WPTQ for the Hessian-weighted loss, Eq. LHW): column blocks in
+    order, block j rounded by Viterbi to the target
+    t_j = w_j + sum_{i<j} (w_i - w_hat_i) M_ij.  H is damped by
+    damp * mean(diag H).  Returns (W_hat, states[nb, rows, block // V],
+    targets[nb, rows, block]) in float64.  With targets_from (a [rows, cols]
+    W_hat) the targets are formed from that rounding instead of this one."""
+    W = np.asarray(W, np.float64)
+    rows, cols = W.shape
+    Hd = np.asarray(H, np.float64)
+    Hd = Hd + damp * np.mean(np.diag(Hd)) * np.eye(cols)
+    M, _ = block_ldl(Hd, block)
+    cb = _codebook(c, n, V).reshape(-1, V)
+    nb = cols // block
+    W_hat = np.zeros_like(W)
+    states = np.zeros((nb, rows, block // V), np.int32)
+    targets = np.zeros((nb, rows, block))
+    for j in range(nb):
+        sl = slice(j * block, (j + 1) * block)
+        ref = W_hat if targets_from is None else np.asarray(targets_from, np.float64)
+        t = W[:, sl] + (W[:, :j * block] - ref[:, :j * block]) @ M[:j * block, sl]
+        targets[j] = t
+        st, _ = viterbi(t, cb, n, k, V=V)
+        states[j] = st
+        W_hat[:, sl] = cb[st].reshape(rows, block)
+    return W_hat, states, targets

@@ -495,3 +495,66 @@ def test_gaussian_codebook_is_the_normal_quantiles(n, V):
     assert abs(c.mean()) < 1e-12
     if n >= 10:
         assert abs(c.var() - 1) < 0.01
+
+
+
+# ---------------------------------------------------------------- BlockLDLQ
+def _hessian(d, seed, n_x=None):
+    r = np.random.default_rng(seed)
+    n_x = n_x or 4 * d
+    X = r.standard_normal((n_x, d)) @ (np.eye(d) + 0.7 * r.standard_normal((d, d)) / np.sqrt(d))
+    return X.T @ X / n_x
+
+
+def test_block_ldl_factorisation():
+    H = _hessian(48, 1)
+    M, D = O.block_ldl(H, 16)
+    np.testing.assert_allclose(M @ D @ M.T, H, rtol=0, atol=1e-12 * np.abs(H).max())
+    assert np.abs(np.tril(M, -1)).max() == 0.0
+    for k in range(0, 48, 16):
+        np.testing.assert_allclose(M[k:k + 16, k:k + 16], np.eye(16), rtol=0, atol=1e-12)
+    for k in range(0, 48, 16):
+        D[k:k + 16, k:k + 16] = 0
+    assert np.abs(D).max() == 0.0
+
+
+def test_ldlq_loss_identity():
+    """e H e^T = sum_k (e M)_k D_k (e M)_k^T for any error e: the quantity the
+    block-by-block rounding controls."""
+    H = _hessian(32, 2)
+    M, D = O.block_ldl(H, 8)
+    e = np.random.default_rng(3).standard_normal((5, 32))
+    lhs = np.einsum("ri,ij,rj->r", e, H, e)
+    eM = e @ M
+    rhs = sum(np.einsum("ri,ij,rj->r", eM[:, k:k + 8], D[k:k + 8, k:k + 8], eM[:, k:k + 8])
+              for k in range(0, 32, 8))
+    np.testing.assert_allclose(lhs, rhs, rtol=1e-12)
+
+
+def test_ldlq_reduces_to_plain_viterbi():
+    """H = I (no coupling between blocks) and a single block both give the
+    plain per-block Viterbi codeword."""
+    n, k = 6, 2
+    r = np.random.default_rng(4)
+    c = r.standard_normal(1 << n)
+    W = r.standard_normal((3, 24))
+    plain, _ = O.viterbi(W.reshape(-1, 8), c, n, k)
+    Wh, _, _ = O.ldlq_viterbi(W, c, n, k, np.eye(24), 8, damp=0.0)
+    np.testing.assert_array_equal(Wh.reshape(-1, 8), c[plain])
+    H = _hessian(24, 5)
+    st1, _ = O.viterbi(W, c, n, k)
+    Wh1, _, _ = O.ldlq_viterbi(W, c, n, k, H, 24)
+    np.testing.assert_array_equal(Wh1, c[st1])
+
+
+def test_ldlq_lowers_the_hessian_weighted_loss():
+    n, k, block = 6, 2, 8
+    r = np.random.default_rng(6)
+    c = r.standard_normal(1 << n)
+    W = r.standard_normal((16, 48))
+    H = _hessian(48, 7)
+    Wh, _, _ = O.ldlq_viterbi(W, c, n, k, H, block, damp=0.0)
+    st, _ = O.viterbi(W.reshape(-1, block), c, n, k)
+    plain = c[st].reshape(W.shape)
+    loss = lambda X: np.einsum("ri,ij,rj->", W - X, H, W - X)
+    assert loss(Wh) < 0.9 * loss(plain)
