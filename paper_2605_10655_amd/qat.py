@@ -154,19 +154,18 @@ def anneal_qat(W_init, codebook, cfg: QATConfig, target=None, H=None, stream=Non
             if cfg.learn_codebook:
                 qat_sgd_step(c, dc, cfg.lr_codebook, 0.0, stream=stream)
 
-    def snap(Wm):
+    def snap(Wm, cb):
         Wb = Wm.contiguous().view(-1, blk)
         if V == 1:
-            return viterbi_decode(Wb, c, n, k, stream=stream)[1].view_as(Wm)
-        return bcjr_vec_viterbi_decode(Wb, c, n, k, V, stream=stream)[1].view_as(Wm)
+            return viterbi_decode(Wb, cb, n, k, stream=stream)[1].view_as(Wm)
+        return bcjr_vec_viterbi_decode(Wb, cb, n, k, V, stream=stream)[1].view_as(Wm)
 
-    W_hard = snap(W)
+    W_hard = snap(W, c)
     loss_hard = _loss_and_grad(W_hard, target, H)[0]
-    c_final = c
-    c = codebook.detach().contiguous()  # the PTQ reference uses the initial codebook
-    loss_ptq = _loss_and_grad(snap(W_init.detach()), target, H)[0]
+    # the PTQ reference: the initial weights snapped with the initial codebook
+    loss_ptq = _loss_and_grad(snap(W_init.detach(), codebook.detach().contiguous()), target, H)[0]
     sigma = float(target.float().std())
-    return QATResult(W=W, codebook=c_final, W_hard=W_hard, temps=temps, losses=losses,
+    return QATResult(W=W, codebook=c, W_hard=W_hard, temps=temps, losses=losses,
                      loss_hard=loss_hard, loss_ptq=loss_ptq,
                      max_drift=float((W - W_init).abs().max()),
                      budget=drift_budget(sigma, 1 << n, cfg.lr, cfg.steps, cfg.grad_clip))
