@@ -425,7 +425,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     float offc = 0.f;     // soft codeword alone: shift of the H vector being read
     float wch = 0.f, gch = 0.f;
     int64_t cbase = 0;
-    float q0[K][K];  // codebook rows of the first super-group, fetched a step ahead
+    float q0[K][K];  // codebook rows of the next super-group, fetched one super-group ahead
 #pragma unroll
     for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, q0[j]);
     for (int64_t t = L - 1;; --t) {
@@ -533,20 +533,18 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
+          // this super-group's codebook rows were fetched one super-group
+          // ahead; fetch the next one's (the first of the next step after the last)
           float cc[K][K];
-          if (i == 0) {
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
+          for (int j = 0; j < K; ++j) {
 #pragma unroll
-              for (int u = 0; u < K; ++u) cc[j][u] = q0[j][u];
-            }
-          } else {
-#pragma unroll
-            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
+            for (int u = 0; u < K; ++u) cc[j][u] = q0[j][u];
           }
-          if (i + 1 >= SGT) {
+          {
+            const int inx = i + 1 < SGT ? i + 1 : 0;
 #pragma unroll
-            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, q0[j]);
+            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((inx * TPB) << KB)) * 4, q0[j]);
           }
           float Hin[K], Bin[K];  // row form: one 16-byte LDS read per K floats
           ld_vec<K>(lds + rrow + i * TPB * K, Hin);
@@ -647,7 +645,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // ahead (the last super-group of a step fetches the first of the next
     // step, so that HBM read is in flight across the barriers).
     float pH[K], pB[K];
-    float p0[K][K];  // codebook rows of the first super-group, fetched a step ahead
+    float p0[K][K];  // codebook rows of the next super-group, fetched one super-group ahead
     if constexpr (PF) {
       hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
 #pragma unroll
@@ -709,7 +707,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             hist_row<K, VJP>(hist, voH, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u, hstep,
                              Hc, Bc);
           }
-          if (PF && i == 0) {
+          if constexpr (PF) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
 #pragma unroll
@@ -720,9 +718,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
           }
           if constexpr (PF) {
-            if (i + 1 >= SGT) {
+            {  // the next super-group's codebook rows (the first of the next step after the last)
+              const int inx = i + 1 < SGT ? i + 1 : 0;
 #pragma unroll
-              for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+              for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((inx * TPB) << KB)) * 4, p0[j]);
             }
             // (a select, not a branch: at t = L - 1 it re-reads row t, unused)
             const bool last = i + 1 >= SGT;
