@@ -55,6 +55,18 @@ Family family(int n, int k, bool dc) {
   return f;
 }
 
+// The fp32 forward-backward kernel at 4096 super-groups runs 512 threads of
+// 8 super-groups each (two waves per SIMD, room for the register-resident
+// codebook); the block count per workgroup and the slots are unchanged.
+Family fb_family(int n, int k, bool dc) {
+  Family f = family(n, k, dc);
+  if (f.nt == 1024) {
+    f.nt = 512;
+    f.sgt = f.sgmax = 8;
+  }
+  return f;
+}
+
 // The VJP switches to fp64 log vectors when the field scale log2(e)/(2T)
 // exceeds this value (T < 0.040 for unit-variance data).  The log values of
 // the states that carry the posterior sit ~(field scale) x O(1) below the
@@ -163,6 +175,7 @@ FbFn fb_pick_kb(int n, const Family& f, bool vjp, bool dc) {
       if (n == n512 + 2) return fb_variant<KB, n512 + 2, 8, 256>(vjp, dc);
     }
     if (n == n512 + 3 && f.nt == 1024) return fb_variant<KB, n512 + 3, 4, 1024>(vjp, dc);
+    if (n == n512 + 3 && f.nt == 512) return fb_variant<KB, n512 + 3, 8, 512>(vjp, dc);
   }
   return nullptr;
 }
@@ -354,7 +367,7 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
-  const Family f = family(n, k, dc);
+  const Family f = fb_family(n, k, dc);
   const FbLayout lay = fb_layout(L, n, k, vjp, dc);
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;

@@ -184,6 +184,25 @@ __device__ __forceinline__ void hist_row(rsrc_t h, uint32_t voff, uint32_t step_
 
 __device__ __forceinline__ void pin_u(uint32_t& x) { asm volatile("" : "+v"(x)); }
 
+// Lane index from the hardware lane count, recomputed at each use so that
+// nothing per-lane has to stay live (or be spilled) to recover it.
+__device__ __forceinline__ int lane_id() {
+  uint32_t lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  return (int)lane;
+}
+
+// Load of a value that is the same for the whole wave (uniform pointer and
+// index) through the scalar unit: it lands in an SGPR and its wait does not
+// share the vector-memory counter with the history stores.
+__device__ __forceinline__ float ld_uniform(const float* p, int64_t i) {
+  typedef const __attribute__((address_space(4))) float cfloat;
+  return ((cfloat*)p)[i];
+}
+
+// Thread index rebuilt the same way from the wave index (a scalar).
+__device__ __forceinline__ uint32_t lane_tid(uint32_t wave) { return (wave << 6) + (uint32_t)lane_id(); }
+
 __device__ __forceinline__ float read_lane(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
@@ -209,7 +228,7 @@ constexpr int kRed = 8;  // floats per wave in the cross-wave reduction area
 struct RedCtx {
   int width;     // lanes combined inside a wave: min(TPB, 64)
   int rw;        // waves per block (1 when TPB <= 64)
-  int lane, wave;
+  int wave;      // wave index in the workgroup (uniform)
   float* red;    // [waves][kRed] floats
 };
 
@@ -240,7 +259,7 @@ __device__ __forceinline__ void red_pre(float (&v)[NQ], const RedCtx& r) {
 #pragma unroll
   for (int q = 0; q < NQ; ++q)
     v[q] = ((MAXMASK >> q) & 1u) ? seg_reduce<true>(v[q], r.width) : seg_reduce<false>(v[q], r.width);
-  if (r.rw > 1 && r.lane == 0) {
+  if (r.rw > 1 && lane_id() == 0) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) r.red[r.wave * kRed + q] = v[q];
   }
@@ -251,7 +270,7 @@ __device__ __forceinline__ void red_pre(float (&v)[NQ], const RedCtx& r) {
 template <int NQ, unsigned MAXMASK>
 __device__ __forceinline__ void red_post(float (&v)[NQ], const RedCtx& r) {
   if (r.rw > 1) {
-    const int src = (r.wave / r.rw) * r.rw + (r.lane & (r.rw - 1));
+    const int src = (r.wave / r.rw) * r.rw + (lane_id() & (r.rw - 1));
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const float x = r.red[src * kRed + q];
@@ -273,7 +292,7 @@ __device__ __forceinline__ void lse_pre(float& m, float& s, const RedCtx& r) {
     const float so = __shfl_xor(s, off);
     lse_pair(m, s, mo, so);
   }
-  if (r.rw > 1 && r.lane == 0) {
+  if (r.rw > 1 && lane_id() == 0) {
     r.red[r.wave * kRed + 0] = m;
     r.red[r.wave * kRed + 1] = s;
   }
@@ -304,7 +323,7 @@ __device__ __forceinline__ void lse3_pre(float& m, float& s, float& y, const Red
     const float yo = __shfl_xor(y, off);
     lse3_pair(m, s, y, mo, so, yo);
   }
-  if (r.rw > 1 && r.lane == 0) {
+  if (r.rw > 1 && lane_id() == 0) {
     r.red[r.wave * kRed + 0] = m;
     r.red[r.wave * kRed + 1] = s;
     r.red[r.wave * kRed + 2] = y;
@@ -356,8 +375,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
-  rc.lane = tid & 63;
-  rc.wave = tid >> 6;
+  rc.wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: a scalar
   // cross-wave partials, [2 parities][waves][kRed]: a sweep with one barrier
   // per step alternates them, so a fast wave's next partial never overwrites
   // one a slow wave is still reading
@@ -385,7 +403,20 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   // same value, read 64 steps at a time and taken with a lane read
   const bool lane_rows = TPB >= 64;
   constexpr bool PF = true;  // forward-sweep prefetches
-
+  // 512-thread families keep every codebook row of the thread's super-groups
+  // in registers for the whole call (the super-groups a thread owns never
+  // change): the sweeps then issue no codebook loads, and no wait for one
+  // also waits for the history stores ahead of it.
+  constexpr bool CBR = NT == 512 && NB != 0;
+  const uint32_t wave_s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index (SGPR)
+  float cbr[CBR ? SGMAX : 1][K][K];
+  if constexpr (CBR) {
+#pragma unroll
+    for (int i = 0; i < SGMAX; ++i) {
+#pragma unroll
+      for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cbr[i][j]);
+    }
+  }
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
     const int64_t blk = base + bw;
@@ -394,6 +425,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
     const float* wb = a.w + bb * L;
     const float* gb = VJP ? a.g + bb * L : nullptr;
+    // when a block spans whole waves its row pointers are wave-uniform:
+    // w_t and g_t are then read with scalar loads, one step ahead
+    const int64_t bbu = lane_rows ? (int64_t)__builtin_amdgcn_readfirstlane((int)bb) : 0;
+    const float* wbu = a.w + bbu * L;
+    const float* gbu = VJP ? a.g + bbu * L : a.w;
     // history of each block: soft codeword alone [L][S/K] (H_t); with the VJP
     // [L][S/K/K][2K] (H_t, B_t of each super-group)
     const int64_t slot0 = (int64_t)blockIdx.x * BPW;
@@ -419,26 +455,33 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       if (VJP) lds[vb + GS + i] = 0.f;
     }
     __syncthreads();
-    double shiftB = 0.0;  // sum of the integer shifts of H (exact)
+    int shiftB = 0;  // sum of the integer shifts of H (exact)
     float lam0 = 0.f;
     float xbar = 0.f;     // VJP: E_p[X_0], see S1
     float offc = 0.f;     // soft codeword alone: shift of the H vector being read
     float wch = 0.f, gch = 0.f;
     int64_t cbase = 0;
+    float wnx = lane_rows ? ld_uniform(wbu, L - 1) : 0.f;
+    float gnx = lane_rows && VJP ? ld_uniform(gbu, L - 1) : 0.f;
     float q0[K][K];  // codebook rows of the next super-group, fetched one super-group ahead
+    if constexpr (!CBR) {
 #pragma unroll
-    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, q0[j]);
+      for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, q0[j]);
+    }
     for (int64_t t = L - 1;; --t) {
+      // with the register-resident codebook the per-lane offsets are
+      // re-derived every step from a pinned thread index, not held live
+      uint32_t tid_s = CBR ? lane_tid(wave_s) : (uint32_t)threadIdx.x;
+      const uint32_t col0_s = CBR ? tid_s : col0, row0_s = CBR ? tid_s * K : row0;
+      const uint32_t voH_s = CBR ? tid_s * hrow * 4u : voH;
       rc.red = red0 + ((L - 1 - t) & 1) * (NT / 64) * kRed;
       float wt, gt = 0.f;
       if (lane_rows) {
-        if (t == L - 1 || (t & 63) == 63) {
-          cbase = t & ~(int64_t)63;
-          wch = row_chunk(wb, cbase, L);
-          if (VJP) gch = row_chunk(gb, cbase, L);
-        }
-        wt = read_lane(wch, (int)(t - cbase));
-        if (VJP) gt = read_lane(gch, (int)(t - cbase));
+        wt = wnx;
+        gt = gnx;
+        const int64_t tn = t > 0 ? t - 1 : 0;
+        wnx = ld_uniform(wbu, tn);
+        if (VJP) gnx = ld_uniform(gbu, tn);
       } else {
         wt = wb[t];
         if (VJP) gt = gb[t];
@@ -446,13 +489,13 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       wt *= kap;
       // read side: the vector holding H_t (row form); write side: column form
       const bool odd = !VJP && ((L - 1 - t) & 1);
-      uint32_t rrow = row0 + (odd ? GS : 0), rrowB = row0 + GS;
-      uint32_t wcol = col0 + (odd ? 0 : GS), wcolB = col0 + GS;
+      uint32_t rrow = row0_s + (odd ? GS : 0), rrowB = row0_s + GS;
+      uint32_t wcol = col0_s + (odd ? 0 : GS), wcolB = col0_s + GS;
       pin_u(rrow);
       pin_u(wcol);
       if (VJP) {
         pin_u(rrowB);
-        wcol = col0;
+        wcol = col0_s;
         pin_u(wcol);
         pin_u(wcolB);
       }
@@ -475,15 +518,20 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
             for (int b = 0; b < K; ++b) Hin[b] -= offc;
             if constexpr (VJP) {
-              buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)), Hin);
-              buf_st<K>(hist, voH, ((i * TPB) << (KB + 3)) + 4 * K, Bin);
+              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 3)), Hin);
+              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 3)) + 4 * K, Bin);
             } else {
-              buf_st<K>(hist, voH, ((i * TPB) << (KB + 2)), Hin);
+              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 2)), Hin);
             }
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               float cc[K];
-              buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
+              if constexpr (CBR) {
+#pragma unroll
+                for (int b = 0; b < K; ++b) cc[b] = cbr[CBR ? i : 0][j][b];
+              } else {
+                buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
+              }
               float x[K];
 #pragma unroll
               for (int b = 0; b < K; ++b) {
@@ -524,7 +572,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         }
         lam0 = lm + lg2(ls);
         if (tb == 0 && valid && a.logZ)
-          a.logZ[bb] = (float)((shiftB + (double)lam0) * 0.69314718055994530942);
+          a.logZ[bb] = (float)(((double)shiftB + (double)lam0) * 0.69314718055994530942);
         __syncthreads();
         break;
       }
@@ -539,9 +587,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
           for (int j = 0; j < K; ++j) {
 #pragma unroll
-            for (int u = 0; u < K; ++u) cc[j][u] = q0[j][u];
+            for (int u = 0; u < K; ++u) cc[j][u] = CBR ? cbr[CBR ? i : 0][j][u] : q0[j][u];
           }
-          {
+          if constexpr (!CBR) {
             const int inx = i + 1 < SGT ? i + 1 : 0;
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((inx * TPB) << KB)) * 4, q0[j]);
@@ -557,10 +605,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
           for (int b = 0; b < K; ++b) Hin[b] -= offc;
           if constexpr (VJP) {
-            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)), Hin);
-            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bin);
+            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 3)), Hin);
+            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bin);
           } else {
-            buf_st<K>(hist, voH, soH + ((i * TPB) << (KB + 2)), Hin);
+            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 2)), Hin);
           }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
@@ -599,7 +647,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       __syncthreads();
       red_post<1, 1u>(vmax, rc);
       const float off = floorf(vmax[0]);
-      shiftB += (double)off;
+      // (wave-uniform when a block spans whole waves; per lane otherwise)
+      shiftB += lane_rows ? __builtin_amdgcn_readfirstlane((int)off) : (int)off;
       if (tb == 0) sm_mB[t - 1] = off;
       if constexpr (VJP) {
 #pragma unroll
@@ -646,21 +695,28 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // step, so that HBM read is in flight across the barriers).
     float pH[K], pB[K];
     float p0[K][K];  // codebook rows of the next super-group, fetched one super-group ahead
+    wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
+    gnx = lane_rows && VJP ? ld_uniform(gbu, 0) : 0.f;
     if constexpr (PF) {
       hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
+      if constexpr (!CBR) {
 #pragma unroll
-      for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+        for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
+      }
     }
     for (int64_t t = 0; t < L; ++t) {
+      // with the register-resident codebook the per-lane offsets are
+      // re-derived every step from a pinned thread index, not held live
+      uint32_t tid_s = CBR ? lane_tid(wave_s) : (uint32_t)threadIdx.x;
+      const uint32_t col0_s = CBR ? tid_s : col0, row0_s = CBR ? tid_s * K : row0;
+      const uint32_t voH_s = CBR ? tid_s * hrow * 4u : voH;
       float wt, gt = 0.f;
       if (lane_rows) {
-        if ((t & 63) == 0) {
-          cbase = t;
-          wch = row_chunk(wb, cbase, L);
-          if (VJP) gch = row_chunk(gb, cbase, L);
-        }
-        wt = read_lane(wch, (int)(t - cbase));
-        if (VJP) gt = read_lane(gch, (int)(t - cbase));
+        wt = wnx;
+        gt = gnx;
+        const int64_t tn = t + 1 < L ? t + 1 : t;
+        wnx = ld_uniform(wbu, tn);
+        if (VJP) gnx = ld_uniform(gbu, tn);
       } else {
         wt = wb[t];
         if (VJP) gt = gb[t];
@@ -668,7 +724,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       wt *= kap;
       if (VJP && t > 0) xbar = fmaf(gt, wt, xbar);  // B_t no longer holds step t
       const float mBt = sm_mB[t];
-      uint32_t rcol = col0, rcolA = col0 + GS, wrow = row0, wrowA = row0 + GS;
+      uint32_t rcol = col0_s, rcolA = col0_s + GS, wrow = row0_s, wrowA = row0_s + GS;
       pin_u(rcol);
       pin_u(wrow);
       if (VJP) {
@@ -693,8 +749,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
           if constexpr (DC) {  // (G_t, A_t) row of the super-group for the dCodebook sweep
             const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-            buf_st<K>(hga, voH, so, Gin);
-            buf_st<K>(hga, voH, so + 4 * K, Ain);
+            buf_st<K>(hga, voH_s, so, Gin);
+            buf_st<K>(hga, voH_s, so + 4 * K, Ain);
           }
           float Hc[K], Bc[K], cc[K][K];
           if constexpr (PF) {
@@ -704,21 +760,21 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               Bc[u] = VJP ? pB[u] : 0.f;
             }
           } else {
-            hist_row<K, VJP>(hist, voH, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u, hstep,
+            hist_row<K, VJP>(hist, voH_s, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u, hstep,
                              Hc, Bc);
           }
           if constexpr (PF) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
 #pragma unroll
-              for (int u = 0; u < K; ++u) cc[j][u] = p0[j][u];
+              for (int u = 0; u < K; ++u) cc[j][u] = CBR ? cbr[CBR ? i : 0][j][u] : p0[j][u];
             }
           } else {
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
           }
           if constexpr (PF) {
-            {  // the next super-group's codebook rows (the first of the next step after the last)
+            if constexpr (!CBR) {  // the next super-group's codebook rows (the first of the next step after the last)
               const int inx = i + 1 < SGT ? i + 1 : 0;
 #pragma unroll
               for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((inx * TPB) << KB)) * 4, p0[j]);
@@ -726,7 +782,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             // (a select, not a branch: at t = L - 1 it re-reads row t, unused)
             const bool last = i + 1 >= SGT;
             const int64_t tn = last && t + 1 < L ? t + 1 : t;
-            hist_row<K, VJP>(hist, voH, (uint32_t)tn * hstep * 4u,
+            hist_row<K, VJP>(hist, voH_s, (uint32_t)tn * hstep * 4u,
                              last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, hstep, pH, pB);
           }
 #pragma unroll
@@ -957,7 +1013,7 @@ __device__ __forceinline__ void lse3d_pre(double& m, float& s, float& y, const R
     const float yo = __shfl_xor(y, off);
     lse3_pair_d(m, s, y, mo, so, yo);
   }
-  if (r.rw > 1 && r.lane == 0) {
+  if (r.rw > 1 && lane_id() == 0) {
     redd[r.wave] = m;
     r.red[r.wave * kRed + 0] = s;
     r.red[r.wave * kRed + 1] = y;
@@ -1001,8 +1057,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
-  rc.lane = tid & 63;
-  rc.wave = tid >> 6;
+  rc.wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: a scalar
   // [2 parities][waves][kRed] floats, then [waves] doubles
   float* red0 = lds + (size_t)BPW * 2 * GS;
   double* redd = reinterpret_cast<double*>(red0 + 2 * (NT / 64) * kRed);

@@ -137,8 +137,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
-  rc.lane = tid & 63;
-  rc.wave = tid >> 6;
+  rc.wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: a scalar
   float* const red0 = lds + (size_t)BPW * 4 * q.VSZ;  // [2 parities][waves][kRed]
   rc.red = red0;
   float* const vec0 = lds + (size_t)bw * 4 * q.VSZ;   // two float2 vectors
@@ -557,8 +556,7 @@ __global__ void __launch_bounds__(NT) fbv_kernel_hp(FbvArgs a) {
   RedCtx rc;
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
-  rc.lane = tid & 63;
-  rc.wave = tid >> 6;
+  rc.wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: a scalar
   float* const red0 = lds + (size_t)BPW * 4 * q.VSZ;  // [2 parities][waves][kRed] floats
   double* const redd = reinterpret_cast<double*>(red0 + 2 * (NT / 64) * kRed);  // [waves]
   rc.red = red0;
