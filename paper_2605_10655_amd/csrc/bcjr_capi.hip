@@ -55,9 +55,10 @@ Family family(int n, int k, bool dc) {
   return f;
 }
 
-// The fp32 forward-backward kernel at 4096 super-groups runs 512 threads of
-// 8 super-groups each (two waves per SIMD, room for the register-resident
-// codebook); the block count per workgroup and the slots are unchanged.
+// The forward-backward kernels at 4096 super-groups run 512 threads of 8
+// super-groups each (two waves per SIMD: room for the fp32 kernel's
+// register-resident codebook and the low-temperature kernel's prefetched
+// rows); the block count per workgroup and the slots are unchanged.
 Family fb_family(int n, int k, bool dc) {
   Family f = family(n, k, dc);
   if (f.nt == 1024) {
@@ -190,8 +191,10 @@ FbFn hp_pick_kb(int n, const Family& f, bool dc) {
       return dc ? fb_kernel_hp<KB, n512 + 1, 4, 256, true> : fb_kernel_hp<KB, n512 + 1, 4, 256, false>;
     if (n == n512 + 2)
       return dc ? fb_kernel_hp<KB, n512 + 2, 8, 256, true> : fb_kernel_hp<KB, n512 + 2, 8, 256, false>;
-    if (n == n512 + 3)
+    if (n == n512 + 3 && f.nt == 1024)
       return dc ? fb_kernel_hp<KB, n512 + 3, 4, 1024, true> : fb_kernel_hp<KB, n512 + 3, 4, 1024, false>;
+    if (n == n512 + 3 && f.nt == 512)
+      return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 8, 512, false>;
   }
   return nullptr;
 }
@@ -309,7 +312,7 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
               const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
               float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const bool dc = dCodebook != nullptr;
-  const Family f = family(n, k, false);
+  const Family f = fb_family(n, k, false);
   const HpLayout lay = hp_layout(L, n, k, dc);
   FbFn fn = hp_pick(n, k, f, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;

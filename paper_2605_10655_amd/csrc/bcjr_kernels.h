@@ -1080,6 +1080,12 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     const float* wb = a.w + bb * L;
     const float* gb = a.g + bb * L;
     const float* rb = a.bref + bb * L;
+    // when a block spans whole waves its rows are wave-uniform: w_t, g_t
+    // and the reference are read with scalar loads, one step ahead
+    const int64_t bbu = lane_rows ? (int64_t)__builtin_amdgcn_readfirstlane((int)bb) : 0;
+    const float* wbu = a.w + bbu * L;
+    const float* gbu = a.g + bbu * L;
+    const float* rbu = a.bref + bbu * L;
     const rsrc_t hist = make_rsrc(a.histHB + slot0 * L * hstep, (uint32_t)BPW * (uint32_t)L * hstep * 4u);
     const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * L * hstep : a.histHB,
                                  DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
@@ -1101,22 +1107,27 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     double lam0 = 0.0;
     float xbar = 0.f;
     float dlag = 0.f;   // shift applied to the values written this step
-    float wch = 0.f, gch = 0.f, rch = 0.f;
+    float wch = 0.f, gch = 0.f;
     int64_t cbase = 0;
+    float wnx = lane_rows ? ld_uniform(wbu, L - 1) : 0.f;
+    float gnx = lane_rows ? ld_uniform(gbu, L - 1) : 0.f;
+    float rnx = lane_rows ? ld_uniform(rbu, L - 1) : 0.f;
+    // codebook rows of the next super-group, fetched one super-group ahead
+    float pc[K][K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
     for (int64_t t = L - 1;; --t) {
       const int par = (int)((L - 1 - t) & 1);
       rc.red = red0 + par * (NT / 64) * kRed;
       float wf, gt, rt;
       if (lane_rows) {
-        if (t == L - 1 || (t & 63) == 63) {
-          cbase = t & ~(int64_t)63;
-          wch = row_chunk(wb, cbase, L);
-          gch = row_chunk(gb, cbase, L);
-          rch = row_chunk(rb, cbase, L);
-        }
-        wf = read_lane(wch, (int)(t - cbase));
-        gt = read_lane(gch, (int)(t - cbase));
-        rt = read_lane(rch, (int)(t - cbase));
+        wf = wnx;
+        gt = gnx;
+        rt = rnx;
+        const int64_t tn = t > 0 ? t - 1 : 0;
+        wnx = ld_uniform(wbu, tn);
+        gnx = ld_uniform(gbu, tn);
+        rnx = ld_uniform(rbu, tn);
       } else {
         wf = wb[t];
         gt = gb[t];
@@ -1177,12 +1188,33 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         break;
       }
       float vmax[1] = {-INFINITY};
+      // exchange rows (lo words, tangents) written before the last barrier:
+      // the first super-group's now, each next one a super-group ahead
+      float pHl[K], pB[K];
+      ld_vec<K>(xlo_r + tb * K, pHl);
+      ld_vec<K>(xtg_r + tb * K, pB);
 #pragma unroll 1
       for (int i = 0; i < SGT; ++i) {
-        float Hh[K], Hl[K], Bin[K];
+        float Hh[K], Hl[K], Bin[K], cc[K][K];
+#pragma unroll
+        for (int b = 0; b < K; ++b) {
+          Hl[b] = pHl[b];
+          Bin[b] = pB[b];
+        }
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+#pragma unroll
+          for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
+        }
+        {  // (clamped index, not a branch: the last super-group re-reads its own rows)
+          const int in = i + 1 < SGT ? i + 1 : i;
+          ld_vec<K>(xlo_r + (in * TPB + tb) * K, pHl);
+          ld_vec<K>(xtg_r + (in * TPB + tb) * K, pB);
+          const int ic = i + 1 < SGT ? i + 1 : 0;  // the codebook wraps to the next step
+#pragma unroll
+          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+        }
         ld_vec<K>(lds + rrow + i * TPB * K, Hh);
-        ld_vec<K>(xlo_r + (i * TPB + tb) * K, Hl);
-        ld_vec<K>(xtg_r + (i * TPB + tb) * K, Bin);
         buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
         buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
         buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
@@ -1191,12 +1223,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-          float cc[K];
-          buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc);
           double x[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) {
-            const double d = wt - (double)cc[b];
+            const double d = wt - (double)cc[j][b];
             x[b] = fma(-d * k2, d, H[b]);
           }
           const double m = max_of<K>(x);
@@ -1207,9 +1237,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
           for (int b = 1; b < K; ++b) s += E[b];
           // B_{t-1}: E-weighted mean of g_t (c - r_t) + B_t over the K successors
-          float num = E[0] * fmaf(gt, cc[0] - rt, Bin[0]);
+          float num = E[0] * fmaf(gt, cc[j][0] - rt, Bin[0]);
 #pragma unroll
-          for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[b] - rt, Bin[b]), num);
+          for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[j][b] - rt, Bin[b]), num);
           const double h = m + (double)lg2(s) - (double)dlag;
           float hi, lo;
           split_df(h, hi, lo);
@@ -1241,20 +1271,31 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     double lam_est = lam0;
     float cprev = 0.f;  // g_{t-1} w_soft_{t-1}: the forward tangent's centring, applied on read
     dlag = 0.f;
+    wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
+    gnx = lane_rows ? ld_uniform(gbu, 0) : 0.f;
+    rnx = lane_rows ? ld_uniform(rbu, 0) : 0.f;
+    // the history row and codebook rows of the next super-group (the first
+    // of the next step after the last) are fetched one super-group ahead;
+    // the shift of H_t one step ahead
+    float pHh[K], pHl2[K], pBc[K];
+    buf_ld<K>(hist, voH, 0, pHh);
+    buf_ld<K>(hist, voH, 4 * K, pHl2);
+    buf_ld<K>(hist, voH, 8 * K, pBc);
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
+    float mBnx = sm_mB[0];
     for (int64_t t = 0; t < L; ++t) {
       const int par = (int)(t & 1);
       rc.red = red0 + par * (NT / 64) * kRed;
       float wf, gt, rt;
       if (lane_rows) {
-        if ((t & 63) == 0) {
-          cbase = t;
-          wch = row_chunk(wb, cbase, L);
-          gch = row_chunk(gb, cbase, L);
-          rch = row_chunk(rb, cbase, L);
-        }
-        wf = read_lane(wch, (int)(t - cbase));
-        gt = read_lane(gch, (int)(t - cbase));
-        rt = read_lane(rch, (int)(t - cbase));
+        wf = wnx;
+        gt = gnx;
+        rt = rnx;
+        const int64_t tn = t + 1 < L ? t + 1 : t;
+        wnx = ld_uniform(wbu, tn);
+        gnx = ld_uniform(gbu, tn);
+        rnx = ld_uniform(rbu, tn);
       } else {
         wf = wb[t];
         gt = gb[t];
@@ -1262,7 +1303,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       }
       if (t > 0) xbar = fmaf(gt, rt, xbar);  // B_t no longer holds step t
       const double wt = (double)wf;
-      const double mBt = (double)sm_mB[t];
+      const double mBt = (double)mBnx;
+      mBnx = sm_mB[t + 1 < L ? t + 1 : t];
       uint32_t rcol = col0 + (par ? GS : 0), wrow = row0 + (par ? 0 : GS);
       pin_u(rcol);
       pin_u(wrow);
@@ -1273,15 +1315,47 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       const uint32_t soH = (uint32_t)t * hstep * 4u;
       // max G_{t+1}, sum p, sum p c, sum p X, sum p c X
       float rv[5] = {-INFINITY, 0.f, 0.f, 0.f, 0.f};
+      // exchange entries (lo words, tangents) of the first super-group now,
+      // each next one a super-group ahead
+      float pGl[K], pAr[K];
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        pGl[j] = xlo_r[j * NSG + tb];
+        pAr[j] = xtg_r[j * NSG + tb];
+      }
 #pragma unroll 1
       for (int i = 0; i < SGT; ++i) {
         float Gh[K], Gl[K], Ar[K];
+        float Hh[K], Hl[K], Bc[K], cc[K][K];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-          Gh[j] = lds[rcol + j * NSG + i * TPB];
-          Gl[j] = xlo_r[j * NSG + i * TPB + tb];
-          Ar[j] = xtg_r[j * NSG + i * TPB + tb] - cprev;
+          Gl[j] = pGl[j];
+          Ar[j] = pAr[j] - cprev;
+          Hh[j] = pHh[j];
+          Hl[j] = pHl2[j];
+          Bc[j] = pBc[j];
+#pragma unroll
+          for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
         }
+        {  // (clamped indices, not branches)
+          const bool last = i + 1 >= SGT;
+          const int in = last ? i : i + 1;
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            pGl[j] = xlo_r[j * NSG + in * TPB + tb];
+            pAr[j] = xtg_r[j * NSG + in * TPB + tb];
+          }
+          const int64_t tn = last && t + 1 < L ? t + 1 : t;
+          const uint32_t so = (uint32_t)tn * hstep * 4u + (last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u);
+          buf_ld<K>(hist, voH, so, pHh);
+          buf_ld<K>(hist, voH, so + 4 * K, pHl2);
+          buf_ld<K>(hist, voH, so + 8 * K, pBc);
+          const int ic = last ? 0 : i + 1;
+#pragma unroll
+          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < K; ++j) Gh[j] = lds[rcol + j * NSG + i * TPB];
         if constexpr (DC) {
           const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
           buf_st<K>(hga, voH, so, Gh);
@@ -1291,13 +1365,6 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         double G[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
-        float Hh[K], Hl[K], Bc[K];
-        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
-        buf_ld<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bc);
-        float cc[K][K];
-#pragma unroll
-        for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cc[j]);
         float go_hi[K], go_lo[K], ao[K];
 #pragma unroll
         for (int u = 0; u < K; ++u) {
