@@ -105,7 +105,7 @@ HpLayout hp_layout(int64_t L, int n, int k, bool dc) {
   HpLayout l;
   l.hist = align_up((size_t)L * 3 * gs * sizeof(float));
   l.histGA = dc ? align_up((size_t)L * 3 * gs * sizeof(float)) : 0;
-  l.xA = align_up(4 * gs * sizeof(float));
+  l.xA = align_up(gs * sizeof(float));
   l.small = align_up((size_t)4 * L * sizeof(float));
   l.dc = dc ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
   l.slot = l.hist + l.histGA + l.xA + l.small + l.dc;

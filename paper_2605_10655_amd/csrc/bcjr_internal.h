@@ -29,7 +29,7 @@ struct FbArgs {
   // then hold rows of 3K floats (hi, lo, tangent) and small [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
   const float* bref;   // [B, L] centring reference of the backward tangent
-  float* xA;           // [slots][4][S/K] exchange: lo words [2], tangents [2]
+  float* xA;           // [slots][S/K] tangent exchange, updated in place
 };
 
 // Vector-emission trellis: k = 4 bits per step (K = 16), V = 2 weights per

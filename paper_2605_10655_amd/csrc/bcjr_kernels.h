@@ -1089,9 +1089,12 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     const rsrc_t hist = make_rsrc(a.histHB + slot0 * L * hstep, (uint32_t)BPW * (uint32_t)L * hstep * 4u);
     const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * L * hstep : a.histHB,
                                  DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
-    // exchange buffer of the slot: [2][S/K] lo words, then [2][S/K] tangents
-    float* xlo = a.xA + slot * 4 * GS;
-    float* xtg = xlo + 2 * GS;
+    // tangent exchange of the slot, [S/K], updated in place (L2-resident),
+    // addressed through a buffer descriptor: row form at tb*K, column form
+    // at tb, the super-group and j parts in the scalar / immediate offset
+    float* xtg = a.xA + slot * GS;
+    const rsrc_t xrs = make_rsrc(xtg, (uint32_t)GS * 4u);
+    const uint32_t vxr = (uint32_t)tb * K * 4u, vxc = (uint32_t)tb * 4u;
     float* sm_mB = a.small + slot * 4 * L;   // shift applied to H_t (integer)
     float* sm_xb = sm_mB + L;                // dCodebook: E_p[X_t]
     double* sm_lam = reinterpret_cast<double*>(sm_xb + L);  // dCodebook: lambda_t (fp64)
@@ -1099,7 +1102,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     // ------------------------------------------------------------------ S0
     for (int i = tb; i < GS; i += TPB) {
       lds[vb + i] = 0.f;
-      xlo[i] = 0.f;
+      lds[vb + GS + i] = 0.f;
       xtg[i] = 0.f;
     }
     __syncthreads();
@@ -1134,13 +1137,13 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         rt = rb[t];
       }
       const double wt = (double)wf;
-      uint32_t rrow = row0 + (par ? GS : 0), wcol = col0 + (par ? 0 : GS);
+      // (H hi, H lo) in LDS and the tangent B in the slot's global vector,
+      // all updated in place: reads, barrier, writes, barrier
+      uint32_t rrow = row0, rrowL = row0 + GS, wcol = col0, wcolL = col0 + GS;
       pin_u(rrow);
+      pin_u(rrowL);
       pin_u(wcol);
-      const float* xlo_r = xlo + (par ? GS : 0);
-      const float* xtg_r = xtg + (par ? GS : 0);
-      float* xlo_w = xlo + (par ? 0 : GS);
-      float* xtg_w = xtg + (par ? 0 : GS);
+      pin_u(wcolL);
       const uint32_t soH = (uint32_t)t * hstep * 4u;
       if (t == 0) {
         // lambda_0 = LSE_s [h_0(s) + H_0] and E_p[g_0 c + B_0]
@@ -1150,8 +1153,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         for (int i = 0; i < SGT; ++i) {
           float Hh[K], Hl[K], Bin[K];
           ld_vec<K>(lds + rrow + i * TPB * K, Hh);
-          ld_vec<K>(xlo_r + (i * TPB + tb) * K, Hl);
-          ld_vec<K>(xtg_r + (i * TPB + tb) * K, Bin);
+          ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
+          buf_ld<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, Bin);
           buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
           buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
           buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
@@ -1188,83 +1191,96 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         break;
       }
       float vmax[1] = {-INFINITY};
-      // exchange rows (lo words, tangents) written before the last barrier:
-      // the first super-group's now, each next one a super-group ahead
-      float pHl[K], pB[K];
-      ld_vec<K>(xlo_r + tb * K, pHl);
-      ld_vec<K>(xtg_r + tb * K, pB);
-#pragma unroll 1
-      for (int i = 0; i < SGT; ++i) {
-        float Hh[K], Hl[K], Bin[K], cc[K][K];
+      float oh[SGMAX][K], ol[SGMAX][K], ot[SGMAX][K];  // outputs, held across the first barrier
+      // the tangent row of the first super-group now, each next one a
+      // super-group ahead
+      float pB[K];
+      buf_ld<K>(xrs, vxr, 0, pB);
 #pragma unroll
-        for (int b = 0; b < K; ++b) {
-          Hl[b] = pHl[b];
-          Bin[b] = pB[b];
-        }
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          float Hh[K], Hl[K], Bin[K], cc[K][K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) {
+          for (int b = 0; b < K; ++b) Bin[b] = pB[b];
 #pragma unroll
-          for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
-        }
-        {  // (clamped index, not a branch: the last super-group re-reads its own rows)
-          const int in = i + 1 < SGT ? i + 1 : i;
-          ld_vec<K>(xlo_r + (in * TPB + tb) * K, pHl);
-          ld_vec<K>(xtg_r + (in * TPB + tb) * K, pB);
-          const int ic = i + 1 < SGT ? i + 1 : 0;  // the codebook wraps to the next step
+          for (int j = 0; j < K; ++j) {
 #pragma unroll
-          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
-        }
-        ld_vec<K>(lds + rrow + i * TPB * K, Hh);
-        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
-        buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
-        double H[K];
-#pragma unroll
-        for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
-#pragma unroll
-        for (int j = 0; j < K; ++j) {
-          double x[K];
-#pragma unroll
-          for (int b = 0; b < K; ++b) {
-            const double d = wt - (double)cc[j][b];
-            x[b] = fma(-d * k2, d, H[b]);
+            for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
           }
-          const double m = max_of<K>(x);
-          float E[K];
+          {  // (clamped index, not a branch: the last super-group re-reads its own row)
+            const int in = i + 1 < SGT ? i + 1 : i;
+            buf_ld<K>(xrs, vxr, (uint32_t)in * TPB * K * 4u, pB);
+            const int ic = i + 1 < SGT ? i + 1 : 0;  // the codebook wraps to the next step
 #pragma unroll
-          for (int b = 0; b < K; ++b) E[b] = ex2((float)(x[b] - m));
-          float s = E[0];
+            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+          }
+          ld_vec<K>(lds + rrow + i * TPB * K, Hh);
+          ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
+          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
+          double H[K];
 #pragma unroll
-          for (int b = 1; b < K; ++b) s += E[b];
-          // B_{t-1}: E-weighted mean of g_t (c - r_t) + B_t over the K successors
-          float num = E[0] * fmaf(gt, cc[j][0] - rt, Bin[0]);
+          for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
 #pragma unroll
-          for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[j][b] - rt, Bin[b]), num);
-          const double h = m + (double)lg2(s) - (double)dlag;
-          float hi, lo;
-          split_df(h, hi, lo);
-          vmax[0] = fmaxf(vmax[0], hi);
-          lds[wcol + j * NSG + i * TPB] = hi;
-          xlo_w[j * NSG + i * TPB + tb] = lo;
-          xtg_w[j * NSG + i * TPB + tb] = num * rcp(s);
+          for (int j = 0; j < K; ++j) {
+            double x[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const double d = wt - (double)cc[j][b];
+              x[b] = fma(-d * k2, d, H[b]);
+            }
+            const double m = max_of<K>(x);
+            float E[K];
+#pragma unroll
+            for (int b = 0; b < K; ++b) E[b] = ex2((float)(x[b] - m));
+            float s = E[0];
+#pragma unroll
+            for (int b = 1; b < K; ++b) s += E[b];
+            // B_{t-1}: E-weighted mean of g_t (c - r_t) + B_t over the K successors
+            float num = E[0] * fmaf(gt, cc[j][0] - rt, Bin[0]);
+#pragma unroll
+            for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[j][b] - rt, Bin[b]), num);
+            const double hv = m + (double)lg2(s) - (double)dlag;
+            split_df(hv, oh[i][j], ol[i][j]);
+            vmax[0] = fmaxf(vmax[0], oh[i][j]);
+            ot[i][j] = num * rcp(s);
+            pin(oh[i][j]);
+            pin(ol[i][j]);
+            pin(ot[i][j]);
+          }
+          sg_fence();
         }
-        sg_fence();
       }
       shiftB += (double)dlag;
       if (tb == 0) sm_mB[t - 1] = dlag;
       red_pre<1, 1u>(vmax, rc);
       __syncthreads();
-      {
-        float vm[1] = {vmax[0]};
-        red_post<1, 1u>(vm, rc);
-        dlag = floorf(vm[0]);
+      red_post<1, 1u>(vmax, rc);
+      dlag = floorf(vmax[0]);
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            lds[wcol + j * NSG + i * TPB] = oh[i][j];
+            lds[wcolL + j * NSG + i * TPB] = ol[i][j];
+            {
+              const float v1[1] = {ot[i][j]};
+              buf_st<1>(xrs, vxc, (uint32_t)(j * NSG + i * TPB) * 4u, v1);
+            }
+          }
+        }
       }
+      __syncthreads();
     }
 
     // ------------------------------------------------------------------ S1
+    // (G hi, G lo) in LDS and the tangent A in the slot's global vector,
+    // updated in place like S0
     for (int i = tb; i < GS; i += TPB) {
       lds[vb + i] = 0.f;
-      xlo[i] = 0.f;
+      lds[vb + GS + i] = 0.f;
       xtg[i] = 0.f;
     }
     __syncthreads();
@@ -1305,108 +1321,112 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       const double wt = (double)wf;
       const double mBt = (double)mBnx;
       mBnx = sm_mB[t + 1 < L ? t + 1 : t];
-      uint32_t rcol = col0 + (par ? GS : 0), wrow = row0 + (par ? 0 : GS);
+      uint32_t rcol = col0, rcolL = col0 + GS, wrow = row0, wrowL = row0 + GS;
       pin_u(rcol);
+      pin_u(rcolL);
       pin_u(wrow);
-      const float* xlo_r = xlo + (par ? GS : 0);
-      const float* xtg_r = xtg + (par ? GS : 0);
-      float* xlo_w = xlo + (par ? 0 : GS);
-      float* xtg_w = xtg + (par ? 0 : GS);
+      pin_u(wrowL);
       const uint32_t soH = (uint32_t)t * hstep * 4u;
       // max G_{t+1}, sum p, sum p c, sum p X, sum p c X
       float rv[5] = {-INFINITY, 0.f, 0.f, 0.f, 0.f};
-      // exchange entries (lo words, tangents) of the first super-group now,
-      // each next one a super-group ahead
-      float pGl[K], pAr[K];
+      float oh[SGMAX][K], ol[SGMAX][K], oa[SGMAX][K];  // outputs, held across the first barrier
+      // tangent entries of the first super-group now, each next one a
+      // super-group ahead
+      float pAr[K];
 #pragma unroll
       for (int j = 0; j < K; ++j) {
-        pGl[j] = xlo_r[j * NSG + tb];
-        pAr[j] = xtg_r[j * NSG + tb];
+        float v1[1];
+        buf_ld<1>(xrs, vxc, (uint32_t)j * NSG * 4u, v1);
+        pAr[j] = v1[0];
       }
-#pragma unroll 1
-      for (int i = 0; i < SGT; ++i) {
-        float Gh[K], Gl[K], Ar[K];
-        float Hh[K], Hl[K], Bc[K], cc[K][K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) {
-          Gl[j] = pGl[j];
-          Ar[j] = pAr[j] - cprev;
-          Hh[j] = pHh[j];
-          Hl[j] = pHl2[j];
-          Bc[j] = pBc[j];
-#pragma unroll
-          for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
-        }
-        {  // (clamped indices, not branches)
-          const bool last = i + 1 >= SGT;
-          const int in = last ? i : i + 1;
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          float Gh[K], Gl[K], Ar[K];
+          float Hh[K], Hl[K], Bc[K], cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            pGl[j] = xlo_r[j * NSG + in * TPB + tb];
-            pAr[j] = xtg_r[j * NSG + in * TPB + tb];
+            Ar[j] = pAr[j] - cprev;
+            Hh[j] = pHh[j];
+            Hl[j] = pHl2[j];
+            Bc[j] = pBc[j];
+#pragma unroll
+            for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
           }
-          const int64_t tn = last && t + 1 < L ? t + 1 : t;
-          const uint32_t so = (uint32_t)tn * hstep * 4u + (last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u);
-          buf_ld<K>(hist, voH, so, pHh);
-          buf_ld<K>(hist, voH, so + 4 * K, pHl2);
-          buf_ld<K>(hist, voH, so + 8 * K, pBc);
-          const int ic = last ? 0 : i + 1;
+          {  // (clamped indices, not branches)
+            const bool last = i + 1 >= SGT;
+            const int in = last ? i : i + 1;
 #pragma unroll
-          for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
-        }
+            for (int j = 0; j < K; ++j) {
+              float v1[1];
+              buf_ld<1>(xrs, vxc, (uint32_t)(j * NSG + in * TPB) * 4u, v1);
+              pAr[j] = v1[0];
+            }
+            const int64_t tn = last && t + 1 < L ? t + 1 : t;
+            const uint32_t so = (uint32_t)tn * hstep * 4u + (last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u);
+            buf_ld<K>(hist, voH, so, pHh);
+            buf_ld<K>(hist, voH, so + 4 * K, pHl2);
+            buf_ld<K>(hist, voH, so + 8 * K, pBc);
+            const int ic = last ? 0 : i + 1;
 #pragma unroll
-        for (int j = 0; j < K; ++j) Gh[j] = lds[rcol + j * NSG + i * TPB];
-        if constexpr (DC) {
-          const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
-          buf_st<K>(hga, voH, so, Gh);
-          buf_st<K>(hga, voH, so + 4 * K, Gl);
-          buf_st<K>(hga, voH, so + 8 * K, Ar);
-        }
-        double G[K];
-#pragma unroll
-        for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
-        float go_hi[K], go_lo[K], ao[K];
-#pragma unroll
-        for (int u = 0; u < K; ++u) {
-          double al[K];
+            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+          }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            const double d = wt - (double)cc[j][u];
-            al[j] = fma(-d * k2, d, G[j]);
+            Gh[j] = lds[rcol + j * NSG + i * TPB];
+            Gl[j] = lds[rcolL + j * NSG + i * TPB];
           }
-          const double m = max_of<K>(al);
-          float E[K];
-#pragma unroll
-          for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
-          // X is centred per state before the sums: at low T the moments of
-          // an uncentred X cancel only to its rounding, amplified by 1/T
-          const float bx = Bc[u] - xbar;
-          float s = E[0], ec = E[0] * cc[0][u], sc = ec;
-          float x = fmaf(gt, cc[0][u], Ar[0]) + bx;
-          float sx = E[0] * x, scx = ec * x;
-#pragma unroll
-          for (int j = 1; j < K; ++j) {
-            s += E[j];
-            ec = E[j] * cc[j][u];
-            sc += ec;
-            x = fmaf(gt, cc[j][u], Ar[j]) + bx;
-            sx = fmaf(E[j], x, sx);
-            scx = fmaf(ec, x, scx);
+          if constexpr (DC) {
+            const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
+            buf_st<K>(hga, voH, so, Gh);
+            buf_st<K>(hga, voH, so + 4 * K, Gl);
+            buf_st<K>(hga, voH, so + 8 * K, Ar);
           }
-          const double gout = m + (double)lg2(s) - (double)dlag;
-          split_df(gout, go_hi[u], go_lo[u]);
-          rv[0] = fmaxf(rv[0], go_hi[u]);
-          const float fac = ex2((float)(m + ((double)Hh[u] + (double)Hl[u]) - lam_est));
-          rv[1] = fmaf(fac, s, rv[1]);
-          rv[2] = fmaf(fac, sc, rv[2]);
-          rv[3] = fmaf(fac, sx, rv[3]);
-          rv[4] = fmaf(fac, scx, rv[4]);
-          ao[u] = fmaf(sx, rcp(s), -bx);  // E-weighted mean of g c + A
+          double G[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
+#pragma unroll
+          for (int u = 0; u < K; ++u) {
+            double al[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              const double d = wt - (double)cc[j][u];
+              al[j] = fma(-d * k2, d, G[j]);
+            }
+            const double m = max_of<K>(al);
+            float E[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) E[j] = ex2((float)(al[j] - m));
+            // X is centred per state before the sums: at low T the moments of
+            // an uncentred X cancel only to its rounding, amplified by 1/T
+            const float bx = Bc[u] - xbar;
+            float s = E[0], ec = E[0] * cc[0][u], sc = ec;
+            float x = fmaf(gt, cc[0][u], Ar[0]) + bx;
+            float sx = E[0] * x, scx = ec * x;
+#pragma unroll
+            for (int j = 1; j < K; ++j) {
+              s += E[j];
+              ec = E[j] * cc[j][u];
+              sc += ec;
+              x = fmaf(gt, cc[j][u], Ar[j]) + bx;
+              sx = fmaf(E[j], x, sx);
+              scx = fmaf(ec, x, scx);
+            }
+            const double gout = m + (double)lg2(s) - (double)dlag;
+            split_df(gout, oh[i][u], ol[i][u]);
+            rv[0] = fmaxf(rv[0], oh[i][u]);
+            const float fac = ex2((float)(m + ((double)Hh[u] + (double)Hl[u]) - lam_est));
+            rv[1] = fmaf(fac, s, rv[1]);
+            rv[2] = fmaf(fac, sc, rv[2]);
+            rv[3] = fmaf(fac, sx, rv[3]);
+            rv[4] = fmaf(fac, scx, rv[4]);
+            oa[i][u] = fmaf(sx, rcp(s), -bx);  // E-weighted mean of g c + A
+            pin(oh[i][u]);
+            pin(ol[i][u]);
+            pin(oa[i][u]);
+          }
+          sg_fence();
         }
-        st_vec<K>(lds + wrow + i * TPB * K, go_hi);
-        st_vec<K>(xlo_w + (i * TPB + tb) * K, go_lo);
-        st_vec<K>(xtg_w + (i * TPB + tb) * K, ao);
-        sg_fence();
       }
       red_pre<5, 1u>(rv, rc);
       __syncthreads();
@@ -1429,6 +1449,15 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       dlag = floorf(rv[0]);
       cprev = gt * wst;
       xbar = xbe - cprev;
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          st_vec<K>(lds + wrow + i * TPB * K, oh[i]);
+          st_vec<K>(lds + wrowL + i * TPB * K, ol[i]);
+          buf_st<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, oa[i]);
+        }
+      }
+      __syncthreads();
     }
 
     // ------------------------------------------------------------------ S2
