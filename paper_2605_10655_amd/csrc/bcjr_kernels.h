@@ -1554,7 +1554,32 @@ __global__ void fill_kernel(float* out, int64_t count, float v) {
 // Min-sum decode (paper Sec. 3.2), fp64 path metrics.  Same super-group
 // layout as the forward sweep: Mn_{t+1}(v) = min_j [d_t(j*S/K + v) + Mn_t(j, v >> k)]
 // with d_t(s) = (w_t - c(s))^2; the winning j is kept per (t, v).
+// The metric vector lives in LDS as two 32-bit planes (low and high words
+// of each double): the row-form writes are then 16-byte stores at a 16-byte
+// lane stride and the column-form reads lane-contiguous 4-byte reads, both
+// free of bank conflicts (8-byte rows at a 32-byte lane stride conflicted
+// 4-way).  The K winning digits of a super-group row go out as one store.
+// w_t comes through the scalar unit when a block spans whole waves.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ double join_d(float lo, float hi) {
+  return __hiloint2double(__float_as_int(hi), __float_as_int(lo));
+}
+
+template <int K>
+__device__ __forceinline__ void st_digits(uint8_t* p, const uint8_t (&arg)[K]) {
+  if constexpr (K == 2) {
+    *reinterpret_cast<uint16_t*>(p) = (uint16_t)(arg[0] | (arg[1] << 8));
+  } else if constexpr (K == 4) {
+    *reinterpret_cast<uint32_t*>(p) =
+        (uint32_t)arg[0] | ((uint32_t)arg[1] << 8) | ((uint32_t)arg[2] << 16) | ((uint32_t)arg[3] << 24);
+  } else {
+#pragma unroll
+    for (int q = 0; q < K / 4; ++q)
+      reinterpret_cast<uint32_t*>(p)[q] = (uint32_t)arg[4 * q] | ((uint32_t)arg[4 * q + 1] << 8) |
+                                          ((uint32_t)arg[4 * q + 2] << 16) | ((uint32_t)arg[4 * q + 3] << 24);
+  }
+}
+
 template <int KB, int NB, int SGMAX, int NT>
 __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
   constexpr int K = 1 << KB;
@@ -1573,9 +1598,11 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
   const int width = TPB < 64 ? TPB : 64;
   const int rw = TPB > 64 ? TPB / 64 : 1;
   const int64_t L = a.L;
-  double* mv = ldsd + (size_t)bw * GS;
+  float* const mlo = reinterpret_cast<float*>(ldsd) + (size_t)bw * 2 * GS;  // low words
+  float* const mhi = mlo + GS;                                               // high words
   double* redv = ldsd + (size_t)BPW * GS;            // [waves]
   int* redi = reinterpret_cast<int*>(redv + NT / 64); // [waves]
+  const bool lane_rows = TPB >= 64;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
     const int64_t blk = base + bw;
@@ -1583,14 +1610,27 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
     const int64_t bb = valid ? blk : a.B - 1;
     const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
     const float* wb = a.w + bb * L;
+    const int64_t bbu = lane_rows ? (int64_t)__builtin_amdgcn_readfirstlane((int)bb) : 0;
+    const float* wbu = a.w + bbu * L;
     uint8_t* bp = a.bp + slot * L * GS;
 
-    for (int i = tb; i < GS; i += TPB) mv[i] = 0.0;
+    for (int i = tb; i < GS; i += TPB) {
+      mlo[i] = 0.f;
+      mhi[i] = 0.f;
+    }
     __syncthreads();
     double bestv = INFINITY;
     int besti = 0x7fffffff;
+    float wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
     for (int64_t t = 0; t < L; ++t) {
-      const double wt = (double)wb[t];
+      float wf;
+      if (lane_rows) {
+        wf = wnx;
+        wnx = ld_uniform(wbu, t + 1 < L ? t + 1 : t);
+      } else {
+        wf = wb[t];
+      }
+      const double wt = (double)wf;
       double Mout[SGMAX][K];
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
@@ -1598,7 +1638,7 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
           const int sg = tb + i * TPB;
           double Min[K];
 #pragma unroll
-          for (int j = 0; j < K; ++j) Min[j] = mv[j * NSG + sg];
+          for (int j = 0; j < K; ++j) Min[j] = join_d(mlo[j * NSG + sg], mhi[j * NSG + sg]);
           float cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
@@ -1621,8 +1661,7 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
               arg[u] = (uint8_t)bj;
             }
             // bp[t+1][sg*K + u] = winning j of G-entry (sg, u)
-#pragma unroll
-            for (int u = 0; u < K; ++u) bp[(t + 1) * GS + sg * K + u] = arg[u];
+            st_digits<K>(bp + (t + 1) * GS + sg * K, arg);
           } else {
 #pragma unroll
             for (int j = 0; j < K; ++j)
@@ -1646,8 +1685,14 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
             const int sg = tb + i * TPB;
+            float lo[K], hi[K];
 #pragma unroll
-            for (int u = 0; u < K; ++u) mv[sg * K + u] = Mout[i][u];
+            for (int u = 0; u < K; ++u) {
+              lo[u] = __int_as_float(__double2loint(Mout[i][u]));
+              hi[u] = __int_as_float(__double2hiint(Mout[i][u]));
+            }
+            st_vec<K>(mlo + sg * K, lo);
+            st_vec<K>(mhi + sg * K, hi);
           }
         }
         __syncthreads();
