@@ -1603,6 +1603,9 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
   double* redv = ldsd + (size_t)BPW * GS;            // [waves]
   int* redi = reinterpret_cast<int*>(redv + NT / 64); // [waves]
   const bool lane_rows = TPB >= 64;
+  // codebook rows through a buffer descriptor, one super-group ahead
+  const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
+  const uint32_t voK = (uint32_t)tb << (KB + 2);
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
     const int64_t blk = base + bw;
@@ -1622,6 +1625,9 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
     double bestv = INFINITY;
     int besti = 0x7fffffff;
     float wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
+    float pc[K][K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
     for (int64_t t = 0; t < L; ++t) {
       float wf;
       if (lane_rows) {
@@ -1641,7 +1647,15 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
           for (int j = 0; j < K; ++j) Min[j] = join_d(mlo[j * NSG + sg], mhi[j * NSG + sg]);
           float cc[K][K];
 #pragma unroll
-          for (int j = 0; j < K; ++j) ld_vec<K>(a.c + (j << (n - KB)) + ((i * TPB) << KB) + toK, cc[j]);
+          for (int j = 0; j < K; ++j) {
+#pragma unroll
+            for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
+          }
+          {  // the next super-group's rows (the first of the next step after the last)
+            const int ic = i + 1 < SGT ? i + 1 : 0;
+#pragma unroll
+            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+          }
           if (t < L - 1) {
             uint8_t arg[K];
 #pragma unroll
