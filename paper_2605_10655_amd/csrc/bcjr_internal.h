@@ -24,9 +24,13 @@ struct FbArgs {
   float* histH;        // [slots][L][S/K]   H_t as read by each super-group (soft codeword)
   float* histHB;       // [slots][L][2 S/K] H_t and the B tangent per super-group (VJP)
   float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group (dCodebook)
+  // (per step and super-group an H (G) plane then a B (A) plane, each
+  // [threads][K] floats: one store of a wave fills whole cache lines)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
   // low-temperature variant (double-float log vectors); histHB and histGA
-  // then hold rows of 3K floats (hi, lo, tangent) and small [slots][4][L]
+  // then hold, per step and super-group, three planes (hi, lo, tangent) of
+  // [threads][K] floats, so that one store of a wave fills whole cache
+  // lines; small is [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
   const float* bref;   // [B, L] centring reference of the backward tangent
   float* xA;           // [slots][S/K] tangent exchange, updated in place

@@ -129,20 +129,26 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
 __device__ __forceinline__ float as_f(unsigned u) { return __uint_as_float(u); }
 __device__ __forceinline__ unsigned as_u(float f) { return __float_as_uint(f); }
 
-template <int N>
+// Cache policy of a buffer access: 0 = default, kStream = non-temporal (the
+// line is inserted in L2 as the first to evict).  Write-once/read-once
+// history rows go through kStream so that they do not push out of L2 the
+// small vectors a block rewrites every step.
+constexpr int kStream = 2;
+
+template <int N, int CP = 0>
 __device__ __forceinline__ void buf_ld(rsrc_t r, uint32_t voff, uint32_t soff, float (&v)[N]) {
   static_assert(N == 1 || N == 2 || N % 4 == 0, "vector width");
   if constexpr (N == 1) {
-    v[0] = as_f(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+    v[0] = as_f(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, CP));
   } else if constexpr (N == 2) {
-    const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+    const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, CP);
     const unsigned x0 = x.x, x1 = x.y;
     v[0] = as_f(x0);
     v[1] = as_f(x1);
   } else {
 #pragma unroll
     for (int q = 0; q < N / 4; ++q) {
-      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)(soff + 16u * q), 0);
+      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)(soff + 16u * q), CP);
       const unsigned x0 = x.x, x1 = x.y, x2 = x.z, x3 = x.w;
       v[4 * q + 0] = as_f(x0);
       v[4 * q + 1] = as_f(x1);
@@ -156,30 +162,31 @@ __device__ __forceinline__ void buf_ld(rsrc_t r, uint32_t voff, uint32_t soff, f
 // register scalar offset the compiler assumes no wait state is needed between
 // a wider-than-8-byte store and a VALU write of its data registers; on this
 // GPU such a write corrupted the stored data.
-template <int N>
+template <int N, int CP = 0>
 __device__ __forceinline__ void buf_st(rsrc_t r, uint32_t voff0, uint32_t soff0, const float (&v)[N]) {
   static_assert(N == 1 || N == 2 || N % 4 == 0, "vector width");
   const uint32_t voff = voff0 + soff0, soff = 0;
   if constexpr (N == 1) {
-    __builtin_amdgcn_raw_buffer_store_b32(as_u(v[0]), r, (int)voff, (int)soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(as_u(v[0]), r, (int)voff, (int)soff, CP);
   } else if constexpr (N == 2) {
     const u32x2 x = {as_u(v[0]), as_u(v[1])};
-    __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)voff, (int)soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)voff, (int)soff, CP);
   } else {
 #pragma unroll
     for (int q = 0; q < N / 4; ++q) {
       const u32x4 x = {as_u(v[4 * q + 0]), as_u(v[4 * q + 1]), as_u(v[4 * q + 2]), as_u(v[4 * q + 3])};
-      __builtin_amdgcn_raw_buffer_store_b128(x, r, (int)voff, (int)(soff + 16u * q), 0);
+      __builtin_amdgcn_raw_buffer_store_b128(x, r, (int)voff, (int)(soff + 16u * q), CP);
     }
   }
 }
 
-// History row of one super-group: H (and B after it with the VJP).
+// History rows of one super-group: the H plane ([threads][K]) and, with the
+// VJP, the B plane `plane` bytes after it; both streamed (read once).
 template <int K, bool VJP>
 __device__ __forceinline__ void hist_row(rsrc_t h, uint32_t voff, uint32_t step_off, uint32_t sg_off,
-                                         uint32_t, float (&H)[K], float (&B)[K]) {
-  buf_ld<K>(h, voff, step_off + sg_off, H);
-  if constexpr (VJP) buf_ld<K>(h, voff, step_off + sg_off + 4 * K, B);
+                                         uint32_t plane, float (&H)[K], float (&B)[K]) {
+  buf_ld<K, kStream>(h, voff, step_off + sg_off, H);
+  if constexpr (VJP) buf_ld<K, kStream>(h, voff, step_off + sg_off + plane, B);
 }
 
 __device__ __forceinline__ void pin_u(uint32_t& x) { asm volatile("" : "+v"(x)); }
@@ -396,9 +403,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const uint32_t voK = (uint32_t)tb << (KB + 2);
   // Histories: one descriptor per workgroup over its BPW slots; the block's
   // slot and the thread's super-group row go into the per-thread offset.
-  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per super-group row
+  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per thread and super-group (H, B planes)
   const uint32_t hstep = (uint32_t)GS * (VJP ? 2 : 1);   // floats per step
-  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * hrow) * 4u;
+  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
   // w and g of the step: when a block spans whole waves every lane needs the
   // same value, read 64 steps at a time and taken with a lane read
   const bool lane_rows = TPB >= 64;
@@ -473,7 +480,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       // re-derived every step from a pinned thread index, not held live
       uint32_t tid_s = CBR ? lane_tid(wave_s) : (uint32_t)threadIdx.x;
       const uint32_t col0_s = CBR ? tid_s : col0, row0_s = CBR ? tid_s * K : row0;
-      const uint32_t voH_s = CBR ? tid_s * hrow * 4u : voH;
+      const uint32_t voH_s = CBR ? tid_s * K * 4u : voH;
       rc.red = red0 + ((L - 1 - t) & 1) * (NT / 64) * kRed;
       float wt, gt = 0.f;
       if (lane_rows) {
@@ -518,10 +525,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
             for (int b = 0; b < K; ++b) Hin[b] -= offc;
             if constexpr (VJP) {
-              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 3)), Hin);
-              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 3)) + 4 * K, Bin);
+              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 3)), Hin);
+              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 3)) + (uint32_t)TPB * K * 4u, Bin);
             } else {
-              buf_st<K>(hist, voH_s, ((i * TPB) << (KB + 2)), Hin);
+              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 2)), Hin);
             }
 #pragma unroll
             for (int j = 0; j < K; ++j) {
@@ -605,10 +612,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
           for (int b = 0; b < K; ++b) Hin[b] -= offc;
           if constexpr (VJP) {
-            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 3)), Hin);
-            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 3)) + 4 * K, Bin);
+            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 3)), Hin);
+            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 3)) + (uint32_t)TPB * K * 4u, Bin);
           } else {
-            buf_st<K>(hist, voH_s, soH + ((i * TPB) << (KB + 2)), Hin);
+            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 2)), Hin);
           }
 #pragma unroll
           for (int j = 0; j < K; ++j) {
@@ -698,7 +705,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
     gnx = lane_rows && VJP ? ld_uniform(gbu, 0) : 0.f;
     if constexpr (PF) {
-      hist_row<K, VJP>(hist, voH, 0, 0, hstep, pH, pB);
+      hist_row<K, VJP>(hist, voH, 0, 0, (uint32_t)TPB * K * 4u, pH, pB);
       if constexpr (!CBR) {
 #pragma unroll
         for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
@@ -709,7 +716,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       // re-derived every step from a pinned thread index, not held live
       uint32_t tid_s = CBR ? lane_tid(wave_s) : (uint32_t)threadIdx.x;
       const uint32_t col0_s = CBR ? tid_s : col0, row0_s = CBR ? tid_s * K : row0;
-      const uint32_t voH_s = CBR ? tid_s * hrow * 4u : voH;
+      const uint32_t voH_s = CBR ? tid_s * K * 4u : voH;
       float wt, gt = 0.f;
       if (lane_rows) {
         wt = wnx;
@@ -749,8 +756,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
           if constexpr (DC) {  // (G_t, A_t) row of the super-group for the dCodebook sweep
             const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-            buf_st<K>(hga, voH_s, so, Gin);
-            buf_st<K>(hga, voH_s, so + 4 * K, Ain);
+            buf_st<K, kStream>(hga, voH_s, so, Gin);
+            buf_st<K, kStream>(hga, voH_s, so + (uint32_t)TPB * K * 4u, Ain);
           }
           float Hc[K], Bc[K], cc[K][K];
           if constexpr (PF) {
@@ -760,8 +767,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               Bc[u] = VJP ? pB[u] : 0.f;
             }
           } else {
-            hist_row<K, VJP>(hist, voH_s, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u, hstep,
-                             Hc, Bc);
+            hist_row<K, VJP>(hist, voH_s, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u,
+                             (uint32_t)TPB * K * 4u, Hc, Bc);
           }
           if constexpr (PF) {
 #pragma unroll
@@ -783,7 +790,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             const bool last = i + 1 >= SGT;
             const int64_t tn = last && t + 1 < L ? t + 1 : t;
             hist_row<K, VJP>(hist, voH_s, (uint32_t)tn * hstep * 4u,
-                             last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, hstep, pH, pB);
+                             last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, (uint32_t)TPB * K * 4u,
+                             pH, pB);
           }
 #pragma unroll
           for (int u = 0; u < K; ++u) {
@@ -897,10 +905,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         float nH[K], nB[K], nG[K], nA[K];
         {
           const uint32_t so = (uint32_t)i * TPB * hrow * 4u;
-          buf_ld<K>(hist, voH, so, nH);
-          buf_ld<K>(hist, voH, so + 4 * K, nB);
-          buf_ld<K>(hga, voH, so, nG);
-          buf_ld<K>(hga, voH, so + 4 * K, nA);
+          buf_ld<K, kStream>(hist, voH, so, nH);
+          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, nB);
+          buf_ld<K, kStream>(hga, voH, so, nG);
+          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
         }
 #pragma unroll 1
         for (int64_t t = 0; t < L; ++t) {
@@ -936,10 +944,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           {  // (a select, not a branch: the last step re-reads its own rows)
             const int64_t tn = t + 1 < L ? t + 1 : t;
             const uint32_t so = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-            buf_ld<K>(hist, voH, so, nH);
-            buf_ld<K>(hist, voH, so + 4 * K, nB);
-            buf_ld<K>(hga, voH, so, nG);
-            buf_ld<K>(hga, voH, so + 4 * K, nA);
+            buf_ld<K, kStream>(hist, voH, so, nH);
+            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, nB);
+            buf_ld<K, kStream>(hga, voH, so, nG);
+            buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
           }
 #pragma unroll
           for (int u = 0; u < K; ++u) {
@@ -984,7 +992,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 //   as centring before the write).  The backward tangent is centred on a
 //   reference path given per block (the minimum-distortion codewords),
 //   which the posterior follows at low temperature.
-//   S0 backward: H and B, history rows (H hi, H lo, B);
+//   S0 backward: H and B, history rows (H hi, H lo, B) as three planes of
+//                [threads][K] per super-group, written and read non-temporal;
 //   S1 forward:  G and A, marginals, w_soft, dW; with dCodebook also the
 //                rows (G hi, G lo, A) and the exact lambda_t, E_p[X_t];
 //   S2 dCodebook as in fb_kernel, with p from the fp64 sums.
@@ -1066,9 +1075,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
   const uint32_t voK = (uint32_t)tb << (KB + 2);
-  const uint32_t hrow = 3 * K;                    // floats per history row: hi, lo, tangent
+  const uint32_t hrow = 3 * K;                    // floats per thread and super-group: hi, lo, tangent planes
   const uint32_t hstep = (uint32_t)GS * 3;        // floats per history step
-  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * hrow) * 4u;
+  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
   const bool lane_rows = TPB >= 64;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
@@ -1155,9 +1164,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           ld_vec<K>(lds + rrow + i * TPB * K, Hh);
           ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
           buf_ld<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, Bin);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 4u, Hl);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 8u, Bin);
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             float cc[K];
@@ -1216,9 +1225,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           }
           ld_vec<K>(lds + rrow + i * TPB * K, Hh);
           ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 4 * K, Hl);
-          buf_st<K>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + 8 * K, Bin);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 4u, Hl);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 8u, Bin);
           double H[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
@@ -1294,9 +1303,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     // of the next step after the last) are fetched one super-group ahead;
     // the shift of H_t one step ahead
     float pHh[K], pHl2[K], pBc[K];
-    buf_ld<K>(hist, voH, 0, pHh);
-    buf_ld<K>(hist, voH, 4 * K, pHl2);
-    buf_ld<K>(hist, voH, 8 * K, pBc);
+    buf_ld<K, kStream>(hist, voH, 0, pHh);
+    buf_ld<K, kStream>(hist, voH, (uint32_t)TPB * K * 4u, pHl2);
+    buf_ld<K, kStream>(hist, voH, (uint32_t)TPB * K * 8u, pBc);
 #pragma unroll
     for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
     float mBnx = sm_mB[0];
@@ -1364,9 +1373,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             }
             const int64_t tn = last && t + 1 < L ? t + 1 : t;
             const uint32_t so = (uint32_t)tn * hstep * 4u + (last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u);
-            buf_ld<K>(hist, voH, so, pHh);
-            buf_ld<K>(hist, voH, so + 4 * K, pHl2);
-            buf_ld<K>(hist, voH, so + 8 * K, pBc);
+            buf_ld<K, kStream>(hist, voH, so, pHh);
+            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, pHl2);
+            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 8u, pBc);
             const int ic = last ? 0 : i + 1;
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
@@ -1378,9 +1387,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           }
           if constexpr (DC) {
             const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
-            buf_st<K>(hga, voH, so, Gh);
-            buf_st<K>(hga, voH, so + 4 * K, Gl);
-            buf_st<K>(hga, voH, so + 8 * K, Ar);
+            buf_st<K, kStream>(hga, voH, so, Gh);
+            buf_st<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, Gl);
+            buf_st<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 8u, Ar);
           }
           double G[K];
 #pragma unroll
@@ -1498,12 +1507,12 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           const double wt = (double)wf;
           const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
           float Hh[K], Hl[K], Bv[K], Gh[K], Gl[K], A[K];
-          buf_ld<K>(hist, voH, so, Hh);
-          buf_ld<K>(hist, voH, so + 4 * K, Hl);
-          buf_ld<K>(hist, voH, so + 8 * K, Bv);
-          buf_ld<K>(hga, voH, so, Gh);
-          buf_ld<K>(hga, voH, so + 4 * K, Gl);
-          buf_ld<K>(hga, voH, so + 8 * K, A);
+          buf_ld<K, kStream>(hist, voH, so, Hh);
+          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, Hl);
+          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 8u, Bv);
+          buf_ld<K, kStream>(hga, voH, so, Gh);
+          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, Gl);
+          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 8u, A);
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             const double hb = ((double)Hh[u] + (double)Hl[u]) - lt;
