@@ -982,16 +982,17 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 // and the VJP loses its 1e-4 relative accuracy.  Here G and H are carried as
 // double-float pairs (hi + lo, two fp32 words, ~48 bits) with fp64 LSE
 // arithmetic; softmax weights and tangents stay fp32.
-//   Exchange between threads: the hi words ping-pong in LDS (2 x S/K fp32,
-//   the footprint of fb_kernel), the lo words and the tangent ping-pong in
-//   a per-slot global buffer (L2-resident), so every step needs a single
-//   barrier and no output is held across it.  For that the integer shift of
-//   a step is the floor of the previous step's maximum (the stored maxima
-//   stay within the per-step drift of 0), and the forward tangent is
-//   centred on w_soft when it is read, one step later (the same arithmetic
-//   as centring before the write).  The backward tangent is centred on a
-//   reference path given per block (the minimum-distortion codewords),
-//   which the posterior follows at low temperature.
+//   Exchange between threads: the hi and lo words fill the two S/K fp32
+//   vectors in LDS (the footprint of fb_kernel) and are updated in place:
+//   reads, barrier, writes, barrier, with the outputs held in registers
+//   across the first barrier; the fp32 tangent is updated in place in a
+//   per-slot global vector (L2-resident).  The integer shift of a step is
+//   the floor of the previous step's maximum (the stored maxima stay within
+//   the per-step drift of 0), and the forward tangent is centred on w_soft
+//   when it is read, one step later (the same arithmetic as centring before
+//   the write).  The backward tangent is centred on a reference path given
+//   per block (the minimum-distortion codewords), which the posterior
+//   follows at low temperature.
 //   S0 backward: H and B, history rows (H hi, H lo, B) as three planes of
 //                [threads][K] per super-group, written and read non-temporal;
 //   S1 forward:  G and A, marginals, w_soft, dW; with dCodebook also the
@@ -1100,8 +1101,14 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
                                  DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
     // tangent exchange of the slot, [S/K], updated in place (L2-resident),
     // addressed through a buffer descriptor: row form at tb*K, column form
-    // at tb, the super-group and j parts in the scalar / immediate offset
-    float* xtg = a.xA + slot * GS;
+    // at tb, the super-group and j parts in the scalar / immediate offset.
+    // Workgroups go to the 8 XCDs round-robin; the vectors of one XCD's
+    // slots are placed next to each other, so that they spread over all of
+    // its L2 sets (at a stride of 8 slots they shared an eighth of them).
+    const int64_t nbk = gridDim.x;
+    const int64_t xslot = (nbk & 7) ? slot
+        : (((int64_t)blockIdx.x & 7) * (nbk >> 3) + ((int64_t)blockIdx.x >> 3)) * BPW + bw;
+    float* xtg = a.xA + xslot * GS;
     const rsrc_t xrs = make_rsrc(xtg, (uint32_t)GS * 4u);
     const uint32_t vxr = (uint32_t)tb * K * 4u, vxc = (uint32_t)tb * 4u;
     float* sm_mB = a.small + slot * 4 * L;   // shift applied to H_t (integer)
