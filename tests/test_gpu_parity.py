@@ -256,6 +256,32 @@ def test_small_workspace_runs_persistent_loop(n):
         np.testing.assert_array_equal(a, b)
 
 
+def test_low_temperature_every_grid_size():
+    """The double-float kernel under every workspace size from one slot up:
+    grids of 1 to 24 workgroups, with and without the persistent loop, and
+    both placements of the per-slot tangent vectors (XCD-contiguous when the
+    grid is a multiple of 8, by slot otherwise) must give the same bits, and
+    the full-size run must match the oracle."""
+    n, k, B, L, T = 12, 2, 24, 20, 0.003
+    w, c, g = WL.random_case(4242, B, L, n)
+    full = full_check(w, c, n, k, T, g, True, "lowT grids")
+    big = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
+    runs = 0
+    for nb in range(1, B + 1):
+        size = big * nb // B
+        try:
+            out = gpu_fwd_vjp(w, c, n, k, T, g, True,
+                              workspace=torch.empty(size, dtype=torch.uint8, device="cuda:0"))
+        except P.BcjrError as e:
+            assert e.status == -3
+            continue
+        runs += 1
+        for a, b in zip(full, out):
+            np.testing.assert_array_equal(a, b)
+    _say(f"[parity] lowT grids: {runs} workspace sizes ran")
+    assert runs >= B // 2
+
+
 def test_deterministic():
     wl = WL.workload(3)
     c = WL.codebook(3)
