@@ -182,6 +182,12 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
     float dl = 0.f;        // shift for the values written this step
     float lam0 = 0.f, xbar = 0.f;
     PairRows rw_, rg_;
+    // each tile's history entry is stored once the next tile's codebook
+    // loads are issued: the vector-memory counter retires loads and stores in
+    // order, so waiting for those loads would otherwise wait for the store
+    float pend[2] = {0.f, 0.f};
+    uint32_t pend_so = 0;
+    bool pend_on = false;
     for (int64_t t = N - 1;; --t) {
       const int par = (int)((N - 1 - t) & 1);
       rc.red = red0 + par * (NT / 64) * kRed;
@@ -195,6 +201,14 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
       w1 *= kap;
       const uint32_t soH = (uint32_t)t * hstep;
       if (t == 0) {
+        if (pend_on) {
+          if constexpr (VJP) {
+            buf_st<2>(hist, voH, pend_so, pend);
+          } else {
+            float o1[1] = {pend[0]};
+            buf_st<1>(hist, voH, pend_so, o1);
+          }
+        }
         // lambda_0 = LSE_s [h_0(s) + H_0(s & (GS - 1))] (log2 alpha_0 = h_0), and
         // with the VJP E_p[<g_0, c(s_0)> + B_0(s_0)], the mean of X_0
         float lm = -INFINITY, ls = 0.f, ly = 0.f;
@@ -273,14 +287,17 @@ __global__ void __launch_bounds__(NT) fbv_kernel(FbvArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) hb[4 * u4 + e] = t4[e];
           }
-          float own[2];
-          ld_vec<2>(cur + 2 * (q.row(m) + tl), own);
-          if constexpr (VJP) {
-            buf_st<2>(hist, voH, soH + (uint32_t)i * tileH, own);
-          } else {
-            float o1[1] = {own[0]};
-            buf_st<1>(hist, voH, soH + (uint32_t)i * tileH, o1);
+          if (pend_on) {
+            if constexpr (VJP) {
+              buf_st<2>(hist, voH, pend_so, pend);
+            } else {
+              float o1[1] = {pend[0]};
+              buf_st<1>(hist, voH, pend_so, o1);
+            }
           }
+          ld_vec<2>(cur + 2 * (q.row(m) + tl), pend);
+          pend_so = soH + (uint32_t)i * tileH;
+          pend_on = true;
           // in place: hb[2u] <- log2 of the row's successor terms, hb[2u+1] <- the
           // summand of B_{t-1}, <g_t, c - w_t> + B_t (E-weighted mean below)
           float x[16];
