@@ -168,14 +168,13 @@ template <int KB>
 FbFn fb_pick_kb(int n, const Family& f, bool vjp, bool dc) {
   if (f.sgmax == 1) return fb_variant<KB, 0, 1, 256>(vjp, dc);
   if constexpr (KB < 3) {
-    // nsg = 2^(n - 2KB): 512, 1024, 2048 -> 256 threads; 4096 -> 1024
+    // nsg = 2^(n - 2KB): 512, 1024, 2048 -> 256 threads; 4096 -> 512 (fb_family)
     constexpr int n512 = 2 * KB + 9;
     if (f.nt == 256) {
       if (n == n512) return fb_variant<KB, n512, 2, 256>(vjp, dc);
       if (n == n512 + 1) return fb_variant<KB, n512 + 1, 4, 256>(vjp, dc);
       if (n == n512 + 2) return fb_variant<KB, n512 + 2, 8, 256>(vjp, dc);
     }
-    if (n == n512 + 3 && f.nt == 1024) return fb_variant<KB, n512 + 3, 4, 1024>(vjp, dc);
     if (n == n512 + 3 && f.nt == 512) return fb_variant<KB, n512 + 3, 8, 512>(vjp, dc);
   }
   return nullptr;
@@ -191,8 +190,6 @@ FbFn hp_pick_kb(int n, const Family& f, bool dc) {
       return dc ? fb_kernel_hp<KB, n512 + 1, 4, 256, true> : fb_kernel_hp<KB, n512 + 1, 4, 256, false>;
     if (n == n512 + 2)
       return dc ? fb_kernel_hp<KB, n512 + 2, 8, 256, true> : fb_kernel_hp<KB, n512 + 2, 8, 256, false>;
-    if (n == n512 + 3 && f.nt == 1024)
-      return dc ? fb_kernel_hp<KB, n512 + 3, 4, 1024, true> : fb_kernel_hp<KB, n512 + 3, 4, 1024, false>;
     if (n == n512 + 3 && f.nt == 512)
       return dc ? fb_kernel_hp<KB, n512 + 3, 8, 512, true> : fb_kernel_hp<KB, n512 + 3, 8, 512, false>;
   }
