@@ -49,7 +49,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-# Roofline of the fused kernel ("Roofline").
+# ALU roofline of the fused kernel: edge-updates/s at full issue of the
+# algorithmic VALU and transcendental work of a K x K group-step.
 CUS, CLOCK_HZ = 256, 2.4e9
 VALU_LANES_PER_CLK = 64          # per CU: 4 SIMDs x 16 fp32 lanes (packed fp32 math disabled)
 TRANS_LANES_PER_CLK = 32         # per CU: v_exp/v_log/v_rcp at half rate (measured)
@@ -324,7 +325,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(blocks are independent: N GPUs would each run B/N blocks, see DESIGN.md)",
+              "(blocks are independent: N GPUs would each run B/N blocks)",
               file=sys.stderr)
         sys.exit(2)
 
