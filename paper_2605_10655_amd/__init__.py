@@ -125,7 +125,10 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _check_in(name, t, shape=None, dtype=None):
+def _check_in(name, t, shape=None, dtype=None, device=None):
+    """Every tensor handed to the library, input or caller-supplied output:
+    a contiguous device tensor of the expected dtype, shape and device (the
+    kernels index it as a dense array of exactly that size)."""
     torch = _torch()
     dtype = dtype or torch.float32
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
@@ -136,11 +139,33 @@ def _check_in(name, t, shape=None, dtype=None):
         raise ValueError(f"{name} must be contiguous")
     if shape is not None and tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the call's tensors on {device}")
+
+
+def _check_out(name, t, shape, device, dtype=None):
+    if t is not None:
+        _check_in(name, t, shape, dtype, device)
+
+
+def _ws_bytes(ws):
+    return ws.numel() * ws.element_size()
+
+
+def _check_ws(ws, device):
+    torch = _torch()
+    if not isinstance(ws, torch.Tensor) or not ws.is_cuda:
+        raise TypeError("workspace must be a CUDA (HIP) tensor")
+    if not ws.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    if ws.device != device:
+        raise ValueError(f"workspace is on {ws.device}, the call's tensors on {device}")
 
 
 def _workspace(workspace, B, L, state_bits, k, op, device):
     torch = _torch()
     if workspace is not None:
+        _check_ws(workspace, device)
         return workspace
     nbytes = bcjr_workspace_bytes(B, L, state_bits, k, op)
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
@@ -165,14 +190,17 @@ def bcjr_soft_codeword(w, codebook, state_bits, k, T, *, w_soft=None, logZ=None,
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _check_in("codebook", codebook, (1 << state_bits,))
+    dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_out("w_soft", w_soft, (B, L), dev)
+    _check_out("logZ", logZ, (B,), dev)
     if w_soft is None:
         w_soft = torch.empty_like(w)
     if logZ is None and want_logZ:
-        logZ = torch.empty(B, dtype=torch.float32, device=w.device)
-    ws = _workspace(workspace, B, L, state_bits, k, OP_FWD, w.device)
+        logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_FWD, dev)
     rc = lib.bcjr_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
-                                _ptr(w_soft), _ptr(logZ), _ptr(ws), ws.numel(), _stream(stream))
+                                _ptr(w_soft), _ptr(logZ), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword", rc)
     return w_soft, logZ
 
@@ -185,16 +213,19 @@ def bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, want_d
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _check_in("codebook", codebook, (1 << state_bits,))
-    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_in("grad_w_soft", grad_w_soft, (B, L), device=dev)
+    _check_out("dW", dW, (B, L), dev)
+    _check_out("dCodebook", dCodebook, (1 << state_bits,), dev)
     if dW is None and want_dW:
         dW = torch.empty_like(w)
     if dCodebook is None and want_dCodebook:
-        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=w.device)
-    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, w.device)
+        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=dev)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, dev)
     rc = lib.bcjr_soft_codeword_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
                                     _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws),
-                                    ws.numel(), _stream(stream))
+                                    _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword_vjp", rc)
     return dW, dCodebook
 
@@ -207,9 +238,12 @@ def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, wa
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _check_in("codebook", codebook, (1 << state_bits,))
-    _check_in("grad_w_soft", grad_w_soft, (B, L))
     dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_in("grad_w_soft", grad_w_soft, (B, L), device=dev)
+    for name, t, shp in (("w_soft", w_soft, (B, L)), ("logZ", logZ, (B,)), ("dW", dW, (B, L)),
+                         ("dCodebook", dCodebook, (1 << state_bits,))):
+        _check_out(name, t, shp, dev)
     if w_soft is None and want_w_soft:
         w_soft = torch.empty_like(w)
     if logZ is None and want_logZ:
@@ -221,7 +255,7 @@ def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, wa
     ws = _workspace(workspace, B, L, state_bits, k, OP_FWD_VJP, dev)
     rc = lib.bcjr_soft_codeword_fwd_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
                                         _ptr(grad_w_soft), _ptr(w_soft), _ptr(logZ), _ptr(dW),
-                                        _ptr(dCodebook), _ptr(ws), ws.numel(), _stream(stream))
+                                        _ptr(dCodebook), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword_fwd_vjp", rc)
     return w_soft, logZ, dW, dCodebook
 
@@ -235,16 +269,19 @@ def bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, grad_w_soft, *, want_dW=
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _check_in("codebook", codebook, (1 << state_bits,))
-    _check_in("w_hard", w_hard, (B, L))
-    _check_in("grad_w_soft", grad_w_soft, (B, L))
+    dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_in("w_hard", w_hard, (B, L), device=dev)
+    _check_in("grad_w_soft", grad_w_soft, (B, L), device=dev)
+    _check_out("dW", dW, (B, L), dev)
+    _check_out("dCodebook", dCodebook, (1 << state_bits,), dev)
     if dW is None and want_dW:
         dW = torch.empty_like(w)
     if dCodebook is None and want_dCodebook:
-        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=w.device)
-    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, w.device)
+        dCodebook = torch.empty(1 << state_bits, dtype=torch.float32, device=dev)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VJP, dev)
     rc = lib.bcjr_ste_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T), _ptr(w_hard),
-                          _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws), ws.numel(),
+                          _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws), _ws_bytes(ws),
                           _stream(stream))
     _raise("bcjr_ste_vjp", rc)
     return dW, dCodebook
@@ -257,14 +294,17 @@ def viterbi_decode(w, codebook, state_bits, k, *, want_w_hard=True, states=None,
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _check_in("codebook", codebook, (1 << state_bits,))
+    dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_out("states", states, (B, L), dev, torch.int32)
+    _check_out("w_hard", w_hard, (B, L), dev)
     if states is None:
-        states = torch.empty((B, L), dtype=torch.int32, device=w.device)
+        states = torch.empty((B, L), dtype=torch.int32, device=dev)
     if w_hard is None and want_w_hard:
         w_hard = torch.empty_like(w)
-    ws = _workspace(workspace, B, L, state_bits, k, OP_VITERBI, w.device)
+    ws = _workspace(workspace, B, L, state_bits, k, OP_VITERBI, dev)
     rc = lib.viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, _ptr(states),
-                            _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
+                            _ptr(w_hard), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("viterbi_decode", rc)
     return states, w_hard
 
@@ -274,16 +314,17 @@ def bcjr_vec_workspace_bytes(B: int, L: int, state_bits: int, k: int, V: int, op
     return int(load_library().bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op))
 
 
-def _vec_codebook(codebook, state_bits, V):
+def _vec_codebook(codebook, state_bits, V, device, name="codebook"):
     S = 1 << state_bits
+    _check_in(name, codebook, device=device)
     if codebook.numel() != S * V:
-        raise ValueError(f"codebook must hold {S} x {V} values, got {tuple(codebook.shape)}")
-    _check_in("codebook", codebook)
+        raise ValueError(f"{name} must hold {S} x {V} values, got {tuple(codebook.shape)}")
 
 
 def _vec_workspace(workspace, B, L, state_bits, k, V, op, device):
     torch = _torch()
     if workspace is not None:
+        _check_ws(workspace, device)
         return workspace
     nbytes = bcjr_vec_workspace_bytes(B, L, state_bits, k, V, op)
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
@@ -296,14 +337,17 @@ def bcjr_vec_soft_codeword(w, codebook, state_bits, k, V, T, *, w_soft=None, log
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _vec_codebook(codebook, state_bits, V)
+    dev = w.device
+    _vec_codebook(codebook, state_bits, V, dev)
+    _check_out("w_soft", w_soft, (B, L), dev)
+    _check_out("logZ", logZ, (B,), dev)
     if w_soft is None:
         w_soft = torch.empty_like(w)
     if logZ is None and want_logZ:
-        logZ = torch.empty(B, dtype=torch.float32, device=w.device)
-    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_FWD, w.device)
+        logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_FWD, dev)
     rc = lib.bcjr_vec_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, float(T),
-                                    _ptr(w_soft), _ptr(logZ), _ptr(ws), ws.numel(), _stream(stream))
+                                    _ptr(w_soft), _ptr(logZ), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_vec_soft_codeword", rc)
     return w_soft, logZ
 
@@ -318,9 +362,13 @@ def bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, grad_w_soft
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _vec_codebook(codebook, state_bits, V)
-    _check_in("grad_w_soft", grad_w_soft, (B, L))
     dev = w.device
+    _vec_codebook(codebook, state_bits, V, dev)
+    _check_in("grad_w_soft", grad_w_soft, (B, L), device=dev)
+    for name, t, shp in (("w_soft", w_soft, (B, L)), ("logZ", logZ, (B,)), ("dW", dW, (B, L))):
+        _check_out(name, t, shp, dev)
+    if dCodebook is not None:
+        _vec_codebook(dCodebook, state_bits, V, dev, "dCodebook")
     if w_soft is None and want_w_soft:
         w_soft = torch.empty_like(w)
     if logZ is None and want_logZ:
@@ -332,7 +380,7 @@ def bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, grad_w_soft
     ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_FWD_VJP, dev)
     rc = lib.bcjr_vec_soft_codeword_fwd_vjp(_ptr(w), B, L, _ptr(codebook), state_bits, k, V,
                                             float(T), _ptr(grad_w_soft), _ptr(w_soft), _ptr(logZ),
-                                            _ptr(dW), _ptr(dCodebook), _ptr(ws), ws.numel(),
+                                            _ptr(dW), _ptr(dCodebook), _ptr(ws), _ws_bytes(ws),
                                             _stream(stream))
     _raise("bcjr_vec_soft_codeword_fwd_vjp", rc)
     return w_soft, logZ, dW, dCodebook
@@ -356,16 +404,19 @@ def bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V, *, want_w_hard=True, 
     lib = load_library()
     B, L = _shape(w)
     _check_in("w", w)
-    _vec_codebook(codebook, state_bits, V)
+    dev = w.device
+    _vec_codebook(codebook, state_bits, V, dev)
     if L % V:
         raise ValueError(f"L = {L} is not a multiple of V = {V}")
+    _check_out("states", states, (B, L // V), dev, torch.int32)
+    _check_out("w_hard", w_hard, (B, L), dev)
     if states is None:
-        states = torch.empty((B, L // V), dtype=torch.int32, device=w.device)
+        states = torch.empty((B, L // V), dtype=torch.int32, device=dev)
     if w_hard is None and want_w_hard:
         w_hard = torch.empty_like(w)
-    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_VITERBI, w.device)
+    ws = _vec_workspace(workspace, B, L, state_bits, k, V, OP_VITERBI, dev)
     rc = lib.bcjr_vec_viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, _ptr(states),
-                                     _ptr(w_hard), _ptr(ws), ws.numel(), _stream(stream))
+                                     _ptr(w_hard), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_vec_viterbi_decode", rc)
     return states, w_hard
 
@@ -392,7 +443,7 @@ def qat_adam_step(param, grad, m, v, lr, beta1=0.9, beta2=0.999, eps=1e-8, step=
     """One Adam step in place on param, m, v (same shape, float32, device)."""
     lib = load_library()
     for name, t in (("param", param), ("grad", grad), ("m", m), ("v", v)):
-        _check_in(name, t, tuple(param.shape))
+        _check_in(name, t, tuple(param.shape), device=param.device)
     rc = lib.qat_adam_step(_ptr(param), _ptr(grad), _ptr(m), _ptr(v), param.numel(), float(lr),
                            float(beta1), float(beta2), float(eps), int(step), float(grad_clip),
                            _stream(stream))
@@ -403,7 +454,7 @@ def qat_sgd_step(param, grad, lr, grad_clip=0.0, stream=None):
     """param -= lr * clamp(grad, -grad_clip, grad_clip), in place."""
     lib = load_library()
     _check_in("param", param)
-    _check_in("grad", grad, tuple(param.shape))
+    _check_in("grad", grad, tuple(param.shape), device=param.device)
     rc = lib.qat_sgd_step(_ptr(param), _ptr(grad), param.numel(), float(lr), float(grad_clip),
                           _stream(stream))
     _raise("qat_sgd_step", rc)

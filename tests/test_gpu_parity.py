@@ -315,3 +315,34 @@ def test_empty_batch_zeroes_dcodebook():
                              workspace=torch.empty(256, dtype=torch.uint8, device="cuda:0"))
     torch.cuda.synchronize()
     assert float(dc.abs().max()) == 0.0
+
+
+def test_binding_rejects_tensors_the_kernels_would_misread():
+    """Caller-supplied outputs and workspaces are checked before any launch:
+    wrong shape, dtype, layout or device raise instead of being written."""
+    n, k, B, L, T = 8, 2, 4, 10, 0.3
+    w, c, g = (dev(a) for a in WL.random_case(11, B, L, n))
+    f32 = torch.float32
+    bad = [
+        dict(w_soft=torch.empty((B, L + 1), dtype=f32, device="cuda:0")),
+        dict(logZ=torch.empty((B + 1,), dtype=f32, device="cuda:0")),
+        dict(dW=torch.empty((L, B), dtype=f32, device="cuda:0").t()),          # not contiguous
+        dict(dCodebook=torch.empty((1 << n,), dtype=torch.float64, device="cuda:0")),
+        dict(dW=torch.empty((B, L), dtype=f32)),                                # host tensor
+        dict(workspace=torch.empty(1 << 20, dtype=torch.uint8)),                # host workspace
+    ]
+    for kw in bad:
+        with pytest.raises((TypeError, ValueError)):
+            P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, **kw)
+    with pytest.raises((TypeError, ValueError)):
+        P.viterbi_decode(w, c, n, k, states=torch.empty((B, L), dtype=f32, device="cuda:0"))
+    with pytest.raises((TypeError, ValueError)):
+        P.bcjr_soft_codeword(w, c, n, k, T, w_soft=torch.empty((B, L), dtype=f32, device="cuda:0")[:, :-1])
+    # a float32 workspace is sized in bytes, not elements: same results as uint8
+    nbytes = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
+    ws32 = torch.empty((nbytes + 3) // 4, dtype=f32, device="cuda:0")
+    a = P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, workspace=ws32)
+    b = P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(host(x), host(y))
