@@ -938,6 +938,10 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
       double* cur = (t & 1) ? mv1 : mv0;
       double* nxt = (t & 1) ? mv0 : mv1;
       const double w0 = (double)wb[2 * t], w1 = (double)wb[2 * t + 1];
+      // the step's winning digits, one byte per tile, stored after the tile
+      // loop: a store between two tiles would make the next tile's codebook
+      // loads wait for it (loads and stores retire in order)
+      uint64_t digs = 0;
 #pragma unroll 1
       for (int i = 0; i < SGT; ++i) {
         {
@@ -963,9 +967,14 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
           }
           if (t < N - 1) {
             nxt[(q.row(m) + tl)] = best;
-            bp[(t + 1) * GS + m * 16 + tl] = (uint8_t)br;
+            digs |= (uint64_t)br << (8 * i);
           }
         }
+      }
+      if (t < N - 1) {
+#pragma unroll
+        for (int i = 0; i < SGMAX; ++i)
+          if (i < SGT) bp[(t + 1) * GS + (tq + i * TQ) * 16 + tl] = (uint8_t)(digs >> (8 * i));
       }
       __syncthreads();
     }
