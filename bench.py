@@ -343,7 +343,17 @@ def main():
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes": src.numel() * 4}), flush=True)
+        # then the copy's own rate (bytes read + written), HIP events, 5 copies
+        st = torch.cuda.current_stream()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(st)
+        for _ in range(5):
+            dst.copy_(src)
+        t1.record(st)
+        torch.cuda.synchronize()
+        sec = t0.elapsed_time(t1) / 1e3 / 5
+        print(json.dumps({"copy_bytes": src.numel() * 4,
+                          "copy_read_plus_write_bytes_per_s": 2 * src.numel() * 4 / sec}), flush=True)
         return
     P.load_library()
     if args.path == "anneal":
