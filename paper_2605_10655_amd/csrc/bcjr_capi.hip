@@ -400,6 +400,12 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
   a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
                  : nullptr;
+  if (vjp) {  // the (H, B) rows of step L - 1 are zero for every block of a slot
+    const int64_t hstep = 2 * ((int64_t)1 << (n - k));
+    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
+                       stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {

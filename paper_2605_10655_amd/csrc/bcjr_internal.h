@@ -22,10 +22,13 @@ struct FbArgs {
   float* dW;           // [B, L] or null
   double* dc_part;     // [slots][S] fp64 partial sums of dCodebook, or null
   float* histH;        // [slots][L][S/K]   H_t as read by each super-group (soft codeword)
-  float* histHB;       // [slots][L][2 S/K] H_t and the B tangent per super-group (VJP)
+  float* histHB;       // [slots][L][2 S/K] H_t, then the B tangent, as [S/K] vectors (VJP)
   float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group (dCodebook)
-  // (per step and super-group an H (G) plane then a B (A) plane, each
-  // [threads][K] floats: one store of a wave fills whole cache lines)
+  // (histHB: per step the H vector then the B vector, indexed by group, so
+  // that super-group x's row is the K entries at x K; the backward sweep
+  // stores them from its outputs, one dword per lane, in its exchange-write
+  // phase; histGA: per step and super-group a G plane then an A plane of
+  // [threads][K] floats; either way one store of a wave fills whole lines)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
   // low-temperature variant (double-float log vectors); histHB and histGA
   // then hold, per step and super-group, three planes (hi, lo, tangent) of

@@ -180,8 +180,8 @@ __device__ __forceinline__ void buf_st(rsrc_t r, uint32_t voff0, uint32_t soff0,
   }
 }
 
-// History rows of one super-group: the H plane ([threads][K]) and, with the
-// VJP, the B plane `plane` bytes after it; both streamed (read once).
+// History row of one super-group: its K entries of H and, with the VJP, of
+// B `plane` bytes after them; streamed (read once).
 template <int K, bool VJP>
 __device__ __forceinline__ void hist_row(rsrc_t h, uint32_t voff, uint32_t step_off, uint32_t sg_off,
                                          uint32_t plane, float (&H)[K], float (&B)[K]) {
@@ -403,9 +403,10 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const uint32_t voK = (uint32_t)tb << (KB + 2);
   // Histories: one descriptor per workgroup over its BPW slots; the block's
   // slot and the thread's super-group row go into the per-thread offset.
-  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per thread and super-group (H, B planes)
+  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per thread and super-group, (G, A) rows
   const uint32_t hstep = (uint32_t)GS * (VJP ? 2 : 1);   // floats per step
   const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
+  const uint32_t voC = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb) * 4u;
   // w and g of the step: when a block spans whole waves every lane needs the
   // same value, read 64 steps at a time and taken with a lane read
   const bool lane_rows = TPB >= 64;
@@ -481,6 +482,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       uint32_t tid_s = CBR ? lane_tid(wave_s) : (uint32_t)threadIdx.x;
       const uint32_t col0_s = CBR ? tid_s : col0, row0_s = CBR ? tid_s * K : row0;
       const uint32_t voH_s = CBR ? tid_s * K * 4u : voH;
+      const uint32_t vcH = CBR ? tid_s * 4u : voC;
       rc.red = red0 + ((L - 1 - t) & 1) * (NT / 64) * kRed;
       float wt, gt = 0.f;
       if (lane_rows) {
@@ -524,12 +526,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             }
 #pragma unroll
             for (int b = 0; b < K; ++b) Hin[b] -= offc;
-            if constexpr (VJP) {
-              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 3)), Hin);
-              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 3)) + (uint32_t)TPB * K * 4u, Bin);
-            } else {
-              buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 2)), Hin);
-            }
+            if constexpr (!VJP) buf_st<K, kStream>(hist, voH_s, ((i * TPB) << (KB + 2)), Hin);
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               float cc[K];
@@ -611,12 +608,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
 #pragma unroll
           for (int b = 0; b < K; ++b) Hin[b] -= offc;
-          if constexpr (VJP) {
-            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 3)), Hin);
-            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 3)) + (uint32_t)TPB * K * 4u, Bin);
-          } else {
-            buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 2)), Hin);
-          }
+          if constexpr (!VJP) buf_st<K, kStream>(hist, voH_s, soH + ((i * TPB) << (KB + 2)), Hin);
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             float x[K], d[K];
@@ -658,13 +650,22 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
       shiftB += lane_rows ? __builtin_amdgcn_readfirstlane((int)off) : (int)off;
       if (tb == 0) sm_mB[t - 1] = off;
       if constexpr (VJP) {
+        // The exchange writes, and with them the history entries of step
+        // t - 1 (the values the next step reads), one dword per lane at group
+        // j NSG + i TPB + tb: stored here, where the VALU waits on the LDS
+        // writes anyway, rather than as rows in the arithmetic phase.  (The
+        // entries of step L - 1 are zero and are filled before the launch.)
 #pragma unroll
         for (int i = 0; i < SGMAX; ++i) {
           if (i < SGT) {
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              lds[wcol + j * NSG + i * TPB] = Hout[i][j] - off;
-              lds[wcolB + j * NSG + i * TPB] = Bout[i][j];
+              const float hv[1] = {Hout[i][j] - off}, bv[1] = {Bout[i][j]};
+              lds[wcol + j * NSG + i * TPB] = hv[0];
+              lds[wcolB + j * NSG + i * TPB] = bv[0];
+              const uint32_t so = soH - hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
+              buf_st<1, kStream>(hist, vcH, so, hv);
+              buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
             }
           }
         }
@@ -705,7 +706,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
     gnx = lane_rows && VJP ? ld_uniform(gbu, 0) : 0.f;
     if constexpr (PF) {
-      hist_row<K, VJP>(hist, voH, 0, 0, (uint32_t)TPB * K * 4u, pH, pB);
+      hist_row<K, VJP>(hist, voH, 0, 0, (uint32_t)GS * 4u, pH, pB);
       if constexpr (!CBR) {
 #pragma unroll
         for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, p0[j]);
@@ -767,8 +768,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
               Bc[u] = VJP ? pB[u] : 0.f;
             }
           } else {
-            hist_row<K, VJP>(hist, voH_s, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * hrow * 4u,
-                             (uint32_t)TPB * K * 4u, Hc, Bc);
+            hist_row<K, VJP>(hist, voH_s, (uint32_t)t * hstep * 4u, (uint32_t)i * TPB * K * 4u,
+                             (uint32_t)GS * 4u, Hc, Bc);
           }
           if constexpr (PF) {
 #pragma unroll
@@ -790,7 +791,7 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             const bool last = i + 1 >= SGT;
             const int64_t tn = last && t + 1 < L ? t + 1 : t;
             hist_row<K, VJP>(hist, voH_s, (uint32_t)tn * hstep * 4u,
-                             last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u, (uint32_t)TPB * K * 4u,
+                             last ? 0u : (uint32_t)(i + 1) * TPB * K * 4u, (uint32_t)GS * 4u,
                              pH, pB);
           }
 #pragma unroll
@@ -904,9 +905,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         // the four history rows of a step, loaded one step ahead
         float nH[K], nB[K], nG[K], nA[K];
         {
-          const uint32_t so = (uint32_t)i * TPB * hrow * 4u;
-          buf_ld<K, kStream>(hist, voH, so, nH);
-          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, nB);
+          const uint32_t so = (uint32_t)i * TPB * hrow * 4u, sh = (uint32_t)i * TPB * K * 4u;
+          buf_ld<K, kStream>(hist, voH, sh, nH);
+          buf_ld<K, kStream>(hist, voH, sh + (uint32_t)GS * 4u, nB);
           buf_ld<K, kStream>(hga, voH, so, nG);
           buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
         }
@@ -944,8 +945,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           {  // (a select, not a branch: the last step re-reads its own rows)
             const int64_t tn = t + 1 < L ? t + 1 : t;
             const uint32_t so = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-            buf_ld<K, kStream>(hist, voH, so, nH);
-            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, nB);
+            const uint32_t sh = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * K * 4u;
+            buf_ld<K, kStream>(hist, voH, sh, nH);
+            buf_ld<K, kStream>(hist, voH, sh + (uint32_t)GS * 4u, nB);
             buf_ld<K, kStream>(hga, voH, so, nG);
             buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
           }
@@ -1559,6 +1561,12 @@ __global__ void dc_reduce_kernel(const double* part, int64_t nslots, int64_t S, 
 __global__ void scale_kernel(const float* c, float kap, float* cs, int64_t S) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < S) cs[i] = c[i] * kap;
+}
+
+// rows[r * stride + c] = v for r < nrows, c < row_len
+__global__ void fill_rows_kernel(float* rows, int64_t stride, int64_t nrows, int64_t row_len, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nrows * row_len) rows[(i / row_len) * stride + i % row_len] = v;
 }
 
 __global__ void fill_kernel(float* out, int64_t count, float v) {
