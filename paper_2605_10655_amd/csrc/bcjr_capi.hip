@@ -405,6 +405,11 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    if (dc) {  // and the (G, A) entries of step 0
+      hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
+                         stream, a.histGA, L * hstep, slots, hstep, 0.f);
+      if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    }
   }
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;

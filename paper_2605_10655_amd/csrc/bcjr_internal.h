@@ -24,11 +24,11 @@ struct FbArgs {
   float* histH;        // [slots][L][S/K]   H_t as read by each super-group (soft codeword)
   float* histHB;       // [slots][L][2 S/K] H_t, then the B tangent, as [S/K] vectors (VJP)
   float* histGA;       // [slots][L][2 S/K] G_t and the A tangent per super-group (dCodebook)
-  // (histHB: per step the H vector then the B vector, indexed by group, so
-  // that super-group x's row is the K entries at x K; the backward sweep
-  // stores them from its outputs, one dword per lane, in its exchange-write
-  // phase; histGA: per step and super-group a G plane then an A plane of
-  // [threads][K] floats; either way one store of a wave fills whole lines)
+  // (per step an H (G) vector then a B (A) vector of S/K floats, indexed by
+  // group, written from the sweeps' exchange-write phases: the backward
+  // sweep one dword per lane (column form), the forward sweep one 16-byte
+  // row per super-group; the entries of step L - 1 (H, B) and step 0 (G, A)
+  // are zero and filled before the launch)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
   // low-temperature variant (double-float log vectors); histHB and histGA
   // then hold, per step and super-group, three planes (hi, lo, tangent) of

@@ -403,7 +403,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
   const uint32_t voK = (uint32_t)tb << (KB + 2);
   // Histories: one descriptor per workgroup over its BPW slots; the block's
   // slot and the thread's super-group row go into the per-thread offset.
-  const uint32_t hrow = VJP ? 2 * K : K;                 // floats per thread and super-group, (G, A) rows
   const uint32_t hstep = (uint32_t)GS * (VJP ? 2 : 1);   // floats per step
   const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
   const uint32_t voC = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb) * 4u;
@@ -755,11 +754,6 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
             Gin[j] = lds[rcol + j * NSG + i * TPB];
             Ain[j] = VJP ? lds[rcolA + j * NSG + i * TPB] : 0.f;
           }
-          if constexpr (DC) {  // (G_t, A_t) row of the super-group for the dCodebook sweep
-            const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-            buf_st<K, kStream>(hga, voH_s, so, Gin);
-            buf_st<K, kStream>(hga, voH_s, so + (uint32_t)TPB * K * 4u, Ain);
-          }
           float Hc[K], Bc[K], cc[K][K];
           if constexpr (PF) {
 #pragma unroll
@@ -863,6 +857,11 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 #pragma unroll
               for (int u = 0; u < K; ++u) ao[u] = fmaf(-gt, wst, Aout[i][u]);
               st_vec<K>(lds + wrowA + i * TPB * K, ao);
+              if constexpr (DC) {  // (G, A) entries of step t + 1 for the dCodebook sweep
+                const uint32_t so = (uint32_t)(t + 1) * hstep * 4u + (uint32_t)i * TPB * K * 4u;
+                buf_st<K, kStream>(hga, voH_s, so, go);
+                buf_st<K, kStream>(hga, voH_s, so + (uint32_t)GS * 4u, ao);
+              }
             }
           }
         }
@@ -887,7 +886,9 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     // No recursion is left, so each thread runs super-group by super-group
     // over all steps with 16 accumulators: p_t(s) = 2^(G_t + h_t + H_t -
     // lambda_t) per state from the (G, A) and (H, B) histories, with the exact
-    // lambda_t and E_p[X_t] recorded by S1.
+    // lambda_t and E_p[X_t] recorded by S1.  The (G, A) entries of a
+  // super-group are K dwords a column apart (S1 stored them as rows of the
+  // next step's outputs), the (H, B) entries one 16-byte row.
     if constexpr (DC) {
       __syncthreads();  // S1's per-step scalars
       const bool first = base == (int64_t)blockIdx.x * BPW;
@@ -905,11 +906,17 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
         // the four history rows of a step, loaded one step ahead
         float nH[K], nB[K], nG[K], nA[K];
         {
-          const uint32_t so = (uint32_t)i * TPB * hrow * 4u, sh = (uint32_t)i * TPB * K * 4u;
+          const uint32_t sh = (uint32_t)i * TPB * K * 4u;
           buf_ld<K, kStream>(hist, voH, sh, nH);
           buf_ld<K, kStream>(hist, voH, sh + (uint32_t)GS * 4u, nB);
-          buf_ld<K, kStream>(hga, voH, so, nG);
-          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            float g1[1], a1[1];
+            buf_ld<1, kStream>(hga, voC, (uint32_t)(j * NSG + i * TPB) * 4u, g1);
+            buf_ld<1, kStream>(hga, voC, (uint32_t)(j * NSG + i * TPB) * 4u + (uint32_t)GS * 4u, a1);
+            nG[j] = g1[0];
+            nA[j] = a1[0];
+          }
         }
 #pragma unroll 1
         for (int64_t t = 0; t < L; ++t) {
@@ -944,12 +951,18 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
           }
           {  // (a select, not a branch: the last step re-reads its own rows)
             const int64_t tn = t + 1 < L ? t + 1 : t;
-            const uint32_t so = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
             const uint32_t sh = (uint32_t)tn * hstep * 4u + (uint32_t)i * TPB * K * 4u;
             buf_ld<K, kStream>(hist, voH, sh, nH);
             buf_ld<K, kStream>(hist, voH, sh + (uint32_t)GS * 4u, nB);
-            buf_ld<K, kStream>(hga, voH, so, nG);
-            buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, nA);
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+              float g1[1], a1[1];
+              const uint32_t sg = (uint32_t)tn * hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
+              buf_ld<1, kStream>(hga, voC, sg, g1);
+              buf_ld<1, kStream>(hga, voC, sg + (uint32_t)GS * 4u, a1);
+              nG[j] = g1[0];
+              nA[j] = a1[0];
+            }
           }
 #pragma unroll
           for (int u = 0; u < K; ++u) {
