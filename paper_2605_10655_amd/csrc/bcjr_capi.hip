@@ -347,6 +347,12 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.xA = reinterpret_cast<float*>(p);                 p += slots * lay.xA;
   a.small = reinterpret_cast<float*>(p);              p += slots * lay.small;
   a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
+  if (dc) {  // the (G, A) entries of step 0 are zero for every block of a slot
+    const int64_t hstep = 3 * ((int64_t)1 << (n - k));
+    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
+                       stream, a.histGA, L * hstep, slots, hstep, 0.f);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {

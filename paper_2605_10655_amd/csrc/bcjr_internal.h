@@ -30,10 +30,12 @@ struct FbArgs {
   // row per super-group; the entries of step L - 1 (H, B) and step 0 (G, A)
   // are zero and filled before the launch)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
-  // low-temperature variant (double-float log vectors); histHB and histGA
-  // then hold, per step and super-group, three planes (hi, lo, tangent) of
-  // [threads][K] floats, so that one store of a wave fills whole cache
-  // lines; small is [slots][4][L]
+  // low-temperature variant (double-float log vectors): histHB holds, per
+  // step and super-group, three planes (hi, lo, tangent) of [threads][K]
+  // floats, so that one store of a wave fills whole cache lines; histGA per
+  // step three [S/K] vectors (G hi, G lo, A), stored by the forward sweep's
+  // write phase for the next step (step 0 filled with zeros before the
+  // launch); small is [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
   const float* bref;   // [B, L] centring reference of the backward tangent
   float* xA;           // [slots][S/K] tangent exchange, updated in place

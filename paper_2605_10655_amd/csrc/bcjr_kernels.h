@@ -1011,7 +1011,8 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 //   S0 backward: H and B, history rows (H hi, H lo, B) as three planes of
 //                [threads][K] per super-group, written and read non-temporal;
 //   S1 forward:  G and A, marginals, w_soft, dW; with dCodebook also the
-//                rows (G hi, G lo, A) and the exact lambda_t, E_p[X_t];
+//                (G hi, G lo, A) rows of the next step, stored from the
+//                write phase, and the exact lambda_t, E_p[X_t];
 //   S2 dCodebook as in fb_kernel, with p from the fp64 sums.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void lse_pair_d(double& m, float& s, double mo, float so) {
@@ -1094,6 +1095,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   const uint32_t hrow = 3 * K;                    // floats per thread and super-group: hi, lo, tangent planes
   const uint32_t hstep = (uint32_t)GS * 3;        // floats per history step
   const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
+  const uint32_t voC = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb) * 4u;
   const bool lane_rows = TPB >= 64;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
@@ -1407,12 +1409,6 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             Gh[j] = lds[rcol + j * NSG + i * TPB];
             Gl[j] = lds[rcolL + j * NSG + i * TPB];
           }
-          if constexpr (DC) {
-            const uint32_t so = soH + (uint32_t)i * TPB * hrow * 4u;
-            buf_st<K, kStream>(hga, voH, so, Gh);
-            buf_st<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, Gl);
-            buf_st<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 8u, Ar);
-          }
           double G[K];
 #pragma unroll
           for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
@@ -1486,6 +1482,17 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           st_vec<K>(lds + wrow + i * TPB * K, oh[i]);
           st_vec<K>(lds + wrowL + i * TPB * K, ol[i]);
           buf_st<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, oa[i]);
+          if constexpr (DC) {  // (G hi, G lo, A) entries of step t + 1, A centred as it is read
+            if (t + 1 < L) {
+              float ac[K];
+#pragma unroll
+              for (int u = 0; u < K; ++u) ac[u] = oa[i][u] - cprev;
+              const uint32_t so = (uint32_t)(t + 1) * hstep * 4u + (uint32_t)i * TPB * K * 4u;
+              buf_st<K, kStream>(hga, voH, so, oh[i]);
+              buf_st<K, kStream>(hga, voH, so + (uint32_t)GS * 4u, ol[i]);
+              buf_st<K, kStream>(hga, voH, so + (uint32_t)GS * 8u, ac);
+            }
+          }
         }
       }
       __syncthreads();
@@ -1532,9 +1539,17 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           buf_ld<K, kStream>(hist, voH, so, Hh);
           buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, Hl);
           buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 8u, Bv);
-          buf_ld<K, kStream>(hga, voH, so, Gh);
-          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 4u, Gl);
-          buf_ld<K, kStream>(hga, voH, so + (uint32_t)TPB * K * 8u, A);
+#pragma unroll
+          for (int j = 0; j < K; ++j) {  // (G, A) entries a column apart
+            float v1[1], v2[1], v3[1];
+            const uint32_t sg = (uint32_t)t * hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
+            buf_ld<1, kStream>(hga, voC, sg, v1);
+            buf_ld<1, kStream>(hga, voC, sg + (uint32_t)GS * 4u, v2);
+            buf_ld<1, kStream>(hga, voC, sg + (uint32_t)GS * 8u, v3);
+            Gh[j] = v1[0];
+            Gl[j] = v2[0];
+            A[j] = v3[0];
+          }
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             const double hb = ((double)Hh[u] + (double)Hl[u]) - lt;
