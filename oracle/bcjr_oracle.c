@@ -490,3 +490,125 @@ int oracle_viterbi(const double *w, int64_t B, int64_t L, const double *c,
                    int n, int k, int32_t *states, double *cost, int nthreads) {
   return oracle_viterbi_v(w, B, L, c, n, k, 1, states, cost, nthreads);
 }
+
+/* ------------------------------------------------------------------ */
+/* Min-sum max-marginals and the margin of the decoded codeword         */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+  const double *w, *c;
+  int64_t B, L;
+  int n, k, V;
+  const int32_t *states;
+  double *gap;
+  int tid, nthreads, status;
+} gjob_t;
+
+static int same_codeword(const double *a, const double *b, int V) {
+  for (int q = 0; q < V; ++q)
+    if (a[q] != b[q]) return 0;
+  return 1;
+}
+
+/* One block, N = L / V steps.  mf[N*S]: the forward min-sum metric (the
+ * smallest distortion of a path prefix ending in s at t, its own step
+ * included); mb[S] / mbn[S]: the backward metric (the smallest distortion of
+ * the steps after t for a path leaving s at t).  Their sum is the
+ * max-marginal M_t(s). */
+static void gap_block(const double *w, int64_t L, const double *c, int n, int k, int V,
+                      const int32_t *st, double *gap, double *mf, double *mb, double *mbn) {
+  const int64_t S = (int64_t)1 << n, K = (int64_t)1 << k, mask = S - 1;
+  const int64_t N = L / V;
+  for (int64_t s = 0; s < S; ++s) mf[s] = sqdist(w, c + s * V, V);
+  for (int64_t t = 1; t < N; ++t) {
+    double *cur = mf + t * S;
+    const double *prev = mf + (t - 1) * S;
+    for (int64_t s = 0; s < S; ++s) cur[s] = INFINITY;
+    for (int64_t sp = 0; sp < S; ++sp)
+      for (int64_t b = 0; b < K; ++b) {
+        int64_t d = ((sp << k) | b) & mask;
+        if (prev[sp] < cur[d]) cur[d] = prev[sp];
+      }
+    for (int64_t s = 0; s < S; ++s) cur[s] = sqdist(w + t * V, c + s * V, V) + cur[s];
+  }
+  for (int64_t s = 0; s < S; ++s) mb[s] = 0.0;
+  for (int64_t t = N - 1; t >= 0; --t) {
+    const double *f = mf + t * S;
+    const int64_t sb = st[t];
+    const double best = f[sb] + mb[sb];
+    double alt = INFINITY;
+    for (int64_t s = 0; s < S; ++s) {
+      if (same_codeword(c + s * V, c + sb * V, V)) continue;
+      double m = f[s] + mb[s];
+      if (m < alt) alt = m;
+    }
+    gap[t] = 0.5 * (alt - best);
+    if (t == 0) break;
+    /* mb_{t-1}(s) = min_b [ d_t(next(s, b)) + mb_t(next(s, b)) ] */
+    for (int64_t s = 0; s < S; ++s) {
+      double m = INFINITY;
+      for (int64_t b = 0; b < K; ++b) {
+        int64_t d = ((s << k) | b) & mask;
+        double v = sqdist(w + t * V, c + d * V, V) + mb[d];
+        if (v < m) m = v;
+      }
+      mbn[s] = m;
+    }
+    double *tmp = mb;
+    mb = mbn;
+    mbn = tmp;
+  }
+}
+
+static void *gjob_main(void *arg) {
+  gjob_t *j = (gjob_t *)arg;
+  const int64_t S = (int64_t)1 << j->n, N = j->L / j->V;
+  double *mf = (double *)malloc(sizeof(double) * (size_t)(N * S));
+  double *mb = (double *)malloc(sizeof(double) * (size_t)S);
+  double *mbn = (double *)malloc(sizeof(double) * (size_t)S);
+  if (!mf || !mb || !mbn) {
+    j->status = -2;
+  } else {
+    for (int64_t b = j->tid; b < j->B; b += j->nthreads)
+      gap_block(j->w + b * j->L, j->L, j->c, j->n, j->k, j->V, j->states + b * N, j->gap + b * N,
+                mf, mb, mbn);
+    j->status = 0;
+  }
+  free(mf);
+  free(mb);
+  free(mbn);
+  return NULL;
+}
+
+int oracle_maxmarginal_gap_v(const double *w, int64_t B, int64_t L, const double *c, int n,
+                             int k, int V, const int32_t *states, double *gap, int nthreads) {
+  if (bad_args(B, L, w, c, n, k, V, 1.0) || !states || !gap) return -1;
+  if (B == 0) return 0;
+  const int64_t S = (int64_t)1 << n, N = L / V;
+  for (int64_t i = 0; i < B * N; ++i)
+    if (states[i] < 0 || states[i] >= S) return -1;
+  if (nthreads < 1) nthreads = 1;
+  if ((int64_t)nthreads > B) nthreads = (int)B;
+  gjob_t *jobs = (gjob_t *)calloc((size_t)nthreads, sizeof(gjob_t));
+  pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+  if (!jobs || !th) {
+    free(jobs);
+    free(th);
+    return -2;
+  }
+  for (int i = 0; i < nthreads; ++i) {
+    gjob_t *j = &jobs[i];
+    j->w = w; j->c = c; j->B = B; j->L = L; j->n = n; j->k = k; j->V = V;
+    j->states = states; j->gap = gap; j->tid = i; j->nthreads = nthreads;
+    j->status = -3;
+  }
+  for (int i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, gjob_main, &jobs[i]);
+  gjob_main(&jobs[0]);
+  for (int i = 1; i < nthreads; ++i) pthread_join(th[i], NULL);
+  int status = 0;
+  for (int i = 0; i < nthreads; ++i)
+    if (jobs[i].status != 0) status = jobs[i].status;
+  free(jobs);
+  free(th);
+  return status;
+}

@@ -80,6 +80,19 @@ int oracle_block_tables_v(const double *w, int64_t L, const double *c, int n,
                           int k, int V, double T, const double *g, double *alpha,
                           double *beta, double *A, double *Bt);
 
+/* Min-sum max-marginals (Sec. 3.2; the T -> 0 limit of Sec. 3.3).  For a
+ * step t and state s, M_t(s) = min over legal paths with s_t = s of
+ * sum_tau ||w_tau - c(s_tau)||^2 (each step's distortion as in
+ * oracle_viterbi).  Given a decoded path states[B*(L/V)] (oracle_viterbi's
+ * output), gap[B*(L/V)] receives per step
+ *     ( min_{s : c(s) != c(states_t)} M_t(s)  -  M_t(states_t) ) / 2,
+ * the energy (Eq. boltzmann, E = distortion / 2) by which the best path
+ * emitting another codeword at step t loses; +inf when every state emits
+ * the same codeword.  Returns -1 for a state index outside [0, S). */
+int oracle_maxmarginal_gap_v(const double *w, int64_t B, int64_t L, const double *c,
+                             int n, int k, int V, const int32_t *states, double *gap,
+                             int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -51,9 +51,10 @@ def lib():
                                                  dp, ci]
         L.oracle_viterbi_v.argtypes = [dp, i64, i64, dp, ci, ci, ci, ip, dp, ci]
         L.oracle_block_tables_v.argtypes = [dp, i64, dp, ci, ci, ci, cd, dp, dp, dp, dp, dp]
+        L.oracle_maxmarginal_gap_v.argtypes = [dp, i64, i64, dp, ci, ci, ci, ip, dp, ci]
         for f in (L.oracle_soft_codeword, L.oracle_soft_codeword_vjp, L.oracle_viterbi,
                   L.oracle_block_tables, L.oracle_soft_codeword_v, L.oracle_soft_codeword_vjp_v,
-                  L.oracle_viterbi_v, L.oracle_block_tables_v):
+                  L.oracle_viterbi_v, L.oracle_block_tables_v, L.oracle_maxmarginal_gap_v):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -134,6 +135,40 @@ def viterbi(w, c, n, k, nthreads=None, V=1):
                                 _ptr(cost), nthreads or default_threads())
     _check(rc, "oracle_viterbi_v")
     return st, cost
+
+
+def maxmarginal_gap(w, c, n, k, states, nthreads=None, V=1):
+    """Energy margin of the decoded codeword at every step (paper Sec. 3.2
+    and the T -> 0 limit of Sec. 3.3): with M_t(s) the smallest distortion
+    sum_tau ||w_tau - c(s_tau)||^2 of a legal path through s at step t,
+    gap_t = (min over states emitting another codeword than c(states_t) of
+    M_t(s) - M_t(states_t)) / 2, in the energy units of Eq. boltzmann.
+    states[B, L // V] is a decoded path (``viterbi``).  float64 [B, L // V]."""
+    w = _d(w)
+    c = _codebook(c, n, V)
+    B, L = w.shape
+    st = np.ascontiguousarray(states, dtype=np.int32)
+    assert st.shape == (B, L // V)
+    gap = np.empty((B, L // V), np.float64)
+    rc = lib().oracle_maxmarginal_gap_v(_ptr(w), B, L, _ptr(c), n, k, V,
+                                        _ptr(st, ctypes.c_int32), _ptr(gap),
+                                        nthreads or default_threads())
+    _check(rc, "oracle_maxmarginal_gap_v")
+    return gap
+
+
+def crisp_positions(w, c, n, k, T, states, tol=2e-5, nthreads=None):
+    """The T -> 0 check's excusal rule: a position must carry the decoded
+    codeword (|w_soft_t - c(s*_t)| <= tol) when its max-marginal energy gap
+    exceeds T ln(max |c_i - c_j| / tol), i.e. when the best competing
+    codeword's Boltzmann weight, relative to the decoded one, times the
+    largest codeword difference is below tol.  Returns (mask [B, L] of the
+    positions held to the check, the gaps, the threshold)."""
+    cf = np.asarray(c, np.float64).reshape(-1)
+    spread = float(cf.max() - cf.min())
+    thr = float(T) * np.log(spread / tol)
+    gap = maxmarginal_gap(w, c, n, k, states, nthreads)
+    return gap > thr, gap, thr
 
 
 def ste(w, c, n, k, T, g, want_dc=True, nthreads=None, V=1):

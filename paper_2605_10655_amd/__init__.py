@@ -148,6 +148,21 @@ def _check_out(name, t, shape, device, dtype=None):
         _check_in(name, t, shape, dtype, device)
 
 
+def _keep_alive(stream, *tensors):
+    """Tensors this module allocated come from PyTorch's caching allocator on
+    the current stream; when the launch went to another stream, tell the
+    allocator so that their memory is not handed out again while the
+    kernels may still use it."""
+    if stream is None:
+        return
+    torch = _torch()
+    if stream == torch.cuda.current_stream(stream.device):
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 def _ws_bytes(ws):
     return ws.numel() * ws.element_size()
 
@@ -202,6 +217,7 @@ def bcjr_soft_codeword(w, codebook, state_bits, k, T, *, w_soft=None, logZ=None,
     rc = lib.bcjr_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, float(T),
                                 _ptr(w_soft), _ptr(logZ), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword", rc)
+    _keep_alive(stream, w_soft, logZ, ws)
     return w_soft, logZ
 
 
@@ -227,6 +243,7 @@ def bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, want_d
                                     _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws),
                                     _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword_vjp", rc)
+    _keep_alive(stream, dW, dCodebook, ws)
     return dW, dCodebook
 
 
@@ -257,6 +274,7 @@ def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, wa
                                         _ptr(grad_w_soft), _ptr(w_soft), _ptr(logZ), _ptr(dW),
                                         _ptr(dCodebook), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword_fwd_vjp", rc)
+    _keep_alive(stream, w_soft, logZ, dW, dCodebook, ws)
     return w_soft, logZ, dW, dCodebook
 
 
@@ -284,6 +302,7 @@ def bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, grad_w_soft, *, want_dW=
                           _ptr(grad_w_soft), _ptr(dW), _ptr(dCodebook), _ptr(ws), _ws_bytes(ws),
                           _stream(stream))
     _raise("bcjr_ste_vjp", rc)
+    _keep_alive(stream, dW, dCodebook, ws)
     return dW, dCodebook
 
 
@@ -306,6 +325,7 @@ def viterbi_decode(w, codebook, state_bits, k, *, want_w_hard=True, states=None,
     rc = lib.viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, _ptr(states),
                             _ptr(w_hard), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("viterbi_decode", rc)
+    _keep_alive(stream, states, w_hard, ws)
     return states, w_hard
 
 
@@ -349,6 +369,7 @@ def bcjr_vec_soft_codeword(w, codebook, state_bits, k, V, T, *, w_soft=None, log
     rc = lib.bcjr_vec_soft_codeword(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, float(T),
                                     _ptr(w_soft), _ptr(logZ), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_vec_soft_codeword", rc)
+    _keep_alive(stream, w_soft, logZ, ws)
     return w_soft, logZ
 
 
@@ -383,6 +404,7 @@ def bcjr_vec_soft_codeword_fwd_vjp(w, codebook, state_bits, k, V, T, grad_w_soft
                                             _ptr(dW), _ptr(dCodebook), _ptr(ws), _ws_bytes(ws),
                                             _stream(stream))
     _raise("bcjr_vec_soft_codeword_fwd_vjp", rc)
+    _keep_alive(stream, w_soft, logZ, dW, dCodebook, ws)
     return w_soft, logZ, dW, dCodebook
 
 
@@ -418,6 +440,7 @@ def bcjr_vec_viterbi_decode(w, codebook, state_bits, k, V, *, want_w_hard=True, 
     rc = lib.bcjr_vec_viterbi_decode(_ptr(w), B, L, _ptr(codebook), state_bits, k, V, _ptr(states),
                                      _ptr(w_hard), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_vec_viterbi_decode", rc)
+    _keep_alive(stream, states, w_hard, ws)
     return states, w_hard
 
 
@@ -435,6 +458,7 @@ def bcjr_gaussian_codebook(state_bits, V=1, seed=0, *, out=None, device="cuda", 
     rc = lib.bcjr_gaussian_codebook(_ptr(out), state_bits, V, int(seed) & ((1 << 64) - 1),
                                     _stream(stream))
     _raise("bcjr_gaussian_codebook", rc)
+    _keep_alive(stream, out)
     return out
 
 

@@ -103,28 +103,28 @@ def test_config1_tiny_all_outputs(T):
     np.testing.assert_array_equal(st, rst)
     np.testing.assert_array_equal(wh, c[st])
     if T <= 1e-4:
-        # T -> 0: the soft codeword equals the Viterbi codeword wherever the
-        # oracle's soft codeword has crystallised (near-ties are excused)
-        rws = O.soft_codeword(w, c, wl.state_bits, wl.k, float(np.float32(T)))[0]
-        crisp = np.abs(rws - c[rst]) <= 1e-7
-        _say(f"[parity] cfg1 T={T}: {int((~crisp).sum())} of {crisp.size} positions excused")
-        assert crisp.mean() > 0.95
-        assert np.abs(ws[crisp] - c[rst][crisp]).max() <= TOL_WS
+        # T -> 0 (Sec. 3.3): the soft codeword equals the decoded codeword
+        # wherever the oracle's min-sum max-marginal energy gap exceeds
+        # T ln(max|c_i - c_j| / 2e-5); positions below it are counted
+        held, gap, thr = O.crisp_positions(w, c, wl.state_bits, wl.k, float(np.float32(T)), rst)
+        _say(f"[parity] cfg1 T={T}: {int((~held).sum())} of {held.size} positions excused "
+             f"(gap <= {thr:.3g})")
+        assert held.mean() > 0.95
+        assert np.abs(ws[held] - c[rst][held]).max() <= TOL_WS
 
 
 # ---------------------------------------------------------------- config 2
 @pytest.mark.parametrize("T", WL.workload(2).temps)
 def test_config2_small_full_batch(T):
+    """Every one of the 4096 blocks against the oracle."""
     wl = WL.workload(2)
     c, w, g = WL.codebook(2), WL.weights(2), WL.upstream(2)
-    _say(f"[parity] cfg2 full batch B={wl.B} T={T}")
+    _say(f"[parity] cfg2 full batch B={wl.B} T={T}, all blocks")
     ws, lz, dW, _ = gpu_fwd_vjp(w, c, wl.state_bits, wl.k, T, g, want_dc=False)
-    idx = WL.parity_subset(2, 256)
-    rws, rlz, rdW, _ = O.soft_codeword_vjp(w[idx], c, wl.state_bits, wl.k, float(np.float32(T)),
-                                           g[idx], want_dc=False)
-    check_ws(ws[idx], rws, "cfg2")
-    check_logz(lz[idx], rlz, "cfg2")
-    check_grad(dW[idx], rdW, "cfg2 dW")
+    rws, rlz, rdW, _ = O.soft_codeword_vjp(w, c, wl.state_bits, wl.k, float(np.float32(T)), g,
+                                           want_dc=False)
+    e = (check_ws(ws, rws, "cfg2"), check_logz(lz, rlz, "cfg2"), check_grad(dW, rdW, "cfg2 dW"))
+    _say(f"[parity] cfg2 T={T} errors {['%.2e' % x for x in e]}")
 
 
 # ---------------------------------------------------------------- config 3
@@ -182,19 +182,21 @@ def test_config4_full_batch_sampled():
 
 
 # ---------------------------------------------------------------- config 5
-@pytest.mark.parametrize("call", [0, 2, 3, 5, 7])
+@pytest.mark.parametrize("call", range(8))
 def test_config5_anneal_subset_with_dcodebook(call):
+    """64 seeded blocks of the 2048 x 8192 matrix per annealed call, as their
+    own launch so that dCodebook is comparable with the oracle's."""
     wl = WL.workload(5)
     c = WL.codebook(5)
-    w = WL.weights(5, rows=8)            # 8 rows x 8192 = 256 blocks
-    g = WL.upstream(5, call=call, B=w.shape[0])
-    idx = np.arange(0, w.shape[0], w.shape[0] // 8)[:8]
+    idx = WL.parity_subset(5, 64)
+    w = WL.weights(5)[idx]
+    g = WL.upstream(5, call=call)[idx]
     T = wl.temps[call]
-    ws, _, _, _ = full_check(w[idx], c, wl.state_bits, wl.k, T, g[idx], True, f"cfg5 call={call}")
+    ws, _, _, _ = full_check(w, c, wl.state_bits, wl.k, T, g, True, f"cfg5 call={call}")
     if call == 7:
-        st, _ = P.viterbi_decode(dev(w[idx]), dev(c), wl.state_bits, wl.k)
+        st, _ = P.viterbi_decode(dev(w), dev(c), wl.state_bits, wl.k)
         st = host(st)
-        rst, _ = O.viterbi(w[idx], c, wl.state_bits, wl.k)
+        rst, _ = O.viterbi(w, c, wl.state_bits, wl.k)
         np.testing.assert_array_equal(st, rst)
 
 
@@ -232,14 +234,19 @@ def test_precision_switch_boundary(T):
     full_check(w, c, 16, 2, T, g, True, f"switch T={T}")
 
 
-@pytest.mark.parametrize("n", [8, 12, 16])
-def test_small_workspace_runs_persistent_loop(n):
+@pytest.mark.parametrize("n,T", [(8, 0.2), (12, 0.2), (16, 0.2), (12, 0.003), (16, 0.003)])
+def test_small_workspace_runs_persistent_loop(n, T):
     """A workspace holding one workgroup's slots forces every workgroup to
-    walk several blocks (the persistent loop) and must give the same bits."""
-    k, L, T = 2, 24, 0.2
+    walk several blocks (the persistent loop) and must give the same bits;
+    at T = 0.003 this is the double-float kernel with dCodebook, whose
+    step-0 (G, A) history entries are filled once per call and must stay
+    valid for every later block of the slot, and whose dCodebook partials
+    add up across the blocks of a slot.  Both runs are also checked against
+    the oracle."""
+    k, L = 2, 24
     B = 40 if n < 16 else 6
     w, c, g = WL.random_case(77 + n, B, L, n)
-    full = gpu_fwd_vjp(w, c, n, k, T, g, True)
+    full = full_check(w, c, n, k, T, g, True, f"one-slot reference n={n} T={T}")
     big = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
     per_wg = None
     for nb in range(1, B + 1):      # smallest size the library accepts
@@ -252,19 +259,21 @@ def test_small_workspace_runs_persistent_loop(n):
         except P.BcjrError as e:
             assert e.status == -3
     assert per_wg is not None and per_wg < big
+    _say(f"[parity] n={n} T={T}: one-slot workspace of {per_wg} bytes (full {big})")
     for a, b in zip(full, out):
         np.testing.assert_array_equal(a, b)
 
 
-def test_low_temperature_every_grid_size():
+@pytest.mark.parametrize("n,B,L", [(12, 24, 20), (16, 16, 12)])
+def test_low_temperature_every_grid_size(n, B, L):
     """The double-float kernel under every workspace size from one slot up:
-    grids of 1 to 24 workgroups, with and without the persistent loop, and
+    grids of 1 to B workgroups, with and without the persistent loop, and
     both placements of the per-slot tangent vectors (XCD-contiguous when the
     grid is a multiple of 8, by slot otherwise) must give the same bits, and
     the full-size run must match the oracle."""
-    n, k, B, L, T = 12, 2, 24, 20, 0.003
-    w, c, g = WL.random_case(4242, B, L, n)
-    full = full_check(w, c, n, k, T, g, True, "lowT grids")
+    k, T = 2, 0.003
+    w, c, g = WL.random_case(4242 + n, B, L, n)
+    full = full_check(w, c, n, k, T, g, True, f"lowT grids n={n}")
     big = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)
     runs = 0
     for nb in range(1, B + 1):
@@ -278,7 +287,7 @@ def test_low_temperature_every_grid_size():
         runs += 1
         for a, b in zip(full, out):
             np.testing.assert_array_equal(a, b)
-    _say(f"[parity] lowT grids: {runs} workspace sizes ran")
+    _say(f"[parity] lowT grids n={n}: {runs} workspace sizes ran")
     assert runs >= B // 2
 
 
@@ -346,3 +355,18 @@ def test_binding_rejects_tensors_the_kernels_would_misread():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         np.testing.assert_array_equal(host(x), host(y))
+
+
+def test_side_stream_call_matches_current_stream():
+    """A call on a stream other than the current one (outputs and workspace
+    allocated by the binding) gives the same bits as on the current stream."""
+    n, k, B, L, T = 12, 2, 40, 32, 0.1
+    w, c, g = WL.random_case(123, B, L, n)
+    ref = gpu_fwd_vjp(w, c, n, k, T, g, True)
+    side = torch.cuda.Stream()
+    wd, cd, gd = dev(w), dev(c), dev(g)
+    torch.cuda.synchronize()
+    out = P.bcjr_soft_codeword_fwd_vjp(wd, cd, n, k, T, gd, stream=side)
+    side.synchronize()
+    for a, b in zip(ref, out):
+        np.testing.assert_array_equal(a, host(b))

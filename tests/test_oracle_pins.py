@@ -558,3 +558,83 @@ def test_ldlq_lowers_the_hessian_weighted_loss():
     plain = c[st].reshape(W.shape)
     loss = lambda X: np.einsum("ri,ij,rj->", W - X, H, W - X)
     assert loss(Wh) < 0.9 * loss(plain)
+
+
+# ---------------------------------------------------------------- T -> 0 check
+def _path_costs(w, c, n, k, V=1):
+    """Every legal path and its distortion, summed step by step."""
+    c = np.asarray(c, np.float64).reshape(1 << n, V)
+    N = len(w) // V
+    P = bf.paths(n, k, N)
+    cost = np.zeros(P.shape[0])
+    for t in range(N):
+        step = np.zeros(P.shape[0])
+        for comp in range(V):
+            d = w[t * V + comp] - c[P[:, t], comp]
+            step = step + d * d
+        cost = cost + step
+    return P, cost, c
+
+
+@pytest.mark.parametrize("n,k,L,V", [(4, 2, 6, 1), (3, 1, 9, 1), (5, 2, 5, 1), (6, 3, 3, 1),
+                                     (4, 2, 8, 2), (8, 4, 6, 2)])
+def test_maxmarginal_gap_matches_enumeration(n, k, L, V):
+    """gap_t = (min over paths whose step-t codeword differs from the decoded
+    one of their distortion - the optimal distortion) / 2, by listing every
+    path."""
+    r = np.random.default_rng(100 * n + 10 * k + L + V)
+    for _ in range(3):
+        c = r.standard_normal((1 << n) * V)
+        w = r.standard_normal(L)
+        st, _ = O.viterbi(w[None], c, n, k, V=V)
+        gap = O.maxmarginal_gap(w[None], c, n, k, st, V=V)[0]
+        P, cost, cv = _path_costs(w, c, n, k, V)
+        best = cost.min()
+        for t in range(L // V):
+            other = np.any(cv[P[:, t]] != cv[st[0, t]][None, :], axis=1)
+            ref = 0.5 * (cost[other].min() - best)
+            np.testing.assert_allclose(gap[t], ref, rtol=1e-12, atol=1e-12)
+            assert gap[t] >= 0
+
+
+def test_maxmarginal_gap_ignores_states_with_the_same_codeword():
+    """Dyadic codebook with repeated values: a competing path that only
+    changes the state, not the emitted codeword, is not a competitor; with
+    every codeword equal the gap is infinite."""
+    n, k, L = 4, 2, 7
+    r = np.random.default_rng(77)
+    for _ in range(4):
+        c = r.integers(-2, 3, 1 << n) / 4.0
+        w = r.integers(-6, 7, L) / 8.0
+        st, _ = O.viterbi(w[None], c, n, k)
+        gap = O.maxmarginal_gap(w[None], c, n, k, st)[0]
+        P, cost, cv = _path_costs(w, c, n, k)
+        for t in range(L):
+            other = cv[P[:, t], 0] != c[st[0, t]]
+            assert gap[t] == 0.5 * (cost[other].min() - cost.min())
+    const = np.full(1 << n, 0.5)
+    st, _ = O.viterbi(w[None], const, n, k)
+    assert np.all(np.isinf(O.maxmarginal_gap(w[None], const, n, k, st)))
+
+
+def test_maxmarginal_gap_bounds_the_soft_codeword_deviation():
+    """At low T the soft codeword leaves the decoded codeword by at most
+    (number of paths) x max|c_i - c_j| x exp(-gap / T) (every competing path
+    has energy at least gap above the best one), and by at least
+    |c_alt - c*| exp(-gap / T) p* for the best competitor, so the rule that
+    holds a position to the check when gap > T ln(max|dc| / tol) is tied to
+    the Boltzmann weights of Eq. boltzmann."""
+    n, k, L, T = 4, 2, 6, 0.02
+    r = np.random.default_rng(5)
+    c = r.standard_normal(1 << n)
+    w = r.standard_normal(L)
+    st, _ = O.viterbi(w[None], c, n, k)
+    gap = O.maxmarginal_gap(w[None], c, n, k, st)[0]
+    ws = O.soft_codeword(w[None], c, n, k, T)[0][0]
+    npaths = (1 << n) * (1 << k) ** (L - 1)
+    spread = c.max() - c.min()
+    dev = np.abs(ws - c[st[0]])
+    assert np.all(dev <= npaths * spread * np.exp(-gap / T) + 1e-15)
+    mask, _, thr = O.crisp_positions(w[None], c, n, k, T, st, tol=1e-3)
+    np.testing.assert_allclose(thr, T * np.log(spread / 1e-3))
+    assert np.array_equal(mask[0], gap > thr)
