@@ -50,13 +50,22 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 # ALU roofline of the fused kernel: edge-updates/s at full issue of the
-# algorithmic VALU and transcendental work of a K x K group-step.
+# algorithmic VALU and transcendental work of a K x K group-step,
+#   t_group = N_V / R_V + N_T / R_T   clocks per CU (issue serialised),
+# at 256 CUs and 2.4 GHz.  R_V is the published fp32 vector peak, 157.3
+# TFLOP/s = 128 FMA lanes per clock per CU.  R_T, the v_exp/v_log/v_rcp
+# rate, has no published figure: the issue-rate probe (--path rates)
+# measures it live, as lane-operations per second over 256 CUs at the
+# shader clock the probe reads during its own run.  The probe also shows
+# that the two kinds of instruction do not overlap (a 1:1 interleave takes
+# the sum of their times), which is the serialised form above.  A second
+# model prices the same counts at the probe's measured rates for both.
 CUS, CLOCK_HZ = 256, 2.4e9
-VALU_LANES_PER_CLK = 64          # per CU: 4 SIMDs x 16 fp32 lanes (packed fp32 math disabled)
-TRANS_LANES_PER_CLK = 32         # per CU: v_exp/v_log/v_rcp at half rate (measured)
+VALU_LANES_PUBLISHED = 128.0     # per CU and clock: 157.3e12 FLOP/s / (2 FLOP x 256 CUs x 2.4e9)
 # algorithmic work per K x K group-step, K = 4, fwd + w_soft + logZ + dW
 ALG_VALU_PER_GROUP = 97.0
 ALG_TRANS_PER_GROUP = 11.0
+ALG_DC_VALU_PER_GROUP = 24.0     # + dCodebook: 6K more VALU, no transcendental
 EDGES_PER_GROUP = 16.0           # K^2
 # vector-emission trellis (K = 16, V = 2): algorithmic work per state-step,
 # fwd + w_soft + logZ + dW (backward row: 10 VALU + 1 exp per state, 4 VALU and
@@ -65,6 +74,54 @@ EDGES_PER_GROUP = 16.0           # K^2
 ALG_VEC_VALU_PER_STATE = 25.0 + (4.0 + 17.0) / 16.0
 ALG_VEC_TRANS_PER_STATE = 2.0 + 5.0 / 16.0
 EDGES_PER_STATE_VEC = 16.0
+
+# issue-rate probe operations (csrc/issue_rates.hip)
+PROBE_OPS = {"fma_f32": 0, "exp_f32": 1, "log_f32": 2, "rcp_f32": 3, "fma_f64": 4,
+             "fma_exp_1to1": 5, "fma_exp_4to1": 6, "fma_exp_8to1": 7, "add_f32": 8, "max_f32": 9}
+
+
+def issue_rates(iters=16384, grid=2048):
+    """Runs every probe once (timed with HIP events) and returns per-op
+    lane-operations per clock per CU at the shader clock the probe read,
+    R_T (the slowest of v_exp, v_log, v_rcp) and R_V_measured (v_fma_f32)."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2605_10655_amd", "libissue_rates.so"))
+    lib.issue_rate_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_double)]
+    lib.issue_rate_run.restype = ctypes.c_int
+    out = {}
+    for name, op in PROBE_OPS.items():
+        ms, ops, clk = ctypes.c_float(), ctypes.c_double(), ctypes.c_double()
+        rc = lib.issue_rate_run(op, iters, grid, ctypes.byref(ms), ctypes.byref(ops), ctypes.byref(clk))
+        if rc != 0:
+            raise RuntimeError(f"issue-rate probe {name} failed ({rc})")
+        sec = ms.value / 1e3
+        out[name] = {"ms": ms.value, "lane_ops": ops.value, "clock_ghz": clk.value / 1e9,
+                     "lanes_per_clk_cu": ops.value / (sec * CUS * clk.value),
+                     "lane_ops_per_s": ops.value / sec}
+    fma = out["fma_f32"]["lane_ops_per_s"]
+    r_t = min(out[k]["lanes_per_clk_cu"] for k in ("exp_f32", "log_f32", "rcp_f32"))
+    # serialised issue predicts a 1:1 interleave at 1/(1/fma + 1/trans) per pair
+    exp = out["exp_f32"]["lane_ops_per_s"]
+    pair_s = out["fma_exp_1to1"]["ms"] / 1e3
+    pairs = out["fma_exp_1to1"]["lane_ops"] / 2
+    serial_s = pairs / fma + pairs / exp
+    overlap_s = max(pairs / fma, pairs / exp)
+    return {"ops": out, "R_T": r_t, "R_V_measured": out["fma_f32"]["lanes_per_clk_cu"],
+            "fma_exp_1to1_s": pair_s, "serialised_model_s": serial_s,
+            "overlapped_model_s": overlap_s}
+
+
+def roofline_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED, dc=False) -> float:
+    n_v = ALG_VALU_PER_GROUP + (ALG_DC_VALU_PER_GROUP if dc else 0.0)
+    t_group = n_v / r_v + ALG_TRANS_PER_GROUP / r_t
+    return EDGES_PER_GROUP * CUS * CLOCK_HZ / t_group
+
+
+def roofline_vec_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED) -> float:
+    t_state = ALG_VEC_VALU_PER_STATE / r_v + ALG_VEC_TRANS_PER_STATE / r_t
+    return EDGES_PER_STATE_VEC * CUS * CLOCK_HZ / t_state
 
 
 # HBM bytes per launch of the timed kernel, from two rocprofv3 --pmc passes
@@ -93,15 +150,16 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def roofline_edges_per_s() -> float:
-    t_group = (ALG_VALU_PER_GROUP / VALU_LANES_PER_CLK + ALG_TRANS_PER_GROUP / TRANS_LANES_PER_CLK)
-    return EDGES_PER_GROUP * CUS * CLOCK_HZ / t_group
-
-
-def roofline_vec_edges_per_s() -> float:
-    t_state = (ALG_VEC_VALU_PER_STATE / VALU_LANES_PER_CLK
-               + ALG_VEC_TRANS_PER_STATE / TRANS_LANES_PER_CLK)
-    return EDGES_PER_STATE_VEC * CUS * CLOCK_HZ / t_state
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(target_s: float = 15.0):
@@ -129,6 +187,7 @@ def cpu_baseline(target_s: float = 15.0):
         nb, t1 = nb2, time.time() - t0
     edges = nb * wl.L * wl.S * (1 << wl.k)
     return {"value": edges / t1, "unit": "edge-updates/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{nb} blocks of the same matrix (first rows), fwd+logZ+dW, fp64, {t1:.1f} s"}
 
 
@@ -188,7 +247,7 @@ def run_anneal(args):
     print(json.dumps(rec), flush=True)
 
 
-def run_anneal_calls(args):
+def anneal_calls_record(warmup, r_t):
     """The annealed gate/up-projection workload as a sequence of library
     calls: 2048 x 8192 N(0,1) weights as 65536 blocks of 256, S = 65536,
     k = 2, N(0,1) codebook, 8 successive calls of the fused forward + VJP
@@ -197,8 +256,9 @@ def run_anneal_calls(args):
     double-float kernel), then the Viterbi decode of the same blocks, against
     which the last call's soft codeword is checked (the fraction of weights
     whose soft codeword sits within 2e-5 of the minimum-distortion codeword).
-    A step is one call; edges per call are B * L * S * K."""
-    import numpy as np
+    A step is one call; edges per call are B * L * S * K.  The roofline is
+    the fwd + dW + dCodebook model (121 VALU + 11 transcendentals per
+    group-step)."""
     import torch
     import paper_2605_10655_amd as P
     from paper_2605_10655_amd import workloads as WL
@@ -221,11 +281,11 @@ def run_anneal_calls(args):
         P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
                                      dCodebook=dc, workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):  # one call on each kernel (fp32 and double-float)
+    for _ in range(warmup):  # one call on each kernel (fp32 and double-float)
         call(temps[0], gs[0])
         call(temps[-1], gs[-1])
         torch.cuda.synchronize()
-        print("warmup done", file=sys.stderr, flush=True)
+        print("anneal calls: warmup done", file=sys.stderr, flush=True)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in temps]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -236,24 +296,147 @@ def run_anneal_calls(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     call_ms = [a.elapsed_time(b) for a, b in ev]
-    print("per call ms: " + " ".join(f"{x:.0f}" for x in call_ms), file=sys.stderr, flush=True)
+    print("anneal calls: per call ms " + " ".join(f"{x:.0f}" for x in call_ms), file=sys.stderr,
+          flush=True)
     _, w_hard = P.viterbi_decode(w, c, n, k)
     torch.cuda.synchronize()
     agree = float(((w_soft - w_hard).abs() <= 2e-5).float().mean().item())
     edges = len(temps) * B * L * wl.S * (1 << k)
+    peak = roofline_edges_per_s(r_t, dc=True)
+    del ws
+    torch.cuda.empty_cache()
+    return {
+        "value": edges / wall, "unit": "edge-updates/s", "seconds": wall, "call_ms": call_ms,
+        "temps": temps, "B": B, "roofline_peak": peak, "roofline_frac": edges / wall / peak,
+        "final_call_soft_equals_viterbi_frac": agree,
+    }
+
+
+def run_anneal_calls(args):
+    import torch
+    rates = issue_rates()
+    r = anneal_calls_record(args.warmup, rates["R_T"])
     rec = {
         "metric": "trellis edge-updates/s fwd+VJP incl. dCodebook, 8 annealed calls at S=65536,k=2,L=256",
-        "value": edges / wall, "unit": "edge-updates/s", "n_gpus": 1, "steps": len(temps),
-        "warmup": args.warmup, "ms_per_step": wall * 1e3 / len(temps), "higher_is_better": True,
+        "value": r["value"], "unit": "edge-updates/s", "n_gpus": 1, "steps": 8,
+        "warmup": args.warmup, "ms_per_step": r["seconds"] * 1e3 / 8, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32 (double-float log vectors below T=0.04)",
         "data": "synthetic",
         "config": {"workload": "2048x8192 N(0,1) weights as 65536 blocks of L=256; S=65536, k=2, "
                                "N(0,1) codebook; 8 calls of fused w_soft+logZ+dW+dCodebook, "
                                "T 0.1 -> 0.001 geometric, fresh upstream gradient per call",
-                   "B": B, "L": L, "S": wl.S, "k": k, "temps": temps},
-        "seconds": wall, "call_ms": call_ms, "roofline": None,
-        "final_call_soft_equals_viterbi_frac": agree,
+                   "B": r["B"], "L": 256, "S": 65536, "k": 2, "temps": r["temps"]},
+        "seconds": r["seconds"], "call_ms": r["call_ms"],
+        "roofline": {"bound": "alu", "achieved": r["value"] / 1e9, "peak": r["roofline_peak"] / 1e9,
+                     "unit": "Gedge/s", "frac": r["roofline_frac"], "traffic": None,
+                     "model": "121 VALU / 128 lanes + 11 trans / R_T per 16-edge group-step",
+                     "R_T": rates["R_T"]},
+        "final_call_soft_equals_viterbi_frac": r["final_call_soft_equals_viterbi_frac"],
     }
+    print(json.dumps(rec), flush=True)
+
+
+def run_config(args):
+    """Configs 1-3, full batch: one step is the fused call at every listed
+    temperature (w_soft + logZ + dW, with dCodebook for configs 1 and 3,
+    and for config 1 the Viterbi decode too).  Edges per step are the sum
+    over the temperatures of B * L * S * K.  The oracle is timed on every
+    block of the same step (fp64, all host cores)."""
+    import numpy as np
+    import torch
+    import paper_2605_10655_amd as P
+    from paper_2605_10655_amd import workloads as WL
+    from oracle import oracle as O
+    cfg = args.config
+    wl = WL.workload(cfg)
+    torch.zeros(1, device="cuda:0")
+    rates = issue_rates()
+    r_t = rates["R_T"]
+    want_dc = "dc" in wl.outputs
+    want_vit = "viterbi" in wl.outputs
+    n, k, L = wl.state_bits, wl.k, wl.L
+    dev = torch.device("cuda:0")
+    cw, ww, gw = WL.codebook(cfg), WL.weights(cfg), WL.upstream(cfg)
+    w, c, g = (torch.from_numpy(a).to(dev) for a in (ww, cw, gw))
+    B = w.shape[0]
+    w_soft, dW = torch.empty_like(w), torch.empty_like(w)
+    logZ = torch.empty(B, dtype=torch.float32, device=dev)
+    dc = torch.empty_like(c) if want_dc else None
+    states = torch.empty((B, L), dtype=torch.int32, device=dev)
+    w_hard = torch.empty_like(w)
+    ws = torch.empty(max(P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP),
+                         P.bcjr_workspace_bytes(B, L, n, k, P.OP_VITERBI)),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    temps = [float(T) for T in wl.temps]
+
+    def step():
+        for T in temps:
+            P.bcjr_soft_codeword_fwd_vjp(w, c, n, k, T, g, w_soft=w_soft, logZ=logZ, dW=dW,
+                                         dCodebook=dc, want_dCodebook=want_dc, workspace=ws,
+                                         stream=stream)
+        if want_vit:
+            P.viterbi_decode(w, c, n, k, states=states, w_hard=w_hard, workspace=ws, stream=stream)
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    a.record(stream)
+    for _ in range(args.steps):
+        step()
+    b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_s = a.elapsed_time(b) / 1e3 / args.steps
+    edges = len(temps) * wl.edges
+    peak = roofline_edges_per_s(r_t, dc=want_dc)
+    print(f"config {cfg}: {wall * 1e3 / args.steps:.3f} ms/step; timing the oracle on all "
+          f"{B} blocks ...", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for T in temps:
+        O.soft_codeword_vjp(ww, cw, n, k, float(np.float32(T)), gw, want_dc=want_dc)
+    if want_vit:
+        O.viterbi(ww, cw, n, k)
+    cpu_s = time.perf_counter() - t0
+    rec = {
+        "metric": f"trellis edge-updates/s fwd+VJP, config {cfg} ({wl.name})",
+        "value": edges / (wall / args.steps), "unit": "edge-updates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name + "; fused " + "+".join(
+            o for o in wl.outputs if o != "viterbi") + (" + Viterbi" if want_vit else "") +
+            f" at T in {temps}, full batch", "B": B, "L": L, "S": wl.S, "k": k, "temps": temps},
+        "blocks_per_s": B * len(temps) / (wall / args.steps),
+        "roofline": {"bound": "alu", "achieved": edges / kern_s / 1e9, "peak": peak / 1e9,
+                     "unit": "Gedge/s", "frac": edges / kern_s / peak, "traffic": None,
+                     "kernel_ms": kern_s * 1e3, "R_T": r_t},
+        "cpu_baseline": {"value": edges / cpu_s, "unit": "edge-updates/s",
+                         "cores": O.default_threads(), "kind": "oracle", "cpu": cpu_model(),
+                         "sample": f"all {B} blocks, every temperature, {cpu_s:.1f} s"},
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def run_rates(args):
+    """The gfx950 issue-rate probe alone: one JSON line of lane-operations
+    per clock per CU for each probed instruction, the clock the probe read,
+    R_T, and the 1:1 fma + exp interleave against the serialised and
+    overlapped issue models."""
+    import torch
+    torch.zeros(1, device="cuda:0")
+    r = issue_rates()
+    ops = {k: {kk: v[kk] for kk in ("ms", "lanes_per_clk_cu", "clock_ghz", "lane_ops")}
+           for k, v in r["ops"].items()}
+    rec = {"metric": "gfx950 VALU issue rates (lane-ops per clock per CU)", "ops": ops,
+           "R_T": r["R_T"], "R_V_measured": r["R_V_measured"],
+           "fma_exp_1to1_s": r["fma_exp_1to1_s"],
+           "serialised_model_s": r["serialised_model_s"],
+           "overlapped_model_s": r["overlapped_model_s"],
+           "probe": "csrc/issue_rates.hip: 2048 workgroups x 256 lanes, 16384 steps of 8 "
+                    "independent chains per lane"}
     print(json.dumps(rec), flush=True)
 
 
@@ -312,8 +495,14 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec", "anneal", "anneal_calls", "ldlq"),
-                    default="fwd_vjp")
+    ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec", "anneal", "anneal_calls", "ldlq",
+                                       "rates"), default="fwd_vjp")
+    ap.add_argument("--config", type=int, choices=(1, 2, 3, 4, 5), default=4,
+                    help="workload: 4 (default) is the headline S=65536 q/o-projection call; 1-3 "
+                         "the small and mid trellises (full batch, every listed temperature, "
+                         "oracle timed on every block); 5 the 8 annealed gate/up-projection calls")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="headline line only: skip the separate-call and 8-call annealed timings")
     ap.add_argument("--T", type=float, default=None)
     ap.add_argument("--op", choices=("fwd_vjp", "soft", "dc", "viterbi"), default="fwd_vjp",
                     help="call timed on the fwd_vjp and vec paths: the fused w_soft+logZ+dW call "
@@ -365,6 +554,20 @@ def main():
     if args.path == "ldlq":
         run_ldlq(args)
         return
+    if args.path == "rates":
+        run_rates(args)
+        return
+    if args.config == 5:
+        run_anneal_calls(args)
+        return
+    if args.config in (1, 2, 3):
+        run_config(args)
+        return
+    torch.zeros(1, device="cuda:0")
+    rates = issue_rates()
+    print(f"issue rates (lanes/clk/CU): R_T = {rates['R_T']:.2f}, fma "
+          f"{rates['R_V_measured']:.1f} at {rates['ops']['fma_f32']['clock_ghz']:.2f} GHz",
+          file=sys.stderr, flush=True)
     wl = WL.workload(4)
     n, k, L, T = wl.state_bits, wl.k, wl.L, wl.temps[0] if args.T is None else args.T
     ste = args.path == "ste"
@@ -455,7 +658,10 @@ def main():
     value = edges / (ms_per_step / 1e3)
     kern_avg_s = float(np.mean(kernel_ms)) / 1e3
     achieved = edges / kern_avg_s
-    peak = roofline_vec_edges_per_s() if vec else roofline_edges_per_s()
+    r_t = rates["R_T"]
+    peak = roofline_vec_edges_per_s(r_t) if vec else roofline_edges_per_s(r_t)
+    r_vm = rates["R_V_measured"]
+    peak_m = (roofline_vec_edges_per_s(r_t, r_vm) if vec else roofline_edges_per_s(r_t, r_vm))
     print(f"timed {args.steps} steps: {ms_per_step:.1f} ms/step (events avg {kern_avg_s * 1e3:.1f} ms)",
           file=sys.stderr, flush=True)
 
@@ -498,11 +704,48 @@ def main():
             "unit": "Gedge/s", "frac": achieved / peak,
             "traffic": None if (ste or args.T is not None)
             else MEASURED_TRAFFIC.get((args.path, kernel_source_digest())),
-            "kernel_ms": kern_avg_s * 1e3},
+            "kernel_ms": kern_avg_s * 1e3,
+            "model": ("per state-step %.2f VALU / R_V + %.4f trans / R_T" %
+                      (ALG_VEC_VALU_PER_STATE, ALG_VEC_TRANS_PER_STATE)) if vec else
+                     ("per 16-edge group-step %g VALU / R_V + %g trans / R_T at 256 CUs x 2.4 GHz"
+                      % (ALG_VALU_PER_GROUP, ALG_TRANS_PER_GROUP)),
+            "R_V": VALU_LANES_PUBLISHED, "R_T": r_t,
+            "R_V_measured": r_vm, "peak_measured_rates": peak_m / 1e9,
+            "frac_measured_rates": achieved / peak_m},
     }
     if op != "fwd_vjp":
         rec["kernel_ms"] = kern_avg_s * 1e3
-    if not args.no_cpu_baseline and not ste and not vec and args.T is None and op == "fwd_vjp":
+    headline = not ste and not vec and args.T is None and op == "fwd_vjp"
+    if headline and not args.no_extras:
+        # the same work as the autograd node issues it: the soft codeword
+        # call, then the VJP call (dW), each a forward-backward pass
+        sep = []
+        for i in range(args.warmup + 3):
+            a, m, b = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            a.record(stream)
+            P.bcjr_soft_codeword(w, c, n, k, T, w_soft=w_soft, logZ=logZ, workspace=ws, stream=stream)
+            m.record(stream)
+            P.bcjr_soft_codeword_vjp(w, c, n, k, T, g, dW=dW, want_dCodebook=False, workspace=ws,
+                                     stream=stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                sep.append((a.elapsed_time(m), m.elapsed_time(b)))
+        soft_ms = float(np.median([x[0] for x in sep]))
+        vjp_ms = float(np.median([x[1] for x in sep]))
+        rec["separate_calls"] = {"soft_ms": soft_ms, "vjp_ms": vjp_ms, "total_ms": soft_ms + vjp_ms,
+                                 "edges_per_s": edges / ((soft_ms + vjp_ms) / 1e3),
+                                 "what": "bcjr_soft_codeword then bcjr_soft_codeword_vjp (dW), "
+                                         "median of 3"}
+        print(f"separate calls: {soft_ms:.1f} + {vjp_ms:.1f} ms", file=sys.stderr, flush=True)
+        del ws
+        torch.cuda.empty_cache()
+        print("timing the 8 annealed gate/up-projection calls ...", file=sys.stderr, flush=True)
+        rec["anneal_calls"] = anneal_calls_record(1, r_t)
+    if headline:
+        rec["issue_rates"] = {k2: round(v["lanes_per_clk_cu"], 3) for k2, v in rates["ops"].items()}
+        rec["issue_rates"]["clock_ghz"] = rates["ops"]["fma_f32"]["clock_ghz"]
+    if not args.no_cpu_baseline and headline:
         print("timing the oracle on the host cores ...", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline()
     print(json.dumps(rec), flush=True)

@@ -1,4 +1,6 @@
-"""Build the gfx950 shared library libbcjr.so in-tree with hipcc."""
+"""Build the gfx950 shared libraries in-tree with hipcc: libbcjr.so (the
+C ABI of include/bcjr.h) and libissue_rates.so (the VALU issue-rate probe
+the benchmark prices its roofline with)."""
 from __future__ import annotations
 
 import os
@@ -12,6 +14,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libbcjr.so")
 SOURCES = [os.path.join(CSRC, "bcjr_capi.hip")]
+RATES_SRC = os.path.join(CSRC, "issue_rates.hip")
+RATES_LIB = os.path.join(PKG, "libissue_rates.so")
 DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_qat.h", "bcjr_internal.h")] + [
     os.path.join(INCLUDE, "bcjr.h")]
 
@@ -23,24 +27,29 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the gfx950 library cannot be built")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
+def _compile(sources, out, verbose):
+    tmp = out + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
            # packed FP32 math stays off (v_pk_* fp32 forms)
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
            "-Wno-unused-command-line-argument",
-           "-I", INCLUDE, "-I", CSRC, "-o", tmp] + SOURCES
+           "-I", INCLUDE, "-I", CSRC, "-o", tmp] + sources
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
-    out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
-                    if "packed-fp32-ops' is not a recognized feature" not in l)
+    out_text = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
+                         if "packed-fp32-ops' is not a recognized feature" not in l)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{out}")
-    if verbose and out.strip():
-        print(out)
-    os.replace(tmp, LIB)
-    return LIB
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{out_text}")
+    if verbose and out_text.strip():
+        print(out_text)
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    _compile([RATES_SRC], RATES_LIB, verbose)
+    return _compile(SOURCES, LIB, verbose)
 
 
 if __name__ == "__main__":

@@ -1,5 +1,5 @@
-"""bench.py's host-side contract: one GPU only, the roofline constants the
-JSON line is priced against, and the measured-traffic table's keys."""
+"""bench.py's host-side contract: one GPU only, the roofline model the JSON
+line is priced against, and the measured-traffic table's keys."""
 import os
 import subprocess
 import sys
@@ -19,19 +19,27 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 
 
 def test_alu_roofline_of_the_scalar_kernel():
-    # 16 edges per K x K group-step at K = 4; 97 VALU at 64 lanes/clk and 11
-    # transcendentals at 32 lanes/clk per CU; 256 CUs at 2.4 GHz
-    t_group = 97.0 / 64 + 11.0 / 32
-    want = 16 * 256 * 2.4e9 / t_group
-    assert abs(bench.roofline_edges_per_s() - want) <= 1e-9 * want
-    assert abs(want - 5.287e12) <= 1e-3 * 5.287e12
+    # 16 edges per K x K group-step at K = 4; 97 VALU at the published 128
+    # fp32 lanes per clock per CU (157.3 TFLOP/s) and 11 transcendentals at
+    # R_T; 256 CUs at 2.4 GHz.  At R_T = 16 this is 6.80e12 edges/s, at 32
+    # 8.92e12; at 64 lanes and R_T = 32 (round one's model) 5.287e12.
+    assert abs(bench.VALU_LANES_PUBLISHED * 2 * 256 * 2.4e9 - 157.3e12) <= 1e-3 * 157.3e12
+    for r_t, want in ((16.0, 6.80e12), (32.0, 8.92e12)):
+        got = bench.roofline_edges_per_s(r_t)
+        t_group = 97.0 / 128 + 11.0 / r_t
+        assert abs(got - 16 * 256 * 2.4e9 / t_group) <= 1e-9 * got
+        assert abs(got - want) <= 2e-3 * want
+    np_ = bench.roofline_edges_per_s(32.0, 64.0)
+    assert abs(np_ - 5.287e12) <= 1e-3 * 5.287e12
+    # the dCodebook variant adds 6K = 24 VALU per group-step
+    dc = bench.roofline_edges_per_s(16.0, dc=True)
+    assert abs(dc - 16 * 256 * 2.4e9 / (121.0 / 128 + 11.0 / 16)) <= 1e-9 * dc
 
 
 def test_alu_roofline_of_the_vector_kernel():
-    t_state = (25.0 + 21.0 / 16) / 64 + (2.0 + 5.0 / 16) / 32
+    t_state = (25.0 + 21.0 / 16) / 128 + (2.0 + 5.0 / 16) / 32
     want = 16 * 256 * 2.4e9 / t_state
-    assert abs(bench.roofline_vec_edges_per_s() - want) <= 1e-9 * want
-    assert abs(want - 2.034e13) <= 1e-3 * 2.034e13
+    assert abs(bench.roofline_vec_edges_per_s(32.0) - want) <= 1e-9 * want
 
 
 def test_measured_traffic_is_keyed_by_path_and_source_digest():
