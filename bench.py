@@ -80,7 +80,7 @@ PROBE_OPS = {"fma_f32": 0, "exp_f32": 1, "log_f32": 2, "rcp_f32": 3, "fma_f64": 
              "fma_exp_1to1": 5, "fma_exp_4to1": 6, "fma_exp_8to1": 7, "add_f32": 8, "max_f32": 9}
 
 
-def issue_rates(iters=16384, grid=2048):
+def issue_rates(iters=16384, grid=2048, ops=None):
     """Runs every probe once (timed with HIP events) and returns per-op
     lane-operations per clock per CU at the shader clock the probe read,
     R_T (the slowest of v_exp, v_log, v_rcp) and R_V_measured (v_fma_f32)."""
@@ -92,14 +92,18 @@ def issue_rates(iters=16384, grid=2048):
     lib.issue_rate_run.restype = ctypes.c_int
     out = {}
     for name, op in PROBE_OPS.items():
-        ms, ops, clk = ctypes.c_float(), ctypes.c_double(), ctypes.c_double()
-        rc = lib.issue_rate_run(op, iters, grid, ctypes.byref(ms), ctypes.byref(ops), ctypes.byref(clk))
+        if ops is not None and name not in ops:
+            continue
+        ms, cnt, clk = ctypes.c_float(), ctypes.c_double(), ctypes.c_double()
+        rc = lib.issue_rate_run(op, iters, grid, ctypes.byref(ms), ctypes.byref(cnt), ctypes.byref(clk))
         if rc != 0:
             raise RuntimeError(f"issue-rate probe {name} failed ({rc})")
         sec = ms.value / 1e3
-        out[name] = {"ms": ms.value, "lane_ops": ops.value, "clock_ghz": clk.value / 1e9,
-                     "lanes_per_clk_cu": ops.value / (sec * CUS * clk.value),
-                     "lane_ops_per_s": ops.value / sec}
+        out[name] = {"ms": ms.value, "lane_ops": cnt.value, "clock_ghz": clk.value / 1e9,
+                     "lanes_per_clk_cu": cnt.value / (sec * CUS * clk.value),
+                     "lane_ops_per_s": cnt.value / sec}
+    if ops is not None:
+        return {"ops": out}
     fma = out["fma_f32"]["lane_ops_per_s"]
     r_t = min(out[k]["lanes_per_clk_cu"] for k in ("exp_f32", "log_f32", "rcp_f32"))
     # serialised issue predicts a 1:1 interleave at 1/(1/fma + 1/trans) per pair
@@ -424,9 +428,17 @@ def run_rates(args):
     """The gfx950 issue-rate probe alone: one JSON line of lane-operations
     per clock per CU for each probed instruction, the clock the probe read,
     R_T, and the 1:1 fma + exp interleave against the serialised and
-    overlapped issue models."""
+    overlapped issue models.  Then one line per occupancy: grids of 256 to
+    4096 workgroups of 4 waves are 1 to 16 waves per SIMD."""
     import torch
     torch.zeros(1, device="cuda:0")
+    for grid in (256, 512, 1024, 2048, 4096):
+        r = issue_rates(grid=grid, ops=("fma_f32", "add_f32", "exp_f32", "fma_f64", "fma_exp_1to1"))
+        print(json.dumps({"grid": grid, "waves_per_simd": grid // 256,
+                          "lanes_per_clk_cu": {k: round(v["lanes_per_clk_cu"], 2)
+                                               for k, v in r["ops"].items()},
+                          "clock_ghz": {k: round(v["clock_ghz"], 3) for k, v in r["ops"].items()}}),
+              flush=True)
     r = issue_rates()
     ops = {k: {kk: v[kk] for kk in ("ms", "lanes_per_clk_cu", "clock_ghz", "lane_ops")}
            for k, v in r["ops"].items()}

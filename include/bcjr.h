@@ -34,13 +34,17 @@
  *     that may run concurrently.
  *   - Calls are asynchronous on `stream`; the returned status covers argument
  *     validation and launch errors only.  No exception crosses the ABI.
- *   - Supported shapes: 1 <= k <= 3 and 2k <= state_bits <= min(16, 2k + 12),
- *     and for k = 3 also state_bits <= 14 (k = 1: 2..14, k = 2: 4..16,
- *     k = 3: 6..14), and L small enough that one workgroup's histories
- *     stay below 2 GiB: the soft codeword and Viterbi take L <= 16383 at
- *     state_bits = 16, k = 2 (at least 16383 for every supported shape),
- *     the VJP L <= 10922 (at least 10922).  Other valid shapes return
- *     BCJR_ERR_UNSUPPORTED and a workspace size of 0.
+ *   - Shapes: every 1 <= k <= state_bits <= 16.  The fp32 super-group
+ *     kernels (double-float log vectors for the VJP below T = 0.04) take
+ *     1 <= k <= 3 with 2k <= state_bits <= min(16, 2k + 12) and, for k = 3,
+ *     state_bits <= 14 (k = 1: 2..14, k = 2: 4..16, k = 3: 6..14), with L
+ *     small enough that one workgroup's histories stay below 2 GiB: the
+ *     soft codeword and Viterbi take L <= 16383 at state_bits = 16, k = 2
+ *     (at least 16383 for every such shape), the VJP L <= 10922 (at least
+ *     10922).  Every other shape -- state_bits < 2k down to the fully
+ *     connected state_bits = k, k >= 4, k = 1 at 15 and 16 state bits, k = 3
+ *     above 14 -- runs fp64 kernels at any temperature, with L <= 2^30.
+ *     Longer L returns BCJR_ERR_UNSUPPORTED and a workspace size of 0.
  *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
  *   - Non-finite w or codebook values give non-finite outputs; they are not
  *     checked.

@@ -9,6 +9,7 @@
 
 #include "bcjr.h"
 #include "bcjr_internal.h"
+#include "bcjr_generic_kernels.h"
 #include "bcjr_kernels.h"
 #include "bcjr_vec_kernels.h"
 #include "bcjr_qat.h"
@@ -31,6 +32,9 @@ struct Family {
   int occ_est = 0;  // workgroups per CU assumed by the workspace query
 };
 
+// Shapes of the super-group families (fp32 / double-float, LDS-resident
+// group vectors); every other 1 <= k <= n <= 16 runs the fp64 generic
+// family of bcjr_generic_kernels.h.
 bool supported(int n, int k) {
   if (k < 1 || k > 3 || n < 2 * k || n > 16) return false;
   const int nsg_bits = n - 2 * k;
@@ -83,6 +87,7 @@ bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double
 // offsets: blocks per workgroup x L x S/K x (8 bytes, 12 for the VJP, whose
 // low-temperature variant keeps three words per group) below 2^31.
 bool length_ok(int64_t L, int n, int k, bool vjp) {
+  if (!supported(n, k)) return L <= ((int64_t)1 << 30);  // generic family: 64-bit offsets
   const Family f = family(n, k, false);
   const int64_t per_step = (int64_t)f.bpw * (vjp ? 12 : 8) * ((int64_t)1 << (n - k));
   return L <= 0x7FFFFFFF / per_step;
@@ -242,7 +247,7 @@ int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, i
   if (B > 0 && (!w || !codebook)) return BCJR_ERR_INVALID_ARG;
   if (codebook && ((uintptr_t)codebook & 15u)) return BCJR_ERR_INVALID_ARG;
   if (w && ((uintptr_t)w & 3u)) return BCJR_ERR_INVALID_ARG;
-  if (!supported(n, k) || !length_ok(L, n, k, vjp)) return BCJR_ERR_UNSUPPORTED;
+  if (!length_ok(L, n, k, vjp)) return BCJR_ERR_UNSUPPORTED;
   return BCJR_OK;
 }
 
@@ -281,10 +286,82 @@ int fill_zero(float* p, int64_t count, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+// ------------------------------------------------------------ generic family
+constexpr int kGenOccEst = 4;  // workgroups per CU assumed by the workspace query
+
+// doubles per slot: H and (VJP) B histories, four group vectors, and with
+// the VJP the fp64 dCodebook partial (a VJP workspace always has room for it)
+int64_t gen_slot_doubles(int64_t L, int n, int k, bool vjp) {
+  const int64_t GS = (int64_t)1 << (n - k);
+  return (vjp ? 2 : 1) * L * GS + 4 * GS + (vjp ? ((int64_t)1 << n) : 0);
+}
+
+// Viterbi: two metric vectors of doubles, then the digits of every slot
+int64_t gen_vit_slot_bytes(int64_t L, int n, int k) {
+  const int64_t GS = (int64_t)1 << (n - k);
+  return 2 * GS * (int64_t)sizeof(double) + L * GS * (int64_t)sizeof(uint16_t);
+}
+
+int run_gen(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
+            const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
+            void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
+  const bool dc = vjp && dCodebook != nullptr;
+  using Fn = void (*)(GenArgs);
+  Fn fn = !vjp ? gen_fb_kernel<false, false> : (dc ? gen_fb_kernel<true, true> : gen_fb_kernel<true, false>);
+  Family f;
+  f.nt = kGenThreads;
+  f.bpw = 1;
+  const int64_t slot_d = gen_slot_doubles(L, n, k, vjp);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)fn, f, 0, B, ws_bytes, (size_t)slot_d * sizeof(double), &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  GenArgs a = {};
+  a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L; a.n = n; a.k = k;
+  a.inv2T = 1.0 / (2.0 * (double)T);
+  a.invT = 1.0 / (double)T;
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW; a.dc = dCodebook;
+  a.ws = static_cast<double*>(workspace);
+  a.slot_doubles = slot_d;
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(kGenThreads), 0, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dc) {
+    const int64_t S = (int64_t)1 << n;
+    hipLaunchKernelGGL(gen_dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, a,
+                       grid);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
+int run_gen_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
+                    int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
+                    hipStream_t stream) {
+  Family f;
+  f.nt = kGenThreads;
+  f.bpw = 1;
+  const int64_t slot = gen_vit_slot_bytes(L, n, k);
+  int herr = 0;
+  const int64_t grid = grid_size((const void*)gen_viterbi_kernel, f, 0, B, ws_bytes, (size_t)slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const int64_t GS = (int64_t)1 << (n - k);
+  GenArgs a = {};
+  a.w = w; a.c = codebook; a.B = B; a.L = L; a.n = n; a.k = k;
+  a.states = states; a.w_hard = w_hard;
+  a.ws = static_cast<double*>(workspace);
+  a.slot_doubles = 2 * GS;
+  a.bp = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + grid * 2 * GS * (int64_t)sizeof(double));
+  hipLaunchKernelGGL(gen_viterbi_kernel, dim3((unsigned)grid), dim3(kGenThreads), 0, stream, a);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
 int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
                 int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
                 hipStream_t stream) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  if (!supported(n, k))
+    return run_gen_viterbi(w, B, L, codebook, n, k, states, w_hard, workspace, ws_bytes, stream);
   const Family f = family(n, k, false);
   VitFn fn = vit_pick(n, k, f);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
@@ -369,6 +446,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
            const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
            float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
+  if (!supported(n, k))
+    return run_gen(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace, ws_bytes,
+                   stream, vjp);
   if (vjp && use_high_precision(T))
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
@@ -711,9 +791,15 @@ extern "C" {
 
 size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op) {
   if (B < 0 || L < 1 || k < 1 || state_bits < k || state_bits > 16) return 0;
-  if (!supported(state_bits, k) || !length_ok(L, state_bits, k, op != BCJR_OP_FWD && op != BCJR_OP_VITERBI))
-    return 0;
+  if (!length_ok(L, state_bits, k, op != BCJR_OP_FWD && op != BCJR_OP_VITERBI)) return 0;
   if (B == 0) return 0;
+  if (op != BCJR_OP_FWD && op != BCJR_OP_VJP && op != BCJR_OP_FWD_VJP && op != BCJR_OP_VITERBI)
+    return 0;
+  if (!supported(state_bits, k)) {
+    const int64_t grid = std::min<int64_t>(B, (int64_t)kDeviceCUs * kGenOccEst);
+    if (op == BCJR_OP_VITERBI) return (size_t)(grid * gen_vit_slot_bytes(L, state_bits, k));
+    return (size_t)(grid * gen_slot_doubles(L, state_bits, k, op != BCJR_OP_FWD)) * sizeof(double);
+  }
   if (op == BCJR_OP_VITERBI) {
     const Family f = family(state_bits, k, false);
     const int64_t grid = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);

@@ -1794,7 +1794,8 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
     if (tb == 0 && valid) {
       int32_t* st = a.states + bb * L;
       float* wh = a.w_hard ? a.w_hard + bb * L : nullptr;
-      int s = besti;
+      // (non-finite inputs leave no state below +inf: start from state 0)
+      int s = (unsigned)besti < (unsigned)(GS << KB) ? besti : 0;
       st[L - 1] = s;
       if (wh) wh[L - 1] = a.c[s];
       for (int64_t t = L - 1; t >= 1; --t) {

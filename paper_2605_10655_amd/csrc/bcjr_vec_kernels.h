@@ -1008,7 +1008,8 @@ __global__ void __launch_bounds__(NT) vitv_kernel(VitvArgs a) {
     if (tb == 0 && valid) {
       int32_t* st = a.states + bb * N;
       float* wh = a.w_hard ? a.w_hard + bb * L : nullptr;
-      int s = besti;
+      // (non-finite inputs leave no state below +inf: start from state 0)
+      int s = (unsigned)besti < (unsigned)(GS * 16) ? besti : 0;
       st[N - 1] = s;
       if (wh) {
         wh[2 * (N - 1)] = a.c[2 * s];

@@ -53,7 +53,7 @@ def test_workspace_bytes_host_arithmetic(lib):
     assert ws(10, 0, 4, 2, P.OP_FWD) == 0
     assert ws(10, 16, 4, 5, P.OP_FWD) == 0
     assert ws(10, 16, 17, 2, P.OP_FWD) == 0
-    assert ws(10, 16, 3, 2, P.OP_FWD) == 0          # n < 2k: unsupported
+    assert ws(10, 16, 4, 2, P.OP_FWD) > 0
     assert ws(0, 16, 4, 2, P.OP_FWD) == 0
     assert ws(10, 16, 4, 2, 9) == 0
     # supported shapes give positive sizes that grow with L and with the VJP
@@ -63,7 +63,19 @@ def test_workspace_bytes_host_arithmetic(lib):
         assert 0 < f < v
         assert ws(100, 64, n, k, P.OP_FWD) > f
         assert ws(100, 32, n, k, P.OP_VITERBI) > 0
-    assert ws(100, 32, 15, 3, P.OP_FWD) == 0           # k = 3 stops at 14 state bits
+    # every 1 <= k <= n <= 16: the super-group families, or the fp64 generic
+    # family (n < 2k, k >= 4, k = 1 at 15-16 bits, k = 3 above 14)
+    for n in range(1, 17):
+        for k in range(1, n + 1):
+            for op in (P.OP_FWD, P.OP_VJP, P.OP_FWD_VJP, P.OP_VITERBI):
+                assert ws(4, 8, n, k, op) > 0, (n, k, op)
+    # generic family: H and B histories of L x S/K doubles, four group
+    # vectors, the S-entry dCodebook partial, per slot; one slot per block here
+    L, n, k = 8, 6, 4
+    assert ws(3, L, n, k, P.OP_FWD_VJP) == 3 * 8 * (2 * L * 4 + 4 * 4 + 64)
+    assert ws(3, L, n, k, P.OP_FWD) == 3 * 8 * (L * 4 + 4 * 4)
+    assert ws(3, L, n, k, P.OP_VITERBI) == 3 * (2 * 4 * 8 + L * 4 * 2)
+    assert ws(1, (1 << 30) + 1, 3, 2, P.OP_FWD) == 0   # generic family: L up to 2^30
     # 32-bit history offsets: one workgroup's histories below 2 GiB
     assert ws(4, 16383, 16, 2, P.OP_FWD) > 0
     assert ws(4, 16383, 16, 2, P.OP_VITERBI) > 0
@@ -100,9 +112,10 @@ def test_soft_codeword_argument_validation(lib):
     assert _soft(lib, out=None) == E
     assert _soft(lib, c=MISALIGNED) == E
     assert _soft(lib, w=FAKE + 2) == E
-    assert _soft(lib, n=3, k=2) == -2                 # valid but unsupported
-    assert _soft(lib, n=16, k=1) == -2
-    assert _soft(lib, n=16, k=4) == -2
+    assert _soft(lib, n=3, k=2) == -3                 # generic family: needs a workspace
+    assert _soft(lib, n=16, k=1) == -3
+    assert _soft(lib, n=16, k=4) == -3
+    assert _soft(lib, n=3, k=2, L=(1 << 30) + 1) == -2  # beyond the generic family's L
     assert _soft(lib, n=16, k=2, L=16384) == -2       # history offsets past 2^31 bytes
     assert _soft(lib, ws=None) == -3                  # no workspace
     assert _soft(lib, ws=FAKE + 8, wsb=1 << 20) == -3  # misaligned workspace
@@ -125,14 +138,15 @@ def test_vjp_and_viterbi_argument_validation(lib):
     assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE + 2, FAKE, FAKE, None, None, 0, None) == -1
     assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, None, FAKE, None, None, 0, None) == -1  # grad
     assert st(FAKE, 4, 8, FAKE, 4, 2, -1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -1
-    assert st(FAKE, 4, 8, FAKE, 3, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -2
+    assert st(FAKE, 4, (1 << 30) + 1, FAKE, 3, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -2
+    assert st(FAKE, 4, 8, FAKE, 3, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -3
     assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, FAKE, FAKE, None, None, 0, None) == -3
     assert st(FAKE, 4, 8, FAKE, 4, 2, 1.0, FAKE, FAKE, None, None, None, 0, None) == 0
     assert st(FAKE, 0, 8, FAKE, 4, 2, 1.0, None, None, None, None, None, 0, None) == 0
     vd = lib.viterbi_decode
     assert vd(FAKE, 4, 8, FAKE, 4, 2, None, None, FAKE, 1 << 20, None) == -1
     assert vd(FAKE, 4, 8, FAKE, 4, 2, FAKE, None, None, 0, None) == -3
-    assert vd(FAKE, 4, 8, FAKE, 3, 2, FAKE, None, FAKE, 1 << 20, None) == -2
+    assert vd(FAKE, 4, (1 << 30) + 1, FAKE, 3, 2, FAKE, None, FAKE, 1 << 20, None) == -2
     assert vd(FAKE, 0, 8, FAKE, 4, 2, FAKE, None, None, 0, None) == 0
 
 
