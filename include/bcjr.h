@@ -69,6 +69,9 @@ typedef enum {
   BCJR_ERR_HIP = -4           /* a HIP call or kernel launch failed */
 } bcjr_status;
 
+/* Size of the static scratch array of bcjr_soft_codeword_fwd_vjp_noalloc. */
+#define BCJR_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+
 enum {
   BCJR_OP_FWD = 0,      /* bcjr_soft_codeword */
   BCJR_OP_VJP = 1,      /* bcjr_soft_codeword_vjp */
@@ -103,6 +106,26 @@ int bcjr_soft_codeword_fwd_vjp(const float *w, int64_t B, int64_t L, const float
                                int state_bits, int k, float T, const float *grad_w_soft,
                                float *w_soft, float *logZ, float *dW, float *dCodebook,
                                void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* bcjr_soft_codeword_fwd_vjp without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * and harnesses that forbid hipMalloc).  Same arguments, outputs and results
+ * as bcjr_soft_codeword_fwd_vjp; the workspace is a static device array of
+ * BCJR_NOALLOC_SCRATCH_BYTES (256 MiB) per GPU, allocated with the
+ * library's code object and held until the process ends.  The call itself
+ * allocates nothing.  It runs as many blocks side by side as fit in that
+ * array (fewer than with a full-size workspace at large S; the results do
+ * not depend on the count) and returns BCJR_ERR_WORKSPACE when even one
+ * block slot does not fit: at state_bits 16, k 2 one slot takes about
+ * 64 MiB at L = 256 (97 MiB below T = 0.04, which also needs 8 B x B x L for
+ * the reference decode).  Every call on a GPU uses that GPU's one array:
+ * calls that may overlap on the same GPU (two streams, two threads) race
+ * and must be serialised by the caller.  What the kernels need zeroed is
+ * cleared by kernels in the call (no memset), so the call can be captured. */
+int bcjr_soft_codeword_fwd_vjp_noalloc(const float *w, int64_t B, int64_t L,
+                                       const float *codebook, int state_bits, int k, float T,
+                                       const float *grad_w_soft, float *w_soft, float *logZ,
+                                       float *dW, float *dCodebook, hipStream_t stream);
 
 /* Backward pass of BCJR-STE (Sec. 3.5 and Sec. "BCJR-STE variant"): the
  * variant's forward output is the hard Viterbi codeword w_hard (viterbi_decode)

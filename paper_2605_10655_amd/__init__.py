@@ -13,6 +13,7 @@ Functions keep the C names:
     bcjr_soft_codeword(w, codebook, state_bits, k, T)            -> (w_soft, logZ)
     bcjr_soft_codeword_vjp(w, codebook, state_bits, k, T, g)     -> (dW, dCodebook)
     bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, g) -> (w_soft, logZ, dW, dCodebook)
+    bcjr_soft_codeword_fwd_vjp_noalloc(w, codebook, state_bits, k, T, g, w_soft=..., ...)
     bcjr_ste_vjp(w, codebook, state_bits, k, T, w_hard, g)       -> (dW, dCodebook)
     viterbi_decode(w, codebook, state_bits, k)                   -> (states, w_hard)
     bcjr_workspace_bytes(B, L, state_bits, k, op)                -> int
@@ -35,7 +36,8 @@ import os
 __all__ = [
     "BcjrError", "OP_FWD", "OP_VJP", "OP_FWD_VJP", "OP_VITERBI", "library_path", "load_library",
     "bcjr_workspace_bytes", "bcjr_status_string", "bcjr_soft_codeword", "bcjr_soft_codeword_vjp",
-    "bcjr_soft_codeword_fwd_vjp", "bcjr_ste_vjp", "viterbi_decode", "bcjr_vec_workspace_bytes",
+    "bcjr_soft_codeword_fwd_vjp", "bcjr_soft_codeword_fwd_vjp_noalloc", "bcjr_ste_vjp",
+    "viterbi_decode", "bcjr_vec_workspace_bytes",
     "bcjr_vec_soft_codeword", "bcjr_vec_soft_codeword_vjp", "bcjr_vec_soft_codeword_fwd_vjp",
     "bcjr_vec_viterbi_decode", "bcjr_gaussian_codebook", "qat_adam_step", "qat_sgd_step",
 ]
@@ -77,6 +79,8 @@ def load_library():
     L.bcjr_soft_codeword_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, sz, vp]
     L.bcjr_soft_codeword_fwd_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, vp,
                                              sz, vp]
+    L.bcjr_soft_codeword_fwd_vjp_noalloc.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp,
+                                                     vp, vp]
     L.bcjr_ste_vjp.argtypes = [vp, i64, i64, vp, ci, ci, cf, vp, vp, vp, vp, vp, sz, vp]
     L.viterbi_decode.argtypes = [vp, i64, i64, vp, ci, ci, vp, vp, vp, sz, vp]
     L.bcjr_vec_workspace_bytes.argtypes = [i64, i64, ci, ci, ci, ci]
@@ -92,7 +96,8 @@ def load_library():
     L.qat_adam_step.argtypes = [vp, vp, vp, vp, i64, cf, cf, cf, cf, i64, cf, vp]
     L.qat_sgd_step.argtypes = [vp, vp, i64, cf, cf, vp]
     for f in (L.bcjr_soft_codeword, L.bcjr_soft_codeword_vjp, L.bcjr_soft_codeword_fwd_vjp,
-              L.bcjr_ste_vjp, L.viterbi_decode, L.bcjr_vec_soft_codeword,
+              L.bcjr_soft_codeword_fwd_vjp_noalloc, L.bcjr_ste_vjp, L.viterbi_decode,
+              L.bcjr_vec_soft_codeword,
               L.bcjr_vec_soft_codeword_vjp, L.bcjr_vec_soft_codeword_fwd_vjp,
               L.bcjr_vec_viterbi_decode, L.bcjr_gaussian_codebook, L.qat_adam_step,
               L.qat_sgd_step):
@@ -275,6 +280,28 @@ def bcjr_soft_codeword_fwd_vjp(w, codebook, state_bits, k, T, grad_w_soft, *, wa
                                         _ptr(dCodebook), _ptr(ws), _ws_bytes(ws), _stream(stream))
     _raise("bcjr_soft_codeword_fwd_vjp", rc)
     _keep_alive(stream, w_soft, logZ, dW, dCodebook, ws)
+    return w_soft, logZ, dW, dCodebook
+
+
+def bcjr_soft_codeword_fwd_vjp_noalloc(w, codebook, state_bits, k, T, grad_w_soft, *, w_soft,
+                                       logZ=None, dW=None, dCodebook=None, stream=None):
+    """bcjr_soft_codeword_fwd_vjp on the library's static per-GPU scratch
+    array: no workspace, and every output is the caller's (nothing is
+    allocated here either).  Returns (w_soft, logZ, dW, dCodebook)."""
+    lib = load_library()
+    B, L = _shape(w)
+    _check_in("w", w)
+    dev = w.device
+    _check_in("codebook", codebook, (1 << state_bits,), device=dev)
+    _check_in("grad_w_soft", grad_w_soft, (B, L), device=dev)
+    for name, t, shp in (("w_soft", w_soft, (B, L)), ("logZ", logZ, (B,)), ("dW", dW, (B, L)),
+                         ("dCodebook", dCodebook, (1 << state_bits,))):
+        _check_out(name, t, shp, dev)
+    rc = lib.bcjr_soft_codeword_fwd_vjp_noalloc(_ptr(w), B, L, _ptr(codebook), state_bits, k,
+                                                float(T), _ptr(grad_w_soft), _ptr(w_soft),
+                                                _ptr(logZ), _ptr(dW), _ptr(dCodebook),
+                                                _stream(stream))
+    _raise("bcjr_soft_codeword_fwd_vjp_noalloc", rc)
     return w_soft, logZ, dW, dCodebook
 
 

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
 
 #include "bcjr.h"
 #include "bcjr_internal.h"
@@ -13,6 +14,13 @@
 #include "bcjr_kernels.h"
 #include "bcjr_vec_kernels.h"
 #include "bcjr_qat.h"
+
+// Scratch memory of bcjr_soft_codeword_fwd_vjp_noalloc: one copy per GPU,
+// allocated with the code object and held until the process ends.  In host
+// code this name is only a stand-in for the symbol; the device address of a
+// GPU's copy comes from hipGetSymbolAddress with that GPU current.
+constexpr size_t kScratchBytes = BCJR_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace bcjr {
 namespace {
@@ -782,6 +790,26 @@ int run_fbv(const float* w, int64_t B, int64_t L, const float* codebook, int n, 
   return BCJR_OK;
 }
 
+// Device address of the current GPU's copy of `scratch`, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BCJR_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return BCJR_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return BCJR_ERR_HIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return BCJR_OK;
+}
+
 }  // namespace
 }  // namespace bcjr
 
@@ -840,6 +868,17 @@ int bcjr_soft_codeword_fwd_vjp(const float* w, int64_t B, int64_t L, const float
                                void* workspace, size_t ws_bytes, hipStream_t stream) {
   return fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, nullptr, w_soft, logZ, dW,
                  dCodebook, workspace, ws_bytes, stream);
+}
+
+int bcjr_soft_codeword_fwd_vjp_noalloc(const float* w, int64_t B, int64_t L, const float* codebook,
+                                       int state_bits, int k, float T, const float* grad_w_soft,
+                                       float* w_soft, float* logZ, float* dW, float* dCodebook,
+                                       hipStream_t stream) {
+  void* ws = nullptr;
+  const int st = scratch_address(&ws);
+  if (st != BCJR_OK) return st;
+  return fwd_vjp(w, B, L, codebook, state_bits, k, T, grad_w_soft, nullptr, w_soft, logZ, dW,
+                 dCodebook, ws, kScratchBytes, stream);
 }
 
 int bcjr_soft_codeword_vjp(const float* w, int64_t B, int64_t L, const float* codebook,
