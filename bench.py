@@ -80,10 +80,13 @@ PROBE_OPS = {"fma_f32": 0, "exp_f32": 1, "log_f32": 2, "rcp_f32": 3, "fma_f64": 
              "fma_exp_1to1": 5, "fma_exp_4to1": 6, "fma_exp_8to1": 7, "add_f32": 8, "max_f32": 9}
 
 
-def issue_rates(iters=16384, grid=2048, ops=None):
+def issue_rates(iters=16384, grid=4096, ops=None):
     """Runs every probe once (timed with HIP events) and returns per-op
     lane-operations per clock per CU at the shader clock the probe read,
-    R_T (the slowest of v_exp, v_log, v_rcp) and R_V_measured (v_fma_f32)."""
+    R_T (the slowest of v_exp, v_log, v_rcp) and R_V_measured (v_fma_f32).
+    The default grid, 4096 workgroups of 4 waves, is the occupancy at which
+    the probe measured the highest rates (1 to 16 waves per SIMD swept by
+    --path rates)."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2605_10655_amd", "libissue_rates.so"))
     lib.issue_rate_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -131,21 +134,21 @@ def roofline_vec_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED) -> float:
 # HBM bytes per launch of the timed kernel, from two rocprofv3 --pmc passes
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map a plain 1 GiB
 # device copy's readings to its 1 GiB read and written), keyed by a digest of
-# the kernel sources they were taken on.  Any other source reports null.
-# Keyed by (path, digest).
+# the sources that define that kernel (its header and the argument block).
+# Any other source reports null.
 MEASURED_TRAFFIC = {
-    ("fwd_vjp", "bb229c0eb73cbd28"): 2.68521e8 * 1024 * 2.0 + 5.34821e8 * 1024 * 1.0,
-    ("vec", "bb229c0eb73cbd28"): 3.38238e7 * 1024 * 2.0 + 6.73976e7 * 1024 * 1.0,
+    ("fwd_vjp", "05062e6e985116e7"): 2.68521e8 * 1024 * 2.0 + 5.34832e8 * 1024 * 1.0,
 }
-KERNEL_SOURCES = ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_capi.hip", "bcjr_internal.h")
+KERNEL_SOURCES = {"fwd_vjp": ("bcjr_kernels.h", "bcjr_internal.h"),
+                  "vec": ("bcjr_vec_kernels.h", "bcjr_internal.h")}
 
 
-def kernel_source_digest() -> str:
-    """SHA-256 (16 hex) of the kernel sources with comments and blank space removed."""
+def kernel_source_digest(path: str = "fwd_vjp") -> str:
+    """SHA-256 (16 hex) of a path's kernel sources with comments and blank space removed."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in KERNEL_SOURCES[path]:
         with open(os.path.join(ROOT, "paper_2605_10655_amd", "csrc", name)) as f:
             text = f.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
@@ -715,7 +718,7 @@ def main():
             "bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9,
             "unit": "Gedge/s", "frac": achieved / peak,
             "traffic": None if (ste or args.T is not None)
-            else MEASURED_TRAFFIC.get((args.path, kernel_source_digest())),
+            else MEASURED_TRAFFIC.get((args.path, kernel_source_digest(args.path))),
             "kernel_ms": kern_avg_s * 1e3,
             "model": ("per state-step %.2f VALU / R_V + %.4f trans / R_T" %
                       (ALG_VEC_VALU_PER_STATE, ALG_VEC_TRANS_PER_STATE)) if vec else

@@ -192,6 +192,43 @@ int bcjr_vec_viterbi_decode(const float *w, int64_t B, int64_t L, const float *c
                             void *workspace, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------
+ * Hessian-weighted rounding (the PTQ reference of the paper's oracle-bound
+ * appendix: the loss L_HW = 1/2 tr((W - W_hat) H (W - W_hat)^T) of Eq. LHW,
+ * minimised BlockLDLQ-style as in Eq. WPTQ).  All arithmetic is fp64 on the
+ * device except the targets handed to the decode (fp32).
+ *
+ * Block LDL: with H' = H + damp * mean(diag H) * I (H symmetric positive
+ * definite, [d, d] fp32 row-major), H' = M D M^T where M is unit block-upper-
+ * triangular and D block-diagonal, blocks of `block` indices: from the upper
+ * Cholesky factor H' = R R^T (the lower factor of the index-reversed matrix),
+ * M = R blockdiag(R_kk)^{-1}, D = blockdiag(R_kk R_kk^T).  M and D are
+ * [d, d] fp64 row-major outputs (D may be NULL).  d must be a multiple of
+ * block, d <= 2^20, damp >= 0.  A matrix that is not positive definite after
+ * damping gives NaN entries (not reported by the status).  Workspace:
+ * bcjr_block_ldl_workspace_bytes(d, block) bytes (0 for invalid sizes). */
+size_t bcjr_block_ldl_workspace_bytes(int64_t d, int64_t block);
+int bcjr_block_ldl(const float *H, int64_t d, int64_t block, double damp, double *M, double *D,
+                   void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* BlockLDLQ rounding of W [rows, cols] (fp32 row-major) to trellis
+ * codewords: the column blocks k = 0, 1, ... of `block` columns are decoded
+ * in order, block k as the minimum-distortion path (viterbi_decode, or
+ * bcjr_vec_viterbi_decode for V > 1) of its target
+ *     t_k = W[:, k] + sum_{j < k} (W - W_hat)[:, j] M_jk
+ * (fp64 sums rounded to fp32), M from bcjr_block_ldl of H [cols, cols] with
+ * damp.  Outputs: W_hat [rows, cols] fp32; states [cols / block, rows,
+ * block / V] int32; targets [cols / block, rows, block] fp32 or NULL.  The
+ * (state_bits, k, V) shapes are those of the decode; cols must be a multiple
+ * of block and block of V.  Workspace: bcjr_ldlq_workspace_bytes(rows, cols,
+ * block, state_bits, k, V) bytes (0 for invalid or unsupported shapes). */
+size_t bcjr_ldlq_workspace_bytes(int64_t rows, int64_t cols, int64_t block, int state_bits, int k,
+                                 int V);
+int bcjr_ldlq_viterbi(const float *W, int64_t rows, int64_t cols, const float *codebook,
+                      int state_bits, int k, int V, const float *H, int64_t block, double damp,
+                      float *W_hat, int32_t *states, float *targets, void *workspace,
+                      size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------
  * Quantisation-aware training helpers.
  *
  * Computed Gaussian codebook (Sec. 3.1: c(s) = Phi^{-1}((s + 1/2) / S) under an

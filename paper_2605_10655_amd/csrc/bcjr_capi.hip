@@ -12,6 +12,7 @@
 #include "bcjr_internal.h"
 #include "bcjr_generic_kernels.h"
 #include "bcjr_kernels.h"
+#include "bcjr_ldlq_kernels.h"
 #include "bcjr_vec_kernels.h"
 #include "bcjr_qat.h"
 
@@ -790,6 +791,60 @@ int run_fbv(const float* w, int64_t B, int64_t L, const float* codebook, int n, 
   return BCJR_OK;
 }
 
+// ------------------------------------------------------------ BlockLDLQ
+// [A: d x d fp64][Rinv: (d / b) blocks of b x b fp64][mean]
+size_t ldl_ws_bytes(int64_t d, int64_t b) {
+  return align_up((size_t)(d * d) * sizeof(double)) + align_up((size_t)(d * b) * sizeof(double)) + kAlign;
+}
+
+bool ldl_args_ok(int64_t d, int64_t b, double damp) {
+  return d >= 1 && b >= 1 && d % b == 0 && d <= ((int64_t)1 << 20) && std::isfinite(damp) && damp >= 0.0;
+}
+
+unsigned blocks_for(int64_t count, int per) { return (unsigned)ceil_div(count, per); }
+
+int run_block_ldl(const float* H, int64_t d, int64_t b, double damp, double* M, double* D, char* ws,
+                  hipStream_t stream) {
+  double* A = reinterpret_cast<double*>(ws);
+  double* Rinv = reinterpret_cast<double*>(ws + align_up((size_t)(d * d) * sizeof(double)));
+  double* mean = reinterpret_cast<double*>(ws + align_up((size_t)(d * d) * sizeof(double)) +
+                                           align_up((size_t)(d * b) * sizeof(double)));
+  hipLaunchKernelGGL(ldl::diag_mean_kernel, dim3(1), dim3(256), 0, stream, H, d, mean);
+  hipLaunchKernelGGL(ldl::flip_damp_kernel, dim3(blocks_for(d * d, 256)), dim3(256), 0, stream, H, d,
+                     damp, (const double*)mean, A);
+  for (int64_t p = 0; p < d; p += ldl::kPanel) {
+    const int w = (int)std::min<int64_t>(ldl::kPanel, d - p);
+    hipLaunchKernelGGL(ldl::chol_diag_kernel, dim3(1), dim3(256), 0, stream, A, d, p, w);
+    const int64_t rest = d - p - w;
+    if (rest > 0) {
+      hipLaunchKernelGGL(ldl::chol_trsm_kernel, dim3(blocks_for(rest, 256)), dim3(256), 0, stream, A, d,
+                         p, w);
+      const int64_t nt = ceil_div(rest, ldl::kPanel);
+      hipLaunchKernelGGL(ldl::chol_update_kernel, dim3((unsigned)(nt * (nt + 1) / 2)), dim3(256), 0,
+                         stream, A, d, p, w);
+    }
+  }
+  hipLaunchKernelGGL(ldl::rinv_kernel, dim3((unsigned)(d / b)), dim3(256), 0, stream, (const double*)A, d,
+                     b, Rinv);
+  hipLaunchKernelGGL(ldl::m_kernel, dim3(blocks_for(d * d, 256)), dim3(256), 0, stream, (const double*)A, d,
+                     b, (const double*)Rinv, M);
+  if (D)
+    hipLaunchKernelGGL(ldl::dblk_kernel, dim3(blocks_for(d * d, 256)), dim3(256), 0, stream,
+                       (const double*)A, d, b, D);
+  return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+}
+
+size_t ldlq_decode_ws(int64_t rows, int64_t b, int n, int k, int V) {
+  return V == 1 ? bcjr_workspace_bytes(rows, b, n, k, BCJR_OP_VITERBI)
+                : bcjr_vec_workspace_bytes(rows, b, n, k, V, BCJR_OP_VITERBI);
+}
+
+// [M: d x d fp64][block LDL workspace][target: rows x b f32][w_hat block: rows x b f32][decode]
+size_t ldlq_ws_bytes(int64_t rows, int64_t cols, int64_t b, int n, int k, int V) {
+  return align_up((size_t)(cols * cols) * sizeof(double)) + ldl_ws_bytes(cols, b) +
+         2 * align_up((size_t)(rows * b) * sizeof(float)) + ldlq_decode_ws(rows, b, n, k, V);
+}
+
 // Device address of the current GPU's copy of `scratch`, looked up once per
 // device (with that device current) and kept.
 constexpr int kMaxDevices = 64;
@@ -977,6 +1032,71 @@ int bcjr_vec_viterbi_decode(const float* w, int64_t B, int64_t L, const float* c
   if (B > 0 && !states) return BCJR_ERR_INVALID_ARG;
   if (B == 0) return BCJR_OK;
   return run_vitv(w, B, L, codebook, state_bits, states, w_hard, workspace, ws_bytes, stream);
+}
+
+size_t bcjr_block_ldl_workspace_bytes(int64_t d, int64_t block) {
+  if (!ldl_args_ok(d, block, 0.0)) return 0;
+  return ldl_ws_bytes(d, block);
+}
+
+int bcjr_block_ldl(const float* H, int64_t d, int64_t block, double damp, double* M, double* D,
+                   void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!ldl_args_ok(d, block, damp) || !H || !M) return BCJR_ERR_INVALID_ARG;
+  if (((uintptr_t)H & 3u) || ((uintptr_t)M & 7u) || ((uintptr_t)D & 7u)) return BCJR_ERR_INVALID_ARG;
+  if (!workspace || ((uintptr_t)workspace & 15u) || ws_bytes < ldl_ws_bytes(d, block))
+    return BCJR_ERR_WORKSPACE;
+  return run_block_ldl(H, d, block, damp, M, D, static_cast<char*>(workspace), stream);
+}
+
+size_t bcjr_ldlq_workspace_bytes(int64_t rows, int64_t cols, int64_t block, int state_bits, int k, int V) {
+  if (rows < 1 || V < 1 || !ldl_args_ok(cols, block, 0.0) || block % V) return 0;
+  if (ldlq_decode_ws(rows, block, state_bits, k, V) == 0) return 0;
+  return ldlq_ws_bytes(rows, cols, block, state_bits, k, V);
+}
+
+int bcjr_ldlq_viterbi(const float* W, int64_t rows, int64_t cols, const float* codebook, int state_bits,
+                      int k, int V, const float* H, int64_t block, double damp, float* W_hat,
+                      int32_t* states, float* targets, void* workspace, size_t ws_bytes,
+                      hipStream_t stream) {
+  if (rows < 1 || V < 1 || !ldl_args_ok(cols, block, damp) || block % V) return BCJR_ERR_INVALID_ARG;
+  if (!W || !codebook || !H || !W_hat || !states) return BCJR_ERR_INVALID_ARG;
+  if (((uintptr_t)W & 3u) || ((uintptr_t)H & 3u) || ((uintptr_t)W_hat & 3u) || ((uintptr_t)states & 3u) ||
+      ((uintptr_t)targets & 3u) || ((uintptr_t)codebook & 15u))
+    return BCJR_ERR_INVALID_ARG;
+  const int st0 = V == 1 ? common_checks(W, rows, block, codebook, state_bits, k, false)
+                         : vec_checks(W, rows, block, codebook, state_bits, k, V, false);
+  if (st0 != BCJR_OK) return st0;
+  if (!workspace || ((uintptr_t)workspace & 15u) ||
+      ws_bytes < ldlq_ws_bytes(rows, cols, block, state_bits, k, V))
+    return BCJR_ERR_WORKSPACE;
+  char* p = static_cast<char*>(workspace);
+  double* M = reinterpret_cast<double*>(p);
+  p += align_up((size_t)(cols * cols) * sizeof(double));
+  char* lws = p;
+  p += ldl_ws_bytes(cols, block);
+  float* tgt = reinterpret_cast<float*>(p);
+  p += align_up((size_t)(rows * block) * sizeof(float));
+  float* wh = reinterpret_cast<float*>(p);
+  p += align_up((size_t)(rows * block) * sizeof(float));
+  const size_t dec_bytes = ws_bytes - (size_t)(p - static_cast<char*>(workspace));
+  int st = run_block_ldl(H, cols, block, damp, M, nullptr, lws, stream);
+  if (st != BCJR_OK) return st;
+  const int64_t nb = cols / block;
+  for (int64_t j = 0; j < nb; ++j) {
+    float* t = targets ? targets + j * rows * block : tgt;
+    hipLaunchKernelGGL(ldl::feedback_kernel, dim3(blocks_for(rows, ldl::kPanel), blocks_for(block, ldl::kPanel)),
+                       dim3(256), 0, stream, W, (const float*)W_hat, (const double*)M, rows, cols, block,
+                       j * block, t);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    int32_t* sj = states + j * rows * (block / V);
+    st = V == 1 ? run_viterbi(t, rows, block, codebook, state_bits, k, sj, wh, p, dec_bytes, stream)
+                : run_vitv(t, rows, block, codebook, state_bits, sj, wh, p, dec_bytes, stream);
+    if (st != BCJR_OK) return st;
+    hipLaunchKernelGGL(ldl::scatter_kernel, dim3(blocks_for(rows * block, 256)), dim3(256), 0, stream,
+                       (const float*)wh, rows, cols, block, j * block, W_hat);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
 }
 
 int bcjr_gaussian_codebook(float* codebook, int state_bits, int V, uint64_t seed,

@@ -7,53 +7,65 @@ over the trellis codewords, reached QTIP-style by BlockLDLQ (Eq. WPTQ).  The
 weights are [rows, cols]; H is the [cols, cols] proxy Hessian of the layer
 inputs; each row is cut into trellis blocks of `block` consecutive columns.
 
-Factor H = M D M^T with M unit block-upper-triangular and D block-diagonal
-(blocks of `block` columns).  Then for one row with error e = w - w_hat,
-    e H e^T = sum_k (e M)_k D_k (e M)_k^T,   (e M)_k = e_k + sum_{j<k} e_j M_jk,
-so the column blocks are rounded in order, block k to the trellis codeword
-nearest to the target
-    t_k = w_k + sum_{j<k} (w_j - w_hat_j) M_jk,
-which makes (e M)_k the block's own rounding error.  Each block's rounding is
-one batched `viterbi_decode` over the rows (exact minimum-distortion path of
-the target; D_k's off-diagonal coupling inside a block is not modelled, as
-in QTIP).  The factorisation and the feedback products are library linear
-algebra (Cholesky, triangular solves, GEMMs) on the device; every trellis
-decode runs in the library's Viterbi kernel.
+With H = M D M^T (M unit block-upper-triangular, D block-diagonal), one
+row's error e = w - w_hat gives e H e^T = sum_k (e M)_k D_k (e M)_k^T with
+(e M)_k = e_k + sum_{j<k} e_j M_jk, so the column blocks are rounded in
+order, block k to the codeword nearest to its target
+    t_k = w_k + sum_{j<k} (w_j - w_hat_j) M_jk.
+
+This module only marshals tensors for the library's C ABI: the damping, the
+factorisation, the feedback products and every decode run in HIP kernels
+(bcjr_block_ldl, bcjr_ldlq_viterbi).  ``hw_loss`` is an evaluation helper
+for reports and tests, not part of the rounding.
 """
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
-from . import bcjr_vec_viterbi_decode, viterbi_decode
+from . import _check_in, _ptr, _raise, _stream, load_library
 
 __all__ = ["block_ldl", "ldlq_viterbi", "hw_loss"]
 
 
-def block_ldl(H: torch.Tensor, block: int):
-    """H = M D M^T, M unit block-upper-triangular, D block-diagonal.
+def _lib():
+    L = load_library()
+    if not getattr(L, "_ldlq_bound", False):
+        vp, i64, ci, cd, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
+        L.bcjr_block_ldl_workspace_bytes.argtypes = [i64, i64]
+        L.bcjr_block_ldl_workspace_bytes.restype = sz
+        L.bcjr_block_ldl.argtypes = [vp, i64, i64, cd, vp, vp, vp, sz, vp]
+        L.bcjr_block_ldl.restype = ci
+        L.bcjr_ldlq_workspace_bytes.argtypes = [i64, i64, i64, ci, ci, ci]
+        L.bcjr_ldlq_workspace_bytes.restype = sz
+        L.bcjr_ldlq_viterbi.argtypes = [vp, i64, i64, vp, ci, ci, ci, vp, i64, cd, vp, vp, vp, vp, sz,
+                                        vp]
+        L.bcjr_ldlq_viterbi.restype = ci
+        L._ldlq_bound = True
+    return L
 
-    From the upper Cholesky factor H = R R^T (R upper triangular, the
-    Cholesky factor of H with the index order reversed): M = R B^{-1} and
-    D = B B^T with B = blockdiag(R_kk)."""
+
+def block_ldl(H: torch.Tensor, block: int, damp: float = 0.0, want_D: bool = True, stream=None):
+    """(H + damp mean(diag H) I) = M D M^T on the device: M unit
+    block-upper-triangular, D block-diagonal, both [d, d] float64."""
+    lib = _lib()
     d = H.shape[0]
-    if H.shape != (d, d) or d % block:
+    if H.dim() != 2 or H.shape != (d, d) or d % block:
         raise ValueError("H must be square with a size that is a multiple of block")
-    Hr = torch.flip(H, (0, 1))
-    C = torch.linalg.cholesky(Hr)                     # Hr = C C^T, C lower
-    R = torch.flip(C, (0, 1))                         # H = R R^T, R upper
-    M = torch.zeros_like(R)
-    D = torch.zeros_like(R)
-    eye = torch.eye(block, dtype=H.dtype, device=H.device)
-    for k in range(0, d, block):
-        Rkk = R[k:k + block, k:k + block]
-        Rinv = torch.linalg.solve_triangular(Rkk, eye, upper=True)
-        M[:, k:k + block] = R[:, k:k + block] @ Rinv
-        D[k:k + block, k:k + block] = Rkk @ Rkk.T
+    _check_in("H", H)
+    M = torch.empty((d, d), dtype=torch.float64, device=H.device)
+    D = torch.empty((d, d), dtype=torch.float64, device=H.device) if want_D else None
+    nbytes = lib.bcjr_block_ldl_workspace_bytes(d, block)
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=H.device)
+    rc = lib.bcjr_block_ldl(_ptr(H), d, block, float(damp), _ptr(M), _ptr(D), _ptr(ws), ws.numel(),
+                            _stream(stream))
+    _raise("bcjr_block_ldl", rc)
     return M, D
 
 
 def hw_loss(W, W_hat, H) -> float:
-    """1/2 tr((W - W_hat) H (W - W_hat)^T)  (Eq. LHW)."""
+    """1/2 tr((W - W_hat) H (W - W_hat)^T)  (Eq. LHW), in float64."""
     E = (W - W_hat).double()
     return 0.5 * float(((E @ H.double()) * E).sum())
 
@@ -61,36 +73,30 @@ def hw_loss(W, W_hat, H) -> float:
 def ldlq_viterbi(W, codebook, state_bits: int, k: int, H, block: int = 256, V: int = 1,
                  damp: float = 0.01, return_targets: bool = False, stream=None):
     """BlockLDLQ rounding of W [rows, cols] (float32, device) to trellis
-    codewords.  H [cols, cols] is damped by damp * mean(diag H) on the
-    diagonal before factorisation (the usual regularisation of a sample
-    Hessian).  Returns (W_hat [rows, cols], states [cols // block, rows,
-    block // V]) and, with return_targets, the per-block targets t_k."""
+    codewords.  H [cols, cols] (float32) is damped by damp * mean(diag H) on
+    the diagonal before factorisation.  Returns (W_hat [rows, cols], states
+    [cols // block, rows, block // V]) and, with return_targets, the
+    per-block targets t_k [cols // block, rows, block]."""
+    lib = _lib()
     rows, cols = W.shape
     if cols % block or block % V:
         raise ValueError("cols must be a multiple of block, block a multiple of V")
-    Hd = H.double()
-    Hd = Hd + damp * Hd.diagonal().mean() * torch.eye(cols, dtype=Hd.dtype, device=Hd.device)
-    M, _ = block_ldl(Hd, block)
-    Mf = M.float()
-    W = W.contiguous()
-    W_hat = torch.empty_like(W)
-    Err = torch.zeros_like(W)
+    _check_in("W", W)
+    dev = W.device
+    _check_in("H", H, (cols, cols), device=dev)
+    _check_in("codebook", codebook, device=dev)
+    if codebook.numel() != (1 << state_bits) * V:
+        raise ValueError("codebook must hold 2^state_bits x V values")
     nb = cols // block
-    states = torch.empty((nb, rows, block // V), dtype=torch.int32, device=W.device)
-    targets = torch.empty((nb, rows, block), dtype=W.dtype, device=W.device) if return_targets else None
-    for kb in range(nb):
-        sl = slice(kb * block, (kb + 1) * block)
-        t = W[:, sl]
-        if kb > 0:
-            t = t + Err[:, :kb * block] @ Mf[:kb * block, sl]
-        t = t.contiguous()
-        if return_targets:
-            targets[kb] = t
-        if V == 1:
-            _, wh = viterbi_decode(t, codebook, state_bits, k, states=states[kb], stream=stream)
-        else:
-            _, wh = bcjr_vec_viterbi_decode(t, codebook, state_bits, k, V, states=states[kb],
-                                            stream=stream)
-        W_hat[:, sl] = wh
-        Err[:, sl] = W[:, sl] - wh
+    W_hat = torch.empty_like(W)
+    states = torch.empty((nb, rows, block // V), dtype=torch.int32, device=dev)
+    targets = torch.empty((nb, rows, block), dtype=W.dtype, device=dev) if return_targets else None
+    nbytes = lib.bcjr_ldlq_workspace_bytes(rows, cols, block, state_bits, k, V)
+    if nbytes == 0:
+        raise ValueError("unsupported shape for the BlockLDLQ decode")
+    ws = torch.empty(int(nbytes), dtype=torch.uint8, device=dev)
+    rc = lib.bcjr_ldlq_viterbi(_ptr(W), rows, cols, _ptr(codebook), state_bits, k, V, _ptr(H), block,
+                               float(damp), _ptr(W_hat), _ptr(states), _ptr(targets), _ptr(ws),
+                               ws.numel(), _stream(stream))
+    _raise("bcjr_ldlq_viterbi", rc)
     return (W_hat, states, targets) if return_targets else (W_hat, states)

@@ -219,3 +219,46 @@ def test_training_helpers_argument_validation(lib):
     assert s(None, None, 0, 0.1, 0.0, None) == 0
     assert s(FAKE, FAKE, 4, -0.1, 0.0, None) == -1
     assert s(FAKE, FAKE, 4, 0.1, -1.0, None) == -1
+
+
+def test_ldlq_argument_validation(lib):
+    import ctypes as C
+    L = lib
+    L.bcjr_block_ldl_workspace_bytes.argtypes = [C.c_int64, C.c_int64]
+    L.bcjr_block_ldl_workspace_bytes.restype = C.c_size_t
+    L.bcjr_block_ldl.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_double, C.c_void_p, C.c_void_p,
+                                 C.c_void_p, C.c_size_t, C.c_void_p]
+    L.bcjr_ldlq_workspace_bytes.argtypes = [C.c_int64, C.c_int64, C.c_int64, C.c_int, C.c_int, C.c_int]
+    L.bcjr_ldlq_workspace_bytes.restype = C.c_size_t
+    L.bcjr_ldlq_viterbi.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_int, C.c_int,
+                                    C.c_int, C.c_void_p, C.c_int64, C.c_double, C.c_void_p, C.c_void_p,
+                                    C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+    # block LDL workspace: A (d^2 doubles), the block inverses (d x block doubles), a scalar
+    d, b = 512, 64
+    assert L.bcjr_block_ldl_workspace_bytes(d, b) >= d * d * 8 + d * b * 8
+    assert L.bcjr_block_ldl_workspace_bytes(d, 48) == 0           # d not a multiple of block
+    assert L.bcjr_block_ldl_workspace_bytes(0, 1) == 0
+    bl = L.bcjr_block_ldl
+    assert bl(FAKE, d, 48, 0.0, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert bl(FAKE, d, b, -0.1, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert bl(None, d, b, 0.0, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert bl(FAKE, d, b, 0.0, FAKE + 4, None, FAKE, 1 << 30, None) == -1   # M not 8-byte aligned
+    assert bl(FAKE, d, b, 0.0, FAKE, None, None, 0, None) == -3
+    assert bl(FAKE, d, b, 0.0, FAKE, None, FAKE, 1024, None) == -3
+    ws = L.bcjr_ldlq_workspace_bytes
+    assert ws(16, 512, 256, 16, 2, 1) > 512 * 512 * 8
+    assert ws(16, 512, 256, 16, 4, 2) > 0
+    assert ws(16, 512, 255, 16, 2, 1) == 0
+    assert ws(16, 512, 256, 16, 2, 3) == 0                        # V = 3 has no decode
+    lv = L.bcjr_ldlq_viterbi
+    args = [FAKE, 16, 512, FAKE, 16, 2, 1, FAKE, 256, 0.01, FAKE, FAKE, None, FAKE, 1 << 40, None]
+    bad = list(args); bad[8] = 255
+    assert lv(*bad) == -1
+    bad = list(args); bad[10] = None
+    assert lv(*bad) == -1
+    bad = list(args); bad[3] = MISALIGNED
+    assert lv(*bad) == -1
+    bad = list(args); bad[13] = None; bad[14] = 0
+    assert lv(*bad) == -3
+    bad = list(args); bad[14] = 1024
+    assert lv(*bad) == -3

@@ -75,3 +75,27 @@ def test_ldlq_matches_oracle(n, k, V, rows, cols, block):
     _say(f"[ldlq] loss gpu {l_gpu:.4f} oracle {l_ref:.4f} plain {l_plain:.4f}")
     assert abs(l_gpu - l_ref) <= 1e-3 * l_ref
     assert l_gpu < l_plain
+
+
+@pytest.mark.parametrize("d,block,damp", [(96, 32, 0.0), (128, 32, 0.01), (256, 64, 0.01),
+                                          (512, 256, 0.01), (80, 16, 0.05)])
+def test_block_ldl_matches_oracle(d, block, damp):
+    """The device factorisation (fp64 Cholesky of the index-reversed damped
+    Hessian, per-block inverses) against the oracle's numpy block_ldl of the
+    same damped matrix, and M D M^T = H + damp mean(diag H) I."""
+    from paper_2605_10655_amd.ldlq import block_ldl
+    _, _, H = _case(d + block, 4, d, 8)
+    _say(f"[ldl] d={d} block={block} damp={damp}")
+    M, D = block_ldl(dev(H), block, damp)
+    torch.cuda.synchronize()
+    M, D = host(M), host(D)
+    Hd = H.astype(np.float64)
+    Hd = Hd + damp * np.mean(np.diag(Hd)) * np.eye(d)
+    Mr, Dr = O.block_ldl(Hd, block)
+    scale = np.abs(Mr).max()
+    assert np.abs(M - Mr).max() <= 1e-9 * scale, np.abs(M - Mr).max()
+    assert np.abs(D - Dr).max() <= 1e-9 * np.abs(Dr).max()
+    assert np.abs(M @ D @ M.T - Hd).max() <= 1e-9 * np.abs(Hd).max()
+    for kb in range(0, d, block):          # unit diagonal blocks, zero below them
+        np.testing.assert_allclose(M[kb:kb + block, kb:kb + block], np.eye(block), atol=1e-9)
+        assert np.all(M[kb + block:, kb:kb + block] == 0.0)
