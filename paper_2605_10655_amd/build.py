@@ -16,7 +16,8 @@ LIB = os.path.join(PKG, "libbcjr.so")
 SOURCES = [os.path.join(CSRC, "bcjr_capi.hip")]
 RATES_SRC = os.path.join(CSRC, "issue_rates.hip")
 RATES_LIB = os.path.join(PKG, "libissue_rates.so")
-DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_qat.h", "bcjr_internal.h")] + [
+DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in ("bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_qat.h", "bcjr_internal.h",
+                                                        "bcjr_generic_kernels.h", "bcjr_ldlq_kernels.h")] + [
     os.path.join(INCLUDE, "bcjr.h")]
 
 

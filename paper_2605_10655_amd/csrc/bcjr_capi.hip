@@ -93,13 +93,15 @@ constexpr double kHighPrecisionK2 = 18.0;
 bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
 
 // The histories of one workgroup's blocks are addressed with 32-bit byte
-// offsets: blocks per workgroup x L x S/K x (8 bytes, 12 for the VJP, whose
-// low-temperature variant keeps three words per group) below 2^31.
+// offsets: blocks per workgroup x L x (S/K x 8 bytes; for the VJP 12, or
+// the low-temperature variant's hp_step_bytes where that is larger, at
+// S/K = 2) below 2^31.
 bool length_ok(int64_t L, int n, int k, bool vjp) {
   if (!supported(n, k)) return L <= ((int64_t)1 << 30);  // generic family: 64-bit offsets
   const Family f = family(n, k, false);
-  const int64_t per_step = (int64_t)f.bpw * (vjp ? 12 : 8) * ((int64_t)1 << (n - k));
-  return L <= 0x7FFFFFFF / per_step;
+  const int64_t gs = (int64_t)1 << (n - k);
+  const int64_t step = vjp ? std::max<int64_t>(12 * gs, hp_step_bytes(n, k)) : 8 * gs;
+  return L <= 0x7FFFFFFF / ((int64_t)f.bpw * step);
 }
 
 // The fp32 forward-backward path keeps the scaled codebook at the front of
@@ -111,24 +113,25 @@ struct FbLayout {
 };
 
 struct HpLayout {
-  size_t hist, histGA, xA, small, dc, slot;
+  size_t hist, histGA, small, dc, slot;
 };
 
 HpLayout hp_layout(int64_t L, int n, int k, bool dc) {
-  const size_t gs = (size_t)1 << (n - k);
+  const size_t step = hp_step_bytes(n, k);
   HpLayout l;
-  l.hist = align_up((size_t)L * 3 * gs * sizeof(float));
-  l.histGA = dc ? align_up((size_t)L * 3 * gs * sizeof(float)) : 0;
-  l.xA = align_up(gs * sizeof(float));
+  l.hist = align_up((size_t)L * step);
+  l.histGA = dc ? align_up((size_t)L * step) : 0;
   l.small = align_up((size_t)4 * L * sizeof(float));
   l.dc = dc ? align_up(((size_t)1 << n) * sizeof(double)) : 0;
-  l.slot = l.hist + l.histGA + l.xA + l.small + l.dc;
+  l.slot = l.hist + l.histGA + l.small + l.dc;
   return l;
 }
 
+// per block [hi, tangent] floats and [lo] bytes of S/K each, then the
+// cross-wave reduction area
 size_t hp_lds_bytes(const Family& f, int n, int k) {
   const size_t gs = (size_t)1 << (n - k);
-  return (size_t)f.bpw * 2 * gs * sizeof(float) +
+  return (size_t)f.bpw * 2 * gs * sizeof(float) + (((size_t)f.bpw * gs + 15) & ~(size_t)15) +
          (size_t)(f.nt / 64) * (2 * kRed * sizeof(float) + sizeof(double));
 }
 
@@ -430,11 +433,10 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.bref = ref;
   a.histHB = reinterpret_cast<float*>(p);             p += slots * lay.hist;
   a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;  p += slots * lay.histGA;
-  a.xA = reinterpret_cast<float*>(p);                 p += slots * lay.xA;
   a.small = reinterpret_cast<float*>(p);              p += slots * lay.small;
   a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
-  if (dc) {  // the (G, A) entries of step 0 are zero for every block of a slot
-    const int64_t hstep = 3 * ((int64_t)1 << (n - k));
+  if (dc) {  // the (G, A, lo) entries of step 0 are zero for every block of a slot
+    const int64_t hstep = hp_step_bytes(n, k) / 4;
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histGA, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;

@@ -30,16 +30,20 @@ struct FbArgs {
   // row per super-group; the entries of step L - 1 (H, B) and step 0 (G, A)
   // are zero and filled before the launch)
   float* small;        // [slots][3][L]     shifts of H, lambda_t, E_p[X_t]
-  // low-temperature variant (double-float log vectors): histHB holds, per
-  // step and super-group, three planes (hi, lo, tangent) of [threads][K]
-  // floats, so that one store of a wave fills whole cache lines; histGA per
-  // step three [S/K] vectors (G hi, G lo, A), stored by the forward sweep's
+  // low-temperature variant (log vectors as hi + 8-bit lo pairs): steps of
+  // hp_step_bytes(); histHB holds, per step and super-group, three planes
+  // (hi, tangent as [threads][K] floats, lo as [threads][K] bytes), so that
+  // one store of a wave fills whole cache lines; histGA per step three [S/K]
+  // vectors (G hi, A floats, G lo bytes), stored by the forward sweep's
   // write phase for the next step (step 0 filled with zeros before the
   // launch); small is [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
   const float* bref;   // [B, L] centring reference of the backward tangent
-  float* xA;           // [slots][S/K] tangent exchange, updated in place
 };
+
+// Bytes of one history step of the low-temperature kernel: 9 per group
+// (hi and tangent floats, one lo byte), rounded up to 16.
+inline uint32_t hp_step_bytes(int n, int k) { return (9u * (1u << (n - k)) + 15u) & ~15u; }
 
 // Vector-emission trellis: k = 4 bits per step (K = 16), V = 2 weights per
 // step.  Blocks hold L = 2 N weights.

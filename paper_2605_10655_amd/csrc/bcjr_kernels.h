@@ -995,23 +995,24 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
 // that carry the posterior lie hundreds of log2 units from the per-step
 // maximum (|h_t| ~ (w - c)^2 / 2T), so fp32 log vectors round them at ~1e-5
 // and the VJP loses its 1e-4 relative accuracy.  Here G and H are carried as
-// double-float pairs (hi + lo, two fp32 words, ~48 bits) with fp64 LSE
-// arithmetic; softmax weights and tangents stay fp32.
-//   Exchange between threads: the hi and lo words fill the two S/K fp32
-//   vectors in LDS (the footprint of fb_kernel) and are updated in place:
-//   reads, barrier, writes, barrier, with the outputs held in registers
-//   across the first barrier; the fp32 tangent is updated in place in a
-//   per-slot global vector (L2-resident).  The integer shift of a step is
-//   the floor of the previous step's maximum (the stored maxima stay within
-//   the per-step drift of 0), and the forward tangent is centred on w_soft
-//   when it is read, one step later (the same arithmetic as centring before
-//   the write).  The backward tangent is centred on a reference path given
-//   per block (the minimum-distortion codewords), which the posterior
-//   follows at low temperature.
-//   S0 backward: H and B, history rows (H hi, H lo, B) as three planes of
-//                [threads][K] per super-group, written and read non-temporal;
+// pairs hi + lo (an fp32 word and an 8-bit correction: 32 significand bits)
+// with fp64 LSE arithmetic; softmax weights and tangents stay fp32.
+//   Exchange between threads: per block, the hi words and the fp32 tangent
+//   fill two S/K vectors in LDS and the lo words a third of S/K bytes, each
+//   lo an int8 multiple of ulp(hi) / 256 (a 32-bit significand in all); all
+//   three are updated in place: reads, barrier, writes, barrier, with the
+//   outputs held in registers across the first barrier.  The integer shift
+//   of a step is the floor of the previous step's maximum (the stored maxima
+//   stay within the per-step drift of 0), and the forward tangent is centred
+//   on w_soft when it is read, one step later (the same arithmetic as
+//   centring before the write).  The backward tangent is centred on a
+//   reference path given per block (the minimum-distortion codewords), which
+//   the posterior follows at low temperature.
+//   S0 backward: H and B, history rows (H hi, B, H lo) as three planes of
+//                [threads][K] per super-group (9 bytes per group-step),
+//                written and read non-temporal;
 //   S1 forward:  G and A, marginals, w_soft, dW; with dCodebook also the
-//                (G hi, G lo, A) rows of the next step, stored from the
+//                (G hi, A, G lo) entries of the next step, stored from the
 //                write phase, and the exact lambda_t, E_p[X_t];
 //   S2 dCodebook as in fb_kernel, with p from the fp64 sums.
 // ---------------------------------------------------------------------------
@@ -1063,6 +1064,68 @@ __device__ __forceinline__ void split_df(double v, float& hi, float& lo) {
   lo = (float)(v - (double)hi);
 }
 
+// The lo word of a double-float pair, kept as a signed 8-bit multiple of
+// ulp(hi) / 256: hi + lo then carries a 32-bit significand, 2^8 times finer
+// than hi alone (the VJP's tolerance needs about 2^5), in a quarter of the
+// bytes.  hi = 0, denormal or non-finite keeps lo = 0.
+__device__ __forceinline__ uint32_t lo8_enc(float hi, float lo) {
+  const int e = (int)((as_u(hi) >> 23) & 0xFFu);
+  const float q = fminf(fmaxf(rintf(ldexpf(lo, 158 - e)), -127.f), 127.f);
+  return (e == 0 || e == 255) ? 0u : ((uint32_t)(int)q & 0xFFu);
+}
+
+__device__ __forceinline__ double df_join(float hi, uint32_t byte) {
+  const int e = (int)((as_u(hi) >> 23) & 0xFFu);
+  const int q = (int)(int8_t)(uint8_t)byte;  // 0 where the encoder keeps lo = 0
+  return (double)hi + (double)ldexpf((float)q, e - 158);
+}
+
+// K lo bytes of one row, packed (byte u of the row in bits 8u..8u+7)
+template <int K>
+__device__ __forceinline__ uint64_t lo_row_lds(const uint8_t* p) {
+  if constexpr (K == 2) return *reinterpret_cast<const uint16_t*>(p);
+  else if constexpr (K == 4) return *reinterpret_cast<const uint32_t*>(p);
+  else return *reinterpret_cast<const uint64_t*>(p);
+}
+
+template <int K>
+__device__ __forceinline__ void lo_row_lds_st(uint8_t* p, uint64_t v) {
+  if constexpr (K == 2) *reinterpret_cast<uint16_t*>(p) = (uint16_t)v;
+  else if constexpr (K == 4) *reinterpret_cast<uint32_t*>(p) = (uint32_t)v;
+  else *reinterpret_cast<uint64_t*>(p) = v;
+}
+
+template <int K, int CP = 0>
+__device__ __forceinline__ uint64_t lo_row_ld(rsrc_t r, uint32_t voff, uint32_t soff) {
+  if constexpr (K == 2) {
+    return (uint64_t)(unsigned short)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, CP);
+  } else if constexpr (K == 4) {
+    return (uint64_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, CP);
+  } else {
+    const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, CP);
+    const unsigned x0 = x.x, x1 = x.y;
+    return (uint64_t)x0 | ((uint64_t)x1 << 32);
+  }
+}
+
+// (whole offset in the VGPR, as for buf_st)
+template <int K, int CP = 0>
+__device__ __forceinline__ void lo_row_st(rsrc_t r, uint32_t voff0, uint32_t soff0, uint64_t v) {
+  const uint32_t voff = voff0 + soff0;
+  if constexpr (K == 2) {
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, r, (int)voff, 0, CP);
+  } else if constexpr (K == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)v, r, (int)voff, 0, CP);
+  } else {
+    const u32x2 x = {(unsigned)v, (unsigned)(v >> 32)};
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)voff, 0, CP);
+  }
+}
+
+__device__ __forceinline__ uint32_t lo_byte_ld(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return (uint32_t)(unsigned char)__builtin_amdgcn_raw_buffer_load_b8(r, (int)voff, (int)soff, kStream);
+}
+
 template <int KB, int NB, int SGMAX, int NT, bool DC>
 __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   constexpr int K = 1 << KB;
@@ -1084,18 +1147,28 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   rc.width = TPB < 64 ? TPB : 64;
   rc.rw = TPB > 64 ? TPB / 64 : 1;
   rc.wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: a scalar
-  // [2 parities][waves][kRed] floats, then [waves] doubles
-  float* red0 = lds + (size_t)BPW * 2 * GS;
+  // LDS: per block [hi: S/K][tangent: S/K] floats, then per block [lo: S/K]
+  // bytes, then [2 parities][waves][kRed] floats and [waves] doubles
+  uint8_t* const lo8 = reinterpret_cast<uint8_t*>(lds + (size_t)BPW * 2 * GS);
+  float* red0 = reinterpret_cast<float*>(lo8 + (((size_t)BPW * GS + 15) & ~(size_t)15));
   double* redd = reinterpret_cast<double*>(red0 + 2 * (NT / 64) * kRed);
 
   const uint32_t vb = (uint32_t)bw * 2 * GS;
-  const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;
+  const uint32_t col0 = vb + tb, row0 = vb + (uint32_t)tb * K;     // float planes
+  const uint32_t lcol0 = (uint32_t)bw * GS + tb, lrow0 = (uint32_t)bw * GS + (uint32_t)tb * K;  // lo bytes
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
   const uint32_t voK = (uint32_t)tb << (KB + 2);
-  const uint32_t hrow = 3 * K;                    // floats per thread and super-group: hi, lo, tangent planes
-  const uint32_t hstep = (uint32_t)GS * 3;        // floats per history step
-  const uint32_t voH = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb * K) * 4u;
-  const uint32_t voC = ((uint32_t)bw * (uint32_t)L * hstep + (uint32_t)tb) * 4u;
+  // History step (bytes): H side, per super-group block of TPB*K entries, a
+  // hi plane, a tangent plane ([threads][K] floats each) and a lo plane
+  // ([threads][K] bytes); G side (dCodebook) three per-step vectors [S/K]
+  // (hi floats, tangent floats, lo bytes).
+  const uint32_t hstep = ((uint32_t)GS * 9u + 15u) & ~15u;
+  const uint32_t sgb = (uint32_t)TPB * K * 9u;          // bytes of one super-group block
+  const uint32_t pT = (uint32_t)TPB * K * 4u, pL = (uint32_t)TPB * K * 8u;  // plane offsets in a block
+  const uint32_t vslot = (uint32_t)bw * (uint32_t)L * hstep;
+  const uint32_t voH = vslot + (uint32_t)tb * K * 4u, voHL = vslot + (uint32_t)tb * K;
+  const uint32_t voC = vslot + (uint32_t)tb * 4u, voCL = vslot + (uint32_t)tb;
+  const uint32_t gT = (uint32_t)GS * 4u, gL = (uint32_t)GS * 8u;  // G-side vector offsets
   const bool lane_rows = TPB >= 64;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
@@ -1113,30 +1186,22 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     const float* wbu = a.w + bbu * L;
     const float* gbu = a.g + bbu * L;
     const float* rbu = a.bref + bbu * L;
-    const rsrc_t hist = make_rsrc(a.histHB + slot0 * L * hstep, (uint32_t)BPW * (uint32_t)L * hstep * 4u);
-    const rsrc_t hga = make_rsrc(DC ? a.histGA + slot0 * L * hstep : a.histHB,
-                                 DC ? (uint32_t)BPW * (uint32_t)L * hstep * 4u : 0u);
-    // tangent exchange of the slot, [S/K], updated in place (L2-resident),
-    // addressed through a buffer descriptor: row form at tb*K, column form
-    // at tb, the super-group and j parts in the scalar / immediate offset.
-    // Workgroups go to the 8 XCDs round-robin; the vectors of one XCD's
-    // slots are placed next to each other, so that they spread over all of
-    // its L2 sets (at a stride of 8 slots they shared an eighth of them).
-    const int64_t nbk = gridDim.x;
-    const int64_t xslot = (nbk & 7) ? slot
-        : (((int64_t)blockIdx.x & 7) * (nbk >> 3) + ((int64_t)blockIdx.x >> 3)) * BPW + bw;
-    float* xtg = a.xA + xslot * GS;
-    const rsrc_t xrs = make_rsrc(xtg, (uint32_t)GS * 4u);
-    const uint32_t vxr = (uint32_t)tb * K * 4u, vxc = (uint32_t)tb * 4u;
+    char* const hbase = reinterpret_cast<char*>(a.histHB) + slot0 * L * (int64_t)hstep;
+    const rsrc_t hist = make_rsrc(hbase, (uint32_t)BPW * (uint32_t)L * hstep);
+    const rsrc_t hga = make_rsrc(DC ? reinterpret_cast<char*>(a.histGA) + slot0 * L * (int64_t)hstep
+                                    : reinterpret_cast<char*>(a.histHB),
+                                 DC ? (uint32_t)BPW * (uint32_t)L * hstep : 0u);
     float* sm_mB = a.small + slot * 4 * L;   // shift applied to H_t (integer)
     float* sm_xb = sm_mB + L;                // dCodebook: E_p[X_t]
     double* sm_lam = reinterpret_cast<double*>(sm_xb + L);  // dCodebook: lambda_t (fp64)
 
     // ------------------------------------------------------------------ S0
+    // H (hi in LDS plane 0, lo bytes) and the tangent B (plane 1), updated in
+    // place: reads, barrier, writes, barrier
     for (int i = tb; i < GS; i += TPB) {
       lds[vb + i] = 0.f;
       lds[vb + GS + i] = 0.f;
-      xtg[i] = 0.f;
+      lo8[(uint32_t)bw * GS + i] = 0;
     }
     __syncthreads();
     double shiftB = 0.0;
@@ -1170,27 +1235,26 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         rt = rb[t];
       }
       const double wt = (double)wf;
-      // (H hi, H lo) in LDS and the tangent B in the slot's global vector,
-      // all updated in place: reads, barrier, writes, barrier
-      uint32_t rrow = row0, rrowL = row0 + GS, wcol = col0, wcolL = col0 + GS;
+      uint32_t rrow = row0, rrowT = row0 + GS, wcol = col0, wcolT = col0 + GS;
+      uint32_t lrow = lrow0, lcol = lcol0;
       pin_u(rrow);
-      pin_u(rrowL);
+      pin_u(rrowT);
       pin_u(wcol);
-      pin_u(wcolL);
-      const uint32_t soH = (uint32_t)t * hstep * 4u;
+      pin_u(wcolT);
+      const uint32_t soH = (uint32_t)t * hstep;
       if (t == 0) {
         // lambda_0 = LSE_s [h_0(s) + H_0] and E_p[g_0 c + B_0]
         double lm = -INFINITY;
         float ls = 0.f, ly = 0.f;
 #pragma unroll 1
         for (int i = 0; i < SGT; ++i) {
-          float Hh[K], Hl[K], Bin[K];
+          float Hh[K], Bin[K];
           ld_vec<K>(lds + rrow + i * TPB * K, Hh);
-          ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
-          buf_ld<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, Bin);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 4u, Hl);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 8u, Bin);
+          ld_vec<K>(lds + rrowT + i * TPB * K, Bin);
+          const uint64_t Hl = lo_row_lds<K>(lo8 + lrow + i * TPB * K);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * sgb, Hh);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * sgb + pT, Bin);
+          lo_row_st<K, kStream>(hist, voHL, soH + (uint32_t)i * sgb + pL, Hl);
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             float cc[K];
@@ -1199,7 +1263,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
             for (int b = 0; b < K; ++b) {
               const double d = wt - (double)cc[b];
-              x[b] = fma(-d * k2, d, (double)Hh[b] + (double)Hl[b]);
+              x[b] = fma(-d * k2, d, df_join(Hh[b], (uint32_t)(Hl >> (8 * b))));
             }
             const double m = max_of<K>(x);
             float s = 0.f, sy = 0.f;
@@ -1224,37 +1288,32 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         break;
       }
       float vmax[1] = {-INFINITY};
-      float oh[SGMAX][K], ol[SGMAX][K], ot[SGMAX][K];  // outputs, held across the first barrier
-      // the tangent row of the first super-group now, each next one a
-      // super-group ahead
-      float pB[K];
-      buf_ld<K>(xrs, vxr, 0, pB);
+      float oh[SGMAX][K], ot[SGMAX][K];  // outputs, held across the first barrier
+      uint64_t ol[SGMAX];                // their lo bytes, packed
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
-          float Hh[K], Hl[K], Bin[K], cc[K][K];
-#pragma unroll
-          for (int b = 0; b < K; ++b) Bin[b] = pB[b];
+          float Hh[K], Bin[K], cc[K][K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
 #pragma unroll
             for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
           }
-          {  // (clamped index, not a branch: the last super-group re-reads its own row)
-            const int in = i + 1 < SGT ? i + 1 : i;
-            buf_ld<K>(xrs, vxr, (uint32_t)in * TPB * K * 4u, pB);
-            const int ic = i + 1 < SGT ? i + 1 : 0;  // the codebook wraps to the next step
+          {  // the codebook wraps to the next step
+            const int ic = i + 1 < SGT ? i + 1 : 0;
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
           }
           ld_vec<K>(lds + rrow + i * TPB * K, Hh);
-          ld_vec<K>(lds + rrowL + i * TPB * K, Hl);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u, Hh);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 4u, Hl);
-          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * TPB * hrow * 4u + (uint32_t)TPB * K * 8u, Bin);
+          ld_vec<K>(lds + rrowT + i * TPB * K, Bin);
+          const uint64_t Hl = lo_row_lds<K>(lo8 + lrow + i * TPB * K);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * sgb, Hh);
+          buf_st<K, kStream>(hist, voH, soH + (uint32_t)i * sgb + pT, Bin);
+          lo_row_st<K, kStream>(hist, voHL, soH + (uint32_t)i * sgb + pL, Hl);
           double H[K];
 #pragma unroll
-          for (int b = 0; b < K; ++b) H[b] = (double)Hh[b] + (double)Hl[b];
+          for (int b = 0; b < K; ++b) H[b] = df_join(Hh[b], (uint32_t)(Hl >> (8 * b)));
+          ol[i] = 0;
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             double x[K];
@@ -1275,11 +1334,12 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
             for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[j][b] - rt, Bin[b]), num);
             const double hv = m + (double)lg2(s) - (double)dlag;
-            split_df(hv, oh[i][j], ol[i][j]);
+            float lo;
+            split_df(hv, oh[i][j], lo);
+            ol[i] |= (uint64_t)lo8_enc(oh[i][j], lo) << (8 * j);
             vmax[0] = fmaxf(vmax[0], oh[i][j]);
             ot[i][j] = num * rcp(s);
             pin(oh[i][j]);
-            pin(ol[i][j]);
             pin(ot[i][j]);
           }
           sg_fence();
@@ -1297,11 +1357,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             lds[wcol + j * NSG + i * TPB] = oh[i][j];
-            lds[wcolL + j * NSG + i * TPB] = ol[i][j];
-            {
-              const float v1[1] = {ot[i][j]};
-              buf_st<1>(xrs, vxc, (uint32_t)(j * NSG + i * TPB) * 4u, v1);
-            }
+            lds[wcolT + j * NSG + i * TPB] = ot[i][j];
+            lo8[lcol + j * NSG + i * TPB] = (uint8_t)(ol[i] >> (8 * j));
           }
         }
       }
@@ -1309,12 +1366,11 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     }
 
     // ------------------------------------------------------------------ S1
-    // (G hi, G lo) in LDS and the tangent A in the slot's global vector,
-    // updated in place like S0
+    // G (hi plane 0, lo bytes) and the tangent A (plane 1), updated in place
     for (int i = tb; i < GS; i += TPB) {
       lds[vb + i] = 0.f;
       lds[vb + GS + i] = 0.f;
-      xtg[i] = 0.f;
+      lo8[(uint32_t)bw * GS + i] = 0;
     }
     __syncthreads();
     double lam_est = lam0;
@@ -1326,10 +1382,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     // the history row and codebook rows of the next super-group (the first
     // of the next step after the last) are fetched one super-group ahead;
     // the shift of H_t one step ahead
-    float pHh[K], pHl2[K], pBc[K];
+    float pHh[K], pBc[K];
     buf_ld<K, kStream>(hist, voH, 0, pHh);
-    buf_ld<K, kStream>(hist, voH, (uint32_t)TPB * K * 4u, pHl2);
-    buf_ld<K, kStream>(hist, voH, (uint32_t)TPB * K * 8u, pBc);
+    buf_ld<K, kStream>(hist, voH, pT, pBc);
+    uint64_t pHl = lo_row_ld<K, kStream>(hist, voHL, pL);
 #pragma unroll
     for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
     float mBnx = sm_mB[0];
@@ -1354,64 +1410,48 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       const double wt = (double)wf;
       const double mBt = (double)mBnx;
       mBnx = sm_mB[t + 1 < L ? t + 1 : t];
-      uint32_t rcol = col0, rcolL = col0 + GS, wrow = row0, wrowL = row0 + GS;
+      uint32_t rcol = col0, rcolT = col0 + GS, wrow = row0, wrowT = row0 + GS;
+      uint32_t lcol = lcol0, lrow = lrow0;
       pin_u(rcol);
-      pin_u(rcolL);
+      pin_u(rcolT);
       pin_u(wrow);
-      pin_u(wrowL);
-      const uint32_t soH = (uint32_t)t * hstep * 4u;
+      pin_u(wrowT);
       // max G_{t+1}, sum p, sum p c, sum p X, sum p c X
       float rv[5] = {-INFINITY, 0.f, 0.f, 0.f, 0.f};
-      float oh[SGMAX][K], ol[SGMAX][K], oa[SGMAX][K];  // outputs, held across the first barrier
-      // tangent entries of the first super-group now, each next one a
-      // super-group ahead
-      float pAr[K];
-#pragma unroll
-      for (int j = 0; j < K; ++j) {
-        float v1[1];
-        buf_ld<1>(xrs, vxc, (uint32_t)j * NSG * 4u, v1);
-        pAr[j] = v1[0];
-      }
+      float oh[SGMAX][K], oa[SGMAX][K];  // outputs, held across the first barrier
+      uint64_t ol[SGMAX];
 #pragma unroll
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
-          float Gh[K], Gl[K], Ar[K];
-          float Hh[K], Hl[K], Bc[K], cc[K][K];
+          float Gh[K], Ar[K];
+          float Hh[K], Bc[K], cc[K][K];
+          const uint64_t Hl = pHl;
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            Ar[j] = pAr[j] - cprev;
             Hh[j] = pHh[j];
-            Hl[j] = pHl2[j];
             Bc[j] = pBc[j];
 #pragma unroll
             for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
           }
           {  // (clamped indices, not branches)
             const bool last = i + 1 >= SGT;
-            const int in = last ? i : i + 1;
-#pragma unroll
-            for (int j = 0; j < K; ++j) {
-              float v1[1];
-              buf_ld<1>(xrs, vxc, (uint32_t)(j * NSG + in * TPB) * 4u, v1);
-              pAr[j] = v1[0];
-            }
             const int64_t tn = last && t + 1 < L ? t + 1 : t;
-            const uint32_t so = (uint32_t)tn * hstep * 4u + (last ? 0u : (uint32_t)(i + 1) * TPB * hrow * 4u);
+            const uint32_t so = (uint32_t)tn * hstep + (last ? 0u : (uint32_t)(i + 1) * sgb);
             buf_ld<K, kStream>(hist, voH, so, pHh);
-            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, pHl2);
-            buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 8u, pBc);
+            buf_ld<K, kStream>(hist, voH, so + pT, pBc);
+            pHl = lo_row_ld<K, kStream>(hist, voHL, so + pL);
             const int ic = last ? 0 : i + 1;
 #pragma unroll
             for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
           }
+          double G[K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             Gh[j] = lds[rcol + j * NSG + i * TPB];
-            Gl[j] = lds[rcolL + j * NSG + i * TPB];
+            Ar[j] = lds[rcolT + j * NSG + i * TPB] - cprev;
+            G[j] = df_join(Gh[j], lo8[lcol + j * NSG + i * TPB]);
           }
-          double G[K];
-#pragma unroll
-          for (int j = 0; j < K; ++j) G[j] = (double)Gh[j] + (double)Gl[j];
+          ol[i] = 0;
 #pragma unroll
           for (int u = 0; u < K; ++u) {
             double al[K];
@@ -1440,16 +1480,17 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
               scx = fmaf(ec, x, scx);
             }
             const double gout = m + (double)lg2(s) - (double)dlag;
-            split_df(gout, oh[i][u], ol[i][u]);
+            float lo;
+            split_df(gout, oh[i][u], lo);
+            ol[i] |= (uint64_t)lo8_enc(oh[i][u], lo) << (8 * u);
             rv[0] = fmaxf(rv[0], oh[i][u]);
-            const float fac = ex2((float)(m + ((double)Hh[u] + (double)Hl[u]) - lam_est));
+            const float fac = ex2((float)(m + df_join(Hh[u], (uint32_t)(Hl >> (8 * u))) - lam_est));
             rv[1] = fmaf(fac, s, rv[1]);
             rv[2] = fmaf(fac, sc, rv[2]);
             rv[3] = fmaf(fac, sx, rv[3]);
             rv[4] = fmaf(fac, scx, rv[4]);
             oa[i][u] = fmaf(sx, rcp(s), -bx);  // E-weighted mean of g c + A
             pin(oh[i][u]);
-            pin(ol[i][u]);
             pin(oa[i][u]);
           }
           sg_fence();
@@ -1480,17 +1521,17 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       for (int i = 0; i < SGMAX; ++i) {
         if (i < SGT) {
           st_vec<K>(lds + wrow + i * TPB * K, oh[i]);
-          st_vec<K>(lds + wrowL + i * TPB * K, ol[i]);
-          buf_st<K>(xrs, vxr, (uint32_t)i * TPB * K * 4u, oa[i]);
-          if constexpr (DC) {  // (G hi, G lo, A) entries of step t + 1, A centred as it is read
+          st_vec<K>(lds + wrowT + i * TPB * K, oa[i]);
+          lo_row_lds_st<K>(lo8 + lrow + i * TPB * K, ol[i]);
+          if constexpr (DC) {  // (G hi, A, G lo) entries of step t + 1, A centred as it is read
             if (t + 1 < L) {
               float ac[K];
 #pragma unroll
               for (int u = 0; u < K; ++u) ac[u] = oa[i][u] - cprev;
-              const uint32_t so = (uint32_t)(t + 1) * hstep * 4u + (uint32_t)i * TPB * K * 4u;
+              const uint32_t so = (uint32_t)(t + 1) * hstep + (uint32_t)i * TPB * K * 4u;
               buf_st<K, kStream>(hga, voH, so, oh[i]);
-              buf_st<K, kStream>(hga, voH, so + (uint32_t)GS * 4u, ol[i]);
-              buf_st<K, kStream>(hga, voH, so + (uint32_t)GS * 8u, ac);
+              buf_st<K, kStream>(hga, voH, so + gT, ac);
+              lo_row_st<K, kStream>(hga, voHL, (uint32_t)(t + 1) * hstep + gL + (uint32_t)i * TPB * K, ol[i]);
             }
           }
         }
@@ -1499,6 +1540,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
     }
 
     // ------------------------------------------------------------------ S2
+    // dCodebook as in fb_kernel: per super-group over all steps, the (H, B,
+    // H lo) row and the (G, A, G lo) column entries of a step loaded one
+    // step ahead.
     if constexpr (DC) {
       __syncthreads();
       const bool first = base == (int64_t)blockIdx.x * BPW;
@@ -1513,6 +1557,26 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           for (int u = 0; u < K; ++u) acc[j][u] = 0.f;
         }
         float xch = 0.f;
+        float nH[K], nB[K], nG[K], nA[K];
+        uint64_t nHl;
+        uint32_t nGl[K];
+        auto fetch = [&](int64_t ts) {
+          const uint32_t so = (uint32_t)ts * hstep + (uint32_t)i * sgb;
+          buf_ld<K, kStream>(hist, voH, so, nH);
+          buf_ld<K, kStream>(hist, voH, so + pT, nB);
+          nHl = lo_row_ld<K, kStream>(hist, voHL, so + pL);
+#pragma unroll
+          for (int j = 0; j < K; ++j) {  // (G, A, lo) entries a column apart
+            float v1[1], v3[1];
+            const uint32_t sg = (uint32_t)ts * hstep + (uint32_t)(j * NSG + i * TPB) * 4u;
+            buf_ld<1, kStream>(hga, voC, sg, v1);
+            buf_ld<1, kStream>(hga, voC, sg + gT, v3);
+            nGl[j] = lo_byte_ld(hga, voCL, (uint32_t)ts * hstep + gL + (uint32_t)(j * NSG + i * TPB));
+            nG[j] = v1[0];
+            nA[j] = v3[0];
+          }
+        };
+        fetch(0);
 #pragma unroll 1
         for (int64_t t = 0; t < L; ++t) {
           float wf, gt, xt;
@@ -1534,30 +1598,29 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           }
           const double lt = sm_lam[t];
           const double wt = (double)wf;
-          const uint32_t so = (uint32_t)t * hstep * 4u + (uint32_t)i * TPB * hrow * 4u;
-          float Hh[K], Hl[K], Bv[K], Gh[K], Gl[K], A[K];
-          buf_ld<K, kStream>(hist, voH, so, Hh);
-          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 4u, Hl);
-          buf_ld<K, kStream>(hist, voH, so + (uint32_t)TPB * K * 8u, Bv);
+          float Hh[K], Bv[K], Gh[K], A[K];
+          uint32_t Gl[K];
+          const uint64_t Hl = nHl;
 #pragma unroll
-          for (int j = 0; j < K; ++j) {  // (G, A) entries a column apart
-            float v1[1], v2[1], v3[1];
-            const uint32_t sg = (uint32_t)t * hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
-            buf_ld<1, kStream>(hga, voC, sg, v1);
-            buf_ld<1, kStream>(hga, voC, sg + (uint32_t)GS * 4u, v2);
-            buf_ld<1, kStream>(hga, voC, sg + (uint32_t)GS * 8u, v3);
-            Gh[j] = v1[0];
-            Gl[j] = v2[0];
-            A[j] = v3[0];
+          for (int q = 0; q < K; ++q) {
+            Hh[q] = nH[q];
+            Bv[q] = nB[q];
+            Gh[q] = nG[q];
+            A[q] = nA[q];
+            Gl[q] = nGl[q];
           }
+          fetch(t + 1 < L ? t + 1 : t);  // (a select: the last step re-reads its own entries)
+          double G[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) G[j] = df_join(Gh[j], Gl[j]);
 #pragma unroll
           for (int u = 0; u < K; ++u) {
-            const double hb = ((double)Hh[u] + (double)Hl[u]) - lt;
+            const double hb = df_join(Hh[u], (uint32_t)(Hl >> (8 * u))) - lt;
             const float bx = Bv[u] - xt;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
               const double d = wt - (double)cc[j][u];
-              const float p = ex2((float)(fma(-d * k2, d, (double)Gh[j] + (double)Gl[j]) + hb));
+              const float p = ex2((float)(fma(-d * k2, d, G[j]) + hb));
               const float X = fmaf(gt, cc[j][u], A[j]) + bx;
               acc[j][u] = fmaf(p, fmaf((wf - cc[j][u]) * X, invT, gt), acc[j][u]);
             }

@@ -91,6 +91,18 @@ def full_check(w, c, n, k, T, g, want_dc=True, what=""):
     return ws, lz, dW, dc
 
 
+def assert_same_up_to_dc_order(full, out):
+    """w_soft, logZ and dW bit-identical; dCodebook is the fp64 sum of
+    per-slot partials, whose order follows the grid: the fp64 sums differ by
+    rounding far below fp32 resolution, so the fp32 results by at most one
+    ulp, plus a floor for entries that cancel to near zero."""
+    for a, b in zip(full[:3], out[:3]):
+        np.testing.assert_array_equal(a, b)
+    a, b = full[3].astype(np.float64), out[3].astype(np.float64)
+    bound = 2.0 ** -23 * np.abs(a) + 2.0 ** -40 * np.abs(a).max()
+    assert np.all(np.abs(a - b) <= bound), float((np.abs(a - b) - bound).max())
+
+
 # ---------------------------------------------------------------- config 1
 @pytest.mark.parametrize("T", WL.workload(1).temps)
 def test_config1_tiny_all_outputs(T):
@@ -237,7 +249,8 @@ def test_precision_switch_boundary(T):
 @pytest.mark.parametrize("n,T", [(8, 0.2), (12, 0.2), (16, 0.2), (12, 0.003), (16, 0.003)])
 def test_small_workspace_runs_persistent_loop(n, T):
     """A workspace holding one workgroup's slots forces every workgroup to
-    walk several blocks (the persistent loop) and must give the same bits;
+    walk several blocks (the persistent loop) and must give the same bits
+    (dCodebook up to the order of its slot sums);
     at T = 0.003 this is the double-float kernel with dCodebook, whose
     step-0 (G, A) history entries are filled once per call and must stay
     valid for every later block of the slot, and whose dCodebook partials
@@ -260,16 +273,14 @@ def test_small_workspace_runs_persistent_loop(n, T):
             assert e.status == -3
     assert per_wg is not None and per_wg < big
     _say(f"[parity] n={n} T={T}: one-slot workspace of {per_wg} bytes (full {big})")
-    for a, b in zip(full, out):
-        np.testing.assert_array_equal(a, b)
+    assert_same_up_to_dc_order(full, out)
 
 
 @pytest.mark.parametrize("n,B,L", [(12, 24, 20), (16, 16, 12)])
 def test_low_temperature_every_grid_size(n, B, L):
     """The double-float kernel under every workspace size from one slot up:
-    grids of 1 to B workgroups, with and without the persistent loop, and
-    both placements of the per-slot tangent vectors (XCD-contiguous when the
-    grid is a multiple of 8, by slot otherwise) must give the same bits, and
+    grids of 1 to B workgroups, with and without the persistent loop, must
+    give the same results (dCodebook up to the order of its slot sums), and
     the full-size run must match the oracle."""
     k, T = 2, 0.003
     w, c, g = WL.random_case(4242 + n, B, L, n)
@@ -285,8 +296,7 @@ def test_low_temperature_every_grid_size(n, B, L):
             assert e.status == -3
             continue
         runs += 1
-        for a, b in zip(full, out):
-            np.testing.assert_array_equal(a, b)
+        assert_same_up_to_dc_order(full, out)
     _say(f"[parity] lowT grids n={n}: {runs} workspace sizes ran")
     assert runs >= B // 2
 
