@@ -120,6 +120,32 @@ def issue_rates(iters=16384, grid=4096, ops=None):
             "overlapped_model_s": overlap_s}
 
 
+def chain_intervals(iters=4096):
+    """Mean shader cycles per VALU instruction of one wave with 2, 4, 8, 16 and
+    32 independent chains per lane, for v_fma_f32 and v_add_f32, at 1, 2 and 4
+    waves per SIMD: {op: {waves_per_simd: {chains: cycles}}}."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2605_10655_amd", "libissue_rates.so"))
+    lib.issue_rate_chains.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_double)]
+    lib.issue_rate_chains.restype = ctypes.c_int
+    out = {}
+    for op, name in ((0, "fma_f32"), (1, "add_f32")):
+        out[name] = {}
+        for wps in (1, 2, 4):
+            row = {}
+            for chains in (2, 4, 8, 16, 32):
+                ms, cyc, clk = ctypes.c_float(), ctypes.c_double(), ctypes.c_double()
+                rc = lib.issue_rate_chains(op, chains, iters, 256 * wps, ctypes.byref(ms),
+                                           ctypes.byref(cyc), ctypes.byref(clk))
+                if rc != 0:
+                    raise RuntimeError(f"chain probe {name}/{chains} failed ({rc})")
+                row[chains] = round(cyc.value, 2)
+            out[name][wps] = row
+    return out
+
+
 def roofline_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED, dc=False) -> float:
     n_v = ALG_VALU_PER_GROUP + (ALG_DC_VALU_PER_GROUP if dc else 0.0)
     t_group = n_v / r_v + ALG_TRANS_PER_GROUP / r_t
@@ -469,9 +495,17 @@ def run_rates(args):
            "fma_exp_1to1_s": r["fma_exp_1to1_s"],
            "serialised_model_s": r["serialised_model_s"],
            "overlapped_model_s": r["overlapped_model_s"],
-           "probe": "csrc/issue_rates.hip: 2048 workgroups x 256 lanes, 16384 steps of 8 "
+           "probe": "csrc/issue_rates.hip: 4096 workgroups x 256 lanes, 16384 steps of 8 "
                     "independent chains per lane"}
     print(json.dumps(rec), flush=True)
+    # dependency latency: shader cycles per VALU instruction of one wave for
+    # 2..32 independent chains per lane at 1, 2 and 4 waves per SIMD
+    lat = chain_intervals()
+    print(json.dumps({"metric": "gfx950 cycles per VALU instruction per wave, by independent "
+                                "chains per lane (v_fma_f32 VOP3 / v_add_f32 VOP2)",
+                      "cycles_per_instr": lat,
+                      "probe": "csrc/issue_rates.hip chain_kernel: 256 x waves-per-SIMD "
+                               "workgroups of 256 lanes, 4096 x 4 steps per chain"}), flush=True)
 
 
 def run_ldlq(args):

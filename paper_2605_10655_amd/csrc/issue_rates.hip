@@ -3,7 +3,11 @@
 //
 // Every lane runs NCH independent chains of one operation (or an interleave
 // of two), so that no instruction waits on the result of the one before it
-// and the issue rate of the SIMD is what limits the kernel.  The host times
+// and, at full occupancy, the issue rate of the SIMD is what limits the
+// kernel.  A second kernel (chain_kernel) varies the number of chains at low
+// occupancy: with few chains per lane a wave waits on VALU results, which
+// exposes the result latency and the per-wave instruction interval a
+// kernel with that much independent work can reach.  The host times
 // one launch with HIP events; the kernel also reads the shader clock
 // counter (s_memtime) and the constant 100 MHz counter (s_memrealtime) at
 // the start and end of every wave, from which the shader clock during the
@@ -83,6 +87,64 @@ __global__ void __launch_bounds__(256) probe_kernel(int iters, float seed, float
   }
 }
 
+// Dependency-latency probe: NC independent chains per lane of one operation
+// whose constants come from kernel arguments (no literal operands), 4 chain
+// steps per loop iteration.  OP 0: v_fma_f32 (VOP3, 8-byte encoding),
+// OP 1: v_add_f32 (VOP2, 4 bytes).  With few chains every instruction waits
+// on the result of one NC instructions earlier, so the per-wave interval
+// exposes the VALU result latency; with many it approaches the issue limit.
+template <int NC, int OP>
+__global__ void __launch_bounds__(256) chain_kernel(int iters, float seed, float a, float b, float* sink,
+                                                     int64_t* clocks) {
+  const int tid = threadIdx.x;
+  uint64_t c0 = 0, r0 = 0;
+  if ((tid & 63) == 0) {
+    c0 = clock64();
+    r0 = wall_clock64();
+  }
+  float x[NC];
+#pragma unroll
+  for (int i = 0; i < NC; ++i) x[i] = seed + 0.01f * (float)(i + 1) + 1e-6f * (float)tid;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        if constexpr (OP == 0) x[i] = fmaf(x[i], a, b);
+        if constexpr (OP == 1) x[i] = x[i] + b;
+      }
+    }
+  }
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < NC; ++i) acc += x[i];
+  if (acc == 1234.5f) sink[blockIdx.x * blockDim.x + tid] = acc;
+  if ((tid & 63) == 0) {
+    const uint64_t c1 = clock64(), r1 = wall_clock64();
+    const int wave = blockIdx.x * (blockDim.x >> 6) + (tid >> 6);
+    clocks[2 * wave + 0] = (int64_t)(c1 - c0);
+    clocks[2 * wave + 1] = (int64_t)(r1 - r0);
+  }
+}
+
+using ChainFn = void (*)(int, float, float, float, float*, int64_t*);
+
+ChainFn pick_chain(int op, int chains) {
+  switch (op * 100 + chains) {
+    case 2: return chain_kernel<2, 0>;
+    case 4: return chain_kernel<4, 0>;
+    case 8: return chain_kernel<8, 0>;
+    case 16: return chain_kernel<16, 0>;
+    case 32: return chain_kernel<32, 0>;
+    case 102: return chain_kernel<2, 1>;
+    case 104: return chain_kernel<4, 1>;
+    case 108: return chain_kernel<8, 1>;
+    case 116: return chain_kernel<16, 1>;
+    case 132: return chain_kernel<32, 1>;
+    default: return nullptr;
+  }
+}
+
 using ProbeFn = void (*)(int, float, float*, int64_t*);
 
 ProbeFn pick(int op) {
@@ -99,6 +161,58 @@ ProbeFn pick(int op) {
     case 9: return probe_kernel<9>;
     default: return nullptr;
   }
+}
+
+// Launches `launch` once untimed and once timed (HIP events) on `grid`
+// workgroups of 256 threads.  Outputs: ms, the median shader clock over
+// waves (clock ticks / real time) and the mean shader cycles per wave.
+template <class F>
+int timed_launches(int grid, F launch, float* ms, double* clock_hz, double* cycles_per_wave) {
+  const int waves = grid * 4;
+  float* sink = nullptr;
+  int64_t* clk = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = 0;
+  if (hipMalloc(&sink, (size_t)grid * 256 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&clk, (size_t)waves * 2 * sizeof(int64_t)) != hipSuccess ||
+      hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    rc = -4;
+  } else {
+    launch(sink, clk);
+    (void)hipEventRecord(e0, 0);
+    launch(sink, clk);
+    (void)hipEventRecord(e1, 0);
+    if (hipEventSynchronize(e1) != hipSuccess || hipGetLastError() != hipSuccess) rc = -4;
+  }
+  if (rc == 0) {
+    (void)hipEventElapsedTime(ms, e0, e1);
+    int64_t* h = new int64_t[(size_t)waves * 2];
+    if (hipMemcpy(h, clk, (size_t)waves * 2 * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess) {
+      rc = -4;
+    } else {
+      int rate_khz = 100000;
+      int dev = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+        rate_khz = 100000;
+      std::vector<double> f;
+      double cyc = 0.0;
+      for (int i = 0; i < waves; ++i) {
+        cyc += (double)h[2 * i];
+        if (h[2 * i + 1] > 0)
+          f.push_back((double)h[2 * i] / ((double)h[2 * i + 1] / ((double)rate_khz * 1e3)));
+      }
+      std::sort(f.begin(), f.end());
+      *clock_hz = f.empty() ? 0.0 : f[f.size() / 2];
+      *cycles_per_wave = cyc / (double)waves;
+    }
+    delete[] h;
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (sink) (void)hipFree(sink);
+  if (clk) (void)hipFree(clk);
+  return rc;
 }
 
 }  // namespace
@@ -124,49 +238,36 @@ int issue_rate_ops_per_step(int op, double* valu, double* trans) {
 int issue_rate_run(int op, int iters, int grid, float* ms, double* lane_ops, double* clock_hz) {
   ProbeFn fn = pick(op);
   if (!fn || iters < 1 || grid < 1 || !ms || !lane_ops || !clock_hz) return -1;
-  const int waves = grid * 4;
-  float* sink = nullptr;
-  int64_t* clk = nullptr;
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  int rc = 0;
-  if (hipMalloc(&sink, (size_t)grid * 256 * sizeof(float)) != hipSuccess ||
-      hipMalloc(&clk, (size_t)waves * 2 * sizeof(int64_t)) != hipSuccess ||
-      hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
-    rc = -4;
-  } else {
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, 0, iters, 0.25f, sink, clk);
-    (void)hipEventRecord(e0, 0);
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, 0, iters, 0.25f, sink, clk);
-    (void)hipEventRecord(e1, 0);
-    if (hipEventSynchronize(e1) != hipSuccess || hipGetLastError() != hipSuccess) rc = -4;
-  }
+  double cyc = 0.0;
+  const int rc = timed_launches(
+      grid, [&](float* sink, int64_t* clk) {
+        hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, 0, iters, 0.25f, sink, clk);
+      },
+      ms, clock_hz, &cyc);
   if (rc == 0) {
-    (void)hipEventElapsedTime(ms, e0, e1);
     double v = 0, t = 0;
     issue_rate_ops_per_step(op, &v, &t);
     *lane_ops = (double)grid * 256.0 * (double)iters * NCH * (v + t);
-    int64_t* h = new int64_t[(size_t)waves * 2];
-    if (hipMemcpy(h, clk, (size_t)waves * 2 * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess) {
-      rc = -4;
-    } else {
-      int rate_khz = 100000;
-      int dev = 0;
-      if (hipGetDevice(&dev) != hipSuccess ||
-          hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
-        rate_khz = 100000;
-      std::vector<double> f;
-      for (int i = 0; i < waves; ++i)
-        if (h[2 * i + 1] > 0)
-          f.push_back((double)h[2 * i] / ((double)h[2 * i + 1] / ((double)rate_khz * 1e3)));
-      std::sort(f.begin(), f.end());
-      *clock_hz = f.empty() ? 0.0 : f[f.size() / 2];
-    }
-    delete[] h;
   }
-  if (e0) (void)hipEventDestroy(e0);
-  if (e1) (void)hipEventDestroy(e1);
-  if (sink) (void)hipFree(sink);
-  if (clk) (void)hipFree(clk);
+  return rc;
+}
+
+// Dependency-latency probe: `chains` (2, 4, 8, 16 or 32) independent chains
+// per lane of v_fma_f32 (op 0) or v_add_f32 (op 1), `iters` x 4 steps each,
+// on `grid` workgroups of 256 threads (grid / 256 waves per SIMD at 256
+// CUs).  Output: ms, the shader clock, and the mean shader cycles per VALU
+// instruction of one wave (cycles per wave / instructions per wave).
+int issue_rate_chains(int op, int chains, int iters, int grid, float* ms, double* cycles_per_instr,
+                      double* clock_hz) {
+  ChainFn fn = pick_chain(op, chains);
+  if (!fn || iters < 1 || grid < 1 || !ms || !cycles_per_instr || !clock_hz) return -1;
+  double cyc = 0.0;
+  const int rc = timed_launches(
+      grid, [&](float* sink, int64_t* clk) {
+        hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, 0, iters, 0.25f, 0.999f, 1e-3f, sink, clk);
+      },
+      ms, clock_hz, &cyc);
+  if (rc == 0) *cycles_per_instr = cyc / ((double)iters * 4.0 * (double)chains);
   return rc;
 }
 

@@ -50,3 +50,32 @@ def test_measured_traffic_is_keyed_by_path_and_source_digest():
         assert value > 0
     d = bench.kernel_source_digest()
     assert len(d) == 16 and d == bench.kernel_source_digest()
+
+
+def test_issue_rate_probe_library_exports_and_rejects_bad_arguments():
+    """The probe library the roofline is priced with: its three entry points
+    exist, and bad arguments are refused before any GPU call."""
+    import ctypes
+    import os
+    path = os.path.join(bench.ROOT, "paper_2605_10655_amd", "libissue_rates.so")
+    if not os.path.exists(path):
+        import pytest
+        pytest.skip("libissue_rates.so not built")
+    lib = ctypes.CDLL(path)
+    for name in ("issue_rate_run", "issue_rate_chains", "issue_rate_ops_per_step"):
+        assert hasattr(lib, name)
+    ms, a, b = ctypes.c_float(), ctypes.c_double(), ctypes.c_double()
+    lib.issue_rate_chains.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_double)]
+    assert lib.issue_rate_chains(0, 3, 16, 256, ctypes.byref(ms), ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.issue_rate_chains(2, 8, 16, 256, ctypes.byref(ms), ctypes.byref(a), ctypes.byref(b)) == -1
+    assert lib.issue_rate_chains(0, 8, 0, 256, ctypes.byref(ms), ctypes.byref(a), ctypes.byref(b)) == -1
+    lib.issue_rate_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
+                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    assert lib.issue_rate_run(10, 16, 256, ctypes.byref(ms), ctypes.byref(a), ctypes.byref(b)) == -1
+    v, t = ctypes.c_double(), ctypes.c_double()
+    lib.issue_rate_ops_per_step.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_double)]
+    assert lib.issue_rate_ops_per_step(5, ctypes.byref(v), ctypes.byref(t)) == 0
+    assert (v.value, t.value) == (1.0, 1.0)
