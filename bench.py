@@ -160,13 +160,15 @@ def roofline_vec_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED) -> float:
 # HBM bytes per launch of the timed kernel, from two rocprofv3 --pmc passes
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map a plain 1 GiB
 # device copy's readings to its 1 GiB read and written), keyed by a digest of
-# the sources that define that kernel (its header and the argument block).
+# the sources that define that kernel (its headers, translation unit and
+# build flags, and the argument block).
 # Any other source reports null.
 MEASURED_TRAFFIC = {
-    ("fwd_vjp", "e91eb97e86fe239b"): 2.68522e8 * 1024 * 2.0 + 5.34823e8 * 1024 * 1.0,
+    ("fwd_vjp", "9b8a8b12e826c6be"): 2.68511e8 * 1024 * 2.0 + 5.34878e8 * 1024 * 1.0,
 }
-KERNEL_SOURCES = {"fwd_vjp": ("bcjr_kernels.h", "bcjr_internal.h"),
-                  "vec": ("bcjr_vec_kernels.h", "bcjr_internal.h")}
+KERNEL_SOURCES = {"fwd_vjp": ("bcjr_rot_kernels.h", "bcjr_rot.hip", "bcjr_device.h", "bcjr_internal.h",
+                              "../build.py"),
+                  "vec": ("bcjr_vec_kernels.h", "bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h")}
 
 
 def kernel_source_digest(path: str = "fwd_vjp") -> str:

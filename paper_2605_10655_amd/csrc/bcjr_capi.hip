@@ -24,6 +24,12 @@ constexpr size_t kScratchBytes = BCJR_NOALLOC_SCRATCH_BYTES;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace bcjr {
+
+// The rotating-exchange kernel for S = 65536, k = 2 (bcjr_rot.hip, its own
+// translation unit and instruction scheduler).
+const void* fb_rot_kernel();
+int fb_rot_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
+
 namespace {
 
 constexpr int kDeviceCUs = 256;     // MI355X; used only to size the workspace query
@@ -468,10 +474,14 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   const FbLayout lay = fb_layout(L, n, k, vjp, dc);
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
+  // S = 65536, k = 2, fwd + dW: the rotating in-place exchange (one block
+  // per 512-thread workgroup, the same workspace layout and arguments)
+  const bool rot = vjp && !dc && n == 16 && k == 2;
+  const void* kern = rot ? fb_rot_kernel() : (const void*)fn;
   const size_t lds = fb_lds_bytes(f, n, k);
   int herr = 0;
   if (ws_bytes < cs_bytes(n)) return BCJR_ERR_WORKSPACE;
-  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes - cs_bytes(n), lay.slot, &herr);
+  const int64_t grid = grid_size(kern, f, lds, B, ws_bytes - cs_bytes(n), lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
   const int64_t slots = grid * f.bpw;
@@ -508,8 +518,12 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
       if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
     }
   }
-  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
-  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (rot) {
+    if (fb_rot_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+  } else {
+    hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
   if (dc) {
     const int64_t used = slots < B ? slots : B;
     hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
