@@ -117,8 +117,9 @@ int bcjr_soft_codeword_fwd_vjp(const float *w, int64_t B, int64_t L, const float
  * array (fewer than with a full-size workspace at large S; the results do
  * not depend on the count) and returns BCJR_ERR_WORKSPACE when even one
  * block slot does not fit: at state_bits 16, k 2 one slot takes about
- * 64 MiB at L = 256 (97 MiB below T = 0.04, which also needs 8 B x B x L for
- * the reference decode).  Every call on a GPU uses that GPU's one array:
+ * 64 MiB at L = 256 with dCodebook, 32 MiB without (below T = 0.04, 73 and
+ * 37 MiB, plus 8 B x B x L for the reference decode).  Every call on a GPU
+ * uses that GPU's one array:
  * calls that may overlap on the same GPU (two streams, two threads) race
  * and must be serialised by the caller.  What the kernels need zeroed is
  * cleared by kernels in the call (no memset), so the call can be captured. */

@@ -42,33 +42,37 @@ def _p(t):
     return ctypes.c_void_p(0 if t is None else t.data_ptr())
 
 
-def _noalloc(lib, w, c, n, k, T, g):
+def _noalloc(lib, w, c, n, k, T, g, want_dc=True):
     d = torch.device("cuda:0")
     wd, cd, gd = (torch.from_numpy(a).to(d) for a in (w, c, g))
     B, L = w.shape
     ws, dW = torch.empty_like(wd), torch.empty_like(wd)
     lz = torch.empty(B, dtype=torch.float32, device=d)
-    dc = torch.full_like(cd, np.nan)
+    dc = torch.full_like(cd, np.nan) if want_dc else None
     stream = torch.cuda.current_stream()
     rc = lib.bcjr_soft_codeword_fwd_vjp_noalloc(_p(wd), B, L, _p(cd), n, k, float(T), _p(gd), _p(ws),
                                                 _p(lz), _p(dW), _p(dc),
                                                 ctypes.c_void_p(stream.cuda_stream))
     assert rc == 0, P.bcjr_status_string(rc)
     torch.cuda.synchronize()
-    return tuple(t.cpu().numpy() for t in (ws, lz, dW, dc))
+    return tuple(None if t is None else t.cpu().numpy() for t in (ws, lz, dW, dc))
 
 
-def _reference(w, c, n, k, T, g):
+def _reference(w, c, n, k, T, g, want_dc=True):
     d = torch.device("cuda:0")
     out = P.bcjr_soft_codeword_fwd_vjp(*(torch.from_numpy(a).to(d) for a in (w, c)), n, k, T,
-                                       torch.from_numpy(g).to(d))
+                                       torch.from_numpy(g).to(d), want_dCodebook=want_dc)
     torch.cuda.synchronize()
-    return tuple(t.cpu().numpy() for t in out)
+    return tuple(None if t is None else t.cpu().numpy() for t in out)
 
 
 def _compare(got, ref, what):
     for name, a, b in zip(("w_soft", "logZ", "dW"), got[:3], ref[:3]):
         np.testing.assert_array_equal(a, b, err_msg=f"{what}: {name}")
+    if got[3] is None:
+        assert ref[3] is None
+        _say(f"[noalloc] {what}: outputs bit-identical")
+        return
     a, b = got[3].astype(np.float64), ref[3].astype(np.float64)
     dev = np.abs(a - b) / np.maximum(np.abs(a) + np.abs(b), 1e-30)
     _say(f"[noalloc] {what}: per-block outputs bit-identical; dc max rel dev {dev.max():.2e}")
@@ -88,6 +92,11 @@ def test_noalloc_matches_workspace_entry_point_on_two_calls(lib):
     _say("[noalloc] call 2: n=12 k=2 B=7 L=20 T=0.003")
     _compare(_noalloc(lib, w2, c2, 12, 2, 0.003, g2), _reference(w2, c2, 12, 2, 0.003, g2),
              "call 2")
+    # third: S = 65536 without dCodebook, the rotating-exchange kernel
+    w3, c3, g3 = WL.random_case(9003, 5, 16, 16)
+    _say("[noalloc] call 3: n=16 k=2 B=5 L=16 T=0.1, no dCodebook")
+    _compare(_noalloc(lib, w3, c3, 16, 2, 0.1, g3, want_dc=False),
+             _reference(w3, c3, 16, 2, 0.1, g3, want_dc=False), "call 3")
 
 
 def test_noalloc_refuses_a_slot_larger_than_the_scratch(lib):
