@@ -205,7 +205,7 @@ def cpu_baseline(target_s: float = 15.0):
     wl = WL.workload(4)
     cores = O.default_threads()
     c = WL.codebook(4)
-    w = WL.weights(4, rows=8)                       # 64 blocks available
+    w = WL.weights(4, rows=32)                      # 256 blocks available
     g = WL.upstream(4, B=w.shape[0])
     T = float(np.float32(wl.temps[0]))
     # calibrate with one block per core, then scale to ~target_s
@@ -563,7 +563,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", choices=("fwd_vjp", "ste", "vec", "anneal", "anneal_calls", "ldlq",
                                        "rates"), default="fwd_vjp")
