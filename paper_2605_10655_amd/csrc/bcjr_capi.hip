@@ -259,6 +259,29 @@ VitFn vit_pick(int n, int k, const Family& f) {
   }
 }
 
+// the fp32 min-sum decode of the centring reference, same families
+template <int KB>
+VitFn vit_ref_pick_kb(int n, const Family& f) {
+  if (f.sgmax == 1) return viterbi_ref_kernel<KB, 0, 1, 256>;
+  if constexpr (KB < 3) {
+    constexpr int n512 = 2 * KB + 9;
+    if (n == n512) return viterbi_ref_kernel<KB, n512, 2, 256>;
+    if (n == n512 + 1) return viterbi_ref_kernel<KB, n512 + 1, 4, 256>;
+    if (n == n512 + 2) return viterbi_ref_kernel<KB, n512 + 2, 8, 256>;
+    if (n == n512 + 3) return viterbi_ref_kernel<KB, n512 + 3, 4, 1024>;
+  }
+  return nullptr;
+}
+
+VitFn vit_ref_pick(int n, int k, const Family& f) {
+  switch (k) {
+    case 1: return vit_ref_pick_kb<1>(n, f);
+    case 2: return vit_ref_pick_kb<2>(n, f);
+    case 3: return vit_ref_pick_kb<3>(n, f);
+    default: return nullptr;
+  }
+}
+
 int common_checks(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
                   bool vjp) {
   if (B < 0 || L < 1 || k < 1 || n < k || n > 16) return BCJR_ERR_INVALID_ARG;
@@ -374,14 +397,16 @@ int run_gen_viterbi(const float* w, int64_t B, int64_t L, const float* codebook,
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
 }
 
+// approx: the fp32 decode of the centring reference (viterbi_ref_kernel)
+// instead of the exact one; the generic family always decodes exactly
 int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
                 int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
-                hipStream_t stream) {
+                hipStream_t stream, bool approx = false) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
   if (!supported(n, k))
     return run_gen_viterbi(w, B, L, codebook, n, k, states, w_hard, workspace, ws_bytes, stream);
   const Family f = family(n, k, false);
-  VitFn fn = vit_pick(n, k, f);
+  VitFn fn = approx ? vit_ref_pick(n, k, f) : vit_pick(n, k, f);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
   const size_t lds = vit_lds_bytes(f, n, k);
   const size_t slot = vit_slot_bytes(L, n, k);
@@ -418,7 +443,7 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
     int32_t* states = reinterpret_cast<int32_t*>(ws + pre / 2);
     rest = ws + pre;
     rest_bytes = ws_bytes - pre;
-    int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream);
+    int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream, true);
     if (st != BCJR_OK) return st;
     ref = w_hard;
   }

@@ -1574,4 +1574,171 @@ __global__ void __launch_bounds__(NT) viterbi_kernel(VitArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Approximate min-sum decode, used only for the centring reference of the
+// low-temperature VJP (fb_kernel_hp): the same recursion, digits and
+// traceback as viterbi_kernel with fp32 path metrics (exact ties and
+// rounding-level near-ties may resolve differently; the VJP's mathematics
+// holds for any reference, which only has to follow the posterior to keep
+// the fp32 tangent well conditioned).  The metric vector is ping-ponged
+// between two S/K planes in LDS (the footprint of viterbi_kernel's two
+// 32-bit planes): one barrier per step and no metrics held across it.
+// ---------------------------------------------------------------------------
+template <int KB, int NB, int SGMAX, int NT>
+__global__ void __launch_bounds__(NT) viterbi_ref_kernel(VitArgs a) {
+  constexpr int K = 1 << KB;
+  extern __shared__ float ldsv[];
+  const int n = NB ? NB : a.n;
+  const int GS = 1 << (n - KB);
+  const int NSG = 1 << (n - 2 * KB);
+  const int SGT = NB ? SGMAX : a.sgt;
+  const int TPB = NSG / SGT;
+  const int BPW = NT / TPB;
+  const int tid = threadIdx.x;
+  const int bw = tid / TPB;
+  const int tb = tid - bw * TPB;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int width = TPB < 64 ? TPB : 64;
+  const int rw = TPB > 64 ? TPB / 64 : 1;
+  const int64_t L = a.L;
+  float* const m0 = ldsv + (size_t)bw * 2 * GS;   // plane read at even steps
+  float* const m1 = m0 + GS;                      // plane read at odd steps
+  float* redv = ldsv + (size_t)BPW * 2 * GS;      // [waves]
+  int* redi = reinterpret_cast<int*>(redv + NT / 64);  // [waves]
+  const bool lane_rows = TPB >= 64;
+  const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
+  const uint32_t voK = (uint32_t)tb << (KB + 2);
+
+  for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    const int64_t blk = base + bw;
+    const bool valid = blk < a.B;
+    const int64_t bb = valid ? blk : a.B - 1;
+    const int64_t slot = (int64_t)blockIdx.x * BPW + bw;
+    const float* wb = a.w + bb * L;
+    const int64_t bbu = lane_rows ? (int64_t)__builtin_amdgcn_readfirstlane((int)bb) : 0;
+    const float* wbu = a.w + bbu * L;
+    uint8_t* bp = a.bp + slot * L * GS;
+
+    for (int i = tb; i < GS; i += TPB) m0[i] = 0.f;
+    __syncthreads();
+    float bestv = INFINITY;
+    int besti = 0x7fffffff;
+    float wnx = lane_rows ? ld_uniform(wbu, 0) : 0.f;
+    float pc[K][K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (j << (n - KB)) * 4, pc[j]);
+    for (int64_t t = 0; t < L; ++t) {
+      float wt;
+      if (lane_rows) {
+        wt = wnx;
+        wnx = ld_uniform(wbu, t + 1 < L ? t + 1 : t);
+      } else {
+        wt = wb[t];
+      }
+      const float* min_ = (t & 1) ? m1 : m0;
+      float* mout = (t & 1) ? m0 : m1;
+#pragma unroll
+      for (int i = 0; i < SGMAX; ++i) {
+        if (i < SGT) {
+          const int sg = tb + i * TPB;
+          float Min[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) Min[j] = min_[j * NSG + sg];
+          float cc[K][K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+#pragma unroll
+            for (int u = 0; u < K; ++u) cc[j][u] = pc[j][u];
+          }
+          {  // the next super-group's rows (the first of the next step after the last)
+            const int ic = i + 1 < SGT ? i + 1 : 0;
+#pragma unroll
+            for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((ic * TPB) << KB)) * 4, pc[j]);
+          }
+          if (t < L - 1) {
+            uint8_t arg[K];
+            float mo[K];
+#pragma unroll
+            for (int u = 0; u < K; ++u) {
+              float best = 0.f;
+              int bj = 0;
+#pragma unroll
+              for (int j = 0; j < K; ++j) {
+                const float d = wt - cc[j][u];
+                const float v = fmaf(d, d, Min[j]);
+                if (j == 0 || v < best) {
+                  best = v;
+                  bj = j;
+                }
+              }
+              mo[u] = best;
+              arg[u] = (uint8_t)bj;
+            }
+            st_vec<K>(mout + sg * K, mo);
+            st_digits<K>(bp + (t + 1) * GS + sg * K, arg);
+          } else {
+#pragma unroll
+            for (int j = 0; j < K; ++j)
+#pragma unroll
+              for (int u = 0; u < K; ++u) {
+                const float d = wt - cc[j][u];
+                const float v = fmaf(d, d, Min[j]);
+                const int s = (j << (n - KB)) | (sg << KB) | u;
+                if (v < bestv || (v == bestv && s < besti)) {
+                  bestv = v;
+                  besti = s;
+                }
+              }
+          }
+          sg_fence();
+        }
+      }
+      if (t < L - 1) __syncthreads();
+    }
+    // block argmin (value, then state index)
+    for (int off = 1; off < width; off <<= 1) {
+      const float ov = __shfl_xor(bestv, off);
+      const int oi = __shfl_xor(besti, off);
+      if (ov < bestv || (ov == bestv && oi < besti)) {
+        bestv = ov;
+        besti = oi;
+      }
+    }
+    if (rw > 1 && lane == 0) {
+      redv[wave] = bestv;
+      redi[wave] = besti;
+    }
+    __syncthreads();  // also publishes every thread's bp stores to the block
+    if (rw > 1) {
+      const int first = (wave / rw) * rw;
+      bestv = redv[first];
+      besti = redi[first];
+      for (int q = 1; q < rw; ++q) {
+        const float ov = redv[first + q];
+        const int oi = redi[first + q];
+        if (ov < bestv || (ov == bestv && oi < besti)) {
+          bestv = ov;
+          besti = oi;
+        }
+      }
+    }
+    if (tb == 0 && valid) {
+      int32_t* st = a.states + bb * L;
+      float* wh = a.w_hard ? a.w_hard + bb * L : nullptr;
+      // (non-finite inputs leave no state below +inf: start from state 0)
+      int s = (unsigned)besti < (unsigned)(GS << KB) ? besti : 0;
+      st[L - 1] = s;
+      if (wh) wh[L - 1] = a.c[s];
+      for (int64_t t = L - 1; t >= 1; --t) {
+        const int v = s >> KB;
+        const int j = bp[t * GS + v];
+        s = (j << (n - KB)) | v;
+        st[t - 1] = s;
+        if (wh) wh[t - 1] = a.c[s];
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace bcjr

@@ -118,13 +118,12 @@ __global__ void __launch_bounds__(512) fb_kernel_rot(FbArgs a) {
   }
 
   for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) {
-    const int64_t bb = base;
+    const int64_t bb = base;            // the block (one per workgroup)
     const int64_t slot = blockIdx.x;
-    const float* gb = a.g + bb * L;
+    // its rows are wave-uniform: w_t and g_t come through scalar loads
     const int64_t bbu = (int64_t)__builtin_amdgcn_readfirstlane((int)bb);
     const float* wbu = a.w + bbu * L;
     const float* gbu = a.g + bbu * L;
-    (void)gb;
     const rsrc_t hist = make_rsrc(a.histHB + slot * L * hstep, (uint32_t)L * hstep * 4u);
     float* sm_mB = a.small + slot * 3 * L;  // shift of H_t (applied on read)
 

@@ -100,8 +100,11 @@ def test_soft_autograd_matches_oracle(n, k, B, L, T):
 @pytest.mark.parametrize("T", [0.2, 0.01])
 def test_ste_vjp_reproduces_soft_vjp(T):
     """With the forward's Viterbi codewords as reference, the STE backward is
-    the soft VJP exactly; below the precision switch it skips the decode the
-    soft VJP runs, and the bits still agree."""
+    the soft VJP.  Above the precision switch the bits agree.  Below it the
+    soft VJP centres on its own fp32 min-sum decode while the STE backward
+    takes the exact decode's codewords; any reference gives the same
+    gradient, so the two agree to the VJP's tolerance (and bit for bit
+    wherever the two decodes pick the same path)."""
     n, k, B, L = 16, 2, 5, 48
     w, c, g = WL.random_case(91, B, L, n)
     wd, cd, gd = dev(w), dev(c), dev(g)
@@ -109,8 +112,12 @@ def test_ste_vjp_reproduces_soft_vjp(T):
     sdW, sdc = P.bcjr_ste_vjp(wd, cd, n, k, T, wh, gd)
     vdW, vdc = P.bcjr_soft_codeword_vjp(wd, cd, n, k, T, gd)
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(host(sdW), host(vdW))
-    np.testing.assert_array_equal(host(sdc), host(vdc))
+    if T >= 0.04:
+        np.testing.assert_array_equal(host(sdW), host(vdW))
+        np.testing.assert_array_equal(host(sdc), host(vdc))
+    else:
+        check_grad(host(vdW), host(sdW).astype(np.float64), "soft vs ste dW")
+        check_grad(host(vdc), host(sdc).astype(np.float64), "soft vs ste dc")
 
 
 def test_ste_vjp_any_reference_same_gradient():
