@@ -29,6 +29,10 @@ namespace bcjr {
 // translation unit and instruction scheduler).
 const void* fb_rot_kernel();
 int fb_rot_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
+// its linear-domain form (blocks it marks are recomputed by the former)
+const void* fb_lin_kernel();
+int fb_lin_threads();
+int fb_lin_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
 
 namespace {
 
@@ -113,6 +117,9 @@ bool length_ok(int64_t L, int n, int k, bool vjp) {
 // The fp32 forward-backward path keeps the scaled codebook at the front of
 // its workspace.
 size_t cs_bytes(int n) { return align_up(((size_t)4) << n); }
+
+// Per-block flags of the linear-domain kernel (after the scaled codebook).
+size_t flag_bytes(int64_t B) { return align_up((size_t)B * sizeof(int32_t)); }
 
 struct FbLayout {
   size_t hist, histGA, small, dc, slot;
@@ -499,21 +506,30 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   const FbLayout lay = fb_layout(L, n, k, vjp, dc);
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
-  // S = 65536, k = 2, fwd + dW: the rotating in-place exchange (one block
-  // per 512-thread workgroup, the same workspace layout and arguments)
+  // S = 65536, k = 2, fwd + dW: the rotating in-place exchange in the
+  // linear domain (one block per 512-thread workgroup, the same workspace
+  // layout and arguments as the log-domain kernel, which recomputes the
+  // blocks the linear one marks)
   const bool rot = vjp && !dc && n == 16 && k == 2;
-  const void* kern = rot ? fb_rot_kernel() : (const void*)fn;
-  const size_t lds = fb_lds_bytes(f, n, k);
+  Family fl = f;
+  if (rot) fl.nt = fb_lin_threads();
+  const void* kern = rot ? fb_lin_kernel() : (const void*)fn;
+  const size_t lds = fb_lds_bytes(fl, n, k);
   int herr = 0;
-  if (ws_bytes < cs_bytes(n)) return BCJR_ERR_WORKSPACE;
-  const int64_t grid = grid_size(kern, f, lds, B, ws_bytes - cs_bytes(n), lay.slot, &herr);
+  const size_t front = cs_bytes(n) + (rot ? flag_bytes(B) : 0);
+  if (ws_bytes < front) return BCJR_ERR_WORKSPACE;
+  const int64_t grid = grid_size(kern, fl, lds, B, ws_bytes - front, lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const size_t lds_rot = fb_lds_bytes(f, n, k);
+  if (rot && hipFuncSetAttribute(fb_rot_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds_rot) != hipSuccess)
+    return BCJR_ERR_HIP;
   const int64_t slots = grid * f.bpw;
   const int64_t S = (int64_t)1 << n;
-  // [scaled codebook][slots: histories][slots: shifts][slots: dCodebook partials]
+  // [scaled codebook][block flags][slots: histories][slots: shifts][slots: dCodebook partials]
   float* cs = static_cast<float*>(workspace);
-  char* base = static_cast<char*>(workspace) + cs_bytes(n);
+  char* base = static_cast<char*>(workspace) + front;
   FbArgs a = {};
   a.w = w; a.g = g; a.c = codebook; a.cs = cs; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   const double Td = (double)T;
@@ -532,8 +548,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
   a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
                  : nullptr;
-  if (vjp) {  // the (H, B) rows of step L - 1 are zero for every block of a slot
+  if (vjp) {  // the (H, B) rows of step L - 1 are the same for every block of a slot
     const int64_t hstep = 2 * ((int64_t)1 << (n - k));
+    // log domain: H = 0, B = 0; linear domain: H = 1, B = 0
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
@@ -544,7 +561,18 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
     }
   }
   if (rot) {
-    if (fb_rot_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+    a.flags = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + cs_bytes(n));
+    const int64_t gs = (int64_t)1 << (n - k);
+    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * gs, 256)), dim3(256), 0,
+                       stream, a.histHB + (L - 1) * 2 * gs, L * 2 * gs, slots, gs, 1.f);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+    // the marked blocks again, in the log domain (its step L - 1 entries are 0)
+    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * gs, 256)), dim3(256), 0,
+                       stream, a.histHB + (L - 1) * 2 * gs, L * 2 * gs, slots, gs, 0.f);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    a.repair = 1;
+    if (fb_rot_launch((unsigned)grid, lds_rot, stream, a) != 0) return BCJR_ERR_HIP;
   } else {
     hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
@@ -937,7 +965,8 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
   const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
-  size_t bytes = cs_bytes(state_bits) + (size_t)slots * fb_layout(L, state_bits, k, vjp, vjp).slot;
+  size_t bytes = cs_bytes(state_bits) + (vjp ? flag_bytes(B) : 0) +
+                 (size_t)slots * fb_layout(L, state_bits, k, vjp, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
     const size_t vit = (size_t)(g2 * f2.bpw) * vit_slot_bytes(L, state_bits, k);
     const size_t hp = (size_t)(g2 * f2.bpw) * hp_layout(L, state_bits, k, true).slot;

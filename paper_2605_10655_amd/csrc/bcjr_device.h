@@ -168,6 +168,11 @@ __device__ __forceinline__ float ld_uniform(const float* p, int64_t i) {
   return ((cfloat*)p)[i];
 }
 
+__device__ __forceinline__ int ld_uniform_i(const int32_t* p, int64_t i) {
+  typedef const __attribute__((address_space(4))) int32_t cint;
+  return ((cint*)p)[i];
+}
+
 // Thread index rebuilt the same way from the wave index (a scalar).
 __device__ __forceinline__ uint32_t lane_tid(uint32_t wave) { return (wave << 6) + (uint32_t)lane_id(); }
 

@@ -39,6 +39,11 @@ struct FbArgs {
   // launch); small is [slots][4][L]
   double k2d;          // log2(e) / (2T) in fp64
   const float* bref;   // [B, L] centring reference of the backward tangent
+  // linear-domain kernel: per block 1 when its group vectors left the fp32
+  // range (the block is then recomputed by the log-domain kernel), else 0;
+  // with `repair` set, the log-domain kernel runs only the blocks marked 1
+  int32_t* flags;      // [B] or null
+  int repair;
 };
 
 // Bytes of one history step of the low-temperature kernel: 9 per group

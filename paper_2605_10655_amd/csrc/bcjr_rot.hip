@@ -1,8 +1,8 @@
-// bcjr_rot.hip -- the rotating-exchange forward-backward kernel
-// (bcjr_rot_kernels.h) in its own translation unit, built with the AMDGPU
+// bcjr_rot.hip -- the rotating-exchange forward-backward kernels
+// (bcjr_rot_kernels.h: log domain and linear domain) in their own translation unit, built with the AMDGPU
 // max-ilp instruction scheduler; the rest of the library keeps the default
 // one, under which the V = 2 kernel runs 8 % faster.  The dispatcher in
-// bcjr_capi.hip reaches the kernel through these two functions.
+// bcjr_capi.hip reaches the kernels through these functions.
 #include <hip/hip_runtime.h>
 
 #include "bcjr_rot_kernels.h"
@@ -14,6 +14,20 @@ const void* fb_rot_kernel() { return reinterpret_cast<const void*>(&fb_kernel_ro
 // 0 on success, -1 when the launch reports a HIP error
 int fb_rot_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a) {
   hipLaunchKernelGGL(fb_kernel_rot, dim3(grid), dim3(512), lds, stream, a);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+#ifndef BCJR_LIN_THREADS
+#define BCJR_LIN_THREADS 512
+#endif
+constexpr int kLinThreads = BCJR_LIN_THREADS;
+
+int fb_lin_threads() { return kLinThreads; }
+
+const void* fb_lin_kernel() { return reinterpret_cast<const void*>(&fb_kernel_lin<kLinThreads>); }
+
+int fb_lin_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a) {
+  hipLaunchKernelGGL(fb_kernel_lin<kLinThreads>, dim3(grid), dim3(kLinThreads), lds, stream, a);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -110,6 +110,12 @@ __global__ void __launch_bounds__(512) fb_kernel_rot(FbArgs a) {
 #pragma unroll
   for (int p = 0; p < 9; ++p) phtb ^= ((tb0 >> p) & 1u) ? rot::kPhiCol[p] : 0u;
   phtb = rot::rep(phtb);
+  // repair pass after the linear-domain kernel: only the blocks it marked
+  if (a.repair) {
+    int any = 0;
+    for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) any |= ld_uniform_i(a.flags, base);
+    if (!any) return;
+  }
   float cbr[SGT][K][K];
 #pragma unroll
   for (int i = 0; i < SGT; ++i) {
@@ -118,6 +124,7 @@ __global__ void __launch_bounds__(512) fb_kernel_rot(FbArgs a) {
   }
 
   for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) {
+    if (a.repair && !ld_uniform_i(a.flags, base)) continue;
     const int64_t bb = base;            // the block (one per workgroup)
     const int64_t slot = blockIdx.x;
     // its rows are wave-uniform: w_t and g_t come through scalar loads
@@ -376,6 +383,319 @@ __global__ void __launch_bounds__(512) fb_kernel_rot(FbArgs a) {
       xbar = fmaf(rv[3], r1, xbar) - cprev;
       r2 = r2 == 12u ? 0u : r2 + 2u;
     }
+    __syncthreads();
+  }
+}
+
+namespace rot {
+constexpr int kTopExp = 40;                  // a rescale puts the largest entry at 2^40
+constexpr float kTop = 1099511627776.0f;     // 2^40
+
+// e with x = m 2^e, 1 <= m < 2, for a positive normal x (-127 for zero or a
+// denormal, 128 for inf or NaN)
+__device__ __forceinline__ int exp_of(float x) { return (int)((__float_as_uint(x) >> 23) & 0xFFu) - 127; }
+}  // namespace rot
+
+// The same call (S = 65536, k = 2, fwd + w_soft + logZ + dW, no dCodebook) on
+// the same rotating layout, workspace and history, with the group vectors
+// kept in the linear domain instead of the log domain:
+//   G_{t+1}(v) = sum_j e_t(j, v) G_t(j, v >> 2),  H_{t-1}(v) = sum_b e_t(v, b) H_t(...),
+// e_t(s) = 2^(h_t(s)) = 2^(-(w'_t - c'_s)^2) (the Boltzmann weight of the
+// local field, Eq. boltzmann), and the tangents carried unnormalised
+// (G A and H B), so that a step needs one exponential per state and no
+// logarithm, maximum or reciprocal per group.  After each step the vector
+// is rescaled by an exact power of two that puts its largest entry at 2^40
+// (the exponent is folded into the next step's exponentials); fp32 then
+// holds every state within ~166 log2 units of the step's maximum at full
+// precision, where the states that carry the posterior lie within ~60-90
+// at T >= 0.04 on unit-variance data.  The marginals and the four dW moments
+// are products of the two sweeps' values, scale-invariant per step.
+//
+// A block whose vectors leave that range -- a step whose largest entry
+// falls below 2^-30 (a single-step decay of 70 log2 units, which the
+// posterior states would not survive) or the forward's per-step mass
+// sum_s alpha_t beta_t departing from Z by more than 2e-4 log2 units -- is
+// marked in a.flags and recomputed by fb_kernel_rot in its repair mode.
+template <int NT>
+__global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
+  constexpr int KB = 2, K = 4, n = 16;
+  constexpr int GS = 1 << (n - KB);        // 16384 groups
+  constexpr int NSG = 1 << (n - 2 * KB);   // 4096 super-groups
+  constexpr int TPB = NT, SGT = NSG / NT;
+  constexpr int TB_BITS = NT == 1024 ? 10 : 9;
+  static_assert(NT == 512 || NT == 1024, "512 or 1024 threads");
+  extern __shared__ float lds[];           // [GS] (value, tangent) pairs, then the reduction area
+  const int64_t L = a.L;
+  const float kap = a.kap;
+
+  RedCtx rc;
+  rc.width = 64;
+  rc.rw = TPB / 64;
+  rc.wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float* const red0 = lds + 2 * GS;
+
+  const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)4 << n);
+  const uint32_t tb0 = threadIdx.x;
+  const uint32_t voK = tb0 << (KB + 2);
+  constexpr uint32_t hstep = (uint32_t)GS * 2;   // floats per history step: H then B, [S/K] each
+  const uint32_t wave_s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint32_t phtb = 0;
+#pragma unroll
+  for (int p = 0; p < TB_BITS; ++p) phtb ^= ((tb0 >> p) & 1u) ? rot::kPhiCol[p] : 0u;
+  phtb = rot::rep(phtb);
+  float cbr[SGT][K][K];
+#pragma unroll
+  for (int i = 0; i < SGT; ++i) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, ((j << (n - KB)) + ((i * TPB) << KB)) * 4, cbr[i][j]);
+  }
+
+  for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) {
+    const int64_t bb = base;
+    const int64_t slot = blockIdx.x;
+    const int64_t bbu = (int64_t)__builtin_amdgcn_readfirstlane((int)bb);
+    const float* wbu = a.w + bbu * L;
+    const float* gbu = a.g + bbu * L;
+    const rsrc_t hist = make_rsrc(a.histHB + slot * L * hstep, (uint32_t)L * hstep * 4u);
+    float* sm_eH = a.small + slot * 3 * L;  // exponent of the stored H_t: stored = true * 2^e
+    bool bad = false;
+
+    // ------------------------------------------------------------------ S0
+    // Backward: H and the unnormalised tangent H B in the pair slots, in
+    // place; H_{L-1} = 1 is stored as 2^40.
+    for (int i = threadIdx.x; i < 2 * GS; i += NT) lds[i] = (i & 1) ? 0.f : rot::kTop;
+    __syncthreads();
+    int ex = rot::kTopExp;  // exponent of the vector being read
+    int off = 0;            // its rescale, folded into this step's exponentials
+    float lz2 = 0.f, xbar = 0.f;
+    float wnx = ld_uniform(wbu, L - 1);
+    float gnx = ld_uniform(gbu, L - 1);
+    uint32_t r2 = (uint32_t)(2 * (((L - 1) + 6) % 7));
+    for (int64_t t = L - 1;; --t) {
+      const uint32_t tid_s = lane_tid(wave_s);
+      const uint32_t vcH = tid_s * 4u;
+      rc.red = red0 + ((L - 1 - t) & 1) * (NT / 64) * kRed;
+      const float wt = wnx * kap, gt = gnx;
+      {
+        const int64_t tn = t > 0 ? t - 1 : 0;
+        wnx = ld_uniform(wbu, tn);
+        gnx = ld_uniform(gbu, tn);
+      }
+      const float noff = -(float)off;
+      const uint32_t rs = __builtin_amdgcn_readfirstlane(r2);
+      const uint32_t tslot = rot::slot8(phtb, rs);
+      const uint32_t soH = (uint32_t)t * hstep * 4u;
+      if (t == 0) {
+        // Z = sum_s alpha_0(s) beta_0(s) and E_p[g_0 c + B_0]
+        float ls = 0.f, ly = 0.f;
+#pragma unroll
+        for (int i = 0; i < SGT; ++i) {
+          uint32_t ts = tslot;
+          float wtl = wt;
+          pin_u(ts);
+          pin(wtl);
+          const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+          float Hin[K], Bin[K];
+#pragma unroll
+          for (int b = 0; b < K; ++b) {
+            const float2 v = rot::ld_pair(lds, si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs));
+            Hin[b] = v.x;
+            Bin[b] = v.y;
+          }
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+#pragma unroll
+            for (int b = 0; b < K; ++b) {
+              const float d = wtl - cbr[i][j][b];
+              const float e = ex2(fmaf(-d, d, noff));
+              ls = fmaf(e, Hin[b], ls);
+              ly = fmaf(e, fmaf(gt * cbr[i][j][b], Hin[b], Bin[b]), ly);
+            }
+          }
+          asm volatile("" ::: "memory");
+        }
+        float sv[2] = {ls, ly};
+        red_pre<2, 0u>(sv, rc);
+        if (threadIdx.x == 0) sm_eH[L - 1] = 0.f;  // the history's H_{L-1} entries are 1
+        __syncthreads();
+        red_post<2, 0u>(sv, rc);
+        if (!(sv[0] > 0.f && sv[0] < INFINITY)) bad = true;
+        lz2 = lg2(sv[0]) - (float)(ex - off);
+        xbar = sv[1] / sv[0];
+        if (threadIdx.x == 0 && a.logZ) a.logZ[bb] = (float)((double)lz2 * 0.69314718055994530942);
+        __syncthreads();
+        break;
+      }
+      float vmax[1] = {0.f};
+#pragma unroll
+      for (int i = 0; i < SGT; ++i) {
+        uint32_t ts = tslot;
+        float wtl = wt;
+        pin_u(ts);
+        pin(wtl);
+        const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+        uint32_t sl[K];
+#pragma unroll
+        for (int b = 0; b < K; ++b) sl[b] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs);
+        float Hin[K], Bin[K];
+#pragma unroll
+        for (int b = 0; b < K; ++b) {
+          const float2 v = rot::ld_pair(lds, sl[b]);
+          Hin[b] = v.x;
+          Bin[b] = v.y;
+        }
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          float e[K], u[K], d[K];
+#pragma unroll
+          for (int b = 0; b < K; ++b) {
+            d[b] = wtl - cbr[i][j][b];
+            e[b] = ex2(fmaf(-d[b], d[b], noff));
+            u[b] = e[b] * Hin[b];
+          }
+          const float hv0 = (u[0] + u[1]) + (u[2] + u[3]);
+          // H B_{t-1} = sum_b e_b (H_b g_t (c_b - w_t) + H B_b)
+          float tb = e[0] * Bin[0], td = u[0] * d[0];
+#pragma unroll
+          for (int b = 1; b < K; ++b) {
+            tb = fmaf(e[b], Bin[b], tb);
+            td = fmaf(u[b], d[b], td);
+          }
+          vmax[0] = fmaxf(vmax[0], hv0);
+          const float hv[1] = {hv0}, bv[1] = {fmaf(-gt, td, tb)};
+          rot::st_pair(lds, sl[j], hv[0], bv[0]);
+          const uint32_t so = soH - hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
+          buf_st<1, kStream>(hist, vcH, so, hv);
+          buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
+        }
+        asm volatile("" ::: "memory");
+      }
+      red_pre<1, 1u>(vmax, rc);
+      __syncthreads();
+      red_post<1, 1u>(vmax, rc);
+      ex -= off;  // the exponent of what this step wrote
+      if (threadIdx.x == 0) sm_eH[t - 1] = (float)ex;
+      if (!(vmax[0] >= 0x1p-30f && vmax[0] <= 0x1p100f)) bad = true;
+      off = bad ? 0 : rot::exp_of(vmax[0]) - rot::kTopExp;
+      r2 = r2 == 0 ? 12u : r2 - 2u;
+    }
+
+    // ------------------------------------------------------------------ S1
+    // Forward: G and the unnormalised tangent G A in the pair slots, in
+    // place; G_0 = 1 stored as 2^40.  A is centred on g_{t-1} w_soft_{t-1}
+    // when it is read (G A - c G).
+    for (int i = threadIdx.x; i < 2 * GS; i += NT) lds[i] = (i & 1) ? 0.f : rot::kTop;
+    __syncthreads();
+    const float dws = a.dws;
+    float cprev = 0.f;
+    ex = rot::kTopExp;
+    off = 0;
+    float pH[K], pB[K];
+    wnx = ld_uniform(wbu, 0);
+    gnx = ld_uniform(gbu, 0);
+    {
+      const uint32_t voH0 = lane_tid(wave_s) * K * 4u;
+      hist_row<K, true>(hist, voH0, 0, 0, (uint32_t)GS * 4u, pH, pB);
+    }
+    r2 = 0;
+    for (int64_t t = 0; t < L; ++t) {
+      const uint32_t tid_s = lane_tid(wave_s);
+      const uint32_t voH_s = tid_s * K * 4u;
+      rc.red = red0 + (t & 1) * (NT / 64) * kRed;
+      const float wt = wnx * kap, gt = gnx;
+      {
+        const int64_t tn = t + 1 < L ? t + 1 : t;
+        wnx = ld_uniform(wbu, tn);
+        gnx = ld_uniform(gbu, tn);
+      }
+      if (t > 0) xbar = fmaf(gt, wt, xbar);  // B_t no longer holds step t
+      const float eHt = sm_eH[t];
+      const float noff = -(float)off;
+      const uint32_t rs = __builtin_amdgcn_readfirstlane(r2);
+      const uint32_t tslot = rot::slot8(phtb, rs);
+      // max G_{t+1}, sum P, sum P c, sum P X, sum P c X with P = alpha_t beta_t
+      float rv[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < SGT; ++i) {
+        uint32_t ts = tslot;
+        float wtl = wt;
+        pin_u(ts);
+        pin(wtl);
+        const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+        uint32_t sl[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) sl[j] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)j << 12)), rs);
+        float Gin[K], Ain[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          const float2 v = rot::ld_pair(lds, sl[j]);
+          Gin[j] = v.x;
+          Ain[j] = fmaf(-cprev, v.x, v.y);
+        }
+        float Hc[K], Bc[K];
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+          Hc[u] = pH[u];
+          Bc[u] = pB[u];
+        }
+        {
+          const bool last = i + 1 >= SGT;
+          const int64_t tn = last && t + 1 < L ? t + 1 : t;
+          hist_row<K, true>(hist, voH_s, (uint32_t)tn * hstep * 4u,
+                            last ? 0u : (uint32_t)(i + 1) * TPB * K * 4u, (uint32_t)GS * 4u, pH, pB);
+        }
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+          float al[K], ac[K], ea[K];
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            const float d = wtl - cbr[i][j][u];
+            const float e = ex2(fmaf(-d, d, noff));
+            al[j] = e * Gin[j];
+            ac[j] = al[j] * cbr[i][j][u];
+            ea[j] = e * Ain[j];
+          }
+          const float go = (al[0] + al[1]) + (al[2] + al[3]);   // sum alpha
+          const float sac = (ac[0] + ac[1]) + (ac[2] + ac[3]);  // sum alpha c
+          const float sea = (ea[0] + ea[1]) + (ea[2] + ea[3]);  // sum e G A
+          float sacc = ac[0] * cbr[i][0][u], seac = ea[0] * cbr[i][0][u];
+#pragma unroll
+          for (int j = 1; j < K; ++j) {
+            sacc = fmaf(ac[j], cbr[i][j][u], sacc);
+            seac = fmaf(ea[j], cbr[i][j][u], seac);
+          }
+          const float aout = fmaf(gt, sac, sea);                // G A of the output group
+          rv[0] = fmaxf(rv[0], go);
+          const float Hu = Hc[u];
+          const float bx = fmaf(-xbar, Hu, Bc[u]);              // H (B - xbar)
+          rv[1] = fmaf(Hu, go, rv[1]);
+          rv[2] = fmaf(Hu, sac, rv[2]);
+          rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
+          rv[4] = fmaf(sac, bx, fmaf(Hu, fmaf(gt, sacc, seac), rv[4]));
+          rot::st_pair(lds, sl[u], go, aout);
+        }
+        asm volatile("" ::: "memory");
+      }
+      red_pre<5, 1u>(rv, rc);
+      __syncthreads();
+      red_post<5, 1u>(rv, rc);
+      const float r1 = 1.f / rv[1];
+      const float wst = rv[2] * r1;
+      if (threadIdx.x == 0) {
+        if (a.w_soft) a.w_soft[bb * L + t] = wst * a.inv_kap;
+        if (a.dW) a.dW[bb * L + t] = (rv[4] - wst * rv[3]) * r1 * dws;
+      }
+      // the step's mass sum_s alpha_t beta_t must equal Z
+      const float lzt = lg2(rv[1]) - (float)(ex - off) - eHt;
+      if (!(fabsf(lzt - lz2) <= 2e-4f)) bad = true;
+      if (!(rv[0] >= 0x1p-30f && rv[0] <= 0x1p100f)) bad = true;
+      ex -= off;
+      off = bad ? 0 : rot::exp_of(rv[0]) - rot::kTopExp;
+      cprev = gt * wst;
+      xbar = fmaf(rv[3], r1, xbar) - cprev;
+      r2 = r2 == 12u ? 0u : r2 + 2u;
+    }
+    if (threadIdx.x == 0) a.flags[bb] = bad ? 1 : 0;
     __syncthreads();
   }
 }
