@@ -548,9 +548,8 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
   a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
                  : nullptr;
-  if (vjp) {  // the (H, B) rows of step L - 1 are the same for every block of a slot
+  if (vjp && !rot) {  // the (H, B) rows of step L - 1 are zero for every block of a slot
     const int64_t hstep = 2 * ((int64_t)1 << (n - k));
-    // log domain: H = 0, B = 0; linear domain: H = 1, B = 0
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
@@ -561,15 +560,14 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
     }
   }
   if (rot) {
+    // the linear-domain kernel (it writes its own step L - 1 history), then
+    // the blocks it marked again in the log domain, whose planar step L - 1
+    // (H, B) entries are zero
     a.flags = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + cs_bytes(n));
-    const int64_t gs = (int64_t)1 << (n - k);
-    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * gs, 256)), dim3(256), 0,
-                       stream, a.histHB + (L - 1) * 2 * gs, L * 2 * gs, slots, gs, 1.f);
-    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
     if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
-    // the marked blocks again, in the log domain (its step L - 1 entries are 0)
-    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * gs, 256)), dim3(256), 0,
-                       stream, a.histHB + (L - 1) * 2 * gs, L * 2 * gs, slots, gs, 0.f);
+    const int64_t hstep = 2 * ((int64_t)1 << (n - k));
+    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
+                       stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
     a.repair = 1;
     if (fb_rot_launch((unsigned)grid, lds_rot, stream, a) != 0) return BCJR_ERR_HIP;

@@ -388,6 +388,20 @@ __global__ void __launch_bounds__(512) fb_kernel_rot(FbArgs a) {
 }
 
 namespace rot {
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) f32x2 lds_f2;
+
+// (value, tangent) pair at an absolute LDS byte address
+__device__ __forceinline__ float2 ld_pair_at(uint32_t addr) {
+  const f32x2 v = *reinterpret_cast<const lds_f2*>(addr);
+  const float x = v.x, y = v.y;
+  return make_float2(x, y);
+}
+__device__ __forceinline__ void st_pair_at(uint32_t addr, float a, float b) {
+  const f32x2 v = {a, b};
+  *reinterpret_cast<lds_f2*>(addr) = v;
+}
+
 constexpr int kTopExp = 40;                  // a rescale puts the largest entry at 2^40
 constexpr float kTop = 1099511627776.0f;     // 2^40
 
@@ -434,10 +448,14 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
   rc.wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* const red0 = lds + 2 * GS;
 
+  // LDS byte address of the pair vector: it starts on a 128 KiB boundary
+  // (at 0: the kernel has no static LDS), so it is XORed into the scalar
+  // slot terms and no address needs an add
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)4 << n);
   const uint32_t tb0 = threadIdx.x;
   const uint32_t voK = tb0 << (KB + 2);
-  constexpr uint32_t hstep = (uint32_t)GS * 2;   // floats per history step: H then B, [S/K] each
+  constexpr uint32_t hstep = (uint32_t)GS * 2;   // floats per history step: H then H B, [S/K] each
   const uint32_t wave_s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   uint32_t phtb = 0;
 #pragma unroll
@@ -459,6 +477,14 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
     const rsrc_t hist = make_rsrc(a.histHB + slot * L * hstep, (uint32_t)L * hstep * 4u);
     float* sm_eH = a.small + slot * 3 * L;  // exponent of the stored H_t: stored = true * 2^e
     bool bad = false;
+    {  // the history's step L - 1 entries: H = 1, then H B = 0
+      const float one[4] = {1.f, 1.f, 1.f, 1.f}, zero[4] = {0.f, 0.f, 0.f, 0.f};
+      const uint32_t so = (uint32_t)(L - 1) * hstep * 4u;
+      for (uint32_t q = threadIdx.x; q < (uint32_t)GS / 4; q += NT) {
+        buf_st<4, kStream>(hist, q * 16u, so, one);
+        buf_st<4, kStream>(hist, q * 16u, so + (uint32_t)GS * 4u, zero);
+      }
+    }
 
     // ------------------------------------------------------------------ S0
     // Backward: H and the unnormalised tangent H B in the pair slots, in
@@ -494,11 +520,11 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
           float wtl = wt;
           pin_u(ts);
           pin(wtl);
-          const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+          const uint32_t si = ts ^ (rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs) ^ lds0);
           float Hin[K], Bin[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) {
-            const float2 v = rot::ld_pair(lds, si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs));
+            const float2 v = rot::ld_pair_at(si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs));
             Hin[b] = v.x;
             Bin[b] = v.y;
           }
@@ -533,14 +559,14 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         float wtl = wt;
         pin_u(ts);
         pin(wtl);
-        const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+        const uint32_t si = ts ^ (rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs) ^ lds0);
         uint32_t sl[K];
 #pragma unroll
         for (int b = 0; b < K; ++b) sl[b] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs);
         float Hin[K], Bin[K];
 #pragma unroll
         for (int b = 0; b < K; ++b) {
-          const float2 v = rot::ld_pair(lds, sl[b]);
+          const float2 v = rot::ld_pair_at(sl[b]);
           Hin[b] = v.x;
           Bin[b] = v.y;
         }
@@ -563,7 +589,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
           }
           vmax[0] = fmaxf(vmax[0], hv0);
           const float hv[1] = {hv0}, bv[1] = {fmaf(-gt, td, tb)};
-          rot::st_pair(lds, sl[j], hv[0], bv[0]);
+          rot::st_pair_at(sl[j], hv[0], bv[0]);
+          // history entries of step t - 1: group j NSG + i TPB + tb
           const uint32_t so = soH - hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
           buf_st<1, kStream>(hist, vcH, so, hv);
           buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
@@ -621,14 +648,14 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         float wtl = wt;
         pin_u(ts);
         pin(wtl);
-        const uint32_t si = ts ^ rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs);
+        const uint32_t si = ts ^ (rot::slot8s(rot::rep(rot::phi((uint32_t)i << TB_BITS)), rs) ^ lds0);
         uint32_t sl[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) sl[j] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)j << 12)), rs);
         float Gin[K], Ain[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-          const float2 v = rot::ld_pair(lds, sl[j]);
+          const float2 v = rot::ld_pair_at(sl[j]);
           Gin[j] = v.x;
           Ain[j] = fmaf(-cprev, v.x, v.y);
         }
@@ -672,7 +699,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
           rv[2] = fmaf(Hu, sac, rv[2]);
           rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
           rv[4] = fmaf(sac, bx, fmaf(Hu, fmaf(gt, sacc, seac), rv[4]));
-          rot::st_pair(lds, sl[u], go, aout);
+          rot::st_pair_at(sl[u], go, aout);
         }
         asm volatile("" ::: "memory");
       }
