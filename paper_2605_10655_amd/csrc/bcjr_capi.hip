@@ -102,6 +102,16 @@ constexpr double kHighPrecisionK2 = 18.0;
 
 bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
 
+// The linear-domain kernel (S = 65536, k = 2, fwd + dW) keeps fp32 accuracy
+// down to a field scale of ~60 (T ~ 0.012: dW within 2.4e-5 of the oracle
+// on the q/o-projection workload, 3 % of its blocks marked for the repair
+// pass); it serves the call up to this field scale (T >= 0.0125).
+constexpr double kLinearK2 = 57.7;
+
+bool linear_ok(int n, int k, float T, bool dc) {
+  return n == 16 && k == 2 && !dc && 1.4426950408889634074 / (2.0 * (double)T) <= kLinearK2;
+}
+
 // The histories of one workgroup's blocks are addressed with 32-bit byte
 // offsets: blocks per workgroup x L x (S/K x 8 bytes; for the VJP 12, or
 // the low-temperature variant's hp_step_bytes where that is larger, at
@@ -432,9 +442,12 @@ int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int
 // `ref` is the centring reference of the backward tangent ([B, L]); when it
 // is null the minimum-distortion codewords are decoded into the front of the
 // workspace first.
+// With `repair_flags` (and ref = w), only the blocks marked there run: the
+// repair pass of the linear-domain kernel below T = 0.04.
 int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
               const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
-              float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream) {
+              float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream,
+              int32_t* repair_flags = nullptr) {
   const bool dc = dCodebook != nullptr;
   const Family f = fb_family(n, k, false);
   const HpLayout lay = hp_layout(L, n, k, dc);
@@ -469,6 +482,8 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.invT = (float)(1.0 / Td);
   a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
   a.bref = ref;
+  a.flags = repair_flags;
+  a.repair = repair_flags ? 1 : 0;
   a.histHB = reinterpret_cast<float*>(p);             p += slots * lay.hist;
   a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;  p += slots * lay.histGA;
   a.small = reinterpret_cast<float*>(p);              p += slots * lay.small;
@@ -498,7 +513,8 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (!supported(n, k))
     return run_gen(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace, ws_bytes,
                    stream, vjp);
-  if (vjp && use_high_precision(T))
+  const bool lin = vjp && linear_ok(n, k, T, dCodebook != nullptr);
+  if (vjp && use_high_precision(T) && !lin)
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
@@ -509,8 +525,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   // S = 65536, k = 2, fwd + dW: the rotating in-place exchange in the
   // linear domain (one block per 512-thread workgroup, the same workspace
   // layout and arguments as the log-domain kernel, which recomputes the
-  // blocks the linear one marks)
-  const bool rot = vjp && !dc && n == 16 && k == 2;
+  // blocks the linear one marks at T >= 0.04; below, the double-float
+  // kernel recomputes them)
+  const bool rot = lin;
   Family fl = f;
   if (rot) fl.nt = fb_lin_threads();
   const void* kern = rot ? fb_lin_kernel() : (const void*)fn;
@@ -518,6 +535,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   int herr = 0;
   const size_t front = cs_bytes(n) + (rot ? flag_bytes(B) : 0);
   if (ws_bytes < front) return BCJR_ERR_WORKSPACE;
+  // below T = 0.04 the repair pass needs room for one double-float slot
+  if (rot && use_high_precision(T) && ws_bytes - front < hp_layout(L, n, k, false).slot)
+    return BCJR_ERR_WORKSPACE;
   const int64_t grid = grid_size(kern, fl, lds, B, ws_bytes - front, lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
@@ -565,6 +585,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
     // (H, B) entries are zero
     a.flags = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + cs_bytes(n));
     if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+    if (use_high_precision(T))  // the marked blocks in double-float, centred on w
+      return run_fb_hp(w, B, L, codebook, n, k, T, g, w, w_soft, logZ, dW, nullptr, base,
+                       ws_bytes - front, stream, a.flags);
     const int64_t hstep = 2 * ((int64_t)1 << (n - k));
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);

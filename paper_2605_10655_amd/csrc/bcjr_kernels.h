@@ -871,8 +871,17 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
   const uint32_t voC = vslot + (uint32_t)tb * 4u, voCL = vslot + (uint32_t)tb;
   const uint32_t gT = (uint32_t)GS * 4u, gL = (uint32_t)GS * 8u;  // G-side vector offsets
   const bool lane_rows = TPB >= 64;
+  // repair pass after the linear-domain kernel (one block per workgroup):
+  // only the blocks it marked
+  const bool repair = BPW == 1 && a.repair;
+  if (repair) {
+    int any = 0;
+    for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) any |= ld_uniform_i(a.flags, base);
+    if (!any) return;
+  }
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    if (repair && !ld_uniform_i(a.flags, base)) continue;
     const int64_t blk = base + bw;
     const bool valid = blk < a.B;
     const int64_t bb = valid ? blk : a.B - 1;

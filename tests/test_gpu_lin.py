@@ -1,7 +1,8 @@
 """GPU parity of the linear-domain forward-backward kernel (fb_kernel_lin:
-S = 65536, k = 2, fused w_soft + logZ + dW, T >= 0.04) and of its repair
+S = 65536, k = 2, fused w_soft + logZ + dW, T >= 0.0125) and of its repair
 pass: blocks whose group vectors leave the fp32 range are recomputed by the
-log-domain kernel.  Batches mix ordinary N(0, 1) blocks with blocks whose
+log-domain kernel (T >= 0.04) or the double-float kernel centred on w
+(below).  Batches mix ordinary N(0, 1) blocks with blocks whose
 weights sit far outside the codebook (every exponential of a step
 underflows, so the block must be marked and recomputed) and blocks with a
 few moderate outliers (large single-step decays that the linear kernel
@@ -68,7 +69,7 @@ def mixed_batch(L, seed):
     return w, g
 
 
-@pytest.mark.parametrize("T", [0.05, 0.1, 1.0])
+@pytest.mark.parametrize("T", [0.0125, 0.02, 0.03, 0.05, 0.1, 1.0])
 @pytest.mark.parametrize("L", [1, 9, 256])
 def test_linear_kernel_and_repair_pass_match_oracle(L, T):
     c = WL.codebook(4)
@@ -86,13 +87,14 @@ def test_linear_kernel_and_repair_pass_match_oracle(L, T):
     assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
 
 
-def test_repair_pass_under_every_grid_size():
+@pytest.mark.parametrize("T", [0.02, 0.05])
+def test_repair_pass_under_every_grid_size(T):
     """Under every workspace size from one slot up (grids of one workgroup,
     which then walks every block in the same slot, to one per block) the
     out-of-range blocks are recomputed and the result is the same bits as
     with a full workspace; the full-size run matches the oracle."""
     c = WL.codebook(4)
-    L, T = 24, 0.05
+    L = 24
     w, g = mixed_batch(L, 4200)
     B = w.shape[0]
     print(f"linear kernel grids: L={L} T={T} B={B}", flush=True)
@@ -122,3 +124,23 @@ def test_repair_pass_under_every_grid_size():
             assert np.array_equal(a, b)
     print(f"  {runs} workspace sizes ran", flush=True)
     assert runs >= 2
+
+
+@pytest.mark.parametrize("T", [0.0139, 0.0268])
+def test_linear_kernel_low_temperature_full_batch_sampled(T):
+    """The q/o-projection matrix (16384 blocks of 256, S = 65536) at two of
+    the annealed temperatures below the log-domain kernel's range: sampled
+    blocks against the oracle (at T = 0.0139 about 1 % of the blocks are
+    recomputed by the double-float repair pass)."""
+    W, C, G = WL.weights(4), WL.codebook(4), WL.upstream(4)
+    print(f"linear kernel full batch: B={W.shape[0]} T={T}", flush=True)
+    ws, lz, dW, _ = P.bcjr_soft_codeword_fwd_vjp(dev(W), dev(C), N, KB, T, dev(G), want_dCodebook=False)
+    torch.cuda.synchronize()
+    idx = WL.parity_subset(4, 16)
+    rws, rlz, rdW, _ = O.soft_codeword_vjp(W[idx], C, N, KB, float(np.float32(T)), G[idx], want_dc=False)
+    ws, lz, dW = ws.cpu().numpy()[idx], lz.cpu().numpy()[idx], dW.cpu().numpy()[idx]
+    e_ws = float(np.abs(ws - rws).max())
+    e_lz = float((np.abs(lz - rlz) / np.abs(rlz)).max())
+    e_dw = grad_err(dW, rdW)
+    print(f"  w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}", flush=True)
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
