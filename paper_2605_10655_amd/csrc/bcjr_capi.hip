@@ -102,14 +102,16 @@ constexpr double kHighPrecisionK2 = 18.0;
 
 bool use_high_precision(float T) { return 1.4426950408889634074 / (2.0 * (double)T) > kHighPrecisionK2; }
 
-// The linear-domain kernel (S = 65536, k = 2, fwd + dW) keeps fp32 accuracy
-// down to a field scale of ~60 (T ~ 0.012: dW within 2.4e-5 of the oracle
-// on the q/o-projection workload, 3 % of its blocks marked for the repair
-// pass); it serves the call up to this field scale (T >= 0.0125).
-constexpr double kLinearK2 = 57.7;
+// The linear-domain kernel (S = 65536, k = 2, fwd + dW) serves the call up
+// to this field scale (T >= 0.0206).  Its error grows steeply at lower T on
+// blocks whose posterior is crisp everywhere (their dW is small, so the
+// tolerance is tight): emulated on such a block of the q/o-projection
+// matrix, dW is within 2.7e-6 of the oracle at T = 0.04, 2.9e-5 at 0.02,
+// 7.7e-5 at 0.015 and 2.7e-4 at 0.0125.
+constexpr double kLinearK2 = 35.0;
 
-bool linear_ok(int n, int k, float T, bool dc) {
-  return n == 16 && k == 2 && !dc && 1.4426950408889634074 / (2.0 * (double)T) <= kLinearK2;
+bool linear_ok(int n, int k, float T) {
+  return n == 16 && k == 2 && 1.4426950408889634074 / (2.0 * (double)T) <= kLinearK2;
 }
 
 // The histories of one workgroup's blocks are addressed with 32-bit byte
@@ -173,6 +175,10 @@ FbLayout fb_layout(int64_t L, int n, int k, bool vjp, bool dc) {
   l.slot = l.hist + l.histGA + l.small + l.dc;
   return l;
 }
+
+// The linear-domain kernel's slot: the same (H, H B) history and per-step
+// vectors as the fp32 kernels (its repair pass reuses them).
+FbLayout lin_layout(int64_t L, int n, int k) { return fb_layout(L, n, k, true, false); }
 
 size_t vit_slot_bytes(int64_t L, int n, int k) {
   return align_up((size_t)L * ((size_t)1 << (n - k)));
@@ -418,7 +424,7 @@ int run_gen_viterbi(const float* w, int64_t B, int64_t L, const float* codebook,
 // instead of the exact one; the generic family always decodes exactly
 int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
                 int32_t* states, float* w_hard, void* workspace, size_t ws_bytes,
-                hipStream_t stream, bool approx = false) {
+                hipStream_t stream, bool approx = false, const int32_t* flags = nullptr) {
   if (!workspace || ((uintptr_t)workspace & 15u)) return BCJR_ERR_WORKSPACE;
   if (!supported(n, k))
     return run_gen_viterbi(w, B, L, codebook, n, k, states, w_hard, workspace, ws_bytes, stream);
@@ -431,9 +437,10 @@ int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int
   const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes, slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
-  VitArgs a;
+  VitArgs a = {};
   a.w = w; a.c = codebook; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   a.states = states; a.w_hard = w_hard;
+  a.flags = approx ? flags : nullptr;
   a.bp = static_cast<uint8_t*>(workspace);
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
@@ -442,8 +449,8 @@ int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int
 // `ref` is the centring reference of the backward tangent ([B, L]); when it
 // is null the minimum-distortion codewords are decoded into the front of the
 // workspace first.
-// With `repair_flags` (and ref = w), only the blocks marked there run: the
-// repair pass of the linear-domain kernel below T = 0.04.
+// With `repair_flags` only the blocks marked there are decoded and run:
+// the repair pass of the linear-domain kernel below T = 0.04.
 int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
               const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
               float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream,
@@ -463,7 +470,8 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
     int32_t* states = reinterpret_cast<int32_t*>(ws + pre / 2);
     rest = ws + pre;
     rest_bytes = ws_bytes - pre;
-    int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream, true);
+    int st = run_viterbi(w, B, L, codebook, n, k, states, w_hard, rest, rest_bytes, stream, true,
+                         repair_flags);
     if (st != BCJR_OK) return st;
     ref = w_hard;
   }
@@ -506,6 +514,70 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   return BCJR_OK;
 }
 
+// The linear-domain kernel (S = 65536, k = 2, fwd + dW at T >= 0.0206):
+// [scaled codebook][block flags][slots: lin_layout].  The blocks it marks
+// are recomputed by the log-domain rotating kernel (T >= 0.04) or, below,
+// by the double-float kernel centred on those blocks' decoded codewords, in
+// a repair pass over the same slot memory once the first pass is complete.
+int run_fb_lin(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
+               const float* g, float* w_soft, float* logZ, float* dW, void* workspace,
+               size_t ws_bytes, hipStream_t stream) {
+  const Family f = fb_family(n, k, false);
+  Family fl = f;
+  fl.nt = fb_lin_threads();
+  const FbLayout lay = lin_layout(L, n, k);
+  const size_t lds = fb_lds_bytes(fl, n, k);
+  const size_t front = cs_bytes(n) + flag_bytes(B);
+  if (ws_bytes < front) return BCJR_ERR_WORKSPACE;
+  const bool hp = use_high_precision(T);
+  // the repair pass needs room for one slot of its own kernel (below T =
+  // 0.04 after the decoded reference)
+  if (hp && ws_bytes - front < hp_prefix_bytes(B, L) + std::max(hp_layout(L, n, k, false).slot,
+                                                                 vit_slot_bytes(L, n, k)))
+    return BCJR_ERR_WORKSPACE;
+  int herr = 0;
+  const int64_t grid = grid_size(fb_lin_kernel(), fl, lds, B, ws_bytes - front, lay.slot, &herr);
+  if (herr) return BCJR_ERR_HIP;
+  if (grid < 1) return BCJR_ERR_WORKSPACE;
+  const size_t lds_rot = fb_lds_bytes(f, n, k);
+  if (!hp && hipFuncSetAttribute(fb_rot_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds_rot) != hipSuccess)
+    return BCJR_ERR_HIP;
+  const int64_t slots = grid * f.bpw;
+  const int64_t S = (int64_t)1 << n;
+  float* cs = static_cast<float*>(workspace);
+  int32_t* flags = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + cs_bytes(n));
+  char* base = static_cast<char*>(workspace) + front;
+  FbArgs a = {};
+  a.w = w; a.g = g; a.c = codebook; a.cs = cs; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
+  const double Td = (double)T;
+  a.k2 = (float)(1.4426950408889634074 / (2.0 * Td));
+  a.invT = (float)(1.0 / Td);
+  a.kap = (float)std::sqrt(1.4426950408889634074 / (2.0 * Td));
+  a.inv_kap = (float)(1.0 / (double)a.kap);
+  a.dws = (float)(1.0 / ((double)a.kap * (double)a.kap * Td));
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  a.flags = flags;
+  hipLaunchKernelGGL(scale_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, codebook,
+                     a.kap, cs, S);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  a.histHB = reinterpret_cast<float*>(base);
+  a.small = reinterpret_cast<float*>(base + slots * lay.hist);
+  if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+  // ---- repair pass over the marked blocks
+  if (hp)
+    return run_fb_hp(w, B, L, codebook, n, k, T, g, nullptr, w_soft, logZ, dW, nullptr, base,
+                     ws_bytes - front, stream, flags);
+  // log domain: its planar step L - 1 (H, B) entries are zero
+  const int64_t hstep = 2 * ((int64_t)1 << (n - k));
+  hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
+                     stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  a.repair = 1;
+  if (fb_rot_launch((unsigned)grid, lds_rot, stream, a) != 0) return BCJR_ERR_HIP;
+  return BCJR_OK;
+}
+
 int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
            const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
            float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream, bool vjp) {
@@ -513,8 +585,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (!supported(n, k))
     return run_gen(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace, ws_bytes,
                    stream, vjp);
-  const bool lin = vjp && linear_ok(n, k, T, dCodebook != nullptr);
-  if (vjp && use_high_precision(T) && !lin)
+  if (vjp && !dCodebook && linear_ok(n, k, T))
+    return run_fb_lin(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, workspace, ws_bytes, stream);
+  if (vjp && use_high_precision(T))
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
   const bool dc = vjp && dCodebook != nullptr;
@@ -522,34 +595,17 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   const FbLayout lay = fb_layout(L, n, k, vjp, dc);
   FbFn fn = fb_pick(n, k, f, vjp, dc);
   if (!fn) return BCJR_ERR_UNSUPPORTED;
-  // S = 65536, k = 2, fwd + dW: the rotating in-place exchange in the
-  // linear domain (one block per 512-thread workgroup, the same workspace
-  // layout and arguments as the log-domain kernel, which recomputes the
-  // blocks the linear one marks at T >= 0.04; below, the double-float
-  // kernel recomputes them)
-  const bool rot = lin;
-  Family fl = f;
-  if (rot) fl.nt = fb_lin_threads();
-  const void* kern = rot ? fb_lin_kernel() : (const void*)fn;
-  const size_t lds = fb_lds_bytes(fl, n, k);
+  const size_t lds = fb_lds_bytes(f, n, k);
   int herr = 0;
-  const size_t front = cs_bytes(n) + (rot ? flag_bytes(B) : 0);
-  if (ws_bytes < front) return BCJR_ERR_WORKSPACE;
-  // below T = 0.04 the repair pass needs room for one double-float slot
-  if (rot && use_high_precision(T) && ws_bytes - front < hp_layout(L, n, k, false).slot)
-    return BCJR_ERR_WORKSPACE;
-  const int64_t grid = grid_size(kern, fl, lds, B, ws_bytes - front, lay.slot, &herr);
+  if (ws_bytes < cs_bytes(n)) return BCJR_ERR_WORKSPACE;
+  const int64_t grid = grid_size((const void*)fn, f, lds, B, ws_bytes - cs_bytes(n), lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
-  const size_t lds_rot = fb_lds_bytes(f, n, k);
-  if (rot && hipFuncSetAttribute(fb_rot_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)lds_rot) != hipSuccess)
-    return BCJR_ERR_HIP;
   const int64_t slots = grid * f.bpw;
   const int64_t S = (int64_t)1 << n;
-  // [scaled codebook][block flags][slots: histories][slots: shifts][slots: dCodebook partials]
+  // [scaled codebook][slots: histories][slots: shifts][slots: dCodebook partials]
   float* cs = static_cast<float*>(workspace);
-  char* base = static_cast<char*>(workspace) + front;
+  char* base = static_cast<char*>(workspace) + cs_bytes(n);
   FbArgs a = {};
   a.w = w; a.g = g; a.c = codebook; a.cs = cs; a.B = B; a.L = L; a.n = n; a.sgt = f.sgt;
   const double Td = (double)T;
@@ -568,7 +624,7 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   a.small = reinterpret_cast<float*>(base + slots * (lay.hist + lay.histGA));
   a.dc_part = dc ? reinterpret_cast<double*>(base + slots * (lay.hist + lay.histGA + lay.small))
                  : nullptr;
-  if (vjp && !rot) {  // the (H, B) rows of step L - 1 are zero for every block of a slot
+  if (vjp) {  // the (H, B) rows of step L - 1 are zero for every block of a slot
     const int64_t hstep = 2 * ((int64_t)1 << (n - k));
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
@@ -579,25 +635,8 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
       if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
     }
   }
-  if (rot) {
-    // the linear-domain kernel (it writes its own step L - 1 history), then
-    // the blocks it marked again in the log domain, whose planar step L - 1
-    // (H, B) entries are zero
-    a.flags = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + cs_bytes(n));
-    if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
-    if (use_high_precision(T))  // the marked blocks in double-float, centred on w
-      return run_fb_hp(w, B, L, codebook, n, k, T, g, w, w_soft, logZ, dW, nullptr, base,
-                       ws_bytes - front, stream, a.flags);
-    const int64_t hstep = 2 * ((int64_t)1 << (n - k));
-    hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
-                       stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
-    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
-    a.repair = 1;
-    if (fb_rot_launch((unsigned)grid, lds_rot, stream, a) != 0) return BCJR_ERR_HIP;
-  } else {
-    hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
-    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
-  }
+  hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {
     const int64_t used = slots < B ? slots : B;
     hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
@@ -992,6 +1031,11 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
     const size_t vit = (size_t)(g2 * f2.bpw) * vit_slot_bytes(L, state_bits, k);
     const size_t hp = (size_t)(g2 * f2.bpw) * hp_layout(L, state_bits, k, true).slot;
     bytes = std::max(bytes, hp_prefix_bytes(B, L) + std::max(vit, hp));
+    // the linear-domain path's repair pass: after its codebook and flags the
+    // decoded reference and one double-float slot
+    bytes = std::max(bytes, cs_bytes(state_bits) + flag_bytes(B) + hp_prefix_bytes(B, L) +
+                                std::max(hp_layout(L, state_bits, k, false).slot,
+                                         vit_slot_bytes(L, state_bits, k)));
   }
   return bytes;
 }

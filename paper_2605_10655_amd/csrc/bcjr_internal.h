@@ -98,6 +98,9 @@ struct VitArgs {
   int32_t* states;     // [B, L]
   float* w_hard;       // [B, L] or null
   uint8_t* bp;         // [slots][L][S/K] winning predecessor digit
+  // fp32 decode (one block per workgroup): when set, only the blocks marked
+  // 1 here are decoded (the centring reference of a repair pass)
+  const int32_t* flags;
 };
 
 }  // namespace bcjr

@@ -1617,8 +1617,10 @@ __global__ void __launch_bounds__(NT) viterbi_ref_kernel(VitArgs a) {
   const bool lane_rows = TPB >= 64;
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)4 << n);
   const uint32_t voK = (uint32_t)tb << (KB + 2);
+  const bool repair = BPW == 1 && a.flags;
 
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    if (repair && !ld_uniform_i(a.flags, base)) continue;
     const int64_t blk = base + bw;
     const bool valid = blk < a.B;
     const int64_t bb = valid ? blk : a.B - 1;

@@ -512,7 +512,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       const uint32_t tslot = rot::slot8(phtb, rs);
       const uint32_t soH = (uint32_t)t * hstep * 4u;
       if (t == 0) {
-        // Z = sum_s alpha_0(s) beta_0(s) and E_p[g_0 c + B_0]
+        // Z = sum_s alpha_0(s) beta_0(s) and E_p[g_0 (c - w_0) + B_0]
         float ls = 0.f, ly = 0.f;
 #pragma unroll
         for (int i = 0; i < SGT; ++i) {
@@ -535,7 +535,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
               const float d = wtl - cbr[i][j][b];
               const float e = ex2(fmaf(-d, d, noff));
               ls = fmaf(e, Hin[b], ls);
-              ly = fmaf(e, fmaf(gt * cbr[i][j][b], Hin[b], Bin[b]), ly);
+              ly = fmaf(e, fmaf(-gt * d, Hin[b], Bin[b]), ly);
             }
           }
           asm volatile("" ::: "memory");
@@ -635,12 +635,13 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         wnx = ld_uniform(wbu, tn);
         gnx = ld_uniform(gbu, tn);
       }
-      if (t > 0) xbar = fmaf(gt, wt, xbar);  // B_t no longer holds step t
       const float eHt = sm_eH[t];
       const float noff = -(float)off;
       const uint32_t rs = __builtin_amdgcn_readfirstlane(r2);
       const uint32_t tslot = rot::slot8(phtb, rs);
-      // max G_{t+1}, sum P, sum P c, sum P X, sum P c X with P = alpha_t beta_t
+      // max G_{t+1}, sum P d, sum P, sum P (X - xbar), sum P (X - xbar) d with
+      // P = alpha_t beta_t and d = w'_t - c' (moments about the weight: their
+      // terms are of the size of the quantisation error, not of c')
       float rv[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
@@ -673,32 +674,33 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         }
 #pragma unroll
         for (int u = 0; u < K; ++u) {
-          float al[K], ac[K], ea[K];
+          float al[K], ad[K], ea[K], dd[K];
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            const float d = wtl - cbr[i][j][u];
-            const float e = ex2(fmaf(-d, d, noff));
+            dd[j] = wtl - cbr[i][j][u];
+            const float e = ex2(fmaf(-dd[j], dd[j], noff));
             al[j] = e * Gin[j];
-            ac[j] = al[j] * cbr[i][j][u];
+            ad[j] = al[j] * dd[j];
             ea[j] = e * Ain[j];
           }
           const float go = (al[0] + al[1]) + (al[2] + al[3]);   // sum alpha
-          const float sac = (ac[0] + ac[1]) + (ac[2] + ac[3]);  // sum alpha c
+          const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);  // sum alpha d
           const float sea = (ea[0] + ea[1]) + (ea[2] + ea[3]);  // sum e G A
-          float sacc = ac[0] * cbr[i][0][u], seac = ea[0] * cbr[i][0][u];
+          float sadd = ad[0] * dd[0], sead = ea[0] * dd[0];
 #pragma unroll
           for (int j = 1; j < K; ++j) {
-            sacc = fmaf(ac[j], cbr[i][j][u], sacc);
-            seac = fmaf(ea[j], cbr[i][j][u], seac);
+            sadd = fmaf(ad[j], dd[j], sadd);
+            sead = fmaf(ea[j], dd[j], sead);
           }
-          const float aout = fmaf(gt, sac, sea);                // G A of the output group
+          // G A of the output group: the step adds g_t (c - w_t) = -g_t d
+          const float aout = fmaf(-gt, sad, sea);
           rv[0] = fmaxf(rv[0], go);
           const float Hu = Hc[u];
           const float bx = fmaf(-xbar, Hu, Bc[u]);              // H (B - xbar)
-          rv[1] = fmaf(Hu, go, rv[1]);
-          rv[2] = fmaf(Hu, sac, rv[2]);
+          rv[1] = fmaf(Hu, sad, rv[1]);
+          rv[2] = fmaf(Hu, go, rv[2]);
           rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
-          rv[4] = fmaf(sac, bx, fmaf(Hu, fmaf(gt, sacc, seac), rv[4]));
+          rv[4] = fmaf(sad, bx, fmaf(Hu, fmaf(-gt, sadd, sead), rv[4]));
           rot::st_pair_at(sl[u], go, aout);
         }
         asm volatile("" ::: "memory");
@@ -706,19 +708,22 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       red_pre<5, 1u>(rv, rc);
       __syncthreads();
       red_post<5, 1u>(rv, rc);
-      const float r1 = 1.f / rv[1];
-      const float wst = rv[2] * r1;
+      const float r1 = 1.f / rv[2];
+      const float md = rv[1] * r1;   // E_p[w' - c'] = w'_t - w_soft'_t
       if (threadIdx.x == 0) {
-        if (a.w_soft) a.w_soft[bb * L + t] = wst * a.inv_kap;
-        if (a.dW) a.dW[bb * L + t] = (rv[4] - wst * rv[3]) * r1 * dws;
+        if (a.w_soft) a.w_soft[bb * L + t] = (wt - md) * a.inv_kap;
+        // dW = Cov_p(X, c') / (kappa^2 T), Cov_p(X, c') = -E[(X - xbar) d] + E[X - xbar] E[d]
+        if (a.dW) a.dW[bb * L + t] = fmaf(rv[3] * r1, rv[1], -rv[4]) * r1 * dws;
       }
       // the step's mass sum_s alpha_t beta_t must equal Z
-      const float lzt = lg2(rv[1]) - (float)(ex - off) - eHt;
+      const float lzt = lg2(rv[2]) - (float)(ex - off) - eHt;
       if (!(fabsf(lzt - lz2) <= 2e-4f)) bad = true;
       if (!(rv[0] >= 0x1p-30f && rv[0] <= 0x1p100f)) bad = true;
       ex -= off;
       off = bad ? 0 : rot::exp_of(rv[0]) - rot::kTopExp;
-      cprev = gt * wst;
+      // the step's term of A moves from g_t (c - w_t) to g_t (c - w_soft_t)
+      // when it is read; E_p[X_{t+1}] = E_p[X_t] - g_t (w_soft_t - w_t)
+      cprev = -gt * md;
       xbar = fmaf(rv[3], r1, xbar) - cprev;
       r2 = r2 == 12u ? 0u : r2 + 2u;
     }
