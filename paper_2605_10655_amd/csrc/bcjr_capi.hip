@@ -30,9 +30,9 @@ namespace bcjr {
 const void* fb_rot_kernel();
 int fb_rot_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
 // its linear-domain form (blocks it marks are recomputed by the former)
-const void* fb_lin_kernel();
+const void* fb_lin_kernel(bool vjp);
 int fb_lin_threads();
-int fb_lin_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
+int fb_lin_launch(bool vjp, unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a);
 
 namespace {
 
@@ -176,9 +176,9 @@ FbLayout fb_layout(int64_t L, int n, int k, bool vjp, bool dc) {
   return l;
 }
 
-// The linear-domain kernel's slot: the same (H, H B) history and per-step
-// vectors as the fp32 kernels (its repair pass reuses them).
-FbLayout lin_layout(int64_t L, int n, int k) { return fb_layout(L, n, k, true, false); }
+// The linear-domain kernel's slot: the same history and per-step vectors
+// as the fp32 kernels (its repair pass reuses them).
+FbLayout lin_layout(int64_t L, int n, int k, bool vjp) { return fb_layout(L, n, k, vjp, false); }
 
 size_t vit_slot_bytes(int64_t L, int n, int k) {
   return align_up((size_t)L * ((size_t)1 << (n - k)));
@@ -514,34 +514,39 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   return BCJR_OK;
 }
 
-// The linear-domain kernel (S = 65536, k = 2, fwd + dW at T >= 0.0206):
-// [scaled codebook][block flags][slots: lin_layout].  The blocks it marks
-// are recomputed by the log-domain rotating kernel (T >= 0.04) or, below,
-// by the double-float kernel centred on those blocks' decoded codewords, in
-// a repair pass over the same slot memory once the first pass is complete.
+// The linear-domain kernel (S = 65536, k = 2, T >= 0.0206; the soft
+// codeword alone, or with dW): [scaled codebook][block flags][slots:
+// lin_layout].  The blocks it marks are recomputed in a repair pass over the
+// same slot memory once the first pass is complete: by the log-domain
+// kernels (the soft codeword at any T, the VJP at T >= 0.04), or below
+// T = 0.04 by the double-float VJP kernel centred on those blocks' decoded
+// codewords.
 int run_fb_lin(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
                const float* g, float* w_soft, float* logZ, float* dW, void* workspace,
-               size_t ws_bytes, hipStream_t stream) {
+               size_t ws_bytes, hipStream_t stream, bool vjp) {
   const Family f = fb_family(n, k, false);
   Family fl = f;
   fl.nt = fb_lin_threads();
-  const FbLayout lay = lin_layout(L, n, k);
+  const FbLayout lay = lin_layout(L, n, k, vjp);
   const size_t lds = fb_lds_bytes(fl, n, k);
   const size_t front = cs_bytes(n) + flag_bytes(B);
   if (ws_bytes < front) return BCJR_ERR_WORKSPACE;
-  const bool hp = use_high_precision(T);
+  const bool hp = vjp && use_high_precision(T);
   // the repair pass needs room for one slot of its own kernel (below T =
   // 0.04 after the decoded reference)
   if (hp && ws_bytes - front < hp_prefix_bytes(B, L) + std::max(hp_layout(L, n, k, false).slot,
                                                                  vit_slot_bytes(L, n, k)))
     return BCJR_ERR_WORKSPACE;
   int herr = 0;
-  const int64_t grid = grid_size(fb_lin_kernel(), fl, lds, B, ws_bytes - front, lay.slot, &herr);
+  const int64_t grid = grid_size(fb_lin_kernel(vjp), fl, lds, B, ws_bytes - front, lay.slot, &herr);
   if (herr) return BCJR_ERR_HIP;
   if (grid < 1) return BCJR_ERR_WORKSPACE;
-  const size_t lds_rot = fb_lds_bytes(f, n, k);
-  if (!hp && hipFuncSetAttribute(fb_rot_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)lds_rot) != hipSuccess)
+  const size_t lds_rep = fb_lds_bytes(f, n, k);
+  FbFn soft_fn = vjp ? nullptr : fb_pick(n, k, f, false, false);
+  if (!vjp && !soft_fn) return BCJR_ERR_UNSUPPORTED;
+  const void* rep_kern = vjp ? fb_rot_kernel() : (const void*)soft_fn;
+  if (!hp && hipFuncSetAttribute(rep_kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_rep) !=
+                 hipSuccess)
     return BCJR_ERR_HIP;
   const int64_t slots = grid * f.bpw;
   const int64_t S = (int64_t)1 << n;
@@ -561,20 +566,25 @@ int run_fb_lin(const float* w, int64_t B, int64_t L, const float* codebook, int 
   hipLaunchKernelGGL(scale_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, codebook,
                      a.kap, cs, S);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
-  a.histHB = reinterpret_cast<float*>(base);
+  a.histH = vjp ? nullptr : reinterpret_cast<float*>(base);
+  a.histHB = vjp ? reinterpret_cast<float*>(base) : nullptr;
   a.small = reinterpret_cast<float*>(base + slots * lay.hist);
-  if (fb_lin_launch((unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
+  if (fb_lin_launch(vjp, (unsigned)grid, lds, stream, a) != 0) return BCJR_ERR_HIP;
   // ---- repair pass over the marked blocks
   if (hp)
     return run_fb_hp(w, B, L, codebook, n, k, T, g, nullptr, w_soft, logZ, dW, nullptr, base,
                      ws_bytes - front, stream, flags);
+  a.repair = 1;
+  if (!vjp) {  // the log-domain soft-codeword kernel writes its own history
+    hipLaunchKernelGGL(soft_fn, dim3((unsigned)grid), dim3(f.nt), lds_rep, stream, a);
+    return hipGetLastError() == hipSuccess ? BCJR_OK : BCJR_ERR_HIP;
+  }
   // log domain: its planar step L - 1 (H, B) entries are zero
   const int64_t hstep = 2 * ((int64_t)1 << (n - k));
   hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                      stream, a.histHB + (L - 1) * hstep, L * hstep, slots, hstep, 0.f);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
-  a.repair = 1;
-  if (fb_rot_launch((unsigned)grid, lds_rot, stream, a) != 0) return BCJR_ERR_HIP;
+  if (fb_rot_launch((unsigned)grid, lds_rep, stream, a) != 0) return BCJR_ERR_HIP;
   return BCJR_OK;
 }
 
@@ -585,8 +595,9 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (!supported(n, k))
     return run_gen(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace, ws_bytes,
                    stream, vjp);
-  if (vjp && !dCodebook && linear_ok(n, k, T))
-    return run_fb_lin(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, workspace, ws_bytes, stream);
+  if (!dCodebook && linear_ok(n, k, T))
+    return run_fb_lin(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, workspace, ws_bytes, stream,
+                      vjp);
   if (vjp && use_high_precision(T))
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);
@@ -1025,7 +1036,7 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
   const int64_t g1 = std::min<int64_t>(ceil_div(B, f.bpw), (int64_t)kDeviceCUs * f.occ_est);
   const int64_t g2 = std::min<int64_t>(ceil_div(B, f2.bpw), (int64_t)kDeviceCUs * f2.occ_est);
   const int64_t slots = std::max<int64_t>(g1 * f.bpw, g2 * f2.bpw);
-  size_t bytes = cs_bytes(state_bits) + (vjp ? flag_bytes(B) : 0) +
+  size_t bytes = cs_bytes(state_bits) + flag_bytes(B) +
                  (size_t)slots * fb_layout(L, state_bits, k, vjp, vjp).slot;
   if (vjp) {  // the temperature decides the variant at call time: cover both
     const size_t vit = (size_t)(g2 * f2.bpw) * vit_slot_bytes(L, state_bits, k);

@@ -126,7 +126,17 @@ __global__ void __launch_bounds__(NT) fb_kernel(FbArgs a) {
     }
   }
 
+  // repair pass of the soft codeword after the linear-domain kernel (one
+  // block per workgroup): only the blocks it marked
+  const bool repair = !VJP && BPW == 1 && a.repair;
+  if (repair) {
+    int any = 0;
+    for (int64_t base = blockIdx.x; base < a.B; base += gridDim.x) any |= ld_uniform_i(a.flags, base);
+    if (!any) return;
+  }
+
   for (int64_t base = (int64_t)blockIdx.x * BPW; base < a.B; base += (int64_t)gridDim.x * BPW) {
+    if (repair && !ld_uniform_i(a.flags, base)) continue;
     const int64_t blk = base + bw;
     const bool valid = blk < a.B;
     const int64_t bb = valid ? blk : a.B - 1;

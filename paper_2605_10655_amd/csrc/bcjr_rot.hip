@@ -24,10 +24,16 @@ constexpr int kLinThreads = 512;
 
 int fb_lin_threads() { return kLinThreads; }
 
-const void* fb_lin_kernel() { return reinterpret_cast<const void*>(&fb_kernel_lin<kLinThreads>); }
+const void* fb_lin_kernel(bool vjp) {
+  return vjp ? reinterpret_cast<const void*>(&fb_kernel_lin<kLinThreads, true>)
+             : reinterpret_cast<const void*>(&fb_kernel_lin<kLinThreads, false>);
+}
 
-int fb_lin_launch(unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a) {
-  hipLaunchKernelGGL(fb_kernel_lin<kLinThreads>, dim3(grid), dim3(kLinThreads), lds, stream, a);
+int fb_lin_launch(bool vjp, unsigned grid, size_t lds, hipStream_t stream, const FbArgs& a) {
+  if (vjp)
+    hipLaunchKernelGGL((fb_kernel_lin<kLinThreads, true>), dim3(grid), dim3(kLinThreads), lds, stream, a);
+  else
+    hipLaunchKernelGGL((fb_kernel_lin<kLinThreads, false>), dim3(grid), dim3(kLinThreads), lds, stream, a);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -430,7 +430,7 @@ __device__ __forceinline__ int exp_of(float x) { return (int)((__float_as_uint(x
 // posterior states would not survive) or the forward's per-step mass
 // sum_s alpha_t beta_t departing from Z by more than 2e-4 log2 units -- is
 // marked in a.flags and recomputed by fb_kernel_rot in its repair mode.
-template <int NT>
+template <int NT, bool VJP>
 __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
   constexpr int KB = 2, K = 4, n = 16;
   constexpr int GS = 1 << (n - KB);        // 16384 groups
@@ -455,7 +455,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
   const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)4 << n);
   const uint32_t tb0 = threadIdx.x;
   const uint32_t voK = tb0 << (KB + 2);
-  constexpr uint32_t hstep = (uint32_t)GS * 2;   // floats per history step: H then H B, [S/K] each
+  // floats per history step: H then (VJP) H B, [S/K] each
+  constexpr uint32_t hstep = (uint32_t)GS * (VJP ? 2 : 1);
   const uint32_t wave_s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   uint32_t phtb = 0;
 #pragma unroll
@@ -473,8 +474,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
     const int64_t slot = blockIdx.x;
     const int64_t bbu = (int64_t)__builtin_amdgcn_readfirstlane((int)bb);
     const float* wbu = a.w + bbu * L;
-    const float* gbu = a.g + bbu * L;
-    const rsrc_t hist = make_rsrc(a.histHB + slot * L * hstep, (uint32_t)L * hstep * 4u);
+    const float* gbu = VJP ? a.g + bbu * L : wbu;
+    const rsrc_t hist = make_rsrc((VJP ? a.histHB : a.histH) + slot * L * hstep, (uint32_t)L * hstep * 4u);
     float* sm_eH = a.small + slot * 3 * L;  // exponent of the stored H_t: stored = true * 2^e
     bool bad = false;
     {  // the history's step L - 1 entries: H = 1, then H B = 0
@@ -482,7 +483,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       const uint32_t so = (uint32_t)(L - 1) * hstep * 4u;
       for (uint32_t q = threadIdx.x; q < (uint32_t)GS / 4; q += NT) {
         buf_st<4, kStream>(hist, q * 16u, so, one);
-        buf_st<4, kStream>(hist, q * 16u, so + (uint32_t)GS * 4u, zero);
+        if constexpr (VJP) buf_st<4, kStream>(hist, q * 16u, so + (uint32_t)GS * 4u, zero);
       }
     }
 
@@ -495,7 +496,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
     int off = 0;            // its rescale, folded into this step's exponentials
     float lz2 = 0.f, xbar = 0.f;
     float wnx = ld_uniform(wbu, L - 1);
-    float gnx = ld_uniform(gbu, L - 1);
+    float gnx = VJP ? ld_uniform(gbu, L - 1) : 0.f;
     uint32_t r2 = (uint32_t)(2 * (((L - 1) + 6) % 7));
     for (int64_t t = L - 1;; --t) {
       const uint32_t tid_s = lane_tid(wave_s);
@@ -505,7 +506,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       {
         const int64_t tn = t > 0 ? t - 1 : 0;
         wnx = ld_uniform(wbu, tn);
-        gnx = ld_uniform(gbu, tn);
+        if constexpr (VJP) gnx = ld_uniform(gbu, tn);
       }
       const float noff = -(float)off;
       const uint32_t rs = __builtin_amdgcn_readfirstlane(r2);
@@ -535,7 +536,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
               const float d = wtl - cbr[i][j][b];
               const float e = ex2(fmaf(-d, d, noff));
               ls = fmaf(e, Hin[b], ls);
-              ly = fmaf(e, fmaf(-gt * d, Hin[b], Bin[b]), ly);
+              if constexpr (VJP) ly = fmaf(e, fmaf(-gt * d, Hin[b], Bin[b]), ly);
             }
           }
           asm volatile("" ::: "memory");
@@ -580,20 +581,26 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
             u[b] = e[b] * Hin[b];
           }
           const float hv0 = (u[0] + u[1]) + (u[2] + u[3]);
-          // H B_{t-1} = sum_b e_b (H_b g_t (c_b - w_t) + H B_b)
-          float tb = e[0] * Bin[0], td = u[0] * d[0];
-#pragma unroll
-          for (int b = 1; b < K; ++b) {
-            tb = fmaf(e[b], Bin[b], tb);
-            td = fmaf(u[b], d[b], td);
-          }
           vmax[0] = fmaxf(vmax[0], hv0);
-          const float hv[1] = {hv0}, bv[1] = {fmaf(-gt, td, tb)};
-          rot::st_pair_at(sl[j], hv[0], bv[0]);
+          const float hv[1] = {hv0};
           // history entries of step t - 1: group j NSG + i TPB + tb
           const uint32_t so = soH - hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
-          buf_st<1, kStream>(hist, vcH, so, hv);
-          buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
+          if constexpr (VJP) {
+            // H B_{t-1} = sum_b e_b (H_b g_t (c_b - w_t) + H B_b)
+            float tb = e[0] * Bin[0], td = u[0] * d[0];
+#pragma unroll
+            for (int b = 1; b < K; ++b) {
+              tb = fmaf(e[b], Bin[b], tb);
+              td = fmaf(u[b], d[b], td);
+            }
+            const float bv[1] = {fmaf(-gt, td, tb)};
+            rot::st_pair_at(sl[j], hv[0], bv[0]);
+            buf_st<1, kStream>(hist, vcH, so, hv);
+            buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
+          } else {
+            rot::st_pair_at(sl[j], hv[0], 0.f);
+            buf_st<1, kStream>(hist, vcH, so, hv);
+          }
         }
         asm volatile("" ::: "memory");
       }
@@ -619,10 +626,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
     off = 0;
     float pH[K], pB[K];
     wnx = ld_uniform(wbu, 0);
-    gnx = ld_uniform(gbu, 0);
+    gnx = VJP ? ld_uniform(gbu, 0) : 0.f;
     {
       const uint32_t voH0 = lane_tid(wave_s) * K * 4u;
-      hist_row<K, true>(hist, voH0, 0, 0, (uint32_t)GS * 4u, pH, pB);
+      hist_row<K, VJP>(hist, voH0, 0, 0, (uint32_t)GS * 4u, pH, pB);
     }
     r2 = 0;
     for (int64_t t = 0; t < L; ++t) {
@@ -633,7 +640,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       {
         const int64_t tn = t + 1 < L ? t + 1 : t;
         wnx = ld_uniform(wbu, tn);
-        gnx = ld_uniform(gbu, tn);
+        if constexpr (VJP) gnx = ld_uniform(gbu, tn);
       }
       const float eHt = sm_eH[t];
       const float noff = -(float)off;
@@ -642,7 +649,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       // max G_{t+1}, sum P d, sum P, sum P (X - xbar), sum P (X - xbar) d with
       // P = alpha_t beta_t and d = w'_t - c' (moments about the weight: their
       // terms are of the size of the quantisation error, not of c')
-      float rv[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+      constexpr int NRV = VJP ? 5 : 3;
+      float rv[NRV];
+#pragma unroll
+      for (int q = 0; q < NRV; ++q) rv[q] = 0.f;
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
         uint32_t ts = tslot;
@@ -658,62 +668,79 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         for (int j = 0; j < K; ++j) {
           const float2 v = rot::ld_pair_at(sl[j]);
           Gin[j] = v.x;
-          Ain[j] = fmaf(-cprev, v.x, v.y);
+          Ain[j] = VJP ? fmaf(-cprev, v.x, v.y) : 0.f;
         }
         float Hc[K], Bc[K];
 #pragma unroll
         for (int u = 0; u < K; ++u) {
           Hc[u] = pH[u];
-          Bc[u] = pB[u];
+          Bc[u] = VJP ? pB[u] : 0.f;
         }
         {
           const bool last = i + 1 >= SGT;
           const int64_t tn = last && t + 1 < L ? t + 1 : t;
-          hist_row<K, true>(hist, voH_s, (uint32_t)tn * hstep * 4u,
+          hist_row<K, VJP>(hist, voH_s, (uint32_t)tn * hstep * 4u,
                             last ? 0u : (uint32_t)(i + 1) * TPB * K * 4u, (uint32_t)GS * 4u, pH, pB);
         }
 #pragma unroll
         for (int u = 0; u < K; ++u) {
-          float al[K], ad[K], ea[K], dd[K];
+          if constexpr (VJP) {
+            float al[K], ad[K], ea[K], dd[K];
+  #pragma unroll
+            for (int j = 0; j < K; ++j) {
+              dd[j] = wtl - cbr[i][j][u];
+              const float e = ex2(fmaf(-dd[j], dd[j], noff));
+              al[j] = e * Gin[j];
+              ad[j] = al[j] * dd[j];
+              ea[j] = e * Ain[j];
+            }
+            const float go = (al[0] + al[1]) + (al[2] + al[3]);   // sum alpha
+            const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);  // sum alpha d
+            const float sea = (ea[0] + ea[1]) + (ea[2] + ea[3]);  // sum e G A
+            float sadd = ad[0] * dd[0], sead = ea[0] * dd[0];
+  #pragma unroll
+            for (int j = 1; j < K; ++j) {
+              sadd = fmaf(ad[j], dd[j], sadd);
+              sead = fmaf(ea[j], dd[j], sead);
+            }
+            // G A of the output group: the step adds g_t (c - w_t) = -g_t d
+            const float aout = fmaf(-gt, sad, sea);
+            rv[0] = fmaxf(rv[0], go);
+            const float Hu = Hc[u];
+            const float bx = fmaf(-xbar, Hu, Bc[u]);              // H (B - xbar)
+            rv[1] = fmaf(Hu, sad, rv[1]);
+            rv[2] = fmaf(Hu, go, rv[2]);
+            rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
+            rv[4] = fmaf(sad, bx, fmaf(Hu, fmaf(-gt, sadd, sead), rv[4]));
+            rot::st_pair_at(sl[u], go, aout);
+          } else {
+            // soft codeword alone: sum alpha, sum alpha d and the two moments
+            float al[K], ad[K];
 #pragma unroll
-          for (int j = 0; j < K; ++j) {
-            dd[j] = wtl - cbr[i][j][u];
-            const float e = ex2(fmaf(-dd[j], dd[j], noff));
-            al[j] = e * Gin[j];
-            ad[j] = al[j] * dd[j];
-            ea[j] = e * Ain[j];
+            for (int j = 0; j < K; ++j) {
+              const float dj = wtl - cbr[i][j][u];
+              al[j] = ex2(fmaf(-dj, dj, noff)) * Gin[j];
+              ad[j] = al[j] * dj;
+            }
+            const float go = (al[0] + al[1]) + (al[2] + al[3]);
+            const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);
+            rv[0] = fmaxf(rv[0], go);
+            rv[1] = fmaf(Hc[u], sad, rv[1]);
+            rv[2] = fmaf(Hc[u], go, rv[2]);
+            rot::st_pair_at(sl[u], go, 0.f);
           }
-          const float go = (al[0] + al[1]) + (al[2] + al[3]);   // sum alpha
-          const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);  // sum alpha d
-          const float sea = (ea[0] + ea[1]) + (ea[2] + ea[3]);  // sum e G A
-          float sadd = ad[0] * dd[0], sead = ea[0] * dd[0];
-#pragma unroll
-          for (int j = 1; j < K; ++j) {
-            sadd = fmaf(ad[j], dd[j], sadd);
-            sead = fmaf(ea[j], dd[j], sead);
-          }
-          // G A of the output group: the step adds g_t (c - w_t) = -g_t d
-          const float aout = fmaf(-gt, sad, sea);
-          rv[0] = fmaxf(rv[0], go);
-          const float Hu = Hc[u];
-          const float bx = fmaf(-xbar, Hu, Bc[u]);              // H (B - xbar)
-          rv[1] = fmaf(Hu, sad, rv[1]);
-          rv[2] = fmaf(Hu, go, rv[2]);
-          rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
-          rv[4] = fmaf(sad, bx, fmaf(Hu, fmaf(-gt, sadd, sead), rv[4]));
-          rot::st_pair_at(sl[u], go, aout);
         }
         asm volatile("" ::: "memory");
       }
-      red_pre<5, 1u>(rv, rc);
+      red_pre<NRV, 1u>(rv, rc);
       __syncthreads();
-      red_post<5, 1u>(rv, rc);
+      red_post<NRV, 1u>(rv, rc);
       const float r1 = 1.f / rv[2];
       const float md = rv[1] * r1;   // E_p[w' - c'] = w'_t - w_soft'_t
       if (threadIdx.x == 0) {
         if (a.w_soft) a.w_soft[bb * L + t] = (wt - md) * a.inv_kap;
         // dW = Cov_p(X, c') / (kappa^2 T), Cov_p(X, c') = -E[(X - xbar) d] + E[X - xbar] E[d]
-        if (a.dW) a.dW[bb * L + t] = fmaf(rv[3] * r1, rv[1], -rv[4]) * r1 * dws;
+        if (VJP && a.dW) a.dW[bb * L + t] = fmaf(rv[VJP ? 3 : 0] * r1, rv[1], -rv[VJP ? 4 : 0]) * r1 * dws;
       }
       // the step's mass sum_s alpha_t beta_t must equal Z
       const float lzt = lg2(rv[2]) - (float)(ex - off) - eHt;
@@ -723,8 +750,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
       off = bad ? 0 : rot::exp_of(rv[0]) - rot::kTopExp;
       // the step's term of A moves from g_t (c - w_t) to g_t (c - w_soft_t)
       // when it is read; E_p[X_{t+1}] = E_p[X_t] - g_t (w_soft_t - w_t)
-      cprev = -gt * md;
-      xbar = fmaf(rv[3], r1, xbar) - cprev;
+      if constexpr (VJP) {
+        cprev = -gt * md;
+        xbar = fmaf(rv[3], r1, xbar) - cprev;
+      }
       r2 = r2 == 12u ? 0u : r2 + 2u;
     }
     if (threadIdx.x == 0) a.flags[bb] = bad ? 1 : 0;

@@ -147,3 +147,68 @@ def test_linear_kernel_low_temperature_full_batch_sampled(T):
     e_dw = grad_err(dW, rdW)
     print(f"  w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}", flush=True)
     assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
+
+
+@pytest.mark.parametrize("T", [0.021, 0.05, 1.0])
+@pytest.mark.parametrize("L", [1, 9, 256])
+def test_linear_soft_codeword_and_repair_match_oracle(L, T):
+    """bcjr_soft_codeword (w_soft and logZ alone) through the linear kernel's
+    soft-codeword form, with the out-of-range blocks of the mixed batch
+    recomputed by the log-domain soft-codeword kernel."""
+    c = WL.codebook(4)
+    w, _ = mixed_batch(L, 4500 + L)
+    print(f"linear soft codeword: L={L} T={T} B=6 (mixed)", flush=True)
+    ws, lz = P.bcjr_soft_codeword(dev(w), dev(c), N, KB, T)
+    torch.cuda.synchronize()
+    rws, rlz = O.soft_codeword(w, c, N, KB, float(np.float32(T)))
+    ws, lz = ws.cpu().numpy(), lz.cpu().numpy()
+    assert np.isfinite(ws).all() and np.isfinite(lz).all()
+    e_ws = float(np.abs(ws - rws).max())
+    e_lz = float((np.abs(lz - rlz) / np.abs(rlz)).max())
+    print(f"  w_soft {e_ws:.2e} logZ {e_lz:.2e}", flush=True)
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ
+
+
+def test_linear_soft_codeword_every_grid_size():
+    """The soft-codeword form under every workspace size from one slot up:
+    the same bits as with a full workspace, out-of-range blocks included."""
+    c = WL.codebook(4)
+    L, T = 24, 0.05
+    w, _ = mixed_batch(L, 4600)
+    B = w.shape[0]
+
+    def run(work=None):
+        out = P.bcjr_soft_codeword(dev(w), dev(c), N, KB, T, workspace=work)
+        torch.cuda.synchronize()
+        return [x.cpu().numpy() for x in out]
+
+    full = run()
+    rws, rlz = O.soft_codeword(w, c, N, KB, float(np.float32(T)))
+    assert float(np.abs(full[0] - rws).max()) <= TOL_WS
+    big = P.bcjr_workspace_bytes(B, L, N, KB, P.OP_FWD)
+    runs = 0
+    for nb in range(1, B + 1):
+        try:
+            out = run(torch.empty(big * nb // B, dtype=torch.uint8, device="cuda:0"))
+        except P.BcjrError as e:
+            assert e.status == -3
+            continue
+        runs += 1
+        for a, b in zip(out, full):
+            assert np.array_equal(a, b)
+    print(f"linear soft codeword grids: {runs} workspace sizes ran", flush=True)
+    assert runs >= 2
+
+
+def test_linear_soft_codeword_full_batch_sampled():
+    """bcjr_soft_codeword on the q/o-projection matrix at T = 0.05: sampled
+    blocks against the oracle."""
+    W, C = WL.weights(4), WL.codebook(4)
+    ws, lz = P.bcjr_soft_codeword(dev(W), dev(C), N, KB, 0.05)
+    torch.cuda.synchronize()
+    idx = WL.parity_subset(4, 16)
+    rws, rlz = O.soft_codeword(W[idx], C, N, KB, float(np.float32(0.05)))
+    e_ws = float(np.abs(ws.cpu().numpy()[idx] - rws).max())
+    e_lz = float((np.abs(lz.cpu().numpy()[idx] - rlz) / np.abs(rlz)).max())
+    print(f"linear soft codeword full batch: w_soft {e_ws:.2e} logZ {e_lz:.2e}", flush=True)
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ
