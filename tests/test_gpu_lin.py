@@ -212,3 +212,25 @@ def test_linear_soft_codeword_full_batch_sampled():
     e_lz = float((np.abs(lz.cpu().numpy()[idx] - rlz) / np.abs(rlz)).max())
     print(f"linear soft codeword full batch: w_soft {e_ws:.2e} logZ {e_lz:.2e}", flush=True)
     assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ
+
+
+@pytest.mark.parametrize("L,T", [(2048, 0.05), (2048, 0.021), (64, 25.0)])
+def test_linear_kernel_long_blocks_and_high_temperature(L, T):
+    """Long blocks (the tracked exponents of the rescales reach thousands)
+    and a temperature at which every step's vector grows: fwd + dW and the
+    soft codeword alone against the oracle."""
+    c = WL.codebook(4)
+    r = np.random.Generator(np.random.PCG64(4700 + L))
+    w = r.standard_normal((2, L)).astype(np.float32)
+    g = r.standard_normal((2, L)).astype(np.float32)
+    print(f"linear kernel: L={L} T={T} B=2", flush=True)
+    ws, lz, dW, _ = P.bcjr_soft_codeword_fwd_vjp(dev(w), dev(c), N, KB, T, dev(g), want_dCodebook=False)
+    ss, sl = P.bcjr_soft_codeword(dev(w), dev(c), N, KB, T)
+    torch.cuda.synchronize()
+    rws, rlz, rdW, _ = O.soft_codeword_vjp(w, c, N, KB, float(np.float32(T)), g, want_dc=False)
+    ws, lz, dW, ss, sl = (x.cpu().numpy() for x in (ws, lz, dW, ss, sl))
+    e_ws = max(float(np.abs(ws - rws).max()), float(np.abs(ss - rws).max()))
+    e_lz = max(float((np.abs(lz - rlz) / np.abs(rlz)).max()), float((np.abs(sl - rlz) / np.abs(rlz)).max()))
+    e_dw = grad_err(dW, rdW)
+    print(f"  w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}", flush=True)
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
