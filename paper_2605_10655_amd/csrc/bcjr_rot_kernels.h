@@ -450,8 +450,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
 
   // LDS byte address of the pair vector: it starts on a 128 KiB boundary
   // (at 0: the kernel has no static LDS), so it is XORed into the scalar
-  // slot terms and no address needs an add
+  // slot terms and no address needs an add.  Were it not aligned, every
+  // block is marked for the repair pass (whose kernels address LDS plainly).
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  const bool lds_aligned = (lds0 & 0x1FFFFu) == 0u;
   const rsrc_t cbk = make_rsrc(a.cs, (uint32_t)4 << n);
   const uint32_t tb0 = threadIdx.x;
   const uint32_t voK = tb0 << (KB + 2);
@@ -477,7 +479,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
     const float* gbu = VJP ? a.g + bbu * L : wbu;
     const rsrc_t hist = make_rsrc((VJP ? a.histHB : a.histH) + slot * L * hstep, (uint32_t)L * hstep * 4u);
     float* sm_eH = a.small + slot * 3 * L;  // exponent of the stored H_t: stored = true * 2^e
-    bool bad = false;
+    bool bad = !lds_aligned;
     {  // the history's step L - 1 entries: H = 1, then H B = 0
       const float one[4] = {1.f, 1.f, 1.f, 1.f}, zero[4] = {0.f, 0.f, 0.f, 0.f};
       const uint32_t so = (uint32_t)(L - 1) * hstep * 4u;
