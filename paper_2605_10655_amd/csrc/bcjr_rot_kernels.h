@@ -429,7 +429,8 @@ __device__ __forceinline__ int exp_of(float x) { return (int)((__float_as_uint(x
 // falls below 2^-30 (a single-step decay of 70 log2 units, which the
 // posterior states would not survive) or the forward's per-step mass
 // sum_s alpha_t beta_t departing from Z by more than 2e-4 log2 units -- is
-// marked in a.flags and recomputed by fb_kernel_rot in its repair mode.
+// marked in a.flags and recomputed by a second launch of the log-domain
+// (or, at field scales above 18, the double-float) kernel in repair mode.
 template <int NT, bool VJP>
 __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
   constexpr int KB = 2, K = 4, n = 16;
@@ -566,36 +567,36 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         uint32_t sl[K];
 #pragma unroll
         for (int b = 0; b < K; ++b) sl[b] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)b << 12)), rs);
-        float Hin[K], Bin[K];
+        float Hin[K], Bin[K], gH[K];
 #pragma unroll
         for (int b = 0; b < K; ++b) {
           const float2 v = rot::ld_pair_at(sl[b]);
           Hin[b] = v.x;
           Bin[b] = v.y;
+          gH[b] = VJP ? gt * v.x : 0.f;  // shared by the K output groups
         }
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-          float e[K], u[K], d[K];
+          float e[K], d[K];
 #pragma unroll
           for (int b = 0; b < K; ++b) {
             d[b] = wtl - cbr[i][j][b];
             e[b] = ex2(fmaf(-d[b], d[b], noff));
-            u[b] = e[b] * Hin[b];
           }
-          const float hv0 = (u[0] + u[1]) + (u[2] + u[3]);
+          float hv0 = e[0] * Hin[0];
+#pragma unroll
+          for (int b = 1; b < K; ++b) hv0 = fmaf(e[b], Hin[b], hv0);
           vmax[0] = fmaxf(vmax[0], hv0);
           const float hv[1] = {hv0};
           // history entries of step t - 1: group j NSG + i TPB + tb
           const uint32_t so = soH - hstep * 4u + (uint32_t)(j * NSG + i * TPB) * 4u;
           if constexpr (VJP) {
-            // H B_{t-1} = sum_b e_b (H_b g_t (c_b - w_t) + H B_b)
-            float tb = e[0] * Bin[0], td = u[0] * d[0];
+            // H B_{t-1} = sum_b e_b (H B_b + g_t H_b (c_b - w_t)), the
+            // step's term -g_t H_b d_b folded in before the product with e_b
+            float bv0 = e[0] * fmaf(-gH[0], d[0], Bin[0]);
 #pragma unroll
-            for (int b = 1; b < K; ++b) {
-              tb = fmaf(e[b], Bin[b], tb);
-              td = fmaf(u[b], d[b], td);
-            }
-            const float bv[1] = {fmaf(-gt, td, tb)};
+            for (int b = 1; b < K; ++b) bv0 = fmaf(e[b], fmaf(-gH[b], d[b], Bin[b]), bv0);
+            const float bv[1] = {bv0};
             rot::st_pair_at(sl[j], hv[0], bv[0]);
             buf_st<1, kStream>(hist, vcH, so, hv);
             buf_st<1, kStream>(hist, vcH, so + (uint32_t)GS * 4u, bv);
@@ -665,12 +666,13 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
         uint32_t sl[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) sl[j] = si ^ rot::slot8s(rot::rep(rot::phi((uint32_t)j << 12)), rs);
-        float Gin[K], Ain[K];
+        float Gin[K], Ain[K], gG[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
           const float2 v = rot::ld_pair_at(sl[j]);
           Gin[j] = v.x;
           Ain[j] = VJP ? fmaf(-cprev, v.x, v.y) : 0.f;
+          gG[j] = VJP ? gt * v.x : 0.f;  // shared by the K output groups
         }
         float Hc[K], Bc[K];
 #pragma unroll
@@ -687,45 +689,44 @@ __global__ void __launch_bounds__(NT) fb_kernel_lin(FbArgs a) {
 #pragma unroll
         for (int u = 0; u < K; ++u) {
           if constexpr (VJP) {
-            float al[K], ad[K], ea[K], dd[K];
+            // per input j: alpha = e G and q = e (G A - g_t G d), the state's
+            // unnormalised tangent with the step's term g_t (c - w_t) = -g_t d
+            float al[K], q[K], dd[K];
   #pragma unroll
             for (int j = 0; j < K; ++j) {
               dd[j] = wtl - cbr[i][j][u];
               const float e = ex2(fmaf(-dd[j], dd[j], noff));
               al[j] = e * Gin[j];
-              ad[j] = al[j] * dd[j];
-              ea[j] = e * Ain[j];
+              q[j] = e * fmaf(-gG[j], dd[j], Ain[j]);
             }
             const float go = (al[0] + al[1]) + (al[2] + al[3]);   // sum alpha
-            const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);  // sum alpha d
-            const float sea = (ea[0] + ea[1]) + (ea[2] + ea[3]);  // sum e G A
-            float sadd = ad[0] * dd[0], sead = ea[0] * dd[0];
+            const float aout = (q[0] + q[1]) + (q[2] + q[3]);     // G A of the output group
+            float sad = al[0] * dd[0], sqd = q[0] * dd[0];        // sum alpha d, sum q d
   #pragma unroll
             for (int j = 1; j < K; ++j) {
-              sadd = fmaf(ad[j], dd[j], sadd);
-              sead = fmaf(ea[j], dd[j], sead);
+              sad = fmaf(al[j], dd[j], sad);
+              sqd = fmaf(q[j], dd[j], sqd);
             }
-            // G A of the output group: the step adds g_t (c - w_t) = -g_t d
-            const float aout = fmaf(-gt, sad, sea);
             rv[0] = fmaxf(rv[0], go);
             const float Hu = Hc[u];
             const float bx = fmaf(-xbar, Hu, Bc[u]);              // H (B - xbar)
             rv[1] = fmaf(Hu, sad, rv[1]);
             rv[2] = fmaf(Hu, go, rv[2]);
             rv[3] = fmaf(go, bx, fmaf(Hu, aout, rv[3]));
-            rv[4] = fmaf(sad, bx, fmaf(Hu, fmaf(-gt, sadd, sead), rv[4]));
+            rv[4] = fmaf(sad, bx, fmaf(Hu, sqd, rv[4]));
             rot::st_pair_at(sl[u], go, aout);
           } else {
             // soft codeword alone: sum alpha, sum alpha d and the two moments
-            float al[K], ad[K];
+            float al[K], dd[K];
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              const float dj = wtl - cbr[i][j][u];
-              al[j] = ex2(fmaf(-dj, dj, noff)) * Gin[j];
-              ad[j] = al[j] * dj;
+              dd[j] = wtl - cbr[i][j][u];
+              al[j] = ex2(fmaf(-dd[j], dd[j], noff)) * Gin[j];
             }
             const float go = (al[0] + al[1]) + (al[2] + al[3]);
-            const float sad = (ad[0] + ad[1]) + (ad[2] + ad[3]);
+            float sad = al[0] * dd[0];
+#pragma unroll
+            for (int j = 1; j < K; ++j) sad = fmaf(al[j], dd[j], sad);
             rv[0] = fmaxf(rv[0], go);
             rv[1] = fmaf(Hc[u], sad, rv[1]);
             rv[2] = fmaf(Hc[u], go, rv[2]);
