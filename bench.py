@@ -164,7 +164,7 @@ def roofline_vec_edges_per_s(r_t, r_v=VALU_LANES_PUBLISHED) -> float:
 # build flags, and the argument block).
 # Any other source reports null.
 MEASURED_TRAFFIC = {
-    ("fwd_vjp", "17c757c00ee3e311"): 2.68510e8 * 1024 * 2.0 + 5.36933e8 * 1024 * 1.0,
+    ("fwd_vjp", "6f9f29842f82571d"): 2.68507e8 * 1024 * 2.0 + 5.36960e8 * 1024 * 1.0,
 }
 KERNEL_SOURCES = {"fwd_vjp": ("bcjr_rot_kernels.h", "bcjr_rot.hip", "bcjr_device.h", "bcjr_internal.h",
                               "../build.py"),
