@@ -955,6 +955,10 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
         rt = rb[t];
       }
       const double wt = (double)wf;
+      // h_t(s) + H = k2 c (2 w - c) + H - k2 w^2: the state's part in two
+      // FMAs, the step's k2 w^2 taken out once with the shift
+      const double k2w2 = 2.0 * k2 * wt;
+      const double hoff = k2 * wt * wt;
       uint32_t rrow = row0, rrowT = row0 + GS, wcol = col0, wcolT = col0 + GS;
       uint32_t lrow = lrow0, lcol = lcol0;
       pin_u(rrow);
@@ -1039,8 +1043,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             double x[K];
 #pragma unroll
             for (int b = 0; b < K; ++b) {
-              const double d = wt - (double)cc[j][b];
-              x[b] = fma(-d * k2, d, H[b]);
+              const double cd = (double)cc[j][b];
+              x[b] = fma(cd, fma(-k2, cd, k2w2), H[b]);
             }
             const double m = max_of<K>(x);
             float E[K];
@@ -1053,7 +1057,7 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             float num = E[0] * fmaf(gt, cc[j][0] - rt, Bin[0]);
 #pragma unroll
             for (int b = 1; b < K; ++b) num = fmaf(E[b], fmaf(gt, cc[j][b] - rt, Bin[b]), num);
-            const double hv = m + (double)lg2(s) - (double)dlag;
+            const double hv = m + (double)lg2(s) - ((double)dlag + hoff);
             float lo;
             split_df(hv, oh[i][j], lo);
             ol[i] |= (uint64_t)lo8_enc(oh[i][j], lo) << (8 * j);
@@ -1128,6 +1132,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
       }
       if (t > 0) xbar = fmaf(gt, rt, xbar);  // B_t no longer holds step t
       const double wt = (double)wf;
+      const double k2w2 = 2.0 * k2 * wt;  // as in S0: k2 w^2 out of the state terms
+      const double hoff = k2 * wt * wt;
+      const double lamh = lam_est + hoff;
       const double mBt = (double)mBnx;
       mBnx = sm_mB[t + 1 < L ? t + 1 : t];
       uint32_t rcol = col0, rcolT = col0 + GS, wrow = row0, wrowT = row0 + GS;
@@ -1177,8 +1184,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             double al[K];
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              const double d = wt - (double)cc[j][u];
-              al[j] = fma(-d * k2, d, G[j]);
+              const double cd = (double)cc[j][u];
+              al[j] = fma(cd, fma(-k2, cd, k2w2), G[j]);
             }
             const double m = max_of<K>(al);
             float E[K];
@@ -1199,12 +1206,12 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
               sx = fmaf(E[j], x, sx);
               scx = fmaf(ec, x, scx);
             }
-            const double gout = m + (double)lg2(s) - (double)dlag;
+            const double gout = m + (double)lg2(s) - ((double)dlag + hoff);
             float lo;
             split_df(gout, oh[i][u], lo);
             ol[i] |= (uint64_t)lo8_enc(oh[i][u], lo) << (8 * u);
             rv[0] = fmaxf(rv[0], oh[i][u]);
-            const float fac = ex2((float)(m + df_join(Hh[u], (uint32_t)(Hl >> (8 * u))) - lam_est));
+            const float fac = ex2((float)(m + df_join(Hh[u], (uint32_t)(Hl >> (8 * u))) - lamh));
             rv[1] = fmaf(fac, s, rv[1]);
             rv[2] = fmaf(fac, sc, rv[2]);
             rv[3] = fmaf(fac, sx, rv[3]);
@@ -1316,8 +1323,9 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             gt = gb[t];
             xt = sm_xb[t];
           }
-          const double lt = sm_lam[t];
           const double wt = (double)wf;
+          const double k2w2 = 2.0 * k2 * wt;
+          const double lt = sm_lam[t] + k2 * wt * wt;
           float Hh[K], Bv[K], Gh[K], A[K];
           uint32_t Gl[K];
           const uint64_t Hl = nHl;
@@ -1339,8 +1347,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
             const float bx = Bv[u] - xt;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-              const double d = wt - (double)cc[j][u];
-              const float p = ex2((float)(fma(-d * k2, d, G[j]) + hb));
+              const double cd = (double)cc[j][u];
+              const float p = ex2((float)(fma(cd, fma(-k2, cd, k2w2), G[j]) + hb));
               const float X = fmaf(gt, cc[j][u], A[j]) + bx;
               acc[j][u] = fmaf(p, fmaf((wf - cc[j][u]) * X, invT, gt), acc[j][u]);
             }
