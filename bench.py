@@ -168,7 +168,9 @@ MEASURED_TRAFFIC = {
 }
 KERNEL_SOURCES = {"fwd_vjp": ("bcjr_rot_kernels.h", "bcjr_rot.hip", "bcjr_device.h", "bcjr_internal.h",
                               "../build.py"),
-                  "vec": ("bcjr_vec_kernels.h", "bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h")}
+                  "vec": ("bcjr_vec_kernels.h", "bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h"),
+                  # the log-domain and double-float kernels (dCodebook, T < 0.04) and their dispatcher
+                  "log": ("bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h", "bcjr_capi.hip")}
 
 
 def kernel_source_digest(path: str = "fwd_vjp") -> str:
