@@ -13,6 +13,7 @@
 #include "bcjr_generic_kernels.h"
 #include "bcjr_kernels.h"
 #include "bcjr_ldlq_kernels.h"
+#include "bcjr_pruned_kernels.h"
 #include "bcjr_vec_kernels.h"
 #include "bcjr_qat.h"
 
@@ -454,8 +455,8 @@ int run_viterbi(const float* w, int64_t B, int64_t L, const float* codebook, int
 int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k, float T,
               const float* g, const float* ref, float* w_soft, float* logZ, float* dW,
               float* dCodebook, void* workspace, size_t ws_bytes, hipStream_t stream,
-              int32_t* repair_flags = nullptr) {
-  const bool dc = dCodebook != nullptr;
+              int32_t* repair_flags = nullptr, double* dc_add = nullptr) {
+  const bool dc = dCodebook != nullptr || dc_add != nullptr;
   const Family f = fb_family(n, k, false);
   const HpLayout lay = hp_layout(L, n, k, dc);
   FbFn fn = hp_pick(n, k, f, dc);
@@ -496,19 +497,143 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
   a.histGA = dc ? reinterpret_cast<float*>(p) : nullptr;  p += slots * lay.histGA;
   a.small = reinterpret_cast<float*>(p);              p += slots * lay.small;
   a.dc_part = dc ? reinterpret_cast<double*>(p) : nullptr;
+  const int64_t S = (int64_t)1 << n;
   if (dc) {  // the (G, A, lo) entries of step 0 are zero for every block of a slot
     const int64_t hstep = hp_step_bytes(n, k) / 4;
     hipLaunchKernelGGL(fill_rows_kernel, dim3((unsigned)ceil_div(slots * hstep, 256)), dim3(256), 0,
                        stream, a.histGA, L * hstep, slots, hstep, 0.f);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   }
+  if (dc_add) {  // a repair pass adds every slot's blocks into zeroed partials
+    hipLaunchKernelGGL(fill_d_kernel, dim3((unsigned)ceil_div(slots * S, 256)), dim3(256), 0, stream,
+                       a.dc_part, slots * S);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
   hipLaunchKernelGGL(fn, dim3((unsigned)grid), dim3(f.nt), lds, stream, a);
   if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   if (dc) {
-    const int64_t S = (int64_t)1 << n;
     const int64_t used = slots < B ? slots : B;
-    hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
-                       a.dc_part, used, S, dCodebook);
+    if (dc_add)
+      hipLaunchKernelGGL(dc_reduce_add_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
+                         a.dc_part, used, S, dc_add);
+    else
+      hipLaunchKernelGGL(dc_reduce_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream,
+                         a.dc_part, used, S, dCodebook);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  return BCJR_OK;
+}
+
+// ------------------------------------------------------------ pruned VJP
+// S = 65536, k = 2 at T <= 0.008: the sum-product and VJP over the states
+// within kPrunedMargin nats of the block's best path (bcjr_pruned_kernels.h).
+// Workspace: [block flags][fp64 dCodebook accumulator][slots: min-sum bytes,
+// kept-state bits, step minima, best cost, kept-state entries].  Blocks are
+// taken in chunks of one slot each; a block the pruned kernel cannot finish
+// (more kept state-steps than its slot holds, or no finite logZ) is marked
+// and recomputed afterwards by the double-float kernel in its repair mode,
+// over the same slot memory, its dCodebook added into the accumulator.
+constexpr double kPrunedMaxT = 0.008;
+constexpr double kPrunedMargin = 40.0;   // nats below the best path
+constexpr int64_t kPrunedMaxL = 2048;
+constexpr int64_t kPrunedMaxSlots = 2048;
+constexpr int64_t kPrunedEntriesPerStep = 256;  // average kept states per step a slot holds
+
+bool pruned_ok(int n, int k, float T, int64_t L) {
+  return n == 16 && k == 2 && T <= (float)kPrunedMaxT && L <= kPrunedMaxL;  // (T as the caller rounded it)
+}
+
+struct PrLayout {
+  size_t q, bm, hmin, best, ent, slot;
+  int64_t ecap;
+};
+
+PrLayout pr_layout(int64_t L) {
+  PrLayout l;
+  l.ecap = kPrunedEntriesPerStep * L;
+  l.q = align_up((size_t)L * pr::GS);
+  l.bm = align_up((size_t)L * pr::WORDS * sizeof(uint64_t));
+  l.hmin = align_up((size_t)L * sizeof(float));
+  l.best = align_up(sizeof(float));
+  l.ent = align_up((size_t)4 * l.ecap * sizeof(double));
+  l.slot = l.q + l.bm + l.hmin + l.best + l.ent;
+  return l;
+}
+
+int run_fb_pruned(const float* w, int64_t B, int64_t L, const float* codebook, int n, int k,
+                  float T, const float* g, float* w_soft, float* logZ, float* dW, float* dCodebook,
+                  void* workspace, size_t ws_bytes, hipStream_t stream) {
+  const int64_t S = (int64_t)1 << n;
+  const size_t fl = flag_bytes(B);
+  const size_t dcb = dCodebook ? align_up((size_t)S * sizeof(double)) : 0;
+  if (ws_bytes <= fl + dcb) return BCJR_ERR_WORKSPACE;
+  const size_t region = ws_bytes - fl - dcb;
+  const PrLayout lay = pr_layout(L);
+  const int64_t slots = std::min<int64_t>(std::min<int64_t>(B, kPrunedMaxSlots), (int64_t)(region / lay.slot));
+  // the chunks must be large enough to fill the GPU, and the repair pass must fit
+  if (slots < std::min<int64_t>(B, 64)) return BCJR_ERR_WORKSPACE;
+  if (region < hp_prefix_bytes(B, L) + std::max(hp_layout(L, n, k, dCodebook != nullptr).slot,
+                                                vit_slot_bytes(L, n, k)))
+    return BCJR_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  int32_t* flags = reinterpret_cast<int32_t*>(ws);
+  double* dcacc = dCodebook ? reinterpret_cast<double*>(ws + fl) : nullptr;
+  char* base = ws + fl + dcb;
+  static std::once_flag attr_once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(attr_once, [] {
+    if (hipFuncSetAttribute((const void*)mm_back_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)pr::kMinSumLds) != hipSuccess ||
+        hipFuncSetAttribute((const void*)mm_fwd_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)pr::kMinSumLds) != hipSuccess ||
+        hipFuncSetAttribute((const void*)pruned_sp_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)pr::kSpLds) != hipSuccess)
+      attr_err = hipErrorInvalidValue;
+  });
+  if (attr_err != hipSuccess) return BCJR_ERR_HIP;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)ceil_div(B, 256)), dim3(256), 0, stream,
+                     reinterpret_cast<float*>(flags), B, 0.f);
+  if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  if (dcacc) {
+    hipLaunchKernelGGL(fill_d_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, dcacc, S);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  PrArgs a = {};
+  a.w = w; a.g = g; a.c = codebook; a.B = B; a.L = L;
+  a.T = (double)T;
+  a.theta = (float)(2.0 * (double)T * kPrunedMargin);
+  a.qscale = (float)(16.0 / (2.0 * (double)T * kPrunedMargin));
+  char* p = base;
+  a.q = reinterpret_cast<uint8_t*>(p);   p += (size_t)slots * lay.q;
+  a.bm = reinterpret_cast<uint64_t*>(p); p += (size_t)slots * lay.bm;
+  a.hmin = reinterpret_cast<float*>(p);  p += (size_t)slots * lay.hmin;
+  a.best = reinterpret_cast<float*>(p);  p += (size_t)slots * lay.best;
+  a.ent = reinterpret_cast<double*>(p);
+  a.ecap = lay.ecap;
+  a.dc = dcacc;
+  a.w_soft = w_soft; a.logZ = logZ; a.dW = dW;
+  a.flags = flags;
+  // (the per-slot strides inside the kernels are L-based; hmin and best are
+  // packed arrays of slots x L and slots floats)
+  for (int64_t b0 = 0; b0 < B; b0 += slots) {
+    a.b0 = b0;
+    a.nblk = std::min<int64_t>(slots, B - b0);
+    hipLaunchKernelGGL(mm_back_kernel, dim3((unsigned)a.nblk), dim3(pr::NT), pr::kMinSumLds, stream, a);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    hipLaunchKernelGGL(mm_fwd_kernel, dim3((unsigned)a.nblk), dim3(pr::NT), pr::kMinSumLds, stream, a);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+    hipLaunchKernelGGL(pruned_sp_kernel, dim3((unsigned)ceil_div(a.nblk, pr::SP_WAVES)),
+                       dim3(pr::SP_WAVES * 64), pr::kSpLds, stream, a);
+    if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
+  }
+  // marked blocks: the double-float kernel (it decodes their centring
+  // reference first); every workgroup exits at once when none is marked
+  int st = run_fb_hp(w, B, L, codebook, n, k, T, g, nullptr, w_soft, logZ, dW, nullptr, base, region,
+                     stream, flags, dcacc);
+  if (st != BCJR_OK) return st;
+  if (dcacc) {
+    hipLaunchKernelGGL(dc_store_kernel, dim3((unsigned)ceil_div(S, 256)), dim3(256), 0, stream, dcacc, S,
+                       dCodebook);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   }
   return BCJR_OK;
@@ -598,6 +723,11 @@ int run_fb(const float* w, int64_t B, int64_t L, const float* codebook, int n, i
   if (!dCodebook && linear_ok(n, k, T))
     return run_fb_lin(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, workspace, ws_bytes, stream,
                       vjp);
+  if (vjp && pruned_ok(n, k, T, L)) {
+    const int st = run_fb_pruned(w, B, L, codebook, n, k, T, g, w_soft, logZ, dW, dCodebook, workspace,
+                                 ws_bytes, stream);
+    if (st != BCJR_ERR_WORKSPACE) return st;  // (a workspace too small for it: the dense kernel)
+  }
   if (vjp && use_high_precision(T))
     return run_fb_hp(w, B, L, codebook, n, k, T, g, ref, w_soft, logZ, dW, dCodebook, workspace,
                      ws_bytes, stream);

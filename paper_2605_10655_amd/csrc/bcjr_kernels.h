@@ -1359,7 +1359,8 @@ __global__ void __launch_bounds__(NT) fb_kernel_hp(FbArgs a) {
           for (int j = 0; j < K; ++j) {
             double* pj = part + ((int64_t)j << (n - KB)) + ((i * TPB) << KB) + ((uint32_t)tb << KB);
 #pragma unroll
-            for (int u = 0; u < K; ++u) pj[u] = first ? (double)acc[j][u] : pj[u] + (double)acc[j][u];
+            for (int u = 0; u < K; ++u)  // (a repair pass adds into partials zeroed before it)
+              pj[u] = first && !repair ? (double)acc[j][u] : pj[u] + (double)acc[j][u];
           }
         }
       }

@@ -1,0 +1,159 @@
+"""GPU parity of the pruned low-temperature VJP (S = 65536, k = 2, T <= 0.008):
+the min-sum sweeps keep, per step, the states within 40 nats of the block's
+best path, and the sum-product, w_soft, logZ, dW and dCodebook run in fp64
+over those states only.  Every output is compared with the fp64 oracle's
+full recursion.  Blocks the pruned kernel cannot finish (more kept
+state-steps than a slot holds) are recomputed by the double-float kernel:
+blocks of (near-)zero weights, where the codebook is densest, force that,
+and the tests check both that those blocks were marked and that every block
+still matches the oracle.
+
+Tolerances as everywhere: w_soft |err| <= 2e-5, logZ 1e-4 relative, dW and
+dCodebook 1e-4 of max(|ref_i|, rms(ref)) with the rms over the whole output.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2605_10655_amd as P
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+TOL_WS, TOL_LOGZ, TOL_GRAD = 2e-5, 1e-4, 1e-4
+N, KB = 16, 2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    P.load_library()
+    yield
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def grad_err(gpu, ref):
+    ref = np.asarray(ref, np.float64)
+    rms = np.sqrt(np.mean(ref * ref))
+    scale = np.maximum(np.abs(ref), rms)
+    return float((np.abs(gpu.astype(np.float64) - ref) / np.where(scale > 0, scale, 1.0)).max())
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_case(w, c, g, T, want_dc=True, ws_bytes=None):
+    B, L = w.shape
+    if ws_bytes is None:
+        ws_bytes = P.bcjr_workspace_bytes(B, L, N, KB, P.OP_FWD_VJP)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda:0")
+    out = P.bcjr_soft_codeword_fwd_vjp(dev(w), dev(c), N, KB, T, dev(g), want_dCodebook=want_dc, workspace=ws)
+    torch.cuda.synchronize()
+    flags = ws[:4 * B].view(torch.int32).cpu().numpy().copy()
+    return [None if x is None else x.cpu().numpy() for x in out], flags
+
+
+def check(w, c, g, T, want_dc=True):
+    (ws_, lz, dW, dc), flags = run_case(w, c, g, T, want_dc)
+    rws, rlz, rdW, rdc = O.soft_codeword_vjp(w, c, N, KB, float(np.float32(T)), g, want_dc=want_dc)
+    e_ws = float(np.abs(ws_ - rws).max())
+    e_lz = float((np.abs(lz - rlz) / np.abs(rlz)).max())
+    e_dw = grad_err(dW, rdW)
+    e_dc = grad_err(dc, rdc) if want_dc else 0.0
+    _say(f"   w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e} dc {e_dc:.2e} marked {int(flags.sum())}")
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD and e_dc <= TOL_GRAD
+    return flags
+
+
+def normal_case(B, L, seed, outliers=False):
+    r = np.random.Generator(np.random.PCG64(seed))
+    c = r.standard_normal(1 << N).astype(np.float32)
+    w = r.standard_normal((B, L)).astype(np.float32)
+    g = r.standard_normal((B, L)).astype(np.float32)
+    if outliers and B >= 3 and L >= 4:
+        w[1, L // 2] = 5.0      # one weight past the codebook's range
+        w[2, :] *= 0.05         # a block of near-zero weights (many close codewords)
+    return w, c, g
+
+
+@pytest.mark.parametrize("T", [0.008, 0.004, 0.001])
+@pytest.mark.parametrize("L", [1, 9, 256])
+def test_pruned_matches_oracle(T, L):
+    """Six blocks: N(0, 1) weights, one with a weight at 5 (past the
+    codebook's range), one of near-zero weights (where the codebook is
+    densest: at T >= 0.004 its kept set can overflow the slot, and it is then
+    recomputed by the double-float kernel).  Short blocks have too little
+    trellis around their steps to narrow the window (at L = 1 a third of the
+    codewords lie within it) and go to the double-float kernel as well; at
+    L = 256 the ordinary blocks stay on the pruned path."""
+    _say(f"[pruned] T={T} L={L} B=6")
+    w, c, g = normal_case(6, L, 100 + L, outliers=True)
+    flags = check(w, c, g, T)
+    if L == 256:
+        assert flags[[0, 3, 4, 5]].sum() == 0, "ordinary blocks stay on the pruned path"
+
+
+@pytest.mark.parametrize("T", [0.0072, 0.001])
+def test_pruned_without_dcodebook(T):
+    _say(f"[pruned] T={T} no dCodebook")
+    w, c, g = normal_case(5, 64, 7)
+    check(w, c, g, T, want_dc=False)
+
+
+def test_pruned_long_blocks():
+    _say("[pruned] L=2048 T=0.004")
+    w, c, g = normal_case(2, 2048, 11)
+    check(w, c, g, 0.004)
+
+
+@pytest.mark.parametrize("want_dc", [True, False])
+def test_pruned_marks_blocks_it_cannot_hold(want_dc):
+    """A block of zero weights sits where the N(0, 1) codebook is densest: at
+    T = 0.004 about 18600 of its 32 steps' states lie within the window
+    (the oracle's own min-sum tables, counted on the CPU), past the slot's
+    256 per step; that block is marked and recomputed by the double-float
+    kernel, the ordinary blocks stay on the pruned path."""
+    _say(f"[pruned] overflow fallback want_dc={want_dc}")
+    r = np.random.Generator(np.random.PCG64(23))
+    c = r.standard_normal(1 << N).astype(np.float32)
+    w = r.standard_normal((4, 32)).astype(np.float32)
+    w[2, :] = 0.0
+    g = r.standard_normal((4, 32)).astype(np.float32)
+    flags = check(w, c, g, 0.004, want_dc=want_dc)
+    assert flags[2] == 1 and flags[[0, 1, 3]].sum() == 0
+
+
+def test_pruned_chunks_and_sum_rule():
+    """160 blocks through a 200 MiB workspace: two chunks of slots (100 and
+    60 blocks).  Blocks on both sides of the chunk boundary match the
+    oracle, and the batch obeys sum dW + sum dc = sum g (moving every weight
+    and codeword together leaves the posterior unchanged and moves each
+    step's codeword by the same amount)."""
+    _say("[pruned] two chunks, sum rule, B=160")
+    r = np.random.Generator(np.random.PCG64(31))
+    c = r.standard_normal(1 << N).astype(np.float32)
+    w = r.standard_normal((160, 64)).astype(np.float32)
+    g = r.standard_normal((160, 64)).astype(np.float32)
+    ws_bytes = 1024 + (1 << N) * 8 + 200 * (1 << 20)
+    (ws_, lz, dW, dc), flags = run_case(w, c, g, 0.002, ws_bytes=ws_bytes)
+    assert flags.sum() == 0
+    lhs = float(dW.astype(np.float64).sum() + dc.astype(np.float64).sum())
+    rhs = float(g.astype(np.float64).sum())
+    _say(f"   sum dW + sum dc {lhs:.6f} sum g {rhs:.6f}")
+    assert abs(lhs - rhs) <= 1e-3 * max(1.0, abs(rhs))
+    idx = np.array([0, 99, 100, 159])
+    rws, rlz, rdW, _ = O.soft_codeword_vjp(w[idx], c, N, KB, float(np.float32(0.002)), g[idx], want_dc=False)
+    e_ws = float(np.abs(ws_[idx] - rws).max())
+    e_lz = float((np.abs(lz[idx] - rlz) / np.abs(rlz)).max())
+    e_dw = grad_err(dW[idx], rdW)
+    _say(f"   blocks 0, 99, 100, 159: w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}")
+    assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
