@@ -170,7 +170,10 @@ KERNEL_SOURCES = {"fwd_vjp": ("bcjr_rot_kernels.h", "bcjr_rot.hip", "bcjr_device
                               "../build.py"),
                   "vec": ("bcjr_vec_kernels.h", "bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h"),
                   # the log-domain and double-float kernels (dCodebook, T < 0.04) and their dispatcher
-                  "log": ("bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h", "bcjr_capi.hip")}
+                  "log": ("bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h", "bcjr_capi.hip"),
+                  # the pruned low-temperature VJP (with its double-float repair pass)
+                  "pruned": ("bcjr_pruned_kernels.h", "bcjr_kernels.h", "bcjr_device.h", "bcjr_internal.h",
+                             "bcjr_capi.hip")}
 
 
 def kernel_source_digest(path: str = "fwd_vjp") -> str:
