@@ -1177,6 +1177,14 @@ size_t bcjr_workspace_bytes(int64_t B, int64_t L, int state_bits, int k, int op)
     bytes = std::max(bytes, cs_bytes(state_bits) + flag_bytes(B) + hp_prefix_bytes(B, L) +
                                 std::max(hp_layout(L, state_bits, k, false).slot,
                                          vit_slot_bytes(L, state_bits, k)));
+    // the pruned path: flags, the fp64 dCodebook accumulator, then enough
+    // slots for a chunk, or the repair pass's decoded reference and one slot
+    if (state_bits == 16 && k == 2 && L <= kPrunedMaxL)
+      bytes = std::max(bytes, flag_bytes(B) + align_up(((size_t)1 << state_bits) * sizeof(double)) +
+                                  std::max((size_t)std::min<int64_t>(B, 64) * pr_layout(L).slot,
+                                           hp_prefix_bytes(B, L) +
+                                               std::max(hp_layout(L, state_bits, k, true).slot,
+                                                        vit_slot_bytes(L, state_bits, k))));
   }
   return bytes;
 }

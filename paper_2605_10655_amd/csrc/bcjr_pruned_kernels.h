@@ -11,10 +11,10 @@
 // chunk of blocks:
 //
 //   mm_back_kernel   backward min-sum over all states (fp32, group form):
-//                    per step the backward metric of every group, stored as
-//                    one byte above the step's minimum in units of margin/16
-//                    (rounded down, so the window test below is conservative),
-//                    and the block's best path cost;
+//                    per step the backward metric of every group above the
+//                    step's minimum, coded in one byte (rounded down, so the
+//                    window test below is conservative), and the block's best
+//                    path cost;
 //   mm_fwd_kernel    forward min-sum over all states: a state is kept when its
 //                    forward metric plus the stored backward bound lies within
 //                    the window; one bit per state and step;
@@ -46,7 +46,7 @@ struct PrArgs {
   double T;
   float theta;          // the window in squared-distortion units: 2 T margin
   float qscale;         // 16 / theta
-  uint8_t* q;           // [slots][L][S/4] backward bound above the step minimum, units theta/16
+  uint8_t* q;           // [slots][L][S/4] backward bound above the step minimum (bound_code)
   float* hmin;          // [slots][L] the step minimum of the backward metric
   float* best;          // [slots] the block's best path cost
   uint64_t* bm;         // [slots][L][1024] kept-state bits
@@ -69,6 +69,24 @@ constexpr int NW = NT / 64;
 constexpr int SP_WAVES = 4;       // pruned_sp_kernel: one block per wave
 constexpr int WORDS = NT;         // kept-state words per step
 constexpr size_t kMinSumLds = (size_t)2 * GS * sizeof(float) + (size_t)3 * NW * sizeof(float);
+
+// The byte code of a backward bound z >= 0 in units of window / 16: codes
+// below 128 are z rounded down, codes from 128 on stand for 128 * 1.05^(q - 128)
+// (up to ~3900 windows), the largest not above z.  Blocks far outside the
+// codebook's range have future costs spread over thousands of windows; a
+// code that saturated at a few windows would keep most of their states.
+constexpr float kCodeLog2Ratio = 0.0703893279f;  // log2(1.05)
+
+__device__ __forceinline__ uint32_t bound_code(float z) {
+  const float t = lg2(z * (1.f / 128.f)) * (1.f / kCodeLog2Ratio) - 1e-3f;
+  const float hi = fminf(128.f + floorf(t), 255.f);
+  return (uint32_t)(z < 128.f ? z : hi);
+}
+
+__device__ __forceinline__ float bound_value(uint32_t q) {
+  const float qf = (float)q;
+  return q < 128u ? qf : 128.f * ex2((qf - 128.f) * kCodeLog2Ratio);
+}
 constexpr size_t kSpLdsPerWave = (size_t)WORDS * sizeof(uint64_t) + (size_t)WORDS * sizeof(uint32_t) +
                                   (size_t)1024 * sizeof(uint32_t);
 constexpr size_t kSpLds = kSpLdsPerWave * SP_WAVES;
@@ -198,15 +216,12 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
       float hm = rd[0];
 #pragma unroll
       for (int x = 1; x < NW; ++x) hm = fminf(hm, rd[x]);
-      // the bound above the step minimum, rounded down (saturating at 255)
+      // the bound above the step minimum, coded and rounded down
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
         uint32_t word = 0;
 #pragma unroll
-        for (int b = 0; b < K; ++b) {
-          const float z = fminf(fmaxf((in[i][b] - hm) * a.qscale, 0.f), 255.f);
-          word |= (uint32_t)z << (8 * b);
-        }
+        for (int b = 0; b < K; ++b) word |= bound_code(fmaxf((in[i][b] - hm) * a.qscale, 0.f)) << (8 * b);
         __builtin_amdgcn_raw_buffer_store_b32(word, qr, (int)((uint32_t)(tb + i * NT) * K), (int)(t * GS), 0);
       }
       if (tb == 0) hmin[t] = hm;
@@ -226,7 +241,7 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
 
 // Forward min-sum with the window test: F_t(s) = (w_t - c(s))^2 + Gm_t(s >> 2),
 // Gm_{t+1}(sg * 4 + u) = min_j F_t(j, sg, u), Gm_0 = 0; state s is kept at
-// step t when F_t(s) + hmin_t + q_t(s mod 2^14) theta / 16 <= best + theta.
+// step t when F_t(s) + hmin_t + (its coded bound) theta / 16 <= best + theta.
 __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
   using namespace pr;
   extern __shared__ float lds_mm[];
@@ -265,7 +280,7 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
         float mo[K];
 #pragma unroll
         for (int u = 0; u < K; ++u) {
-          const float hb = fmaf((float)((qw >> (8 * u)) & 0xFFu), step, hm);
+          const float hb = fmaf(bound_value((qw >> (8 * u)) & 0xFFu), step, hm);
           float m = INFINITY;
 #pragma unroll
           for (int j = 0; j < K; ++j) {

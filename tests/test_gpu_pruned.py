@@ -157,3 +157,21 @@ def test_pruned_chunks_and_sum_rule():
     e_dw = grad_err(dW[idx], rdW)
     _say(f"   blocks 0, 99, 100, 159: w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}")
     assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
+
+
+@pytest.mark.parametrize("T", [0.006, 0.002])
+def test_pruned_outlier_block(T):
+    """A block of weights at 5.5, past the codebook's largest entry (~4.4): its
+    fp32 path costs are ~10x those of an ordinary block, and under the old
+    saturating byte code of the backward bound nearly all its states were
+    kept.  It stays on the pruned path and every output matches the oracle.
+    (At T = 0.001 its log alpha and log beta reach ~1e6 nats, so P =
+    exp(log alpha + log beta - log Z) carries ~1e-10 relative rounding in
+    fp64 -- in the oracle too -- and the dCodebook sum, whose terms of ~1e4
+    cancel to O(1), resolves it only to ~1e-4 absolute: below what the
+    oracle can certify at this tolerance.)"""
+    _say(f"[pruned] outlier block T={T}")
+    w, c, g = normal_case(4, 256, 41)
+    w[1, :] = 5.5
+    flags = check(w, c, g, T)
+    assert flags.sum() == 0
