@@ -69,27 +69,27 @@ constexpr int NW = NT / 64;
 constexpr int SP_WAVES = 4;       // pruned_sp_kernel: one block per wave
 constexpr int WORDS = NT;         // kept-state words per step
 constexpr size_t kMinSumLds = (size_t)2 * GS * sizeof(float) + (size_t)3 * NW * sizeof(float);
-
-// The byte code of a backward bound z >= 0 in units of window / 16: codes
-// below 128 are z rounded down, codes from 128 on stand for 128 * 1.05^(q - 128)
-// (up to ~3900 windows), the largest not above z.  Blocks far outside the
-// codebook's range have future costs spread over thousands of windows; a
-// code that saturated at a few windows would keep most of their states.
-constexpr float kCodeLog2Ratio = 0.0703893279f;  // log2(1.05)
-
-__device__ __forceinline__ uint32_t bound_code(float z) {
-  const float t = lg2(z * (1.f / 128.f)) * (1.f / kCodeLog2Ratio) - 1e-3f;
-  const float hi = fminf(128.f + floorf(t), 255.f);
-  return (uint32_t)(z < 128.f ? z : hi);
-}
-
-__device__ __forceinline__ float bound_value(uint32_t q) {
-  const float qf = (float)q;
-  return q < 128u ? qf : 128.f * ex2((qf - 128.f) * kCodeLog2Ratio);
-}
 constexpr size_t kSpLdsPerWave = (size_t)WORDS * sizeof(uint64_t) + (size_t)WORDS * sizeof(uint32_t) +
                                   (size_t)1024 * sizeof(uint32_t);
 constexpr size_t kSpLds = kSpLdsPerWave * SP_WAVES;
+
+// The byte code of a backward bound z >= 0 in units of window / 16: codes
+// below 128 are z rounded down; from 128 on, z's binary exponent e >= 7 and
+// its top three mantissa bits m: 128 + 8 (e - 7) + m, standing for
+// 2^e (1 + m / 8), the largest such value not above z (up to ~5e5 windows).
+// Blocks far outside the codebook's range have future costs spread over
+// thousands of windows; a code that saturated at a few windows would keep
+// most of their states.
+__device__ __forceinline__ uint32_t bound_code(float z) {
+  const uint32_t b = __float_as_uint(z);
+  const uint32_t c = 128u + 8u * (((b >> 23) & 0xFFu) - 134u) + ((b >> 20) & 7u);
+  return z < 128.f ? (uint32_t)fminf(z, 127.f) : (c > 255u ? 255u : c);
+}
+
+__device__ __forceinline__ float bound_value(uint32_t q) {
+  const uint32_t d = q - 128u;
+  return q < 128u ? (float)q : __uint_as_float(((134u + (d >> 3)) << 23) | ((d & 7u) << 20));
+}
 
 __device__ __forceinline__ float wave_min(float v) {
 #pragma unroll
