@@ -81,8 +81,9 @@ constexpr size_t kSpLds = kSpLdsPerWave * SP_WAVES;
 // thousands of windows; a code that saturated at a few windows would keep
 // most of their states.
 __device__ __forceinline__ uint32_t bound_code(float z) {
-  const uint32_t b = __float_as_uint(z);
-  const uint32_t c = 128u + 8u * (((b >> 23) & 0xFFu) - 134u) + ((b >> 20) & 7u);
+  // (z >= 0: bits 20 and up hold 8 x the biased exponent e + 127, plus m, so
+  // 128 + 8 (e - 7) + m = (bits >> 20) - (8 * 134 - 128))
+  const uint32_t c = (__float_as_uint(z) >> 20) - 944u;
   return z < 128.f ? (uint32_t)fminf(z, 127.f) : (c > 255u ? 255u : c);
 }
 
