@@ -48,11 +48,11 @@
  *   - B == 0 is a no-op returning BCJR_OK (dCodebook, if given, is zeroed).
  *   - Non-finite w or codebook values give non-finite outputs; they are not
  *     checked.
- *   - At state_bits = 16, k = 2, T <= 0.008 and L <= 2048 the VJP (and the
- *     fused call) sums over the states within 40 nats of each block's best
- *     path only: every path through a dropped state weighs at most e^-40 of
- *     the best one, far below fp32 resolution.  A block with more such
- *     state-steps than the workspace slot holds (256 per step on average) is
+ *   - At state_bits = 16, k = 2, T <= 0.015 and L <= 2048 the VJP (and the
+ *     fused call) sums over the states within 30 nats of each block's best
+ *     path only: every path through a dropped state weighs at most e^-30 of
+ *     the best one, below fp32 resolution.  A block with more such
+ *     state-steps than the workspace slot holds (1024 per step on average) is
  *     computed by the full double-float recursion instead.  dCodebook is then
  *     accumulated with fp64 atomic adds, so its last fp32 bit may differ
  *     between runs.

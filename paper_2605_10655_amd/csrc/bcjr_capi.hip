@@ -525,7 +525,7 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
 }
 
 // ------------------------------------------------------------ pruned VJP
-// S = 65536, k = 2 at T <= 0.008: the sum-product and VJP over the states
+// S = 65536, k = 2 at T <= 0.015: the sum-product and VJP over the states
 // within kPrunedMargin nats of the block's best path (bcjr_pruned_kernels.h).
 // Workspace: [block flags][fp64 dCodebook accumulator][slots: min-sum bytes,
 // kept-state bits, step minima, best cost, kept-state entries].  Blocks are
@@ -533,11 +533,11 @@ int run_fb_hp(const float* w, int64_t B, int64_t L, const float* codebook, int n
 // (more kept state-steps than its slot holds, or no finite logZ) is marked
 // and recomputed afterwards by the double-float kernel in its repair mode,
 // over the same slot memory, its dCodebook added into the accumulator.
-constexpr double kPrunedMaxT = 0.008;
-constexpr double kPrunedMargin = 40.0;   // nats below the best path
+constexpr double kPrunedMaxT = 0.015;
+constexpr double kPrunedMargin = 30.0;   // nats below the best path
 constexpr int64_t kPrunedMaxL = 2048;
 constexpr int64_t kPrunedMaxSlots = 2048;
-constexpr int64_t kPrunedEntriesPerStep = 256;  // average kept states per step a slot holds
+constexpr int64_t kPrunedEntriesPerStep = 1024;  // average kept states per step a slot holds
 
 bool pruned_ok(int n, int k, float T, int64_t L) {
   return n == 16 && k == 2 && T <= (float)kPrunedMaxT && L <= kPrunedMaxL;  // (T as the caller rounded it)
@@ -555,7 +555,7 @@ PrLayout pr_layout(int64_t L) {
   l.bm = align_up((size_t)L * pr::WORDS * sizeof(uint64_t));
   l.hmin = align_up((size_t)L * sizeof(float));
   l.best = align_up(sizeof(float));
-  l.ent = align_up((size_t)4 * l.ecap * sizeof(double));
+  l.ent = align_up((size_t)2 * l.ecap * sizeof(double));
   l.slot = l.q + l.bm + l.hmin + l.best + l.ent;
   return l;
 }
@@ -569,9 +569,17 @@ int run_fb_pruned(const float* w, int64_t B, int64_t L, const float* codebook, i
   if (ws_bytes <= fl + dcb) return BCJR_ERR_WORKSPACE;
   const size_t region = ws_bytes - fl - dcb;
   const PrLayout lay = pr_layout(L);
-  const int64_t slots = std::min<int64_t>(std::min<int64_t>(B, kPrunedMaxSlots), (int64_t)(region / lay.slot));
+  int64_t slots = std::min<int64_t>(std::min<int64_t>(B, kPrunedMaxSlots), (int64_t)(region / lay.slot));
   // the chunks must be large enough to fill the GPU, and the repair pass must fit
   if (slots < std::min<int64_t>(B, 64)) return BCJR_ERR_WORKSPACE;
+  {  // a chunk of whole rounds of one min-sum workgroup per CU (a partial last
+     // round costs as much as a full one)
+    int dev = 0, cus = kDeviceCUs;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return BCJR_ERR_HIP;
+    if (slots < B && slots > cus) slots -= slots % cus;
+  }
   if (region < hp_prefix_bytes(B, L) + std::max(hp_layout(L, n, k, dCodebook != nullptr).slot,
                                                 vit_slot_bytes(L, n, k)))
     return BCJR_ERR_WORKSPACE;

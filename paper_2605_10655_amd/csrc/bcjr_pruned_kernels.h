@@ -6,8 +6,8 @@
 // min-sum max-marginal, Sec. 3.2's recursion run from both ends).  Every
 // path through a state outside that window weighs at most e^{-margin}
 // relative to the best one, so dropping those states changes w_soft, logZ,
-// dW and dCodebook by far less than fp32 resolves (a margin of 40 nats
-// leaves errors of ~1e-12 against the full recursion).  Three launches per
+// dW and dCodebook by far less than fp32 resolves (a margin of 30 nats
+// leaves errors of ~1e-10 to 1e-8 against the full recursion).  Three launches per
 // chunk of blocks:
 //
 //   mm_back_kernel   backward min-sum over all states (fp32, group form):
@@ -51,7 +51,7 @@ struct PrArgs {
   float* best;          // [slots] the block's best path cost
   uint64_t* bm;         // [slots][L][1024] kept-state bits
   int64_t ecap;         // kept state-steps a slot can hold
-  double* ent;          // [slots][4][ecap] log alpha, A, log beta, B per kept state-step
+  double* ent;          // [slots][2][ecap] per kept state-step log alpha and A, then log beta and B
   double* dc;           // [S] fp64 dCodebook accumulator, or null
   float* w_soft;        // [B, L] or null
   float* logZ;          // [B] or null
@@ -387,10 +387,10 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64) pruned_sp_kernel(PrArgs a) 
     const float* wb = a.w + bb * L;
     const float* gb = a.g + bb * L;
     const uint64_t* bm = a.bm + sl * L * (int64_t)WORDS;
-    double* la = a.ent + sl * 4 * a.ecap;
+    // an entry holds log alpha and A until the backward sweep reaches it,
+    // then log beta and B (its own forward values are read first)
+    double* la = a.ent + sl * 2 * a.ecap;
     double* aa = la + a.ecap;
-    double* lb = aa + a.ecap;
-    double* bv = lb + a.ecap;
     bool bad = false;
     // ------------------------------------------------------------ forward
     int64_t base = 0, base_prev = 0;
@@ -486,6 +486,7 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64) pruned_sp_kernel(PrArgs a) 
           const int s = (int)list[k];
           const int64_t e = bt + r0 + k;
           const double cs = (double)a.c[s];
+          const double lae = la[e], aae = aa[e];
           double lbv = 0.0, bvv = 0.0;
           if (t + 1 < L) {
             // successors (s mod 2^14) * 4 + b: one word, bits id * 16 + jd * 4 + b
@@ -502,16 +503,16 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64) pruned_sp_kernel(PrArgs a) 
                 const int64_t ed = base_next + pr0 + __popcll(word & ((1ull << nb) - 1ull));
                 const double cd = (double)a.c[(s14 << 2) | b];
                 const double hd = -(wn - cd) * (wn - cd) * i2T;
-                lse_add(nm, ns, ny, hd + lb[ed], gn * cd + bv[ed]);
+                lse_add(nm, ns, ny, hd + la[ed], gn * cd + aa[ed]);  // (step t + 1: beta, B)
               }
             }
             lbv = (nm > -INFINITY) ? nm + log(ns) : -INFINITY;
             bvv = (nm > -INFINITY) ? ny / ns : 0.0;
           }
-          lb[e] = lbv;
-          bv[e] = bvv;
-          const double P = exp(la[e] + lbv - logZ);
-          const double X = aa[e] + bvv - EF;
+          la[e] = lbv;
+          aa[e] = bvv;
+          const double P = exp(lae + lbv - logZ);
+          const double X = aae + bvv - EF;
           sPc += P * cs;
           sPX += P * X;
           sPcX += P * cs * X;

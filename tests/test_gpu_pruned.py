@@ -1,5 +1,5 @@
-"""GPU parity of the pruned low-temperature VJP (S = 65536, k = 2, T <= 0.008):
-the min-sum sweeps keep, per step, the states within 40 nats of the block's
+"""GPU parity of the pruned low-temperature VJP (S = 65536, k = 2, T <= 0.015):
+the min-sum sweeps keep, per step, the states within 30 nats of the block's
 best path, and the sum-product, w_soft, logZ, dW and dCodebook run in fp64
 over those states only.  Every output is compared with the fp64 oracle's
 full recursion.  Blocks the pruned kernel cannot finish (more kept
@@ -85,12 +85,12 @@ def normal_case(B, L, seed, outliers=False):
     return w, c, g
 
 
-@pytest.mark.parametrize("T", [0.008, 0.004, 0.001])
+@pytest.mark.parametrize("T", [0.0139, 0.008, 0.004, 0.001])
 @pytest.mark.parametrize("L", [1, 9, 256])
 def test_pruned_matches_oracle(T, L):
     """Six blocks: N(0, 1) weights, one with a weight at 5 (past the
     codebook's range), one of near-zero weights (where the codebook is
-    densest: at T >= 0.004 its kept set can overflow the slot, and it is then
+    densest: at T >= 0.008 its kept set can overflow the slot, and it is then
     recomputed by the double-float kernel).  Short blocks have too little
     trellis around their steps to narrow the window (at L = 1 a third of the
     codewords lie within it) and go to the double-float kernel as well; at
@@ -118,27 +118,28 @@ def test_pruned_long_blocks():
 @pytest.mark.parametrize("want_dc", [True, False])
 def test_pruned_marks_blocks_it_cannot_hold(want_dc):
     """A block of zero weights sits where the N(0, 1) codebook is densest: at
-    T = 0.004 about 18600 of its 32 steps' states lie within the window
-    (the oracle's own min-sum tables, counted on the CPU), past the slot's
-    256 per step; that block is marked and recomputed by the double-float
-    kernel, the ordinary blocks stay on the pruned path."""
+    T = 0.008 about 77500 of its 32 steps' states lie within the window
+    (the oracle's own min-sum tables, counted on the CPU; 1600-5900 for the
+    ordinary blocks), past the slot's 1024 per step; that block is marked and
+    recomputed by the double-float kernel, the ordinary blocks stay on the
+    pruned path."""
     _say(f"[pruned] overflow fallback want_dc={want_dc}")
     r = np.random.Generator(np.random.PCG64(23))
     c = r.standard_normal(1 << N).astype(np.float32)
     w = r.standard_normal((4, 32)).astype(np.float32)
     w[2, :] = 0.0
     g = r.standard_normal((4, 32)).astype(np.float32)
-    flags = check(w, c, g, 0.004, want_dc=want_dc)
+    flags = check(w, c, g, 0.008, want_dc=want_dc)
     assert flags[2] == 1 and flags[[0, 1, 3]].sum() == 0
 
 
 def test_pruned_chunks_and_sum_rule():
-    """160 blocks through a 200 MiB workspace: two chunks of slots (100 and
-    60 blocks).  Blocks on both sides of the chunk boundary match the
-    oracle, and the batch obeys sum dW + sum dc = sum g (moving every weight
+    """160 blocks through a 200 MiB workspace: 79 slots of ~2.6 MB at L = 64,
+    so three chunks (79, 79 and 2 blocks).  Blocks on both sides of the chunk
+    boundaries match the oracle, and the batch obeys sum dW + sum dc = sum g (moving every weight
     and codeword together leaves the posterior unchanged and moves each
     step's codeword by the same amount)."""
-    _say("[pruned] two chunks, sum rule, B=160")
+    _say("[pruned] three chunks, sum rule, B=160")
     r = np.random.Generator(np.random.PCG64(31))
     c = r.standard_normal(1 << N).astype(np.float32)
     w = r.standard_normal((160, 64)).astype(np.float32)
@@ -150,12 +151,12 @@ def test_pruned_chunks_and_sum_rule():
     rhs = float(g.astype(np.float64).sum())
     _say(f"   sum dW + sum dc {lhs:.6f} sum g {rhs:.6f}")
     assert abs(lhs - rhs) <= 1e-3 * max(1.0, abs(rhs))
-    idx = np.array([0, 99, 100, 159])
+    idx = np.array([0, 78, 79, 157, 158, 159])
     rws, rlz, rdW, _ = O.soft_codeword_vjp(w[idx], c, N, KB, float(np.float32(0.002)), g[idx], want_dc=False)
     e_ws = float(np.abs(ws_[idx] - rws).max())
     e_lz = float((np.abs(lz[idx] - rlz) / np.abs(rlz)).max())
     e_dw = grad_err(dW[idx], rdW)
-    _say(f"   blocks 0, 99, 100, 159: w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}")
+    _say(f"   blocks 0, 78, 79, 157, 158, 159: w_soft {e_ws:.2e} logZ {e_lz:.2e} dW {e_dw:.2e}")
     assert e_ws <= TOL_WS and e_lz <= TOL_LOGZ and e_dw <= TOL_GRAD
 
 
