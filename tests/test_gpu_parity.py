@@ -246,12 +246,13 @@ def test_precision_switch_boundary(T):
     full_check(w, c, 16, 2, T, g, True, f"switch T={T}")
 
 
-@pytest.mark.parametrize("n,T", [(8, 0.2), (12, 0.2), (16, 0.2), (12, 0.003), (16, 0.003)])
+@pytest.mark.parametrize("n,T", [(8, 0.2), (12, 0.2), (16, 0.2), (12, 0.003), (16, 0.02)])
 def test_small_workspace_runs_persistent_loop(n, T):
     """A workspace holding one workgroup's slots forces every workgroup to
     walk several blocks (the persistent loop) and must give the same bits
     (dCodebook up to the order of its slot sums);
-    at T = 0.003 this is the double-float kernel with dCodebook, whose
+    at T = 0.003 (12 state bits) and 0.02 (16) this is the double-float
+    kernel with dCodebook, whose
     step-0 (G, A) history entries are filled once per call and must stay
     valid for every later block of the slot, and whose dCodebook partials
     add up across the blocks of a slot.  Both runs are also checked against
@@ -276,13 +277,15 @@ def test_small_workspace_runs_persistent_loop(n, T):
     assert_same_up_to_dc_order(full, out)
 
 
-@pytest.mark.parametrize("n,B,L", [(12, 24, 20), (16, 16, 12)])
-def test_low_temperature_every_grid_size(n, B, L):
+@pytest.mark.parametrize("n,B,L,T", [(12, 24, 20, 0.003), (16, 16, 12, 0.02)])
+def test_low_temperature_every_grid_size(n, B, L, T):
     """The double-float kernel under every workspace size from one slot up:
     grids of 1 to B workgroups, with and without the persistent loop, must
     give the same results (dCodebook up to the order of its slot sums), and
-    the full-size run must match the oracle."""
-    k, T = 2, 0.003
+    the full-size run must match the oracle.  (With dCodebook at 16 state
+    bits it serves 0.015 < T < 0.04; at T <= 0.015 the pruned kernels take
+    the call when the workspace holds them.)"""
+    k = 2
     w, c, g = WL.random_case(4242 + n, B, L, n)
     full = full_check(w, c, n, k, T, g, True, f"lowT grids n={n}")
     big = P.bcjr_workspace_bytes(B, L, n, k, P.OP_FWD_VJP)

@@ -5,8 +5,8 @@ bcjr_soft_codeword_fwd_vjp with its own workspace.
 The two calls run the same kernels with different workspaces and so with
 different grids; a block's arithmetic does not depend on the slot it runs
 in, so w_soft, logZ and dW must agree bit for bit, and dCodebook (fp64
-per-slot partials summed in another order, then rounded to fp32 once) to a
-few fp32 roundings.  Two calls in a row share the GPU's one scratch array:
+per-slot partials, or fp64 atomic sums on the pruned low-temperature path,
+added in another order, then rounded to fp32 once) to a few fp32 roundings.  Two calls in a row share the GPU's one scratch array:
 the second, smaller call (another trellis size, the double-float
 low-temperature kernel and its reference decode) must not see the first
 call's leftovers.  A shape whose single block slot exceeds the array is
@@ -97,6 +97,12 @@ def test_noalloc_matches_workspace_entry_point_on_two_calls(lib):
     _say("[noalloc] call 3: n=16 k=2 B=5 L=16 T=0.1, no dCodebook")
     _compare(_noalloc(lib, w3, c3, 16, 2, 0.1, g3, want_dc=False),
              _reference(w3, c3, 16, 2, 0.1, g3, want_dc=False), "call 3")
+    # fourth: S = 65536 at T = 0.008, the pruned kernels (min-sum sweeps,
+    # kept-state bitmaps and fp64 entries in the scratch, dCodebook through
+    # an fp64 accumulator there)
+    w4, c4, g4 = WL.random_case(9004, 5, 32, 16)
+    _say("[noalloc] call 4: n=16 k=2 B=5 L=32 T=0.008")
+    _compare(_noalloc(lib, w4, c4, 16, 2, 0.008, g4), _reference(w4, c4, 16, 2, 0.008, g4), "call 4")
 
 
 def test_noalloc_refuses_a_slot_larger_than_the_scratch(lib):
