@@ -174,6 +174,12 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
   const int64_t L = a.L;
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)GS * K * 4u);
   const uint32_t voK = (uint32_t)tb * K * 4u;
+  // this thread's 64 codewords, the same at every step and block
+  float cb[SGT][K][K];
+#pragma unroll
+  for (int i = 0; i < SGT; ++i)
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (uint32_t)(j * GS + i * NT * K) * 4u, cb[i][j]);
   for (int64_t sl = blockIdx.x; sl < a.nblk; sl += gridDim.x) {
     const int64_t bb = a.b0 + sl;
     const float* wb = a.w + bb * L;
@@ -199,16 +205,15 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
       for (int i = 0; i < SGT; ++i)
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-          float cr[K];
-          buf_ld<K>(cbk, voK, (uint32_t)(j * GS + i * NT * K) * 4u, cr);
           float m = INFINITY;
 #pragma unroll
           for (int b = 0; b < K; ++b) {
-            const float d = wt - cr[b];
+            const float d = wt - cb[i][j][b];
             m = fminf(m, fmaf(d, d, in[i][b]));
           }
-          if (t > 0) pout[j * NSG + tb + i * NT] = m;
-          else bestv = fminf(bestv, m);
+          // (at t = 0 these are the best path costs through each state;
+          // the half no later step reads holds them)
+          pout[j * NSG + tb + i * NT] = m;
         }
       mn = wave_min(mn);
       float* rd = red + (t & 1) * NW;
@@ -227,6 +232,8 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
       }
       if (tb == 0) hmin[t] = hm;
     }
+    // (the step-0 rows were written before that step's barrier)
+    for (int x = tb; x < GS; x += NT) bestv = fminf(bestv, lds_mm[GS + x]);
     bestv = wave_min(bestv);
     float* rb = red + 2 * NW;
     if (lane == 0) rb[wave] = bestv;
@@ -251,6 +258,11 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
   const float step = a.theta * (1.f / 16.f);
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)GS * K * 4u);
   const uint32_t voK = (uint32_t)tb * K * 4u;
+  float cb[SGT][K][K];  // as in the backward sweep
+#pragma unroll
+  for (int i = 0; i < SGT; ++i)
+#pragma unroll
+    for (int j = 0; j < K; ++j) buf_ld<K>(cbk, voK, (uint32_t)(j * GS + i * NT * K) * 4u, cb[i][j]);
   for (int64_t sl = blockIdx.x; sl < a.nblk; sl += gridDim.x) {
     const int64_t bb = a.b0 + sl;
     const float* wb = a.w + bb * L;
@@ -267,35 +279,37 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
       float* pout = lds_mm + ((t + 1) & 1) * GS;
       const float wt = ld_uniform(wb, t);
       const float hm = ld_uniform(hmin, t);
-      uint64_t mask = 0;
+      uint32_t mask[2] = {0u, 0u};
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
         const int sg = tb + i * NT;
-        float gin[K], cr[K][K];
+        float gin[K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) {
-          gin[j] = pin[j * NSG + sg];
-          buf_ld<K>(cbk, voK, (uint32_t)(j * GS + i * NT * K) * 4u, cr[j]);
-        }
+        for (int j = 0; j < K; ++j) gin[j] = pin[j * NSG + sg];
         const uint32_t qw = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(qr, (int)((uint32_t)sg * K), (int)(t * GS), 0);
         float mo[K];
+        uint32_t bits = 0;
 #pragma unroll
         for (int u = 0; u < K; ++u) {
           const float hb = fmaf(bound_value((qw >> (8 * u)) & 0xFFu), step, hm);
           float m = INFINITY;
 #pragma unroll
           for (int j = 0; j < K; ++j) {
-            const float d = wt - cr[j][u];
+            const float d = wt - cb[i][j][u];
             const float f = fmaf(d, d, gin[j]);
             m = fminf(m, f);
-            if (f + hb <= lim) mask |= 1ull << (i * 16 + j * 4 + u);
+            bits |= (f + hb <= lim ? 1u : 0u) << (j * 4 + u);
           }
           mo[u] = m;
         }
-        if (t + 1 < L) *reinterpret_cast<float4*>(pout + sg * K) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+        // (after the last step this row goes to the buffer half no later
+        // step reads; the next block clears it behind the step's barrier)
+        *reinterpret_cast<float4*>(pout + sg * K) = make_float4(mo[0], mo[1], mo[2], mo[3]);
+        pin_u(bits);
+        mask[i >> 1] |= bits << (16 * (i & 1));
         sg_fence();
       }
-      bm[t * WORDS + tb] = mask;
+      *reinterpret_cast<uint2*>(bm + t * WORDS + tb) = make_uint2(mask[0], mask[1]);
       __syncthreads();
     }
   }
