@@ -387,7 +387,7 @@ __device__ __forceinline__ void pos_of(int s, int& q, int& bit) {
 }
 }  // namespace pr
 
-__global__ void __launch_bounds__(pr::SP_WAVES * 64) pruned_sp_kernel(PrArgs a) {
+__global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs a) {
   using namespace pr;
   extern __shared__ uint64_t lds_sp[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
