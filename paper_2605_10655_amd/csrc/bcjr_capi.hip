@@ -538,6 +538,9 @@ constexpr double kPrunedMargin = 30.0;   // nats below the best path
 constexpr int64_t kPrunedMaxL = 2048;
 constexpr int64_t kPrunedMaxSlots = 2048;
 constexpr int64_t kPrunedEntriesPerStep = 1024;  // average kept states per step a slot holds
+// from this temperature up the sum-product takes two kept states per lane and
+// pass (a step keeps hundreds of states there; below, a few)
+constexpr double kPrunedPairT = 0.01;
 
 bool pruned_ok(int n, int k, float T, int64_t L) {
   return n == 16 && k == 2 && T <= (float)kPrunedMaxT && L <= kPrunedMaxL;  // (T as the caller rounded it)
@@ -594,7 +597,9 @@ int run_fb_pruned(const float* w, int64_t B, int64_t L, const float* codebook, i
                             (int)pr::kMinSumLds) != hipSuccess ||
         hipFuncSetAttribute((const void*)mm_fwd_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)pr::kMinSumLds) != hipSuccess ||
-        hipFuncSetAttribute((const void*)pruned_sp_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+        hipFuncSetAttribute((const void*)pruned_sp_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)pr::kSpLds) != hipSuccess ||
+        hipFuncSetAttribute((const void*)pruned_sp_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)pr::kSpLds) != hipSuccess)
       attr_err = hipErrorInvalidValue;
   });
@@ -623,6 +628,7 @@ int run_fb_pruned(const float* w, int64_t B, int64_t L, const float* codebook, i
   a.flags = flags;
   // (the per-slot strides inside the kernels are L-based; hmin and best are
   // packed arrays of slots x L and slots floats)
+  const bool pair = T >= (float)kPrunedPairT;
   for (int64_t b0 = 0; b0 < B; b0 += slots) {
     a.b0 = b0;
     a.nblk = std::min<int64_t>(slots, B - b0);
@@ -630,8 +636,9 @@ int run_fb_pruned(const float* w, int64_t B, int64_t L, const float* codebook, i
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
     hipLaunchKernelGGL(mm_fwd_kernel, dim3((unsigned)a.nblk), dim3(pr::NT), pr::kMinSumLds, stream, a);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
-    hipLaunchKernelGGL(pruned_sp_kernel, dim3((unsigned)ceil_div(a.nblk, pr::SP_WAVES)),
-                       dim3(pr::SP_WAVES * 64), pr::kSpLds, stream, a);
+    hipLaunchKernelGGL(pair ? pruned_sp_kernel<2> : pruned_sp_kernel<1>,
+                       dim3((unsigned)ceil_div(a.nblk, pr::SP_WAVES)), dim3(pr::SP_WAVES * 64), pr::kSpLds,
+                       stream, a);
     if (hipGetLastError() != hipSuccess) return BCJR_ERR_HIP;
   }
   // marked blocks: the double-float kernel (it decodes their centring

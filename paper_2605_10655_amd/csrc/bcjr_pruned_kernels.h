@@ -385,10 +385,94 @@ __device__ __forceinline__ void pos_of(int s, int& q, int& bit) {
   q = sg & (NT - 1);
   bit = (sg >> 10) * 16 + j * 4 + u;
 }
+
+// log alpha and A of the kept predecessors (s >> 2) + j 2^14 of state s
+// (one word, bits ip * 16 + j * 4 + up); -inf and 0 for the others
+__device__ __forceinline__ void pred_vals(int s, const uint64_t* nbm, const uint32_t* npre,
+                                          int64_t base_prev, const double* la, const double* aa,
+                                          double (&v)[K], double (&y)[K]) {
+  int qp, b0;
+  pos_of(s >> 2, qp, b0);  // (j = 0)
+  const uint64_t word = nbm[qp];
+  const uint32_t pr0 = npre[qp];
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const int pb = b0 + j * 4;
+    v[j] = -INFINITY;
+    y[j] = 0.0;
+    if ((word >> pb) & 1ull) {
+      const int64_t ep = base_prev + pr0 + __popcll(word & ((1ull << pb) - 1ull));
+      v[j] = la[ep];
+      y[j] = aa[ep];
+    }
+  }
+}
+
+// h_{t+1}(d) + log beta_{t+1}(d) and g_{t+1} c(d) + B_{t+1}(d) of the kept
+// successors d = (s mod 2^14) * 4 + b (one word, bits id * 16 + jd * 4 + b);
+// -inf and 0 for the others
+__device__ __forceinline__ void succ_vals(int s, const uint64_t* nbm, const uint32_t* npre,
+                                          int64_t base_next, const double* la, const double* aa,
+                                          const float* c, double wn, double gn, double i2T,
+                                          double (&v)[K], double (&y)[K]) {
+  const int s14 = s & (GS - 1);
+  int qd, b0;
+  pos_of(s14 << 2, qd, b0);  // (b = 0)
+  const uint64_t word = nbm[qd];
+  const uint32_t pr0 = npre[qd];
+  const float4 c4 = *reinterpret_cast<const float4*>(c + (s14 << 2));
+  const float cd[K] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+  for (int b = 0; b < K; ++b) {
+    const int nb = b0 + b;
+    v[b] = -INFINITY;
+    y[b] = 0.0;
+    if ((word >> nb) & 1ull) {
+      const int64_t ed = base_next + pr0 + __popcll(word & ((1ull << nb) - 1ull));
+      const double cdb = (double)cd[b];
+      v[b] = -(wn - cdb) * (wn - cdb) * i2T + la[ed];
+      y[b] = gn * cdb + aa[ed];
+    }
+  }
+}
+
+// log sum_j exp(v_j), and the exp(v_j)-weighted mean of y_j, over the
+// finite v_j (-inf and 0 when there are none); the largest term is taken
+// as 1 without an exponential
+__device__ __forceinline__ void lse4(const double (&v)[K], const double (&y)[K], double& lse, double& mean) {
+  const double m = fmax(fmax(v[0], v[1]), fmax(v[2], v[3]));
+  if (!(m > -INFINITY)) {
+    lse = -INFINITY;
+    mean = 0.0;
+    return;
+  }
+  double s = 0.0, sy = 0.0;
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    if (v[j] == m) {
+      s += 1.0;
+      sy += y[j];
+    } else if (v[j] > -INFINITY) {
+      const double r = exp(v[j] - m);
+      s += r;
+      sy += r * y[j];
+    }
+  }
+  lse = m + log(s);
+  mean = sy / s;
+}
 }  // namespace pr
 
+// U: kept states per lane and pass.  U = 2 issues two states' loads before
+// either's stores (the neighbouring step's entries never overlap this
+// step's), which pays where a step keeps hundreds of states; U = 1 keeps the
+// registers for fetching the next step's words one step ahead, which pays
+// where a step keeps a few.
+template <int U>
 __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs a) {
   using namespace pr;
+  static_assert(U == 1 || U == 2, "states per lane and pass");
+  constexpr bool kAhead = U == 1;
   extern __shared__ uint64_t lds_sp[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint64_t* nbm = lds_sp + (size_t)wave * (kSpLdsPerWave / sizeof(uint64_t));  // [WORDS] neighbour words
@@ -409,12 +493,16 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
     // ------------------------------------------------------------ forward
     int64_t base = 0, base_prev = 0;
     double zm = -INFINITY, zs = 0.0, zy = 0.0;  // logZ and E[F] at the last step
-    uint64_t wd[WPL], nx[WPL];
-    fetch_step(bm, lane, nx);
+    uint64_t wd[WPL], nx[kAhead ? WPL : 1];
+    if constexpr (kAhead) fetch_step(bm, lane, nx);
     for (int64_t t = 0; t < L; ++t) {
+      if constexpr (kAhead) {
 #pragma unroll
-      for (int r = 0; r < WPL; ++r) wd[r] = nx[r];
-      if (t + 1 < L) fetch_step(bm + (t + 1) * WORDS, lane, nx);
+        for (int r = 0; r < WPL; ++r) wd[r] = nx[r];
+        if (t + 1 < L) fetch_step(bm + (t + 1) * WORDS, lane, nx);
+      } else {
+        fetch_step(bm + t * WORDS, lane, wd);
+      }
       int run;
       const int m = step_ranks(wd, lane, run);
       if (base + m > a.ecap || m == 0) {
@@ -425,36 +513,68 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
       for (int r0 = 0; r0 < m; r0 += LIST) {
         list_round(wd, lane, run, r0, list);
         const int mr = m - r0 < LIST ? m - r0 : LIST;
-        for (int k = lane; k < mr; k += 64) {
-          const int s = (int)list[k];
-          const int64_t e = base + r0 + k;
-          const double cs = (double)a.c[s];
-          const double h = -(wt - cs) * (wt - cs) * i2T;
-          double lv, av;
-          if (t == 0) {
-            lv = h;
-            av = gt * cs;
-          } else {
-            // predecessors (s >> 2) + j 2^14: one word, bits ip * 16 + j * 4 + up
-            int qp, b0;
-            pos_of(s >> 2, qp, b0);  // (j = 0)
-            const uint64_t word = nbm[qp];
-            const uint32_t pr0 = npre[qp];
-            double pm = -INFINITY, ps = 0.0, py = 0.0;
+        if constexpr (U == 1) {
+          for (int k = lane; k < mr; k += 64) {
+            const int s = (int)list[k];
+            const int64_t e = base + r0 + k;
+            const double cs = (double)a.c[s];
+            const double h = -(wt - cs) * (wt - cs) * i2T;
+            double lv, av;
+            if (t == 0) {
+              lv = h;
+              av = gt * cs;
+            } else {
+              // predecessors (s >> 2) + j 2^14: one word, bits ip * 16 + j * 4 + up
+              int qp, b0;
+              pos_of(s >> 2, qp, b0);  // (j = 0)
+              const uint64_t word = nbm[qp];
+              const uint32_t pr0 = npre[qp];
+              double pm = -INFINITY, ps = 0.0, py = 0.0;
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-              const int pb = b0 + j * 4;
-              if ((word >> pb) & 1ull) {
-                const int64_t ep = base_prev + pr0 + __popcll(word & ((1ull << pb) - 1ull));
-                lse_add(pm, ps, py, la[ep], aa[ep]);
+              for (int j = 0; j < K; ++j) {
+                const int pb = b0 + j * 4;
+                if ((word >> pb) & 1ull) {
+                  const int64_t ep = base_prev + pr0 + __popcll(word & ((1ull << pb) - 1ull));
+                  lse_add(pm, ps, py, la[ep], aa[ep]);
+                }
               }
+              lv = (pm > -INFINITY) ? h + pm + log(ps) : -INFINITY;
+              av = gt * cs + ((pm > -INFINITY) ? py / ps : 0.0);
             }
-            lv = (pm > -INFINITY) ? h + pm + log(ps) : -INFINITY;
-            av = gt * cs + ((pm > -INFINITY) ? py / ps : 0.0);
+            la[e] = lv;
+            aa[e] = av;
+            if (t == L - 1) lse_add(zm, zs, zy, lv, av);
           }
-          la[e] = lv;
-          aa[e] = av;
-          if (t == L - 1) lse_add(zm, zs, zy, lv, av);
+        } else {
+          // (this step's entries lie above the previous step's)
+          for (int k = lane; k < mr; k += 64 * U) {
+            const bool two = U == 2 && k + 64 < mr;
+            int st[U];
+            st[0] = (int)list[k];
+            if constexpr (U == 2) st[1] = two ? (int)list[k + 64] : st[0];
+            double cs[U], v[U][K], y[U][K];
+#pragma unroll
+            for (int x = 0; x < U; ++x) {
+              cs[x] = (double)a.c[st[x]];
+              if (t > 0) pred_vals(st[x], nbm, npre, base_prev, la, aa, v[x], y[x]);
+            }
+#pragma unroll
+            for (int x = 0; x < U; ++x) {
+              if (x == 1 && !two) break;
+              const double h = -(wt - cs[x]) * (wt - cs[x]) * i2T;
+              double lv = h, av = gt * cs[x];
+              if (t > 0) {
+                double lp, mp;
+                lse4(v[x], y[x], lp, mp);
+                lv = h + lp;
+                av += mp;
+              }
+              const int64_t e = base + r0 + k + 64 * x;
+              la[e] = lv;
+              aa[e] = av;
+              if (t == L - 1) lse_add(zm, zs, zy, lv, av);
+            }
+          }
         }
       }
       keep_tables(wd, lane, run, nbm, npre);
@@ -481,11 +601,15 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
     }
     // ----------------------------------------------------------- backward
     int64_t base_next = base;  // base of step t + 1
-    fetch_step(bm + (L - 1) * WORDS, lane, nx);
+    if constexpr (kAhead) fetch_step(bm + (L - 1) * WORDS, lane, nx);
     for (int64_t t = L - 1; t >= 0; --t) {
+      if constexpr (kAhead) {
 #pragma unroll
-      for (int r = 0; r < WPL; ++r) wd[r] = nx[r];
-      if (t > 0) fetch_step(bm + (t - 1) * WORDS, lane, nx);
+        for (int r = 0; r < WPL; ++r) wd[r] = nx[r];
+        if (t > 0) fetch_step(bm + (t - 1) * WORDS, lane, nx);
+      } else {
+        fetch_step(bm + t * WORDS, lane, wd);
+      }
       int run;
       const int m = step_ranks(wd, lane, run);
       const int64_t bt = base_next - m;
@@ -496,41 +620,75 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
       for (int r0 = 0; r0 < m; r0 += LIST) {
         list_round(wd, lane, run, r0, list);
         const int mr = m - r0 < LIST ? m - r0 : LIST;
-        for (int k = lane; k < mr; k += 64) {
-          const int s = (int)list[k];
-          const int64_t e = bt + r0 + k;
-          const double cs = (double)a.c[s];
-          const double lae = la[e], aae = aa[e];
-          double lbv = 0.0, bvv = 0.0;
-          if (t + 1 < L) {
-            // successors (s mod 2^14) * 4 + b: one word, bits id * 16 + jd * 4 + b
-            const int s14 = s & (GS - 1);
-            int qd, b0;
-            pos_of(s14 << 2, qd, b0);  // (b = 0)
-            const uint64_t word = nbm[qd];
-            const uint32_t pr0 = npre[qd];
-            double nm = -INFINITY, ns = 0.0, ny = 0.0;
+        if constexpr (U == 1) {
+          for (int k = lane; k < mr; k += 64) {
+            const int s = (int)list[k];
+            const int64_t e = bt + r0 + k;
+            const double cs = (double)a.c[s];
+            const double lae = la[e], aae = aa[e];
+            double lbv = 0.0, bvv = 0.0;
+            if (t + 1 < L) {
+              // successors (s mod 2^14) * 4 + b: one word, bits id * 16 + jd * 4 + b
+              const int s14 = s & (GS - 1);
+              int qd, b0;
+              pos_of(s14 << 2, qd, b0);  // (b = 0)
+              const uint64_t word = nbm[qd];
+              const uint32_t pr0 = npre[qd];
+              double nm = -INFINITY, ns = 0.0, ny = 0.0;
 #pragma unroll
-            for (int b = 0; b < K; ++b) {
-              const int nb = b0 + b;
-              if ((word >> nb) & 1ull) {
-                const int64_t ed = base_next + pr0 + __popcll(word & ((1ull << nb) - 1ull));
-                const double cd = (double)a.c[(s14 << 2) | b];
-                const double hd = -(wn - cd) * (wn - cd) * i2T;
-                lse_add(nm, ns, ny, hd + la[ed], gn * cd + aa[ed]);  // (step t + 1: beta, B)
+              for (int b = 0; b < K; ++b) {
+                const int nb = b0 + b;
+                if ((word >> nb) & 1ull) {
+                  const int64_t ed = base_next + pr0 + __popcll(word & ((1ull << nb) - 1ull));
+                  const double cd = (double)a.c[(s14 << 2) | b];
+                  const double hd = -(wn - cd) * (wn - cd) * i2T;
+                  lse_add(nm, ns, ny, hd + la[ed], gn * cd + aa[ed]);  // (step t + 1: beta, B)
+                }
               }
+              lbv = (nm > -INFINITY) ? nm + log(ns) : -INFINITY;
+              bvv = (nm > -INFINITY) ? ny / ns : 0.0;
             }
-            lbv = (nm > -INFINITY) ? nm + log(ns) : -INFINITY;
-            bvv = (nm > -INFINITY) ? ny / ns : 0.0;
+            la[e] = lbv;
+            aa[e] = bvv;
+            const double P = exp(lae + lbv - logZ);
+            const double X = aae + bvv - EF;
+            sPc += P * cs;
+            sPX += P * X;
+            sPcX += P * cs * X;
+            if (a.dc && P > 0.0) atomicAdd(a.dc + s, P * (gt + (wt - cs) * X * iT));
           }
-          la[e] = lbv;
-          aa[e] = bvv;
-          const double P = exp(lae + lbv - logZ);
-          const double X = aae + bvv - EF;
-          sPc += P * cs;
-          sPX += P * X;
-          sPcX += P * cs * X;
-          if (a.dc && P > 0.0) atomicAdd(a.dc + s, P * (gt + (wt - cs) * X * iT));
+        } else {
+          // (the successors' entries lie above this step's)
+          for (int k = lane; k < mr; k += 64 * U) {
+            const bool two = U == 2 && k + 64 < mr;
+            int st[U];
+            st[0] = (int)list[k];
+            if constexpr (U == 2) st[1] = two ? (int)list[k + 64] : st[0];
+            double cs[U], lae[U], aae[U], v[U][K], y[U][K];
+#pragma unroll
+            for (int x = 0; x < U; ++x) {
+              const int64_t e = bt + r0 + (two ? k + 64 * x : k);
+              cs[x] = (double)a.c[st[x]];
+              lae[x] = la[e];
+              aae[x] = aa[e];
+              if (t + 1 < L) succ_vals(st[x], nbm, npre, base_next, la, aa, a.c, wn, gn, i2T, v[x], y[x]);
+            }
+#pragma unroll
+            for (int x = 0; x < U; ++x) {
+              if (x == 1 && !two) break;
+              double lbv = 0.0, bvv = 0.0;
+              if (t + 1 < L) lse4(v[x], y[x], lbv, bvv);
+              const int64_t e = bt + r0 + k + 64 * x;
+              la[e] = lbv;
+              aa[e] = bvv;
+              const double P = exp(lae[x] + lbv - logZ);
+              const double X = aae[x] + bvv - EF;
+              sPc += P * cs[x];
+              sPX += P * X;
+              sPcX += P * cs[x] * X;
+              if (a.dc && P > 0.0) atomicAdd(a.dc + st[x], P * (gt + (wt - cs[x]) * X * iT));
+            }
+          }
         }
       }
       keep_tables(wd, lane, run, nbm, npre);
