@@ -291,14 +291,16 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
         uint32_t bits = 0;
 #pragma unroll
         for (int u = 0; u < K; ++u) {
-          const float hb = fmaf(bound_value((qw >> (8 * u)) & 0xFFu), step, hm);
+          // (the forward cost a kept state may reach: one subtraction for
+          // the four states of this bound, inside the window's widening)
+          const float thr = lim - fmaf(bound_value((qw >> (8 * u)) & 0xFFu), step, hm);
           float m = INFINITY;
 #pragma unroll
           for (int j = 0; j < K; ++j) {
             const float d = wt - cb[i][j][u];
             const float f = fmaf(d, d, gin[j]);
             m = fminf(m, f);
-            bits |= (f + hb <= lim ? 1u : 0u) << (j * 4 + u);
+            bits |= (f <= thr ? 1u : 0u) << (j * 4 + u);
           }
           mo[u] = m;
         }
