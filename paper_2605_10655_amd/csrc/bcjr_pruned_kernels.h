@@ -80,16 +80,20 @@ constexpr size_t kSpLds = kSpLdsPerWave * SP_WAVES;
 // Blocks far outside the codebook's range have future costs spread over
 // thousands of windows; a code that saturated at a few windows would keep
 // most of their states.
+//
+// The exponent code is z's bits above bit 20 (8 x the biased exponent
+// e + 127, plus m) minus 8 x 134 - 128 = 944.  Below z = 128 it exceeds
+// floor(z) (it is 8 e + 72 + m there), from 128 on it is at most floor(z),
+// so the code is the smaller of the two, with floor(z) capped at 255 (a NaN
+// codes as 255).  Its value back is (code + 944) << 20 as a float.
 __device__ __forceinline__ uint32_t bound_code(float z) {
-  // (z >= 0: bits 20 and up hold 8 x the biased exponent e + 127, plus m, so
-  // 128 + 8 (e - 7) + m = (bits >> 20) - (8 * 134 - 128))
-  const uint32_t c = (__float_as_uint(z) >> 20) - 944u;
-  return z < 128.f ? (uint32_t)fminf(z, 127.f) : (c > 255u ? 255u : c);
+  const uint32_t lin = (uint32_t)fminf(z, 255.f);
+  const uint32_t ex = (__float_as_uint(z) >> 20) - 944u;
+  return lin < ex ? lin : ex;
 }
 
 __device__ __forceinline__ float bound_value(uint32_t q) {
-  const uint32_t d = q - 128u;
-  return q < 128u ? (float)q : __uint_as_float(((134u + (d >> 3)) << 23) | ((d & 7u) << 20));
+  return q < 128u ? (float)q : __uint_as_float((q + 944u) << 20);
 }
 
 __device__ __forceinline__ float wave_min(float v) {
@@ -227,7 +231,7 @@ __global__ void __launch_bounds__(pr::NT) mm_back_kernel(PrArgs a) {
       for (int i = 0; i < SGT; ++i) {
         uint32_t word = 0;
 #pragma unroll
-        for (int b = 0; b < K; ++b) word |= bound_code(fmaxf((in[i][b] - hm) * a.qscale, 0.f)) << (8 * b);
+        for (int b = 0; b < K; ++b) word |= bound_code((in[i][b] - hm) * a.qscale) << (8 * b);  // (in >= hm)
         __builtin_amdgcn_raw_buffer_store_b32(word, qr, (int)((uint32_t)(tb + i * NT) * K), (int)(t * GS), 0);
       }
       if (tb == 0) hmin[t] = hm;
