@@ -27,7 +27,7 @@ RATES_SRC = os.path.join(CSRC, "issue_rates.hip")
 RATES_LIB = os.path.join(PKG, "libissue_rates.so")
 DEPENDS = SOURCES + [os.path.join(CSRC, f) for f in (
     "bcjr_device.h", "bcjr_kernels.h", "bcjr_vec_kernels.h", "bcjr_qat.h", "bcjr_internal.h",
-    "bcjr_generic_kernels.h", "bcjr_ldlq_kernels.h", "bcjr_rot_kernels.h")] + [
+    "bcjr_generic_kernels.h", "bcjr_ldlq_kernels.h", "bcjr_rot_kernels.h", "bcjr_pruned_kernels.h")] + [
     os.path.join(INCLUDE, "bcjr.h")]
 
 BASE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
