@@ -68,7 +68,8 @@ constexpr int K = 4;
 constexpr int NW = NT / 64;
 constexpr int SP_WAVES = 4;       // pruned_sp_kernel: one block per wave
 constexpr int WORDS = NT;         // kept-state words per step
-constexpr size_t kMinSumLds = (size_t)2 * GS * sizeof(float) + (size_t)3 * NW * sizeof(float);
+constexpr size_t kMinSumLds = (size_t)2 * GS * sizeof(float) + (size_t)3 * NW * sizeof(float) +
+                              (size_t)256 * sizeof(float);  // (the forward sweep's bound values)
 constexpr size_t kSpLdsPerWave = (size_t)WORDS * sizeof(uint64_t) + (size_t)WORDS * sizeof(uint32_t) +
                                   (size_t)1024 * sizeof(uint32_t);
 constexpr size_t kSpLds = kSpLdsPerWave * SP_WAVES;
@@ -260,6 +261,9 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
   const int tb = threadIdx.x;
   const int64_t L = a.L;
   const float step = a.theta * (1.f / 16.f);
+  // the distortion each byte code stands for, the same at every step
+  float* bval = lds_mm + 2 * GS + 3 * NW;
+  for (int x = tb; x < 256; x += NT) bval[x] = bound_value((uint32_t)x) * step;
   const rsrc_t cbk = make_rsrc(a.c, (uint32_t)GS * K * 4u);
   const uint32_t voK = (uint32_t)tb * K * 4u;
   float cb[SGT][K][K];  // as in the backward sweep
@@ -282,7 +286,7 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
       const float* pin = lds_mm + (t & 1) * GS;
       float* pout = lds_mm + ((t + 1) & 1) * GS;
       const float wt = ld_uniform(wb, t);
-      const float hm = ld_uniform(hmin, t);
+      const float lmh = lim - ld_uniform(hmin, t);
       uint32_t mask[2] = {0u, 0u};
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
@@ -297,7 +301,7 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
         for (int u = 0; u < K; ++u) {
           // (the forward cost a kept state may reach: one subtraction for
           // the four states of this bound, inside the window's widening)
-          const float thr = lim - fmaf(bound_value((qw >> (8 * u)) & 0xFFu), step, hm);
+          const float thr = lmh - bval[(qw >> (8 * u)) & 0xFFu];
           float m = INFINITY;
 #pragma unroll
           for (int j = 0; j < K; ++j) {
