@@ -103,26 +103,48 @@ __device__ __forceinline__ float wave_min(float v) {
   return v;
 }
 
-__device__ __forceinline__ int wave_sum_i(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+// Wave reductions by DPP lane permutations within each 16-lane row, then the
+// four row results read from lanes 0, 16, 32, 48 (or 15, 31, 47, 63) and
+// combined in a fixed order: no LDS round trip, and every lane gets the
+// same bits.  Called in wave-uniform control flow (all 64 lanes active).
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = dpp_i<CTRL>((int)b), hi = dpp_i<CTRL>((int)(b >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)b, l), hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
 }
 
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return __shfl(v, 0);
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);  // row_half_mirror
+  v += dpp_d<0x140>(v);  // row_mirror: every lane holds its row's sum
+  return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
 }
 
-// exclusive prefix over the wave's lanes
-__device__ __forceinline__ int wave_excl_scan(int v, int lane) {
+// exclusive prefix over the wave's lanes, and the wave's total
+__device__ __forceinline__ int wave_excl_scan(int v, int lane, int& total) {
   int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  x += dpp_i<0x111>(x);  // row_shr:1 (lanes without a source add 0)
+  x += dpp_i<0x112>(x);  // row_shr:2
+  x += dpp_i<0x114>(x);  // row_shr:4
+  x += dpp_i<0x118>(x);  // row_shr:8: inclusive prefix within the row
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31),
+            r2 = __builtin_amdgcn_readlane(x, 47), r3 = __builtin_amdgcn_readlane(x, 63);
+  const int row = lane >> 4;
+  x += (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+  total = r0 + r1 + r2 + r3;
   return x - v;
 }
 
@@ -354,8 +376,9 @@ __device__ __forceinline__ int step_ranks(const uint64_t (&wd)[WPL], int lane, i
   int cnt = 0;
 #pragma unroll
   for (int r = 0; r < WPL; ++r) cnt += __popcll(wd[r]);
-  run = wave_excl_scan(cnt, lane);
-  return wave_sum_i(cnt);
+  int total;
+  run = wave_excl_scan(cnt, lane, total);
+  return total;
 }
 
 // kept states of ranks [r0, r0 + LIST) into list[rank - r0]
