@@ -152,6 +152,12 @@ __device__ __forceinline__ int wave_excl_scan(int v, int lane, int& total) {
 // weighted mean of the payload
 __device__ __forceinline__ void lse_add(double& m, double& s, double& y, double v, double yv) {
   if (!(v > -INFINITY)) return;
+  if (!(m > -INFINITY)) {  // the first term: no exponential
+    m = v;
+    s = 1.0;
+    y = yv;
+    return;
+  }
   if (v > m) {
     const double r = exp(m - v);
     s = s * r + 1.0;
@@ -181,6 +187,12 @@ __device__ __forceinline__ void lse_merge(double& m, double& s, double& y, doubl
     y += yo * r;
   }
 }
+
+// The entries and LDS tables of a block are written and read by its one
+// wave only, whose memory operations take effect in program order: a fence
+// at wavefront scope keeps the compiler from reordering them and emits no
+// wait.
+__device__ __forceinline__ void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
 // state of bit `bit` of word `q`
 __device__ __forceinline__ int state_of(int q, int bit) {
@@ -491,7 +503,7 @@ __device__ __forceinline__ void lse4(const double (&v)[K], const double (&y)[K],
       sy += r * y[j];
     }
   }
-  lse = m + log(s);
+  lse = m + (s == 1.0 ? 0.0 : log(s));
   mean = sy / s;
 }
 }  // namespace pr
@@ -571,7 +583,7 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
                   lse_add(pm, ps, py, la[ep], aa[ep]);
                 }
               }
-              lv = (pm > -INFINITY) ? h + pm + log(ps) : -INFINITY;
+              lv = (pm > -INFINITY) ? h + pm + (ps == 1.0 ? 0.0 : log(ps)) : -INFINITY;
               av = gt * cs + ((pm > -INFINITY) ? py / ps : 0.0);
             }
             la[e] = lv;
@@ -611,7 +623,7 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
         }
       }
       keep_tables(wd, lane, run, nbm, npre);
-      __threadfence_block();
+      wave_fence();
       base_prev = base;
       base += m;
     }
@@ -678,7 +690,7 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
                   lse_add(nm, ns, ny, hd + la[ed], gn * cd + aa[ed]);  // (step t + 1: beta, B)
                 }
               }
-              lbv = (nm > -INFINITY) ? nm + log(ns) : -INFINITY;
+              lbv = (nm > -INFINITY) ? nm + (ns == 1.0 ? 0.0 : log(ns)) : -INFINITY;
               bvv = (nm > -INFINITY) ? ny / ns : 0.0;
             }
             la[e] = lbv;
@@ -725,7 +737,7 @@ __global__ void __launch_bounds__(pr::SP_WAVES * 64, 2) pruned_sp_kernel(PrArgs 
         }
       }
       keep_tables(wd, lane, run, nbm, npre);
-      __threadfence_block();
+      wave_fence();
       sPc = wave_sum_d(sPc);
       sPX = wave_sum_d(sPX);
       sPcX = wave_sum_d(sPcX);
