@@ -315,12 +315,30 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
     const float best = ld_uniform(a.best, sl);
     const float lim = best + a.theta + 1e-5f * (fabsf(best) + a.theta);
     for (int x = tb; x < GS; x += NT) lds_mm[x] = 0.f;
+    // the step's bound words, weight and minimum are fetched one step ahead
+    uint32_t qn[SGT];
+#pragma unroll
+    for (int i = 0; i < SGT; ++i)
+      qn[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(qr, (int)((uint32_t)(tb + i * NT) * K), 0, 0);
+    float wn = ld_uniform(wb, 0), hn = ld_uniform(hmin, 0);
     __syncthreads();
     for (int64_t t = 0; t < L; ++t) {
       const float* pin = lds_mm + (t & 1) * GS;
       float* pout = lds_mm + ((t + 1) & 1) * GS;
-      const float wt = ld_uniform(wb, t);
-      const float lmh = lim - ld_uniform(hmin, t);
+      const float wt = wn;
+      const float lmh = lim - hn;
+      uint32_t qc[SGT];
+#pragma unroll
+      for (int i = 0; i < SGT; ++i) qc[i] = qn[i];
+      {
+        const int64_t tn = t + 1 < L ? t + 1 : t;
+#pragma unroll
+        for (int i = 0; i < SGT; ++i)
+          qn[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(qr, (int)((uint32_t)(tb + i * NT) * K),
+                                                                 (int)(tn * GS), 0);
+        wn = ld_uniform(wb, tn);
+        hn = ld_uniform(hmin, tn);
+      }
       uint32_t mask[2] = {0u, 0u};
 #pragma unroll
       for (int i = 0; i < SGT; ++i) {
@@ -328,7 +346,7 @@ __global__ void __launch_bounds__(pr::NT) mm_fwd_kernel(PrArgs a) {
         float gin[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) gin[j] = pin[j * NSG + sg];
-        const uint32_t qw = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(qr, (int)((uint32_t)sg * K), (int)(t * GS), 0);
+        const uint32_t qw = qc[i];
         float mo[K];
         uint32_t bits = 0;
 #pragma unroll
